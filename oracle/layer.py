@@ -26,10 +26,18 @@ Readings where the paper is silent or differs from the workloads built here:
     scaling), so d(beta)/d(qq.kk) carries the scaler there.
 
 Mixed precision: the paper stores data in fp16 and accumulates in fp32
-(Sec. "Evaluation Details" of the appendix).  With store_dtype set, every
-tensor that an operator of Table 3 materialises is rounded to that storage
-type (round-to-nearest-even); all arithmetic stays float64.  store_dtype
-"f64" gives the plain float64 definition.
+(Sec. "Evaluation Details" of the appendix) but does not fix which tensors
+are materialised, which depends on the fusion.  With store_dtype set, each
+tensor written by a fused operator or contraction is rounded to that
+storage type (round-to-nearest-even) where it is written; values that stay
+inside one fused operator are not rounded, and a fused operator that writes
+two tensors derives both from its unrounded value (e.g. the softmax writes
+the probabilities and, from the same unrounded values, the dropped-out
+probabilities).  The fusion boundaries are the paper's kernel list, with
+two further fusions: the residual + LayerNorm-scale/shift backward ("ebsb")
+feeds the LayerNorm backward ("blnrd") directly, and the encoder-input
+residual ("bei") is added where the Q/K/V input gradient is formed.  All
+arithmetic stays float64; store_dtype "f64" gives the plain definition.
 
 Parity: forward pinned to torch.nn.TransformerEncoderLayer and
 torch.nn.MultiheadAttention at p = 0 (float64); forward and every gradient
@@ -194,9 +202,10 @@ def mha_forward(q, k, v, prm: Dict[str, np.ndarray], cfg: Config, out_bias: bool
     # QK^T, scaled.
     beta = r(cfg.s * contract("phbk,phbj->hbjk", kk, qq))
     # Softmax over k, then dropout on the probabilities.
-    prob = r(softmax_k(beta))
+    prob_x = softmax_k(beta)
+    prob = r(prob_x)
     m_attn = attn_dropout(cfg)
-    alpha = r(prob * m_attn)
+    alpha = r(prob_x * m_attn)
     # Gamma and Out.
     gamma = r(contract("whbk,hbjk->whbj", vv, alpha))
     out = contract("whi,whbj->ibj", wo, gamma)
@@ -282,8 +291,9 @@ def encoder_backward(dy_bji, cache, prm: Dict[str, np.ndarray], cfg: Config):
     g["g2"] = (dY * cache["xhat2"]).sum(axis=(1, 2))
     g["be2"] = dY.sum(axis=(1, 2))
     # LayerNorm dX and dropout dX (blnrd); dS2 also feeds the residual.
-    dS2 = r(layernorm_i_bwd(dY, cache["xhat2"], cache["rstd2"], prm["g2"]))
-    dO = r(dS2 * cache["m_ffn"])
+    dS2_x = layernorm_i_bwd(dY, cache["xhat2"], cache["rstd2"], prm["g2"])
+    dS2 = r(dS2_x)
+    dO = r(dS2_x * cache["m_ffn"])
     # Linear (second) dX and dW.
     dA = r(contract("if,ibj->fbj", prm["w2"], dO))
     g["w2"] = contract("ibj,fbj->if", dO, cache["a"])
@@ -294,19 +304,20 @@ def encoder_backward(dy_bji, cache, prm: Dict[str, np.ndarray], cfg: Config):
     # Linear (first) dX and dW.
     dY1f = r(contract("fi,fbj->ibj", prm["w1"], dH))
     g["w1"] = contract("fbj,ibj->fi", dH, cache["y1"])
-    # Residual and LayerNorm dW (ebsb).
-    dY1 = r(dY1f + dS2)
+    # Residual and LayerNorm dW (ebsb), fused with the LayerNorm backward.
+    dY1 = dY1f + dS2
     g["g1"] = (dY1 * cache["xhat1"]).sum(axis=(1, 2))
     g["be1"] = dY1.sum(axis=(1, 2))
     # LayerNorm dX and dropout dX (blnrd), output-bias dW (baob).
-    dS1 = r(layernorm_i_bwd(dY1, cache["xhat1"], cache["rstd1"], prm["g1"]))
-    dAO = r(dS1 * cache["m_ao"])
+    dS1_x = layernorm_i_bwd(dY1, cache["xhat1"], cache["rstd1"], prm["g1"])
+    dS1 = r(dS1_x)
+    dAO = r(dS1_x * cache["m_ao"])
     g["bo"] = dAO.sum(axis=(1, 2))
     # Attention backward (Out ... Q,K,V dW, input-bias dW).
     dq, dk, dv, ga, inter = mha_backward(dAO, cache, prm, cfg, out_bias=False)
     g.update(ga)
     # Encoder-input residual (bei): self-attention sums the three input grads.
-    dXa = r(dq + dk + dv)
+    dXa = dq + dk + dv
     dX = r(dXa + dS1)
     inter.update(dS2=dS2, dO=dO, dA=dA, dH=dH, dY1f=dY1f, dY1=dY1, dS1=dS1, dAO=dAO, dXa=dXa)
     return np.ascontiguousarray(np.transpose(dX, (1, 2, 0))), g, inter
