@@ -1,0 +1,212 @@
+#!/usr/bin/env python
+"""Benchmark: forward + backward of one BERT-large post-LN encoder layer
+(fp16, B=8, L=512, I=1024, H=16, P=64, FFN 4096, three dropouts p=0.1) on
+one MI355X, through the library's C ABI.
+
+Prints one JSON line: ms per fwd+bwd step (inputs resident in HBM), the
+roofline position of the dominant kernel (per-launch durations measured
+with HIP events on the launch stream), the aggregate HBM rate of the fused
+memory-bound operators, and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "BERT-large layer fwd+bwd ms/iter; fused-kernel HBM GB/s vs peak"
+
+
+def csrc_hash() -> str:
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2007_00072_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        h.update(f.encode())
+        h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(label: str):
+    """HBM bytes per launch of `label` from the committed counter summary, if
+    it was taken on the current kernel sources."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        t = json.load(open(p))
+    except ValueError:
+        return None
+    e = t.get("kernels", {}).get(label)
+    if not e or t.get("csrc_sha") != csrc_hash():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, sample_b: int):
+    """The oracle (float64, numpy) on the first `sample_b` sequences of the
+    batch, forward + backward, scaled to ms per full step."""
+    import numpy as np
+    from oracle import layer as OL
+    from paper_2007_00072_amd.inputs import make_activation, make_params
+
+    s = wl.shape
+    params = {n: t.double().numpy() for n, t in make_params(wl).items()}
+    x = make_activation(wl, 0).double().numpy()[:sample_b]
+    dy = make_activation(wl, 1).double().numpy()[:sample_b]
+    cfg = OL.Config(B=sample_b, J=s.J, K=s.K, H=s.H, P=s.P, W=s.W, I=s.I, F=s.F, p_attn=wl.p_attn,
+                    p_attn_out=wl.p_attn_out, p_ffn_out=wl.p_ffn_out, seed=wl.seed, eps=1e-12,
+                    store_dtype=wl.dtype)
+    t0 = time.perf_counter()
+    _, cache = OL.encoder_forward(x, params, cfg)
+    OL.encoder_backward(dy, cache, params, cfg)
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    whole = sample_b == s.B
+    return {"value": round(dt * 1e3 * s.B / sample_b, 1),
+            "unit": "ms/iter" if whole else "ms/iter (extrapolated from sample)",
+            "cores": threads, "kind": "oracle",
+            "sample": (f"one full fwd+bwd step ({s.B} sequences)" if whole else
+                       f"first {sample_b} of {s.B} sequences, fwd+bwd, scaled x{s.B / sample_b:g}") +
+                      f"; float64 numpy, BLAS threads={threads}, element-wise steps single-threaded",
+            "sample_seconds": round(dt, 2)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="bert_large_f16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=0, help="sequences in the CPU-oracle sample (0: the whole batch)")
+    ap.add_argument("--kernels-json", default=None, help="write the per-kernel table here")
+    a = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": a.gpus}))
+        return 2
+
+    import torch
+    from paper_2007_00072_amd import dataflow, lib
+    from paper_2007_00072_amd.inputs import WORKLOADS, make_activation, make_params
+    from paper_2007_00072_amd.runner import EncoderLayer, desc_for
+
+    wl = WORKLOADS[a.workload]
+    s = wl.shape
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layer = EncoderLayer(desc_for(wl), make_params(wl), dev)
+    x = make_activation(wl, 0).to(dev)
+    dy = make_activation(wl, 1).to(dev)
+    y = torch.empty_like(x)
+    dx = torch.empty_like(x)
+
+    def step():
+        layer.forward(x, y)
+        layer.backward(x, dy, dx)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(st)
+    for _ in range(a.steps):
+        step()
+    e1.record(st)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / a.steps
+
+    # per-launch durations: the library brackets each launch with events on this stream
+    lib.dm_trace_enable(True)
+    for _ in range(a.steps):
+        step()
+    torch.cuda.synchronize()
+    recs = lib.trace_records()
+    lib.dm_trace_enable(False)
+    per = {}
+    for lab, t in recs:
+        per.setdefault(lab, []).append(t)
+    work = dataflow.encoder_layer(s, wl.dtype)
+    table = []
+    for lab, ts in per.items():
+        w = work.get(lab)
+        avg = sum(ts) / len(ts)
+        launches_per_step = len(ts) / a.steps
+        row = {"kernel": lab, "us": round(avg * 1e3, 2), "launches_per_step": launches_per_step}
+        if w is not None:
+            row.update(bound=w.bound, gflop=round(w.flop / 1e9, 4), mbytes=round(w.bytes / 1e6, 3))
+            if avg > 0:
+                row["tflops"] = round(w.flop / (avg * 1e-3) / 1e12, 1)
+                row["gbs"] = round(w.bytes / (avg * 1e-3) / 1e9, 1)
+        table.append(row)
+    traced_ms = sum(r["us"] * r["launches_per_step"] for r in table) / 1e3
+    dom = max(table, key=lambda r: r["us"] * r["launches_per_step"])
+    dw = work[dom["kernel"]]
+    dom_s = dom["us"] * 1e-6
+    if dw.bound == "mfma":
+        achieved = dw.flop / dom_s / 1e12
+        peak = dataflow.MFMA_PEAK_TFLOPS[wl.dtype]
+        unit = "TFLOP/s"
+    else:
+        achieved = dw.bytes / dom_s / 1e9
+        peak = dataflow.HBM_PEAK_GBS
+        unit = "GB/s"
+    roof = {"bound": dw.bound, "kernel": dom["kernel"], "achieved": round(achieved, 1), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(dom["kernel"]),
+            "per_launch_us": dom["us"],
+            "algorithmic_per_launch": dw.flop if dw.bound == "mfma" else dw.bytes}
+    fused = [r for r in table if work.get(r["kernel"]) is not None and work[r["kernel"]].bound == "hbm"
+             and work[r["kernel"]].flop == 0.0]
+    fb = sum(work[r["kernel"]].bytes * r["launches_per_step"] for r in fused)
+    ft = sum(r["us"] * r["launches_per_step"] for r in fused) * 1e-6
+    fused_summary = {"GB/s": round(fb / ft / 1e9, 1), "frac_of_peak": round(fb / ft / 1e9 / dataflow.HBM_PEAK_GBS, 4),
+                     "us_per_step": round(ft * 1e6, 1), "mbytes_per_step": round(fb / 1e6, 2)}
+    contraction = [r for r in table if work.get(r["kernel"]) is not None and work[r["kernel"]].flop > 0]
+    cf = sum(work[r["kernel"]].flop * r["launches_per_step"] for r in contraction)
+    ct = sum(r["us"] * r["launches_per_step"] for r in contraction) * 1e-6
+    mf = [r for r in contraction if work[r["kernel"]].bound == "mfma"]
+    mff = sum(work[r["kernel"]].flop for r in mf)
+    mft = sum(r["us"] for r in mf) * 1e-6
+
+    out = {
+        "metric": METRIC, "value": round(ms, 4), "unit": "ms", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic (seeded N(0,1) inputs, N(0,0.02) weights)",
+        "config": {"workload": f"{wl.name}: BERT-large encoder layer fwd+bwd, B={s.B}, L={s.J}, I={s.I}, "
+                               f"H={s.H}, P={s.P}, FFN={s.F}, GELU, post-LN, dropout p={wl.p_attn} x3",
+                   "global_batch": s.B, "seq_len": s.J, "parallelism": "single GPU"},
+        "roofline": roof,
+        "fused_hbm": fused_summary,
+        "contractions": {"tflops_all": round(cf / ct / 1e12, 1), "us_per_step": round(ct * 1e6, 1),
+                         "mfma_bound_tflops": round(mff / mft / 1e12, 1),
+                         "mfma_bound_frac": round(mff / mft / 1e12 / dataflow.MFMA_PEAK_TFLOPS[wl.dtype], 4)},
+        "traced_ms_per_step": round(traced_ms, 4),
+        "wall_s": round(wall, 3),
+    }
+    if a.kernels_json:
+        with open(a.kernels_json, "w") as f:
+            json.dump({"workload": wl.name, "ms_per_step": ms, "kernels": table}, f, indent=1)
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, a.cpu_sample or s.B)
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,378 @@
+// C ABI: error state, argument validation and the fused-operator entry
+// points.  Every entry point validates all arguments before its first
+// launch, so a call that fails has enqueued nothing.
+#include <stdarg.h>
+#include <stdio.h>
+#include <math.h>
+
+#include <atomic>
+#include <mutex>
+#include <vector>
+
+#include "gemm.hpp"
+#include "internal.hpp"
+
+namespace dm {
+
+static thread_local char g_err[512] = "";
+
+int set_error(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int check_launch(const char* what) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(DM_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+    return DM_OK;
+}
+
+// ------------------------------------------------------------ timing
+namespace {
+struct TraceRec {
+    const char* label;
+    hipEvent_t a, b;
+};
+std::atomic<bool> g_trace_on{false};
+std::mutex g_trace_mu;
+std::vector<TraceRec> g_trace;     // records of the current session
+std::vector<hipEvent_t> g_events;  // event pool, reused across sessions
+size_t g_events_used = 0;
+
+hipEvent_t pooled_event() {
+    if (g_events_used == g_events.size()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        g_events.push_back(e);
+    }
+    return g_events[g_events_used++];
+}
+}  // namespace
+
+TraceScope::TraceScope(const char* label, hipStream_t s) : idx(-1), st(s) {
+    if (!g_trace_on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    hipEvent_t a = pooled_event(), b = pooled_event();
+    if (!a || !b) return;
+    (void)hipEventRecord(a, st);
+    g_trace.push_back({label, a, b});
+    idx = (int)g_trace.size() - 1;
+}
+
+void TraceScope::stop() {
+    if (idx < 0) return;
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    (void)hipEventRecord(g_trace[idx].b, st);
+    idx = -1;
+}
+
+DropParams make_drop(float p, uint64_t seed, uint32_t site, uint32_t layer) {
+    DropParams d{};
+    d.seed = seed;
+    d.site = site;
+    d.layer = layer;
+    d.enabled = p > 0.f;
+    double thr = floor((1.0 - (double)p) * 4294967296.0);
+    d.thr = (uint64_t)thr;
+    d.scale = (float)(1.0 / (1.0 - (double)p));
+    if (!d.enabled) { d.thr = 1ull << 32; d.scale = 1.f; }
+    return d;
+}
+
+}  // namespace dm
+
+using namespace dm;
+
+namespace {
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_ptr(const void* p, const char* name) {
+    if (!p) return set_error(DM_ERR_ARG, "%s is NULL", name);
+    if (!aligned16(p)) return set_error(DM_ERR_ARG, "%s is not 16-byte aligned", name);
+    return DM_OK;
+}
+
+int check_dtype(int32_t dt) {
+    if (dt != DM_F32 && dt != DM_F16 && dt != DM_BF16)
+        return set_error(DM_ERR_UNSUPPORTED, "unsupported dtype %d", dt);
+    return DM_OK;
+}
+
+int check_drop(const dm_dropout* d) {
+    if (d && !(d->p >= 0.f && d->p < 1.f)) return set_error(DM_ERR_ARG, "dropout p=%g outside [0,1)", d->p);
+    return DM_OK;
+}
+
+int check_rows(int64_t rows, int32_t cols, int32_t max_cols) {
+    if (rows < 0 || cols <= 0) return set_error(DM_ERR_ARG, "bad shape rows=%lld cols=%d", (long long)rows, cols);
+    if (cols % 8) return set_error(DM_ERR_UNSUPPORTED, "row length %d is not a multiple of 8", cols);
+    if (max_cols && cols > max_cols) return set_error(DM_ERR_UNSUPPORTED, "row length %d above %d", cols, max_cols);
+    if (rows > (int64_t)INT32_MAX * 8) return set_error(DM_ERR_UNSUPPORTED, "too many rows");
+    return DM_OK;
+}
+
+#define DM_TRY(x)                      \
+    do {                               \
+        int _rc = (x);                 \
+        if (_rc != DM_OK) return _rc;  \
+    } while (0)
+
+hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+const char* dm_last_error(void) { return g_err; }
+
+int dm_trace_enable(int32_t on) {
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    if (on) {
+        g_trace.clear();
+        g_events_used = 0;
+    }
+    g_trace_on.store(on != 0);
+    return DM_OK;
+}
+
+int32_t dm_trace_count(void) {
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    return (int32_t)g_trace.size();
+}
+
+int dm_trace_get(int32_t i, const char** label, float* ms) {
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    if (i < 0 || i >= (int32_t)g_trace.size()) return set_error(DM_ERR_ARG, "trace index %d out of range", i);
+    hipError_t e = hipEventSynchronize(g_trace[i].b);
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, g_trace[i].a, g_trace[i].b);
+    if (e != hipSuccess) return set_error(DM_ERR_DEVICE, "trace event: %s", hipGetErrorString(e));
+    if (label) *label = g_trace[i].label;
+    if (ms) *ms = t;
+    return DM_OK;
+}
+
+size_t colsum_ws_bytes(int64_t rows, int32_t cols) {
+    if (rows <= 0 || cols <= 0) return 0;
+    return (size_t)3 * colsum_blocks(rows) * (size_t)cols * sizeof(float);
+}
+
+int bdrln_fwd(int32_t dtype, int64_t rows, int32_t cols, const void* x, const void* bias, const void* resid,
+              const void* gamma, const void* beta, float eps, const dm_dropout* drop, void* y, void* xhat,
+              float* rstd, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, cols, 4096));
+    DM_TRY(check_drop(drop));
+    if (!(eps > 0.f)) return set_error(DM_ERR_ARG, "eps must be > 0");
+    if (rows == 0) return DM_OK;
+    DM_TRY(check_ptr(x, "x")); DM_TRY(check_ptr(bias, "bias")); DM_TRY(check_ptr(resid, "resid"));
+    DM_TRY(check_ptr(gamma, "gamma")); DM_TRY(check_ptr(beta, "beta")); DM_TRY(check_ptr(y, "y"));
+    if (xhat) DM_TRY(check_ptr(xhat, "xhat"));
+    run_bdrln_fwd(dtype, rows, cols, x, bias, resid, gamma, beta, eps, make_drop(drop), y, xhat, rstd, S(stream));
+    return check_launch("bdrln_fwd");
+}
+
+int softmax_dropout_fwd(int32_t dtype, int32_t B, int32_t H, int32_t J, int32_t K, float scale, const void* beta,
+                        const dm_dropout* drop, void* prob, void* alpha, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    if (B < 0 || H < 0 || J < 0) return set_error(DM_ERR_ARG, "negative size");
+    DM_TRY(check_rows((int64_t)B * H * J, K, 4096));
+    DM_TRY(check_drop(drop));
+    if ((int64_t)B * H * J == 0) return DM_OK;
+    DM_TRY(check_ptr(beta, "beta")); DM_TRY(check_ptr(prob, "prob")); DM_TRY(check_ptr(alpha, "alpha"));
+    run_softmax_fwd(dtype, B, H, J, K, scale, beta, make_drop(drop), prob, alpha, S(stream));
+    return check_launch("softmax_dropout_fwd");
+}
+
+int bias_act_fwd(int32_t dtype, int64_t rows, int32_t cols, const void* x, const void* bias, int32_t act,
+                 const dm_dropout* drop, void* y, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, cols, 0));
+    DM_TRY(check_drop(drop));
+    if (act != DM_GELU && act != DM_RELU) return set_error(DM_ERR_UNSUPPORTED, "unknown activation %d", act);
+    if (rows == 0) return DM_OK;
+    DM_TRY(check_ptr(x, "x")); DM_TRY(check_ptr(bias, "bias")); DM_TRY(check_ptr(y, "y"));
+    run_bias_act_fwd(dtype, rows, cols, x, bias, act, make_drop(drop), y, S(stream));
+    return check_launch("bias_act_fwd");
+}
+
+int attn_input_bias(int32_t dtype, int64_t rows, int32_t H, int32_t P, const void* x, const void* bq,
+                    const void* bk, const void* bv, void* y, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    if (H <= 0 || P <= 0 || P % 8) return set_error(DM_ERR_UNSUPPORTED, "P must be a positive multiple of 8");
+    DM_TRY(check_rows(rows, 3 * H * P, 0));
+    if (rows == 0) return DM_OK;
+    DM_TRY(check_ptr(x, "x")); DM_TRY(check_ptr(y, "y"));
+    if (!bq || !bk || !bv) return set_error(DM_ERR_ARG, "bias pointer is NULL");
+    run_attn_input_bias(dtype, rows, H, P, x, bq, bk, bv, y, S(stream));
+    return check_launch("attn_input_bias");
+}
+
+int ln_param_bwd(int32_t dtype, int64_t rows, int32_t cols, const void* dy, const void* xhat, float* dgamma,
+                 float* dbeta, void* ws, size_t ws_bytes, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, cols, 2048));
+    if (rows == 0) return set_error(DM_ERR_ARG, "rows must be > 0");
+    DM_TRY(check_ptr(dy, "dy")); DM_TRY(check_ptr(xhat, "xhat"));
+    DM_TRY(check_ptr(dgamma, "dgamma")); DM_TRY(check_ptr(dbeta, "dbeta")); DM_TRY(check_ptr(ws, "ws"));
+    if (ws_bytes < colsum_ws_bytes(rows, cols)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
+    LnBwdArgs a{};
+    a.dtype = dtype; a.rows = rows; a.cols = cols; a.dya = dy; a.xhat = xhat;
+    a.dp = make_drop(0.f, 0, 0, 0); a.part = (float*)ws;
+    run_ln_bwd(a, S(stream));
+    const int nb = colsum_blocks(rows);
+    run_colsum_finish(rows, cols, (float*)ws, dgamma, S(stream));
+    run_colsum_finish(rows, cols, (float*)ws + (size_t)nb * cols, dbeta, S(stream));
+    return check_launch("ln_param_bwd");
+}
+
+int ln_dropout_bwd(int32_t dtype, int64_t rows, int32_t cols, const void* dy, const void* xhat, const void* gamma,
+                   const float* rstd, const dm_dropout* drop, void* ds, void* dsub, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, cols, 4096));
+    DM_TRY(check_drop(drop));
+    if (rows == 0) return DM_OK;
+    DM_TRY(check_ptr(dy, "dy")); DM_TRY(check_ptr(xhat, "xhat")); DM_TRY(check_ptr(gamma, "gamma"));
+    DM_TRY(check_ptr(rstd, "rstd")); DM_TRY(check_ptr(dsub, "dsub"));
+    if (ds) DM_TRY(check_ptr(ds, "ds"));
+    LnBwdArgs a{};
+    a.dtype = dtype; a.rows = rows; a.cols = cols; a.dya = dy; a.xhat = xhat; a.gamma = gamma; a.rstd = rstd;
+    a.dp = make_drop(drop); a.ds = ds; a.dsub = dsub;
+    run_ln_bwd(a, S(stream));
+    return check_launch("ln_dropout_bwd");
+}
+
+int residual_ln_param_bwd(int32_t dtype, int64_t rows, int32_t cols, const void* da, const void* db,
+                          const void* xhat, void* dsum, float* dgamma, float* dbeta, void* ws, size_t ws_bytes,
+                          void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, cols, 2048));
+    if (rows == 0) return set_error(DM_ERR_ARG, "rows must be > 0");
+    DM_TRY(check_ptr(da, "da")); DM_TRY(check_ptr(db, "db")); DM_TRY(check_ptr(xhat, "xhat"));
+    DM_TRY(check_ptr(dsum, "dsum")); DM_TRY(check_ptr(dgamma, "dgamma")); DM_TRY(check_ptr(dbeta, "dbeta"));
+    DM_TRY(check_ptr(ws, "ws"));
+    if (ws_bytes < colsum_ws_bytes(rows, cols)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
+    LnBwdArgs a{};
+    a.dtype = dtype; a.rows = rows; a.cols = cols; a.dya = da; a.dyb = db; a.xhat = xhat;
+    a.dp = make_drop(0.f, 0, 0, 0); a.dysum = dsum; a.part = (float*)ws;
+    run_ln_bwd(a, S(stream));
+    const int nb = colsum_blocks(rows);
+    run_colsum_finish(rows, cols, (float*)ws, dgamma, S(stream));
+    run_colsum_finish(rows, cols, (float*)ws + (size_t)nb * cols, dbeta, S(stream));
+    return check_launch("residual_ln_param_bwd");
+}
+
+int act_bias_bwd(int32_t dtype, int64_t rows, int32_t F, int32_t I, const void* da, const void* h, const void* b1,
+                 int32_t act, const dm_dropout* drop, const void* dout, void* dh, float* db1, float* db2, void* ws,
+                 size_t ws_bytes, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, F, 16384));
+    DM_TRY(check_rows(rows, I, 16384));
+    DM_TRY(check_drop(drop));
+    if (act != DM_GELU && act != DM_RELU) return set_error(DM_ERR_UNSUPPORTED, "unknown activation %d", act);
+    if (rows == 0) return set_error(DM_ERR_ARG, "rows must be > 0");
+    DM_TRY(check_ptr(da, "da")); DM_TRY(check_ptr(h, "h")); DM_TRY(check_ptr(b1, "b1"));
+    DM_TRY(check_ptr(dout, "dout")); DM_TRY(check_ptr(dh, "dh")); DM_TRY(check_ptr(db1, "db1"));
+    DM_TRY(check_ptr(db2, "db2")); DM_TRY(check_ptr(ws, "ws"));
+    const int mx = F > I ? F : I;
+    if (ws_bytes < colsum_ws_bytes(rows, mx)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
+    float* part = (float*)ws;
+    run_act_bwd(dtype, rows, F, da, h, b1, act, make_drop(drop), dh, part, S(stream));
+    run_colsum_finish(rows, F, part, db1, S(stream));
+    run_colsum_partial(dtype, rows, I, dout, part, S(stream));
+    run_colsum_finish(rows, I, part, db2, S(stream));
+    return check_launch("act_bias_bwd");
+}
+
+int softmax_dropout_bwd(int32_t dtype, int32_t B, int32_t H, int32_t J, int32_t K, float scale,
+                        const void* dalpha, const void* prob, const dm_dropout* drop, void* dbeta, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    if (B < 0 || H < 0 || J < 0) return set_error(DM_ERR_ARG, "negative size");
+    DM_TRY(check_rows((int64_t)B * H * J, K, 4096));
+    DM_TRY(check_drop(drop));
+    if ((int64_t)B * H * J == 0) return DM_OK;
+    DM_TRY(check_ptr(dalpha, "dalpha")); DM_TRY(check_ptr(prob, "prob")); DM_TRY(check_ptr(dbeta, "dbeta"));
+    run_softmax_bwd(dtype, B, H, J, K, scale, dalpha, prob, make_drop(drop), dbeta, S(stream));
+    return check_launch("softmax_dropout_bwd");
+}
+
+int bias_grad(int32_t dtype, int64_t rows, int32_t cols, const void* x, float* db, void* ws, size_t ws_bytes,
+              void* stream) {
+    DM_TRY(check_dtype(dtype));
+    DM_TRY(check_rows(rows, cols, 16384));
+    if (rows == 0) return set_error(DM_ERR_ARG, "rows must be > 0");
+    DM_TRY(check_ptr(x, "x")); DM_TRY(check_ptr(db, "db")); DM_TRY(check_ptr(ws, "ws"));
+    if (ws_bytes < colsum_ws_bytes(rows, cols)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
+    run_colsum_partial(dtype, rows, cols, x, (float*)ws, S(stream));
+    run_colsum_finish(rows, cols, (float*)ws, db, S(stream));
+    return check_launch("bias_grad");
+}
+
+int attn_input_bias_grad(int32_t dtype, int64_t rows, int32_t H, int32_t P, const void* x, float* dbq, float* dbk,
+                         float* dbv, void* ws, size_t ws_bytes, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    if (H <= 0 || P <= 0 || P % 8) return set_error(DM_ERR_UNSUPPORTED, "P must be a positive multiple of 8");
+    DM_TRY(check_rows(rows, 3 * H * P, 16384));
+    if (rows == 0) return set_error(DM_ERR_ARG, "rows must be > 0");
+    DM_TRY(check_ptr(x, "x")); DM_TRY(check_ptr(ws, "ws"));
+    if (!dbq || !dbk || !dbv) return set_error(DM_ERR_ARG, "bias gradient pointer is NULL");
+    if (ws_bytes < colsum_ws_bytes(rows, 3 * H * P)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
+    run_colsum_partial(dtype, rows, 3 * H * P, x, (float*)ws, S(stream));
+    run_colsum_finish_qkv(rows, H, P, 3, (float*)ws, dbq, dbk, dbv, S(stream));
+    return check_launch("attn_input_bias_grad");
+}
+
+int residual_add(int32_t dtype, int64_t n, const void* a, const void* b, void* out, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    if (n < 0 || n % 8) return set_error(DM_ERR_UNSUPPORTED, "n must be a non-negative multiple of 8");
+    if (n == 0) return DM_OK;
+    DM_TRY(check_ptr(a, "a")); DM_TRY(check_ptr(b, "b")); DM_TRY(check_ptr(out, "out"));
+    run_add(dtype, n, a, b, out, S(stream));
+    return check_launch("residual_add");
+}
+
+int dropout_mask(uint64_t seed, uint32_t site, uint32_t layer, float p, uint64_t offset, uint64_t n, uint8_t* out,
+                 void* stream) {
+    if (!(p >= 0.f && p < 1.f)) return set_error(DM_ERR_ARG, "dropout p=%g outside [0,1)", p);
+    if (offset % 8 || n % 8) return set_error(DM_ERR_ARG, "offset and n must be multiples of 8");
+    if (n == 0) return DM_OK;
+    if (!out) return set_error(DM_ERR_ARG, "out is NULL");
+    if (((uintptr_t)out & 7u) != 0) return set_error(DM_ERR_ARG, "out is not 8-byte aligned");
+    run_dropout_mask(make_drop(p, seed, site, layer), offset, n, out, S(stream));
+    return check_launch("dropout_mask");
+}
+
+int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, float alpha, const void* A,
+             int32_t a_trans, int64_t sa, const void* B, int32_t b_trans, int64_t sb, const void* bias, void* C,
+             int32_t out_f32, int64_t sc, void* stream) {
+    DM_TRY(check_dtype(dtype));
+    if (batch < 0 || M < 0 || N < 0 || K <= 0) return set_error(DM_ERR_ARG, "bad contraction shape");
+    if ((int64_t)batch * M * N == 0) return DM_OK;
+    if (dtype != DM_F32 && (M % 8 || N % 8 || K % 8))
+        return set_error(DM_ERR_UNSUPPORTED, "M, N, K must be multiples of 8");
+    DM_TRY(check_ptr(A, "A")); DM_TRY(check_ptr(B, "B")); DM_TRY(check_ptr(C, "C"));
+    if (bias) DM_TRY(check_ptr(bias, "bias"));
+    if (dtype == DM_F32 && !out_f32) out_f32 = 1;
+    GemmArgs g{};
+    g.M = M; g.N = N; g.K = K; g.batch = batch;
+    g.a.ptr[0] = A; g.a.nseg = 1;
+    g.a.kcontig = a_trans ? 0 : 1;
+    g.a.row = linear_map(a_trans ? M : K);
+    g.a.batch = linear_map(sa);
+    g.b.ptr[0] = B; g.b.nseg = 1;
+    g.b.kcontig = b_trans ? 1 : 0;
+    g.b.row = linear_map(b_trans ? K : N);
+    g.b.batch = linear_map(sb);
+    g.c.ptr[0] = C; g.c.nseg = 1;
+    g.c.mmap = linear_map(N); g.c.nmap = linear_map(1); g.c.batch = linear_map(sc);
+    g.c.contig_n = 1; g.c.alpha = alpha;
+    g.c.bias[0] = bias; g.c.bias_nseg = 1; g.c.bias_map = linear_map(1);
+    g.c.out_f32 = out_f32;
+    return launch_gemm(dtype, g, S(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,182 @@
+// Shared device helpers for the gfx950 kernels: storage types, 16-byte
+// vector I/O, wave64 reductions and the counter-based dropout generator.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dm {
+
+typedef _Float16 half_t;
+typedef __bf16 bf16_t;
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ------------------------------------------------------------ conversions
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(half_t x) { return (float)x; }
+__device__ __forceinline__ float to_f(bf16_t x) { return (float)x; }
+
+template <typename T> __device__ __forceinline__ T from_f(float x);
+template <> __device__ __forceinline__ float from_f<float>(float x) { return x; }
+template <> __device__ __forceinline__ half_t from_f<half_t>(float x) { return (half_t)x; }
+template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float x) { return (bf16_t)x; }
+
+// --------------------------------------------- 8-element vector load/store
+// Every activation row has a multiple of 8 elements and 16-byte aligned
+// bases, so 8 consecutive elements are one (half/bf16) or two (float)
+// 16-byte transactions.
+template <typename T> struct V8;
+
+template <> struct V8<half_t> {
+    __device__ __forceinline__ static void load(const half_t* p, float v[8]) {
+        u32x4 r = *reinterpret_cast<const u32x4*>(p);
+        half8 h = __builtin_bit_cast(half8, r);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = (float)h[i];
+    }
+    __device__ __forceinline__ static void store(half_t* p, const float v[8]) {
+        half8 h;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) h[i] = (half_t)v[i];
+        *reinterpret_cast<u32x4*>(p) = __builtin_bit_cast(u32x4, h);
+    }
+};
+
+template <> struct V8<bf16_t> {
+    __device__ __forceinline__ static void load(const bf16_t* p, float v[8]) {
+        u32x4 r = *reinterpret_cast<const u32x4*>(p);
+        // bf16 -> fp32 is a 16-bit shift of the bit pattern
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = __builtin_bit_cast(float, r[i] << 16);
+            v[2 * i + 1] = __builtin_bit_cast(float, r[i] & 0xFFFF0000u);
+        }
+    }
+    __device__ __forceinline__ static void store(bf16_t* p, const float v[8]) {
+        bf16x8 h;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) h[i] = (bf16_t)v[i];
+        *reinterpret_cast<u32x4*>(p) = __builtin_bit_cast(u32x4, h);
+    }
+};
+
+template <> struct V8<float> {
+    __device__ __forceinline__ static void load(const float* p, float v[8]) {
+        floatx4 a = *reinterpret_cast<const floatx4*>(p);
+        floatx4 b = *reinterpret_cast<const floatx4*>(p + 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { v[i] = a[i]; v[4 + i] = b[i]; }
+    }
+    __device__ __forceinline__ static void store(float* p, const float v[8]) {
+        floatx4 a, b;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { a[i] = v[i]; b[i] = v[4 + i]; }
+        *reinterpret_cast<floatx4*>(p) = a;
+        *reinterpret_cast<floatx4*>(p + 4) = b;
+    }
+};
+
+// ------------------------------------------------------ wave64 reductions
+// Butterfly over `width` consecutive lanes (a power of two <= 64).
+template <int WIDTH>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+    for (int o = WIDTH / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+template <int WIDTH>
+__device__ __forceinline__ float group_max(float v) {
+#pragma unroll
+    for (int o = WIDTH / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// ------------------------------------------------- counter-based dropout
+// Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11): the round
+// multiplies counter words 0 and 2 by two constants and mixes the high
+// product halves with words 1 and 3 and the round key; the key is bumped by
+// two Weyl constants between rounds.
+struct Philox {
+    static constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    static constexpr uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    __device__ __forceinline__ static u32x4 gen(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                                uint32_t k0, uint32_t k1) {
+#pragma unroll
+        for (int r = 0; r < 10; ++r) {
+            uint32_t lo0 = c0 * M0, hi0 = __umulhi(c0, M0);
+            uint32_t lo1 = c2 * M1, hi1 = __umulhi(c2, M1);
+            uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+            c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+            k0 += W0; k1 += W1;
+        }
+        u32x4 o; o[0] = c0; o[1] = c1; o[2] = c2; o[3] = c3;
+        return o;
+    }
+};
+
+// Dropout parameters as the kernels see them.  The mask of logical element
+// e is word (e & 3) of Philox(counter = (lo(e>>2), hi(e>>2), site, layer),
+// key = (lo(seed), hi(seed))); keep iff word < thr.  thr == 2^32 keeps all.
+struct DropParams {
+    uint64_t seed;
+    uint64_t thr;      // floor((1-p) * 2^32), in [0, 2^32]
+    uint32_t site, layer;
+    float scale;       // 1/(1-p)
+    int enabled;       // p > 0
+};
+
+// Multiplies 8 values of logical elements e0..e0+7 (e0 % 8 == 0) by the
+// dropout factor.
+__device__ __forceinline__ void dropout8(const DropParams& d, uint64_t e0, float v[8]) {
+    if (!d.enabled) return;
+    uint64_t blk = e0 >> 2;
+    uint32_t k0 = (uint32_t)d.seed, k1 = (uint32_t)(d.seed >> 32);
+    u32x4 a = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
+    blk += 1;
+    u32x4 b = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[i] = ((uint64_t)a[i] < d.thr) ? v[i] * d.scale : 0.0f;
+        v[4 + i] = ((uint64_t)b[i] < d.thr) ? v[4 + i] * d.scale : 0.0f;
+    }
+}
+
+// Keep bits of logical elements e0..e0+7 as 0/1 bytes.
+__device__ __forceinline__ void keep8(const DropParams& d, uint64_t e0, uint8_t out[8]) {
+    if (!d.enabled) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) out[i] = 1;
+        return;
+    }
+    uint64_t blk = e0 >> 2;
+    uint32_t k0 = (uint32_t)d.seed, k1 = (uint32_t)(d.seed >> 32);
+    u32x4 a = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
+    blk += 1;
+    u32x4 b = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        out[i] = (uint64_t)a[i] < d.thr;
+        out[4 + i] = (uint64_t)b[i] < d.thr;
+    }
+}
+
+// ----------------------------------------------------------- activations
+enum Act { ACT_GELU = 0, ACT_RELU = 1 };
+
+__device__ __forceinline__ float act_fwd(float u, int act) {
+    if (act == ACT_RELU) return fmaxf(u, 0.0f);
+    return 0.5f * u * (1.0f + erff(u * 0.70710678118654752f));
+}
+// d/du of the activation: GELU' = Phi(u) + u * phi(u)
+__device__ __forceinline__ float act_grad(float u, int act) {
+    if (act == ACT_RELU) return u > 0.0f ? 1.0f : 0.0f;
+    float cdf = 0.5f * (1.0f + erff(u * 0.70710678118654752f));
+    float pdf = 0.39894228040143268f * __expf(-0.5f * u * u);
+    return cdf + u * pdf;
+}
+
+}  // namespace dm

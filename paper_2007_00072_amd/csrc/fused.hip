@@ -1,0 +1,667 @@
+// Memory-bound fused operators of the encoder layer (the paper's kernel
+// list in Sec. "Fusion Implementation", Table 3 brackets), for gfx950.
+//
+// Row operators (LayerNorm and softmax, forward and backward) give each row
+// to a group of LPR lanes of one wave64 (LPR = 64 for rows of 512..2048
+// elements, fewer lanes for short rows so a wave holds several rows); each
+// lane keeps NV 8-element vectors of its row in registers, so the
+// reduce-then-apply structure of a statistical normalisation reads every
+// input exactly once from HBM.  Reductions are xor-butterflies inside the
+// lane group.  Dropout masks are regenerated with Philox from the logical
+// element index, never loaded.  Column reductions (bias, LayerNorm scale
+// and shift gradients) write per-block partial sums that a second small
+// kernel adds in a fixed order, so results are deterministic.
+#include <math.h>
+
+#include "internal.hpp"
+
+namespace dm {
+namespace {
+
+constexpr int NT = 256;  // threads per block: 4 wave64s
+
+// ------------------------------------------------------ bias+dropout+residual+LayerNorm
+template <typename T, int LPR, int NV>
+__global__ __launch_bounds__(NT) void bdrln_fwd_k(int64_t rows, int cols, const T* __restrict__ x,
+                                                  const T* __restrict__ bias, const T* __restrict__ resid,
+                                                  const T* __restrict__ gamma, const T* __restrict__ beta,
+                                                  float eps, DropParams dp, T* __restrict__ y,
+                                                  T* __restrict__ xhat, float* __restrict__ rstd) {
+    constexpr int RPW = 64 / LPR;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / LPR, gl = lane % LPR;
+    const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * RPW + gi;
+    const bool active = row < rows;
+    const int64_t base = row * cols;
+    float v[NV][8];
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (active && c < cols) {
+            float a[8], b[8], r[8];
+            V8<T>::load(x + base + c, a);
+            V8<T>::load(bias + c, b);
+            V8<T>::load(resid + base + c, r);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) a[q] += b[q];
+            dropout8(dp, (uint64_t)(base + c), a);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) { v[i][q] = a[q] + r[q]; sum += v[i][q]; }
+        } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[i][q] = 0.f;
+        }
+    }
+    const float inv = 1.0f / (float)cols;
+    const float mean = group_sum<LPR>(sum) * inv;
+    float sq = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (active && c < cols) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) { float d = v[i][q] - mean; sq += d * d; }
+        }
+    }
+    const float var = group_sum<LPR>(sq) * inv;
+    const float rs = 1.0f / sqrtf(var + eps);
+    if (!active) return;
+    if (rstd && gl == 0) rstd[row] = rs;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (c < cols) {
+            float g[8], b[8], xh[8], o[8];
+            V8<T>::load(gamma + c, g);
+            V8<T>::load(beta + c, b);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) { xh[q] = (v[i][q] - mean) * rs; o[q] = g[q] * xh[q] + b[q]; }
+            V8<T>::store(y + base + c, o);
+            if (xhat) V8<T>::store(xhat + base + c, xh);
+        }
+    }
+}
+
+// ------------------------------------------------------ scaled softmax + dropout
+// Physical rows are [B][H][J]; the dropout logical index is (h, b, j, k).
+template <typename T, int LPR, int NV>
+__global__ __launch_bounds__(NT) void softmax_fwd_k(int64_t rows, int B, int H, int J, int K, float scale,
+                                                    const T* __restrict__ beta, DropParams dp,
+                                                    T* __restrict__ prob, T* __restrict__ alpha) {
+    constexpr int RPW = 64 / LPR;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / LPR, gl = lane % LPR;
+    const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * RPW + gi;
+    const bool active = row < rows;
+    const int64_t base = row * K;
+    float v[NV][8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (active && c < K) {
+            V8<T>::load(beta + base + c, v[i]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) { v[i][q] *= scale; mx = fmaxf(mx, v[i][q]); }
+        } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[i][q] = -INFINITY;
+        }
+    }
+    mx = group_max<LPR>(mx);
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { v[i][q] = __expf(v[i][q] - mx); sum += v[i][q]; }
+    sum = group_sum<LPR>(sum);
+    if (!active) return;
+    const float rinv = 1.0f / sum;
+    const int j = (int)(row % J);
+    const int64_t bh = row / J;
+    const int h = (int)(bh % H), b = (int)(bh / H);
+    const int64_t ebase = (((int64_t)h * B + b) * J + j) * (int64_t)K;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (c < K) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[i][q] *= rinv;
+            V8<T>::store(prob + base + c, v[i]);
+            dropout8(dp, (uint64_t)(ebase + c), v[i]);
+            V8<T>::store(alpha + base + c, v[i]);
+        }
+    }
+}
+
+// ------------------------------------------------------ softmax + dropout backward
+template <typename T, int LPR, int NV>
+__global__ __launch_bounds__(NT) void softmax_bwd_k(int64_t rows, int B, int H, int J, int K, float scale,
+                                                    const T* __restrict__ dalpha, const T* __restrict__ prob,
+                                                    DropParams dp, T* __restrict__ dbeta) {
+    constexpr int RPW = 64 / LPR;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / LPR, gl = lane % LPR;
+    const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * RPW + gi;
+    const bool active = row < rows;
+    const int64_t base = row * K;
+    int64_t ebase = 0;
+    if (active) {
+        const int j = (int)(row % J);
+        const int64_t bh = row / J;
+        const int h = (int)(bh % H), b = (int)(bh / H);
+        ebase = (((int64_t)h * B + b) * J + j) * (int64_t)K;
+    }
+    float dp_[NV][8], p[NV][8];
+    float dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (active && c < K) {
+            V8<T>::load(dalpha + base + c, dp_[i]);
+            V8<T>::load(prob + base + c, p[i]);
+            dropout8(dp, (uint64_t)(ebase + c), dp_[i]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) dot += dp_[i][q] * p[i][q];
+        } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) { dp_[i][q] = 0.f; p[i][q] = 0.f; }
+        }
+    }
+    dot = group_sum<LPR>(dot);
+    if (!active) return;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (c < K) {
+            float o[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) o[q] = scale * p[i][q] * (dp_[i][q] - dot);
+            V8<T>::store(dbeta + base + c, o);
+        }
+    }
+}
+
+// ------------------------------------------------------ LayerNorm backward family
+// Each block takes a contiguous range of rows; one lane group per row.
+// Column partial sums are kept per lane (a lane always owns the same
+// columns), reduced over the wave's lane groups with shuffles and over the
+// block's 4 waves through LDS, and written as part[q][blockIdx.x][cols].
+template <typename T, int LPR, int NV>
+__global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, int nblk) {
+    constexpr int RPW = 64 / LPR;
+    constexpr int GROUPS = 4 * RPW;  // row slots per block iteration
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int gi = lane / LPR, gl = lane % LPR;
+    const int cols = a.cols;
+    const T* dya = reinterpret_cast<const T*>(a.dya);
+    const T* dyb = reinterpret_cast<const T*>(a.dyb);
+    const T* xhat = reinterpret_cast<const T*>(a.xhat);
+    const T* gamma = reinterpret_cast<const T*>(a.gamma);
+    const bool do_ds = a.ds || a.dsub;
+    const bool do_part = a.part != nullptr;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min<int64_t>(a.rows, r0 + rows_per_block);
+
+    float g[NV][8];
+    float p_dyx[NV][8], p_dy[NV][8], p_dsub[NV][8];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (do_ds && c < cols) V8<T>::load(gamma + c, g[i]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { p_dyx[i][q] = 0.f; p_dy[i][q] = 0.f; p_dsub[i][q] = 0.f; }
+    }
+
+    for (int64_t rb = r0; rb < r1; rb += GROUPS) {
+        const int64_t row = rb + wave * RPW + gi;
+        const bool active = row < r1;
+        const int64_t base = row * cols;
+        float dy[NV][8], xh[NV][8];
+        float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int c = (gl + i * LPR) * 8;
+            if (active && c < cols) {
+                V8<T>::load(dya + base + c, dy[i]);
+                if (dyb) {
+                    float t[8];
+                    V8<T>::load(dyb + base + c, t);
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) dy[i][q] += t[q];
+                }
+                if (a.dysum) V8<T>::store(reinterpret_cast<T*>(a.dysum) + base + c, dy[i]);
+                V8<T>::load(xhat + base + c, xh[i]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    if (do_part) { p_dyx[i][q] += dy[i][q] * xh[i][q]; p_dy[i][q] += dy[i][q]; }
+                    if (do_ds) { float gy = dy[i][q] * g[i][q]; s1 += gy; s2 += gy * xh[i][q]; }
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) { dy[i][q] = 0.f; xh[i][q] = 0.f; }
+            }
+        }
+        if (do_ds) {
+            const float inv = 1.0f / (float)cols;
+            const float m1 = group_sum<LPR>(s1) * inv;
+            const float m2 = group_sum<LPR>(s2) * inv;
+            if (active) {
+                const float rs = a.rstd[row];
+#pragma unroll
+                for (int i = 0; i < NV; ++i) {
+                    const int c = (gl + i * LPR) * 8;
+                    if (c < cols) {
+                        float o[8];
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) o[q] = rs * (dy[i][q] * g[i][q] - m1 - xh[i][q] * m2);
+                        if (a.ds) V8<T>::store(reinterpret_cast<T*>(a.ds) + base + c, o);
+                        if (a.dsub) {
+                            dropout8(a.dp, (uint64_t)(base + c), o);
+                            V8<T>::store(reinterpret_cast<T*>(a.dsub) + base + c, o);
+                            if (do_part && a.want_dsub_sum) {
+                                // sum the stored (rounded) values that later consumers see
+#pragma unroll
+                                for (int q = 0; q < 8; ++q) p_dsub[i][q] += to_f(from_f<T>(o[q]));
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+    if (!do_part) return;
+
+    // reduce partials over the RPW lane groups of the wave
+    __shared__ float red[4][2048];
+    const int nq = a.want_dsub_sum ? 3 : 2;
+    for (int qn = 0; qn < nq; ++qn) {
+        float(*pp)[8] = qn == 0 ? p_dyx : (qn == 1 ? p_dy : p_dsub);
+#pragma unroll
+        for (int i = 0; i < NV; ++i)
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                float t = pp[i][q];
+#pragma unroll
+                for (int o = LPR; o < 64; o <<= 1) t += __shfl_xor(t, o, 64);
+                pp[i][q] = t;
+            }
+        __syncthreads();
+        if (gi == 0) {
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                const int c = (gl + i * LPR) * 8;
+                if (c < cols) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) red[wave][c + q] = pp[i][q];
+                }
+            }
+        }
+        __syncthreads();
+        float* out = a.part + ((int64_t)qn * nblk + blockIdx.x) * cols;
+        for (int c = threadIdx.x; c < cols; c += NT)
+            out[c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+    }
+}
+
+// ------------------------------------------------------ activation backward + bias grad
+// Each thread owns up to CV column vectors for all rows of its block.
+template <typename T, int CV>
+__global__ __launch_bounds__(NT) void act_bwd_k(int64_t rows, int F, const T* __restrict__ da,
+                                                const T* __restrict__ h, const T* __restrict__ b1, int act,
+                                                DropParams dp, T* __restrict__ dh, float* __restrict__ part,
+                                                int rows_per_block) {
+    const int nvec = F / 8;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min<int64_t>(rows, r0 + rows_per_block);
+    float bb[CV][8], acc[CV][8];
+#pragma unroll
+    for (int i = 0; i < CV; ++i) {
+        const int v = threadIdx.x + i * NT;
+        if (v < nvec) V8<T>::load(b1 + v * 8, bb[i]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[i][q] = 0.f;
+    }
+    for (int64_t r = r0; r < r1; ++r) {
+#pragma unroll
+        for (int i = 0; i < CV; ++i) {
+            const int v = threadIdx.x + i * NT;
+            if (v < nvec) {
+                const int64_t off = r * F + v * 8;
+                float g[8], u[8];
+                V8<T>::load(da + off, g);
+                V8<T>::load(h + off, u);
+                dropout8(dp, (uint64_t)off, g);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) g[q] *= act_grad(u[q] + bb[i][q], act);
+                V8<T>::store(dh + off, g);
+                // sum the stored (rounded) values that consumers of dh read
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[i][q] += to_f(from_f<T>(g[q]));
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < CV; ++i) {
+        const int v = threadIdx.x + i * NT;
+        if (v < nvec) V8<float>::store(part + (int64_t)blockIdx.x * F + v * 8, acc[i]);
+    }
+}
+
+template <typename T, int CV>
+__global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, const T* __restrict__ x,
+                                                       float* __restrict__ part, int rows_per_block) {
+    const int nvec = cols / 8;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min<int64_t>(rows, r0 + rows_per_block);
+    float acc[CV][8];
+#pragma unroll
+    for (int i = 0; i < CV; ++i)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[i][q] = 0.f;
+    for (int64_t r = r0; r < r1; ++r) {
+#pragma unroll
+        for (int i = 0; i < CV; ++i) {
+            const int v = threadIdx.x + i * NT;
+            if (v < nvec) {
+                float t[8];
+                V8<T>::load(x + r * cols + v * 8, t);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[i][q] += t[q];
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < CV; ++i) {
+        const int v = threadIdx.x + i * NT;
+        if (v < nvec) V8<float>::store(part + (int64_t)blockIdx.x * cols + v * 8, acc[i]);
+    }
+}
+
+// out[c] = sum over nblk partial rows, fixed order; 64 columns x 4 row phases per block.
+__global__ __launch_bounds__(NT) void colsum_finish_k(int nblk, int cols, const float* __restrict__ part,
+                                                      float* __restrict__ out, int qkv_H, int qkv_P,
+                                                      float* o1, float* o2) {
+    __shared__ float red[4][64];
+    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int ph = threadIdx.x >> 6;
+    float s = 0.f;
+    if (c < cols)
+        for (int b = ph; b < nblk; b += 4) s += part[(int64_t)b * cols + c];
+    red[ph][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (ph == 0 && c < cols) {
+        float t = (red[0][threadIdx.x] + red[1][threadIdx.x]) + (red[2][threadIdx.x] + red[3][threadIdx.x]);
+        if (qkv_H > 0) {
+            // column (s, h, p) of a fused projection -> bias gradient b_s[p][h]
+            const int I = qkv_H * qkv_P;
+            const int sg = c / I, hp = c - sg * I, hh = hp / qkv_P, pp = hp - hh * qkv_P;
+            float* dst = sg == 0 ? out : (sg == 1 ? o1 : o2);
+            dst[pp * qkv_H + hh] = t;
+        } else {
+            out[c] = t;
+        }
+    }
+}
+
+// ------------------------------------------------------ element-wise
+template <typename T>
+__global__ __launch_bounds__(NT) void bias_act_fwd_k(int64_t nvec, int cols, const T* __restrict__ x,
+                                                     const T* __restrict__ bias, int act, DropParams dp,
+                                                     T* __restrict__ y) {
+    const int cv = cols / 8;
+    for (int64_t v = (int64_t)blockIdx.x * NT + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * NT) {
+        const int64_t r = v / cv;
+        const int c = (int)(v - r * cv) * 8;
+        float a[8], b[8];
+        V8<T>::load(x + r * cols + c, a);
+        V8<T>::load(bias + c, b);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) a[q] = act_fwd(a[q] + b[q], act);
+        dropout8(dp, (uint64_t)(r * cols + c), a);
+        V8<T>::store(y + r * cols + c, a);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void attn_input_bias_k(int64_t nvec, int H, int P, const T* __restrict__ x,
+                                                        const T* __restrict__ bq, const T* __restrict__ bk,
+                                                        const T* __restrict__ bv, T* __restrict__ y) {
+    const int I = H * P, rowv = 3 * I / 8;
+    for (int64_t v = (int64_t)blockIdx.x * NT + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * NT) {
+        const int64_t r = v / rowv;
+        const int c = (int)(v - r * rowv) * 8;
+        const int s = c / I, hp = c - s * I, hh = hp / P, p0 = hp - hh * P;
+        const T* b = s == 0 ? bq : (s == 1 ? bk : bv);
+        float a[8];
+        V8<T>::load(x + r * 3 * I + c, a);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) a[q] += to_f(b[(p0 + q) * H + hh]);
+        V8<T>::store(y + r * 3 * I + c, a);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void add_k(int64_t nvec, const T* __restrict__ a, const T* __restrict__ b,
+                                            T* __restrict__ out) {
+    for (int64_t v = (int64_t)blockIdx.x * NT + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * NT) {
+        float x[8], y[8];
+        V8<T>::load(a + v * 8, x);
+        V8<T>::load(b + v * 8, y);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) x[q] += y[q];
+        V8<T>::store(out + v * 8, x);
+    }
+}
+
+// one wave per row: out[r] = sum over the row (fixed lane order, then butterfly)
+template <typename T>
+__global__ __launch_bounds__(NT) void rowsum_k(int64_t rows, int len, const T* __restrict__ x,
+                                               float* __restrict__ out) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= rows) return;
+    float s = 0.f;
+    for (int c = lane * 8; c < len; c += 512) {
+        float v[8];
+        V8<T>::load(x + r * len + c, v);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) s += v[q];
+    }
+    s = group_sum<64>(s);
+    if (lane == 0) out[r] = s;
+}
+
+__global__ __launch_bounds__(NT) void dropout_mask_k(DropParams dp, uint64_t offset, uint64_t nvec,
+                                                     uint8_t* __restrict__ out) {
+    for (uint64_t v = (uint64_t)blockIdx.x * NT + threadIdx.x; v < nvec; v += (uint64_t)gridDim.x * NT) {
+        uint8_t k[8];
+        keep8(dp, offset + v * 8, k);
+        u32x2 w;
+        w[0] = k[0] | (k[1] << 8) | (k[2] << 16) | ((uint32_t)k[3] << 24);
+        w[1] = k[4] | (k[5] << 8) | (k[6] << 16) | ((uint32_t)k[7] << 24);
+        *reinterpret_cast<u32x2*>(out + v * 8) = w;
+    }
+}
+
+int grid_for(int64_t nvec) {
+    int64_t g = (nvec + NT - 1) / NT;
+    return (int)(g < 8192 ? (g < 1 ? 1 : g) : 8192);
+}
+
+// Row-kernel dispatch on the row length: (lanes per row, vectors per lane).
+#define DM_ROW_CASES(LAUNCH)                                                   \
+    if (len <= 32) { LAUNCH(4, 1); }                                           \
+    else if (len <= 64) { LAUNCH(8, 1); }                                      \
+    else if (len <= 128) { LAUNCH(16, 1); }                                    \
+    else if (len <= 256) { LAUNCH(32, 1); }                                    \
+    else if (len <= 512) { LAUNCH(64, 1); }                                    \
+    else if (len <= 1024) { LAUNCH(64, 2); }                                   \
+    else if (len <= 2048) { LAUNCH(64, 4); }                                   \
+    else { LAUNCH(64, 8); }
+
+template <typename T>
+void bdrln_t(int64_t rows, int len, const void* x, const void* bias, const void* resid, const void* gamma,
+             const void* beta, float eps, const DropParams& dp, void* y, void* xhat, float* rstd,
+             hipStream_t st) {
+#define L(LPR, NV)                                                                              \
+    {                                                                                           \
+        int64_t rpb = 4 * (64 / LPR);                                                           \
+        hipLaunchKernelGGL((bdrln_fwd_k<T, LPR, NV>), dim3((rows + rpb - 1) / rpb), dim3(NT), 0, \
+                           st, rows, len, (const T*)x, (const T*)bias, (const T*)resid,         \
+                           (const T*)gamma, (const T*)beta, eps, dp, (T*)y, (T*)xhat, rstd);    \
+    }
+    DM_ROW_CASES(L)
+#undef L
+}
+
+template <typename T>
+void softmax_t(int B, int H, int J, int len, float scale, const void* beta, const DropParams& dp,
+               void* prob, void* alpha, hipStream_t st) {
+    int64_t rows = (int64_t)B * H * J;
+#define L(LPR, NV)                                                                                \
+    {                                                                                             \
+        int64_t rpb = 4 * (64 / LPR);                                                             \
+        hipLaunchKernelGGL((softmax_fwd_k<T, LPR, NV>), dim3((rows + rpb - 1) / rpb), dim3(NT), 0, \
+                           st, rows, B, H, J, len, scale, (const T*)beta, dp, (T*)prob, (T*)alpha); \
+    }
+    DM_ROW_CASES(L)
+#undef L
+}
+
+template <typename T>
+void softmax_bwd_t(int B, int H, int J, int len, float scale, const void* dalpha, const void* prob,
+                   const DropParams& dp, void* dbeta, hipStream_t st) {
+    int64_t rows = (int64_t)B * H * J;
+#define L(LPR, NV)                                                                                \
+    {                                                                                             \
+        int64_t rpb = 4 * (64 / LPR);                                                             \
+        hipLaunchKernelGGL((softmax_bwd_k<T, LPR, NV>), dim3((rows + rpb - 1) / rpb), dim3(NT), 0, \
+                           st, rows, B, H, J, len, scale, (const T*)dalpha, (const T*)prob, dp,   \
+                           (T*)dbeta);                                                            \
+    }
+    DM_ROW_CASES(L)
+#undef L
+}
+
+template <typename T>
+void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
+    const int len = a.cols;
+    const int nblk = colsum_blocks(a.rows);
+    const int rpb = (int)((a.rows + nblk - 1) / nblk);
+#define L(LPR, NV) \
+    { hipLaunchKernelGGL((ln_bwd_k<T, LPR, NV>), dim3(nblk), dim3(NT), 0, st, a, rpb, nblk); }
+    DM_ROW_CASES(L)
+#undef L
+}
+
+}  // namespace
+
+int colsum_blocks(int64_t rows) {
+    int64_t b = (rows + 15) / 16;
+    if (b > 256) b = 256;
+    return (int)(b < 1 ? 1 : b);
+}
+
+#define DM_DTYPE_SWITCH(dtype, ...)                                \
+    do {                                                           \
+        if ((dtype) == DM_F32) { typedef float T; __VA_ARGS__; }   \
+        else if ((dtype) == DM_F16) { typedef half_t T; __VA_ARGS__; } \
+        else { typedef bf16_t T; __VA_ARGS__; }                    \
+    } while (0)
+
+void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias, const void* resid,
+                   const void* gamma, const void* beta, float eps, const DropParams& dp, void* y, void* xhat,
+                   float* rstd, hipStream_t st) {
+    DM_DTYPE_SWITCH(dtype, bdrln_t<T>(rows, cols, x, bias, resid, gamma, beta, eps, dp, y, xhat, rstd, st));
+}
+
+void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta, const DropParams& dp,
+                     void* prob, void* alpha, hipStream_t st) {
+    DM_DTYPE_SWITCH(dtype, softmax_t<T>(B, H, J, K, scale, beta, dp, prob, alpha, st));
+}
+
+void run_softmax_bwd(int dtype, int B, int H, int J, int K, float scale, const void* dalpha, const void* prob,
+                     const DropParams& dp, void* dbeta, hipStream_t st) {
+    DM_DTYPE_SWITCH(dtype, softmax_bwd_t<T>(B, H, J, K, scale, dalpha, prob, dp, dbeta, st));
+}
+
+void run_ln_bwd(const LnBwdArgs& a, hipStream_t st) { DM_DTYPE_SWITCH(a.dtype, ln_bwd_t<T>(a, st)); }
+
+void run_bias_act_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias, int act,
+                      const DropParams& dp, void* y, hipStream_t st) {
+    int64_t nvec = rows * cols / 8;
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((bias_act_fwd_k<T>), dim3(grid_for(nvec)), dim3(NT), 0, st, nvec,
+                                               cols, (const T*)x, (const T*)bias, act, dp, (T*)y));
+}
+
+void run_attn_input_bias(int dtype, int64_t rows, int H, int P, const void* x, const void* bq, const void* bk,
+                         const void* bv, void* y, hipStream_t st) {
+    int64_t nvec = rows * 3 * H * P / 8;
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((attn_input_bias_k<T>), dim3(grid_for(nvec)), dim3(NT), 0, st,
+                                               nvec, H, P, (const T*)x, (const T*)bq, (const T*)bk,
+                                               (const T*)bv, (T*)y));
+}
+
+void run_act_bwd(int dtype, int64_t rows, int F, const void* da, const void* h, const void* b1, int act,
+                 const DropParams& dp, void* dh, float* part, hipStream_t st) {
+    const int nblk = colsum_blocks(rows);
+    const int rpb = (int)((rows + nblk - 1) / nblk);
+    const int cv = (F / 8 + NT - 1) / NT;
+#define L(CV)                                                                                          \
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((act_bwd_k<T, CV>), dim3(nblk), dim3(NT), 0, st, rows, F, \
+                                               (const T*)da, (const T*)h, (const T*)b1, act, dp, (T*)dh, \
+                                               part, rpb))
+    if (cv <= 1) L(1);
+    else if (cv <= 2) L(2);
+    else if (cv <= 4) L(4);
+    else L(8);
+#undef L
+}
+
+void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float* part, hipStream_t st) {
+    const int nblk = colsum_blocks(rows);
+    const int rpb = (int)((rows + nblk - 1) / nblk);
+    const int cv = (cols / 8 + NT - 1) / NT;
+#define L(CV)                                                                                     \
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((colsum_partial_k<T, CV>), dim3(nblk), dim3(NT), 0, st, \
+                                               rows, cols, (const T*)x, part, rpb))
+    if (cv <= 1) L(1);
+    else if (cv <= 2) L(2);
+    else if (cv <= 4) L(4);
+    else L(8);
+#undef L
+}
+
+void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st) {
+    const int nblk = colsum_blocks(rows);
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64), dim3(NT), 0, st, nblk, cols, part, out, 0, 0,
+                       nullptr, nullptr);
+}
+
+void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* part, float* dbq, float* dbk,
+                           float* dbv, hipStream_t st) {
+    const int nblk = colsum_blocks(rows);
+    const int cols = nseg * H * P;
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64), dim3(NT), 0, st, nblk, cols, part, dbq, H, P,
+                       dbk, dbv);
+}
+
+void run_rowsum(int dtype, int64_t rows, int len, const void* x, float* out, hipStream_t st) {
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((rowsum_k<T>), dim3((rows + 3) / 4), dim3(NT), 0, st, rows, len,
+                                               (const T*)x, out));
+}
+
+void run_add(int dtype, int64_t n, const void* a, const void* b, void* out, hipStream_t st) {
+    int64_t nvec = n / 8;
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((add_k<T>), dim3(grid_for(nvec)), dim3(NT), 0, st, nvec,
+                                               (const T*)a, (const T*)b, (T*)out));
+}
+
+void run_dropout_mask(const DropParams& dp, uint64_t offset, uint64_t n, uint8_t* out, hipStream_t st) {
+    uint64_t nvec = n / 8;
+    hipLaunchKernelGGL(dropout_mask_k, dim3(grid_for((int64_t)nvec)), dim3(NT), 0, st, dp, offset, nvec, out);
+}
+
+}  // namespace dm

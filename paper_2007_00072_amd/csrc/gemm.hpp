@@ -1,0 +1,89 @@
+// Contraction kernels: every einsum of the layer (Fig. 1a and the
+// Table 3 contraction rows, forward dX/dW split in backward) is one launch
+// of a single MFMA GEMM whose operand and output addressing is general
+// enough that no tensor is ever transposed or permuted in a separate pass.
+//
+// C[z][m][n] = alpha * sum_k A(z, m, k) * B(z, k, n)  (+ bias) (+ resid)
+//
+// Each operand is stored either contiguous along k ("k-contiguous": element
+// (outer, k) at row(outer) + k) or contiguous along its outer index
+// ("outer-contiguous": element (outer, k) at row(k) + outer).  The strided
+// ("row") index goes through a mixed-radix map, which expresses plain
+// strides, the paper's (p, h) <-> head-major (h, p) permutation, the split
+// of a fused Q/K/V projection into per-head tensors, and a choice among up
+// to three base pointers (the stacked [Wq Wk Wv] of algebraic fusion).
+#pragma once
+
+#include "common.hpp"
+
+namespace dm {
+
+// Mixed-radix index map: x = (d2 * r1 + d1) * r0 + d0, offset = d0*s0 + d1*s1
+// + d2*s2 (elements).  r = 0 means the digit is unbounded.  When the map
+// selects among several base pointers (nseg > 1) the top digit d2 picks the
+// pointer and contributes no offset.
+struct IdxMap {
+    uint32_t r0, r1;
+    uint32_t mul0, shr0, mul1, shr1;  // division by r0 / r1: q = (umulhi(x, mul) + x) >> shr
+    int64_t s0, s1, s2;
+};
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t x, uint32_t mul, uint32_t shr) {
+    return (__umulhi(x, mul) + x) >> shr;
+}
+
+// offset and segment of index x
+__device__ __forceinline__ int64_t map_off(const IdxMap& m, uint32_t x, int nseg, int* seg) {
+    uint32_t d0 = x, d1 = 0, d2 = 0;
+    if (m.r0) {
+        uint32_t q = fdiv(x, m.mul0, m.shr0);
+        d0 = x - q * m.r0;
+        d1 = q;
+        if (m.r1) { d2 = fdiv(q, m.mul1, m.shr1); d1 = q - d2 * m.r1; }
+    }
+    int64_t off = (int64_t)d0 * m.s0 + (int64_t)d1 * m.s1;
+    if (nseg > 1) *seg = (int)d2; else off += (int64_t)d2 * m.s2;
+    return off;
+}
+
+struct Operand {
+    const void* ptr[3];
+    int nseg;
+    int kcontig;      // 1: rows indexed by the outer (m or n) index, contiguous along k
+    IdxMap row;       // strided index -> offset
+    IdxMap batch;     // z -> offset
+};
+
+struct Epilogue {
+    void* ptr[3];
+    int nseg;          // > 1: the segment digit of mmap (seg_on_m) or nmap picks the pointer
+    int seg_on_m;
+    IdxMap mmap, nmap, batch;
+    int contig_n;      // 1: nmap has unit stride over aligned groups of 8; 0: mmap does
+    float alpha;
+    const void* bias[3];
+    int bias_nseg;
+    int bias_on_m;     // bias indexed by m instead of n
+    IdxMap bias_map;
+    const void* resid;  // optional, same addressing as C (single pointer)
+    int out_f32;        // C (and resid) stored as float instead of the input dtype
+};
+
+struct GemmArgs {
+    int M, N, K, batch;
+    Operand a, b;
+    Epilogue c;
+    int tiles_m, tiles_n;
+};
+
+// Host-side construction helpers.
+IdxMap make_map(uint32_t r0, uint32_t r1, int64_t s0, int64_t s1, int64_t s2);
+inline IdxMap linear_map(int64_t stride) { return make_map(0, 0, stride, 0, 0); }
+
+enum GemmDtype { G_F32 = 0, G_F16 = 1, G_BF16 = 2 };
+
+// Validates and launches one contraction; returns 0 on success, else a
+// message is stored for dm_last_error and a nonzero code returned.
+int launch_gemm(int dtype, const GemmArgs& args, hipStream_t stream);
+
+}  // namespace dm

@@ -1,0 +1,102 @@
+// Host-side internals shared by the library's translation units: error
+// state, dropout parameter setup and the launchers of the fused operators.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/dmtx.h"
+#include "common.hpp"
+
+namespace dm {
+
+// Records a message for dm_last_error() on the calling thread; returns code.
+int set_error(int code, const char* fmt, ...);
+int check_launch(const char* what);
+
+// Per-launch timing (dm_trace_*): brackets the launches made in its scope
+// with two events on `st` when tracing is enabled.
+struct TraceScope {
+    TraceScope(const char* label, hipStream_t st);
+    ~TraceScope() { stop(); }
+    void stop();  // records the end event now (idempotent)
+    int idx;
+    hipStream_t st;
+};
+
+// p in [0,1); seed/site/layer -> kernel parameters (thr, scale computed in double).
+DropParams make_drop(float p, uint64_t seed, uint32_t site, uint32_t layer);
+inline DropParams make_drop(const dm_dropout* d) {
+    if (!d) return make_drop(0.f, 0, 0, 0);
+    return make_drop(d->p, d->seed, d->site, d->layer);
+}
+
+// Column-sum scratch: partial sums of `nblk` row blocks.
+int colsum_blocks(int64_t rows);
+
+// ------------------------------------------------------- kernel launchers
+// All take element counts, device pointers and a stream, and assume the
+// caller validated alignment and sizes.  dtype: DM_F32 / DM_F16 / DM_BF16.
+void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias,
+                   const void* resid, const void* gamma, const void* beta, float eps,
+                   const DropParams& dp, void* y, void* xhat, float* rstd, hipStream_t st);
+
+void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta,
+                     const DropParams& dp, void* prob, void* alpha, hipStream_t st);
+
+void run_bias_act_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias, int act,
+                      const DropParams& dp, void* y, hipStream_t st);
+
+void run_attn_input_bias(int dtype, int64_t rows, int H, int P, const void* x, const void* bq,
+                         const void* bk, const void* bv, void* y, hipStream_t st);
+
+// LayerNorm backward row kernel, in the fused forms the layer uses:
+//   dy = dya (+ dyb if non-null); optional dysum = dy written out;
+//   optional ds = LN backward of dy; optional dsub = dropout(ds);
+//   optional column partial sums of dy*xhat, dy and dsub into `part`
+//   ([3][nblk][cols] floats) finished by run_colsum_finish.
+struct LnBwdArgs {
+    int dtype;
+    int64_t rows;
+    int cols;
+    const void* dya;
+    const void* dyb;
+    const void* xhat;
+    const void* gamma;
+    const float* rstd;
+    DropParams dp;
+    void* dysum;
+    void* ds;
+    void* dsub;
+    float* part;  // null: no column sums
+    int want_dsub_sum;
+};
+void run_ln_bwd(const LnBwdArgs& a, hipStream_t st);
+
+void run_softmax_bwd(int dtype, int B, int H, int J, int K, float scale, const void* dalpha,
+                     const void* prob, const DropParams& dp, void* dbeta, hipStream_t st);
+
+// dh = dropout'(da) * act'(h + b1) with column partials of dh into part.
+void run_act_bwd(int dtype, int64_t rows, int F, const void* da, const void* h, const void* b1,
+                 int act, const DropParams& dp, void* dh, float* part, hipStream_t st);
+
+// Column partial sums of x (rows x cols) into part[nblk][cols].
+void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float* part,
+                        hipStream_t st);
+
+// out[map(c)] = sum_b part[b][c] for c < cols.  With H, P > 0 the columns
+// are (s, h, p) of a fused projection and go to outs[s][p*H + h].
+void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st);
+void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* part, float* dbq,
+                           float* dbk, float* dbv, hipStream_t st);
+
+// out[r] = sum_c x[r][c] (float) for rows of length len (multiple of 8).
+void run_rowsum(int dtype, int64_t rows, int len, const void* x, float* out, hipStream_t st);
+
+void run_add(int dtype, int64_t n, const void* a, const void* b, void* out, hipStream_t st);
+
+void run_dropout_mask(const DropParams& dp, uint64_t offset, uint64_t n, uint8_t* out,
+                      hipStream_t st);
+
+}  // namespace dm

@@ -1,0 +1,748 @@
+// Layer drivers: multi-head attention (Fig. 1a) and the post-LN encoder
+// layer (Table 3), forward and backward, sequenced on one stream.
+//
+// Internal layouts (chosen so that every contraction reads its operands in
+// place and every statistical normalisation reduces a contiguous row):
+//   residual stream, LayerNorm outputs, FFN activations: token-major [T][.]
+//   per-head projections Q, K, V:                         [B][H][J or K][P]
+//   attention scores beta, probabilities, alpha:          [B][H][J][K]
+//   attention context gamma:                              [T][H][W]
+//   gradients of Q, K, V:                                 token-major [T][3][H][P]
+// The paper's (p, h) ordering of projection rows and weights is reached by
+// index maps inside the contraction kernel, never by a transpose pass.
+#include <math.h>
+
+#include "gemm.hpp"
+#include "internal.hpp"
+
+using namespace dm;
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+struct Dims {
+    int64_t B, J, K, H, P, W, I, F;
+    int64_t Tq, Tk, N, S;
+    int es;  // element size
+    int dtype;
+    int layout;
+};
+
+Dims dims_of(const dm_layer_desc* d) {
+    Dims x{};
+    x.B = d->B; x.J = d->J; x.K = d->K; x.H = d->H; x.P = d->P; x.W = d->W; x.I = d->I; x.F = d->F;
+    x.Tq = x.B * x.J; x.Tk = x.B * x.K; x.N = x.Tq * x.I; x.S = x.B * x.H * x.J * x.K;
+    x.dtype = d->dtype;
+    x.layout = d->layout;
+    x.es = d->dtype == DM_F32 ? 4 : 2;
+    return x;
+}
+
+// ------------------------------------------------------------ buffer plans
+struct Carver {
+    size_t total = 0;
+    size_t take(size_t bytes) { size_t o = total; total += up(bytes); return o; }
+};
+
+struct MhaPlan {
+    // saved
+    size_t q, k, v, prob, alpha, gamma;
+    // forward workspace
+    size_t beta;
+    // backward workspace
+    size_t dgamma, dalpha, dbeta, dq, dk, dv, part;
+    int64_t ldq, ldk, ldv;  // row strides (elements) of the Q/K/V gradient buffers
+    size_t fused_dqkv;      // self-attention: one [T][3][H][P] buffer at dq
+};
+
+struct EncPlan {
+    MhaPlan m;
+    size_t xhat1, rstd1, y1, h, a, xhat2, rstd2, saved_total;
+    size_t ao, o, fwd_total;
+    size_t dS2, dO, dA, dH, dY1f, dS1, dAO, bwd_total;
+};
+
+int64_t max3(int64_t a, int64_t b, int64_t c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
+
+void plan_attention(const Dims& x, bool fused, Carver& sv, Carver& fw, Carver& bw, MhaPlan& p) {
+    const size_t es = x.es;
+    p.q = sv.take(es * x.B * x.H * x.J * x.P);
+    p.k = sv.take(es * x.B * x.H * x.K * x.P);
+    p.v = sv.take(es * x.B * x.H * x.K * x.W);
+    p.prob = sv.take(es * x.S);
+    p.alpha = sv.take(es * x.S);
+    p.gamma = sv.take(es * x.Tq * x.H * x.W);
+    p.beta = fw.take(es * x.S);
+    p.dgamma = bw.take(es * x.Tq * x.H * x.W);
+    p.dalpha = bw.take(es * x.S);
+    p.dbeta = bw.take(es * x.S);
+    if (fused) {
+        p.ldq = p.ldk = p.ldv = 3 * x.H * x.P;
+        p.dq = bw.take(es * x.Tq * p.ldq);
+        p.dk = p.dq;  // column offsets are added at use
+        p.dv = p.dq;
+    } else {
+        p.ldq = x.H * x.P; p.ldk = x.H * x.P; p.ldv = x.H * x.W;
+        p.dq = bw.take(es * x.Tq * p.ldq);
+        p.dk = bw.take(es * x.Tk * p.ldk);
+        p.dv = bw.take(es * x.Tk * p.ldv);
+    }
+}
+
+EncPlan plan_encoder(const Dims& x) {
+    EncPlan e{};
+    Carver sv, fw, bw;
+    plan_attention(x, true, sv, fw, bw, e.m);
+    const size_t es = x.es, T = x.Tq;
+    e.xhat1 = sv.take(es * x.N);
+    e.rstd1 = sv.take(4 * T);
+    e.y1 = sv.take(es * x.N);
+    e.h = sv.take(es * T * x.F);
+    e.a = sv.take(es * T * x.F);
+    e.xhat2 = sv.take(es * x.N);
+    e.rstd2 = sv.take(4 * T);
+    e.saved_total = sv.total;
+    e.ao = fw.take(es * x.N);
+    e.o = fw.take(es * x.N);
+    e.fwd_total = fw.total;
+    e.dS2 = bw.take(es * x.N);
+    e.dO = bw.take(es * x.N);
+    e.dA = bw.take(es * T * x.F);
+    e.dH = bw.take(es * T * x.F);
+    e.dY1f = bw.take(es * x.N);
+    e.dS1 = bw.take(es * x.N);
+    e.dAO = bw.take(es * x.N);
+    e.m.part = bw.take(colsum_ws_bytes(T, (int32_t)max3(3 * x.I, x.F, x.I)));
+    e.bwd_total = bw.total;
+    return e;
+}
+
+struct MhaSizes { MhaPlan p; size_t saved, fwd, bwd; };
+MhaSizes plan_mha(const Dims& x, bool fused) {
+    MhaSizes s{};
+    Carver sv, fw, bw;
+    plan_attention(x, fused, sv, fw, bw, s.p);
+    int64_t cols = max3(fused ? 3 * x.H * x.P : x.H * x.P, x.H * x.W, x.I);
+    s.p.part = bw.take(colsum_ws_bytes(x.Tq > x.Tk ? x.Tq : x.Tk, (int32_t)cols) + 4 * x.I);
+    s.saved = sv.total; s.fwd = fw.total; s.bwd = bw.total;
+    return s;
+}
+
+// ------------------------------------------------------------ validation
+#define DM_TRY(x)                      \
+    do {                               \
+        int _rc = (x);                 \
+        if (_rc != DM_OK) return _rc;  \
+    } while (0)
+
+int need(const void* p, const char* name) {
+    if (!p) return set_error(DM_ERR_ARG, "%s is NULL", name);
+    if ((uintptr_t)p & 15u) return set_error(DM_ERR_ARG, "%s is not 16-byte aligned", name);
+    return DM_OK;
+}
+
+int check_desc(const dm_layer_desc* d, bool encoder) {
+    if (!d) return set_error(DM_ERR_ARG, "descriptor is NULL");
+    if (d->dtype != DM_F32 && d->dtype != DM_F16 && d->dtype != DM_BF16)
+        return set_error(DM_ERR_UNSUPPORTED, "unsupported dtype %d", d->dtype);
+    if (d->layout != DM_BJI && d->layout != DM_IBJ) return set_error(DM_ERR_UNSUPPORTED, "unsupported layout");
+    if (d->B <= 0 || d->J <= 0 || d->K <= 0 || d->H <= 0 || d->P <= 0 || d->W <= 0 || d->I <= 0)
+        return set_error(DM_ERR_ARG, "sizes must be positive");
+    if (d->J % 8 || d->K % 8 || d->P % 8 || d->W % 8 || d->I % 8)
+        return set_error(DM_ERR_UNSUPPORTED, "J, K, P, W, I must be multiples of 8");
+    if (d->K > 4096) return set_error(DM_ERR_UNSUPPORTED, "key length above 4096");
+    if ((int64_t)d->B * d->H > 65535) return set_error(DM_ERR_UNSUPPORTED, "B*H above 65535");
+    if ((int64_t)d->B * d->H * d->J * d->K > ((int64_t)1 << 40)) return set_error(DM_ERR_UNSUPPORTED, "too large");
+    if ((int64_t)d->B * (d->J > d->K ? d->J : d->K) * 3 * d->I >= ((int64_t)1 << 31))
+        return set_error(DM_ERR_UNSUPPORTED, "token count too large");
+    const float ps[4] = {d->p_attn, d->p_attn_out, d->p_ffn_out, d->p_ffn_act};
+    for (float p : ps)
+        if (!(p >= 0.f && p < 1.f)) return set_error(DM_ERR_ARG, "dropout probability %g outside [0,1)", p);
+    if (encoder) {
+        if (d->layout != DM_BJI) return set_error(DM_ERR_UNSUPPORTED, "encoder layer supports layout BJI only");
+        if (d->I != d->H * d->P || d->W != d->P) return set_error(DM_ERR_ARG, "encoder needs I == H*P and W == P");
+        if (d->J != d->K) return set_error(DM_ERR_ARG, "encoder self-attention needs J == K");
+        if (d->F <= 0 || d->F % 8) return set_error(DM_ERR_UNSUPPORTED, "F must be a positive multiple of 8");
+        if (d->I > 2048) return set_error(DM_ERR_UNSUPPORTED, "I above 2048");
+        if (d->F > 16384) return set_error(DM_ERR_UNSUPPORTED, "F above 16384");
+        if (d->act != DM_GELU && d->act != DM_RELU) return set_error(DM_ERR_UNSUPPORTED, "unknown activation");
+        if (!(d->ln_eps > 0.f)) return set_error(DM_ERR_ARG, "ln_eps must be > 0");
+    } else {
+        if (d->self_attention && (d->J != d->K || d->W != d->P))
+            return set_error(DM_ERR_ARG, "self-attention needs J == K and W == P");
+        if (3 * d->H * d->P > 16384 || d->I > 16384) return set_error(DM_ERR_UNSUPPORTED, "width above 16384");
+    }
+    return DM_OK;
+}
+
+int check_params(const dm_layer_params* p, bool encoder) {
+    if (!p) return set_error(DM_ERR_ARG, "params is NULL");
+    DM_TRY(need(p->wq, "wq")); DM_TRY(need(p->bq, "bq")); DM_TRY(need(p->wk, "wk")); DM_TRY(need(p->bk, "bk"));
+    DM_TRY(need(p->wv, "wv")); DM_TRY(need(p->bv, "bv")); DM_TRY(need(p->wo, "wo")); DM_TRY(need(p->bo, "bo"));
+    if (encoder) {
+        DM_TRY(need(p->g1, "g1")); DM_TRY(need(p->be1, "be1")); DM_TRY(need(p->w1, "w1"));
+        DM_TRY(need(p->b1, "b1")); DM_TRY(need(p->w2, "w2")); DM_TRY(need(p->b2, "b2"));
+        DM_TRY(need(p->g2, "g2")); DM_TRY(need(p->be2, "be2"));
+    }
+    return DM_OK;
+}
+
+int check_grads(const dm_layer_grads* g, bool encoder) {
+    if (!g) return set_error(DM_ERR_ARG, "grads is NULL");
+    DM_TRY(need(g->dwq, "dwq")); DM_TRY(need(g->dbq, "dbq")); DM_TRY(need(g->dwk, "dwk"));
+    DM_TRY(need(g->dbk, "dbk")); DM_TRY(need(g->dwv, "dwv")); DM_TRY(need(g->dbv, "dbv"));
+    DM_TRY(need(g->dwo, "dwo")); DM_TRY(need(g->dbo, "dbo"));
+    if (encoder) {
+        DM_TRY(need(g->dg1, "dg1")); DM_TRY(need(g->dbe1, "dbe1")); DM_TRY(need(g->dw1, "dw1"));
+        DM_TRY(need(g->db1, "db1")); DM_TRY(need(g->dw2, "dw2")); DM_TRY(need(g->db2, "db2"));
+        DM_TRY(need(g->dg2, "dg2")); DM_TRY(need(g->dbe2, "dbe2"));
+    }
+    return DM_OK;
+}
+
+// ------------------------------------------------------------ GEMM builders
+IdxMap zero_map() { return linear_map(0); }
+
+Operand opnd(const void* p, bool kcontig, IdxMap row, IdxMap batch = zero_map()) {
+    Operand o{};
+    o.ptr[0] = p; o.nseg = 1; o.kcontig = kcontig; o.row = row; o.batch = batch;
+    return o;
+}
+Operand opnd3(const void* p0, const void* p1, const void* p2, bool kcontig, IdxMap row) {
+    Operand o = opnd(p0, kcontig, row);
+    o.ptr[1] = p1; o.ptr[2] = p2; o.nseg = 3;
+    return o;
+}
+Epilogue epi(void* p, IdxMap mmap, IdxMap nmap, bool contig_n, bool out_f32, IdxMap batch = zero_map()) {
+    Epilogue e{};
+    e.ptr[0] = p; e.nseg = 1; e.mmap = mmap; e.nmap = nmap; e.batch = batch;
+    e.contig_n = contig_n; e.alpha = 1.f; e.out_f32 = out_f32; e.bias_nseg = 1;
+    e.bias_map = linear_map(1);
+    return e;
+}
+GemmArgs gemm(int64_t M, int64_t N, int64_t K, int64_t batch, const Operand& a, const Operand& b,
+              const Epilogue& c) {
+    GemmArgs g{};
+    g.M = (int)M; g.N = (int)N; g.K = (int)K; g.batch = (int)batch;
+    g.a = a; g.b = b; g.c = c;
+    return g;
+}
+
+// An activation x (t, i) in the given layout, as the (m, k) operand with m = t, k = i...
+Operand act_mk(const void* p, int layout, int64_t T, int64_t I) {
+    return layout == DM_BJI ? opnd(p, true, linear_map(I)) : opnd(p, false, linear_map(T));
+}
+// ... and as the (k, n) operand with k = t, n = i.
+Operand act_kn(const void* p, int layout, int64_t T, int64_t I) {
+    return layout == DM_BJI ? opnd(p, false, linear_map(I)) : opnd(p, true, linear_map(T));
+}
+// Output element (t, i) of an activation in the given layout.
+Epilogue act_out(void* p, int layout, int64_t T, int64_t I) {
+    return layout == DM_BJI ? epi(p, linear_map(I), linear_map(1), true, false)
+                            : epi(p, linear_map(1), linear_map(T), false, false);
+}
+
+char* B8(void* base, size_t off) { return reinterpret_cast<char*>(base) + off; }
+const char* B8(const void* base, size_t off) { return reinterpret_cast<const char*>(base) + off; }
+
+float scaler_of(const dm_layer_desc* d) { return d->scaler > 0.f ? d->scaler : 1.0f / sqrtf((float)d->P); }
+
+// ------------------------------------------------------------ attention pieces
+// Projection of one input into a per-head tensor [B][H][L][n] (n = P or W),
+// with the input bias in the epilogue.  w: [n][H][I] (paper order), b: [n][H].
+int project(const Dims& x, int layout, const void* in, int64_t L, int64_t n, const void* w, const void* b,
+            void* out, hipStream_t st) {
+    const int64_t T = x.B * L;
+    Operand A = act_mk(in, layout, T, x.I);
+    Operand Bw = opnd(w, true, make_map((uint32_t)n, 0, x.H * x.I, x.I, 0));
+    Epilogue c = epi(out, make_map((uint32_t)L, 0, n, x.H * L * n, 0), make_map((uint32_t)n, 0, 1, L * n, 0),
+                     true, false);
+    c.bias[0] = b; c.bias_map = make_map((uint32_t)n, 0, x.H, 1, 0);
+    return launch_gemm(x.dtype, gemm(T, x.H * n, x.I, 1, A, Bw, c), st);
+}
+
+// Fused [Wq Wk Wv] projection of one input (self-attention, W == P): the
+// output columns (s, h, p) go to qkv + s*Nh with Nh = B*H*J*P.
+int project_fused(const Dims& x, int layout, const void* in, const dm_layer_params* prm, void* q, void* k,
+                  void* v, hipStream_t st) {
+    const int64_t T = x.Tq, P = x.P, H = x.H;
+    Operand A = act_mk(in, layout, T, x.I);
+    Operand Bw = opnd3(prm->wq, prm->wk, prm->wv, true, make_map((uint32_t)P, (uint32_t)H, H * x.I, x.I, 0));
+    Epilogue c = epi(q, make_map((uint32_t)x.J, 0, P, H * x.J * P, 0),
+                     make_map((uint32_t)P, (uint32_t)H, 1, x.J * P, 0), true, false);
+    c.ptr[1] = k; c.ptr[2] = v; c.nseg = 3; c.seg_on_m = 0;
+    c.bias[0] = prm->bq; c.bias[1] = prm->bk; c.bias[2] = prm->bv; c.bias_nseg = 3;
+    c.bias_map = make_map((uint32_t)P, (uint32_t)H, H, 1, 0);
+    return launch_gemm(x.dtype, gemm(T, 3 * H * P, x.I, 1, A, Bw, c), st);
+}
+
+// QK^T -> softmax + dropout -> alpha.V ; gamma token-major [Tq][H][W].
+int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const void* q, const void* k,
+                       const void* v, void* beta, void* prob, void* alpha, void* gamma, hipStream_t st) {
+    const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, HW = x.H * x.W;
+    // beta[z][j][k] = scaler * sum_p Q[z][j][p] K[z][k][p]
+    Epilogue cb = epi(beta, linear_map(K), linear_map(1), true, false, linear_map(J * K));
+    cb.alpha = scaler;
+    {
+        TraceScope t_("F2 qkt", st);
+        DM_TRY(launch_gemm(x.dtype,
+                           gemm(J, K, P, Z, opnd(q, true, linear_map(P), linear_map(J * P)),
+                                opnd(k, true, linear_map(P), linear_map(K * P)), cb),
+                           st));
+    }
+    {
+        TraceScope t_("F3 softmax", st);
+        run_softmax_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, 1.0f, beta, dp, prob, alpha, st);
+    }
+    DM_TRY(check_launch("softmax"));
+    // gamma[(b,j)][(h,w)] = sum_k alpha[z][j][k] V[z][k][w]
+    Epilogue cg = epi(gamma, linear_map(HW), linear_map(1), true, false, make_map((uint32_t)x.H, 0, W, J * HW, 0));
+    TraceScope t_("F4 gamma", st);
+    return launch_gemm(x.dtype,
+                       gemm(J, W, K, Z, opnd(alpha, true, linear_map(K), linear_map(J * K)),
+                            opnd(v, false, linear_map(W), linear_map(K * W)), cg),
+                       st);
+}
+
+// out(t, i) = sum_{h,w} gamma[t][(h,w)] wo[w][h][i] (+ bo)
+int out_projection(const Dims& x, const void* gamma, const void* wo, const void* bo, void* out, int layout,
+                   hipStream_t st) {
+    const int64_t HW = x.H * x.W;
+    Operand A = opnd(gamma, true, linear_map(HW));
+    Operand Bw = opnd(wo, false, make_map((uint32_t)x.W, 0, x.H * x.I, x.I, 0));
+    Epilogue c = act_out(out, layout, x.Tq, x.I);
+    if (bo) { c.bias[0] = bo; c.bias_map = linear_map(1); }
+    TraceScope t_("F5 out", st);
+    return launch_gemm(x.dtype, gemm(x.Tq, x.I, HW, 1, A, Bw, c), st);
+}
+
+// Backward of attention from d(out) (layout `layout`) down to the gradients
+// of Q, K, V (written token-major into dq/dk/dv at row strides ldq/ldk/ldv),
+// plus dwo.
+int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const void* dout, int layout,
+                       const void* q, const void* k, const void* v, const void* prob, const void* alpha,
+                       const void* gamma, const void* wo, float* dwo, void* dgamma, void* dalpha, void* dbeta,
+                       void* dq, int64_t ldq, void* dk, int64_t ldk, void* dv, int64_t ldv, hipStream_t st) {
+    const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, H = x.H, HW = x.H * x.W, I = x.I;
+    // Out dX: dgamma[t][(h,w)] = sum_i dout(t,i) wo[w][h][i]
+    TraceScope t11("B11 out_dx", st);
+    DM_TRY(launch_gemm(x.dtype,
+                       gemm(x.Tq, HW, I, 1, act_mk(dout, layout, x.Tq, I),
+                            opnd(wo, true, make_map((uint32_t)W, 0, H * I, I, 0)),
+                            epi(dgamma, linear_map(HW), linear_map(1), true, false)),
+                       st));
+    t11.stop();
+    // Out dW: dwo[w][h][i] = sum_t gamma[t][(h,w)] dout(t,i)
+    TraceScope t12("B12 out_dw", st);
+    DM_TRY(launch_gemm(x.dtype,
+                       gemm(HW, I, x.Tq, 1, opnd(gamma, false, linear_map(HW)), act_kn(dout, layout, x.Tq, I),
+                            epi(dwo, make_map((uint32_t)W, 0, H * I, I, 0), linear_map(1), true, true)),
+                       st));
+    const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
+    t12.stop();
+    // Gamma dX1: dalpha[z][j][k] = sum_w dgamma[(b,j)][(h,w)] V[z][k][w]
+    TraceScope t13("B13 gamma_dx1", st);
+    DM_TRY(launch_gemm(x.dtype,
+                       gemm(J, K, W, Z, opnd(dgamma, true, linear_map(HW), zg),
+                            opnd(v, true, linear_map(W), linear_map(K * W)),
+                            epi(dalpha, linear_map(K), linear_map(1), true, false, linear_map(J * K))),
+                       st));
+    t13.stop();
+    // Gamma dX2: dV[z][k][w] = sum_j alpha[z][j][k] dgamma[(b,j)][(h,w)]
+    TraceScope t14("B14 gamma_dx2", st);
+    DM_TRY(launch_gemm(x.dtype,
+                       gemm(K, W, J, Z, opnd(alpha, false, linear_map(K), linear_map(J * K)),
+                            opnd(dgamma, false, linear_map(HW), zg),
+                            epi(dv, linear_map(ldv), linear_map(1), true, false,
+                                make_map((uint32_t)H, 0, W, K * ldv, 0))),
+                       st));
+    t14.stop();
+    // Scaled softmax dX
+    TraceScope t15("B15 softmax_bwd", st);
+    run_softmax_bwd(x.dtype, (int)x.B, (int)H, (int)J, (int)K, scaler, dalpha, prob, dp, dbeta, st);
+    DM_TRY(check_launch("softmax backward"));
+    t15.stop();
+    // QK^T dX1: dQ[z][j][p] = sum_k dbeta[z][j][k] K[z][k][p]
+    TraceScope t16("B16 qkt_dx1", st);
+    DM_TRY(launch_gemm(x.dtype,
+                       gemm(J, P, K, Z, opnd(dbeta, true, linear_map(K), linear_map(J * K)),
+                            opnd(k, false, linear_map(P), linear_map(K * P)),
+                            epi(dq, linear_map(ldq), linear_map(1), true, false,
+                                make_map((uint32_t)H, 0, P, J * ldq, 0))),
+                       st));
+    t16.stop();
+    // QK^T dX2: dK[z][k][p] = sum_j dbeta[z][j][k] Q[z][j][p]
+    TraceScope t17("B17 qkt_dx2", st);
+    DM_TRY(launch_gemm(x.dtype,
+                       gemm(K, P, J, Z, opnd(dbeta, false, linear_map(K), linear_map(J * K)),
+                            opnd(q, false, linear_map(P), linear_map(J * P)),
+                            epi(dk, linear_map(ldk), linear_map(1), true, false,
+                                make_map((uint32_t)H, 0, P, K * ldk, 0))),
+                       st));
+    return DM_OK;
+}
+
+// dX(t,i) = sum_{(h,n)} dproj[t][(h,n)] w[n][h][i] and dw[n][h][i] = sum_t dproj[t][(h,n)] X(t,i).
+int project_bwd(const Dims& x, int layout, const void* in, int64_t T, int64_t n, const void* dproj, int64_t ld,
+                const void* w, void* dx, float* dw, const void* resid, hipStream_t st) {
+    const int64_t H = x.H, I = x.I;
+    if (dx) {
+        Epilogue c = act_out(dx, layout, T, I);
+        c.resid = resid;
+        DM_TRY(launch_gemm(x.dtype,
+                           gemm(T, I, H * n, 1, opnd(dproj, true, linear_map(ld)),
+                                opnd(w, false, make_map((uint32_t)n, 0, H * I, I, 0)), c),
+                           st));
+    }
+    return launch_gemm(x.dtype,
+                       gemm(H * n, I, T, 1, opnd(dproj, false, linear_map(ld)), act_kn(in, layout, T, I),
+                            epi(dw, make_map((uint32_t)n, 0, H * I, I, 0), linear_map(1), true, true)),
+                       st);
+}
+
+int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqkv, const dm_layer_params* prm,
+                      void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st) {
+    const int64_t H = x.H, I = x.I, P = x.P, T = x.Tq;
+    const IdxMap wmap = make_map((uint32_t)P, (uint32_t)H, H * I, I, 0);
+    Epilogue c = act_out(dx, layout, T, I);
+    c.resid = resid;
+    Operand Bw = opnd3(prm->wq, prm->wk, prm->wv, false, wmap);
+    {
+        TraceScope t_("B18 qkv_dx", st);
+        DM_TRY(launch_gemm(x.dtype, gemm(T, I, 3 * H * P, 1, opnd(dqkv, true, linear_map(3 * H * P)), Bw, c), st));
+    }
+    Epilogue cw = epi(g->dwq, wmap, linear_map(1), true, true);
+    cw.ptr[1] = g->dwk; cw.ptr[2] = g->dwv; cw.nseg = 3; cw.seg_on_m = 1;
+    TraceScope t_("B19 qkv_dw", st);
+    return launch_gemm(x.dtype,
+                       gemm(3 * H * P, I, T, 1, opnd(dqkv, false, linear_map(3 * H * P)), act_kn(in, layout, T, I),
+                            cw),
+                       st);
+}
+
+}  // namespace
+
+extern "C" {
+
+// ------------------------------------------------------------ encoder layer
+int encoder_layer_sizes(const dm_layer_desc* d, size_t* saved_bytes, size_t* fwd_ws_bytes, size_t* bwd_ws_bytes) {
+    DM_TRY(check_desc(d, true));
+    EncPlan e = plan_encoder(dims_of(d));
+    if (saved_bytes) *saved_bytes = e.saved_total;
+    if (fwd_ws_bytes) *fwd_ws_bytes = e.fwd_total;
+    if (bwd_ws_bytes) *bwd_ws_bytes = e.bwd_total;
+    return DM_OK;
+}
+
+int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t* bytes) {
+    DM_TRY(check_desc(d, true));
+    const Dims x = dims_of(d);
+    EncPlan e = plan_encoder(x);
+    const size_t es = x.es;
+    size_t o = 0, b = 0;
+    switch (id) {
+        case DM_SAVED_QKV: o = e.m.q; b = 3 * es * x.N; break;
+        case DM_SAVED_PROB: o = e.m.prob; b = es * x.S; break;
+        case DM_SAVED_ALPHA: o = e.m.alpha; b = es * x.S; break;
+        case DM_SAVED_GAMMA: o = e.m.gamma; b = es * x.N; break;
+        case DM_SAVED_XHAT1: o = e.xhat1; b = es * x.N; break;
+        case DM_SAVED_RSTD1: o = e.rstd1; b = 4 * x.Tq; break;
+        case DM_SAVED_Y1: o = e.y1; b = es * x.N; break;
+        case DM_SAVED_H: o = e.h; b = es * x.Tq * x.F; break;
+        case DM_SAVED_A: o = e.a; b = es * x.Tq * x.F; break;
+        case DM_SAVED_XHAT2: o = e.xhat2; b = es * x.N; break;
+        case DM_SAVED_RSTD2: o = e.rstd2; b = 4 * x.Tq; break;
+        default: return set_error(DM_ERR_ARG, "unknown saved tensor id %d", id);
+    }
+    if (offset) *offset = o;
+    if (bytes) *bytes = b;
+    return DM_OK;
+}
+
+int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* x_in, void* y, void* saved,
+                      void* ws, size_t ws_bytes, void* stream) {
+    DM_TRY(check_desc(d, true));
+    DM_TRY(check_params(prm, true));
+    DM_TRY(need(x_in, "x")); DM_TRY(need(y, "y")); DM_TRY(need(saved, "saved")); DM_TRY(need(ws, "ws"));
+    const Dims x = dims_of(d);
+    const EncPlan e = plan_encoder(x);
+    if (ws_bytes < e.fwd_total) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const int dt = x.dtype;
+    const int64_t T = x.Tq;
+    void *q = B8(saved, e.m.q), *k = B8(saved, e.m.k), *v = B8(saved, e.m.v);
+    void *prob = B8(saved, e.m.prob), *alpha = B8(saved, e.m.alpha), *gamma = B8(saved, e.m.gamma);
+    void *xhat1 = B8(saved, e.xhat1), *y1 = B8(saved, e.y1), *hbuf = B8(saved, e.h), *abuf = B8(saved, e.a);
+    void* xhat2 = B8(saved, e.xhat2);
+    float *rstd1 = (float*)B8(saved, e.rstd1), *rstd2 = (float*)B8(saved, e.rstd2);
+    void *beta = B8(ws, e.m.beta), *ao = B8(ws, e.ao), *o = B8(ws, e.o);
+
+    // Q, K, V (algebraically fused) with the input bias
+    {
+        TraceScope t_("F1 qkv", st);
+        DM_TRY(project_fused(x, DM_BJI, x_in, prm, q, k, v, st));
+    }
+    // QK^T, scaled softmax + dropout, Gamma
+    DM_TRY(attention_core_fwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), q, k, v, beta, prob,
+                              alpha, gamma, st));
+    // Out
+    DM_TRY(out_projection(x, gamma, prm->wo, nullptr, ao, DM_BJI, st));
+    // bias + dropout + residual + LayerNorm 1
+    {
+        TraceScope t_("F6 bdrln1", st);
+        run_bdrln_fwd(dt, T, (int)x.I, ao, prm->bo, x_in, prm->g1, prm->be1, d->ln_eps,
+                      make_drop(d->p_attn_out, d->seed, 1, d->layer_id), y1, xhat1, rstd1, st);
+    }
+    DM_TRY(check_launch("bdrln 1"));
+    // Linear 1
+    {
+        TraceScope t_("F7 linear1", st);
+        DM_TRY(launch_gemm(dt,
+                           gemm(T, x.F, x.I, 1, opnd(y1, true, linear_map(x.I)),
+                                opnd(prm->w1, true, linear_map(x.I)),
+                                epi(hbuf, linear_map(x.F), linear_map(1), true, false)),
+                           st));
+    }
+    // bias + activation (+ dropout)
+    {
+        TraceScope t_("F8 bias_act", st);
+        run_bias_act_fwd(dt, T, (int)x.F, hbuf, prm->b1, d->act, make_drop(d->p_ffn_act, d->seed, 3, d->layer_id),
+                         abuf, st);
+    }
+    DM_TRY(check_launch("bias+activation"));
+    // Linear 2
+    {
+        TraceScope t_("F9 linear2", st);
+        DM_TRY(launch_gemm(dt,
+                           gemm(T, x.I, x.F, 1, opnd(abuf, true, linear_map(x.F)),
+                                opnd(prm->w2, true, linear_map(x.F)),
+                                epi(o, linear_map(x.I), linear_map(1), true, false)),
+                           st));
+    }
+    // bias + dropout + residual + LayerNorm 2
+    TraceScope t10("F10 bdrln2", st);
+    run_bdrln_fwd(dt, T, (int)x.I, o, prm->b2, y1, prm->g2, prm->be2, d->ln_eps,
+                  make_drop(d->p_ffn_out, d->seed, 2, d->layer_id), y, xhat2, rstd2, st);
+    return check_launch("bdrln 2");
+}
+
+int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* x_in, const void* saved,
+                      const void* dy, void* dx, const dm_layer_grads* g, void* ws, size_t ws_bytes, void* stream) {
+    DM_TRY(check_desc(d, true));
+    DM_TRY(check_params(prm, true));
+    DM_TRY(check_grads(g, true));
+    DM_TRY(need(x_in, "x")); DM_TRY(need(saved, "saved")); DM_TRY(need(dy, "dy")); DM_TRY(need(dx, "dx"));
+    DM_TRY(need(ws, "ws"));
+    const Dims x = dims_of(d);
+    const EncPlan e = plan_encoder(x);
+    if (ws_bytes < e.bwd_total) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const int dt = x.dtype;
+    const int64_t T = x.Tq, I = x.I, F = x.F;
+    const int es = x.es;
+    const void *q = B8(saved, e.m.q), *k = B8(saved, e.m.k), *v = B8(saved, e.m.v);
+    const void *prob = B8(saved, e.m.prob), *alpha = B8(saved, e.m.alpha), *gamma = B8(saved, e.m.gamma);
+    const void *xhat1 = B8(saved, e.xhat1), *y1 = B8(saved, e.y1), *hbuf = B8(saved, e.h), *abuf = B8(saved, e.a);
+    const void* xhat2 = B8(saved, e.xhat2);
+    const float *rstd1 = (const float*)B8(saved, e.rstd1), *rstd2 = (const float*)B8(saved, e.rstd2);
+    void *dS2 = B8(ws, e.dS2), *dO = B8(ws, e.dO), *dA = B8(ws, e.dA), *dH = B8(ws, e.dH);
+    void *dY1f = B8(ws, e.dY1f), *dS1 = B8(ws, e.dS1), *dAO = B8(ws, e.dAO);
+    void *dgamma = B8(ws, e.m.dgamma), *dalpha = B8(ws, e.m.dalpha), *dbeta = B8(ws, e.m.dbeta);
+    void* dqkv = B8(ws, e.m.dq);
+    float* part = (float*)B8(ws, e.m.part);
+    const int nb = colsum_blocks(T);
+
+    // LayerNorm-2 scale/shift grads, LayerNorm-2 dX, dropout dX, Linear-2 bias grad
+    LnBwdArgs l2{};
+    l2.dtype = dt; l2.rows = T; l2.cols = (int)I; l2.dya = dy; l2.xhat = xhat2; l2.gamma = prm->g2; l2.rstd = rstd2;
+    l2.dp = make_drop(d->p_ffn_out, d->seed, 2, d->layer_id); l2.ds = dS2; l2.dsub = dO; l2.part = part;
+    l2.want_dsub_sum = 1;
+    {
+        TraceScope t_("B1-2 ln2_bwd", st);
+        run_ln_bwd(l2, st);
+    }
+    {
+        TraceScope t_("B1-2 colsum", st);
+        run_colsum_finish(T, (int)I, part, g->dg2, st);
+        run_colsum_finish(T, (int)I, part + (size_t)nb * I, g->dbe2, st);
+        run_colsum_finish(T, (int)I, part + (size_t)2 * nb * I, g->db2, st);
+    }
+    DM_TRY(check_launch("LayerNorm-2 backward"));
+    // Linear 2 dX and dW
+    {
+        TraceScope t_("B3 linear2_dx", st);
+        DM_TRY(launch_gemm(dt,
+                           gemm(T, F, I, 1, opnd(dO, true, linear_map(I)), opnd(prm->w2, false, linear_map(F)),
+                                epi(dA, linear_map(F), linear_map(1), true, false)),
+                           st));
+    }
+    {
+        TraceScope t_("B4 linear2_dw", st);
+        DM_TRY(launch_gemm(dt,
+                           gemm(I, F, T, 1, opnd(dO, false, linear_map(I)), opnd(abuf, false, linear_map(F)),
+                                epi(g->dw2, linear_map(F), linear_map(1), true, true)),
+                           st));
+    }
+    // dropout / activation backward, Linear-1 bias grad
+    {
+        TraceScope t_("B5 act_bwd", st);
+        run_act_bwd(dt, T, (int)F, dA, hbuf, prm->b1, d->act, make_drop(d->p_ffn_act, d->seed, 3, d->layer_id), dH,
+                    part, st);
+    }
+    {
+        TraceScope t_("B5 colsum", st);
+        run_colsum_finish(T, (int)F, part, g->db1, st);
+    }
+    DM_TRY(check_launch("activation backward"));
+    // Linear 1 dX and dW
+    {
+        TraceScope t_("B6 linear1_dx", st);
+        DM_TRY(launch_gemm(dt,
+                           gemm(T, I, F, 1, opnd(dH, true, linear_map(F)), opnd(prm->w1, false, linear_map(I)),
+                                epi(dY1f, linear_map(I), linear_map(1), true, false)),
+                           st));
+    }
+    {
+        TraceScope t_("B7 linear1_dw", st);
+        DM_TRY(launch_gemm(dt,
+                           gemm(F, I, T, 1, opnd(dH, false, linear_map(F)), opnd(y1, false, linear_map(I)),
+                                epi(g->dw1, linear_map(I), linear_map(1), true, true)),
+                           st));
+    }
+    // residual + LayerNorm-1 scale/shift grads, LayerNorm-1 dX, dropout dX, output-bias grad
+    LnBwdArgs l1{};
+    l1.dtype = dt; l1.rows = T; l1.cols = (int)I; l1.dya = dY1f; l1.dyb = dS2; l1.xhat = xhat1; l1.gamma = prm->g1;
+    l1.rstd = rstd1; l1.dp = make_drop(d->p_attn_out, d->seed, 1, d->layer_id); l1.ds = dS1; l1.dsub = dAO;
+    l1.part = part; l1.want_dsub_sum = 1;
+    {
+        TraceScope t_("B8-10 ln1_bwd", st);
+        run_ln_bwd(l1, st);
+    }
+    {
+        TraceScope t_("B8-10 colsum", st);
+        run_colsum_finish(T, (int)I, part, g->dg1, st);
+        run_colsum_finish(T, (int)I, part + (size_t)nb * I, g->dbe1, st);
+        run_colsum_finish(T, (int)I, part + (size_t)2 * nb * I, g->dbo, st);
+    }
+    DM_TRY(check_launch("LayerNorm-1 backward"));
+    // attention backward into the token-major [T][3][H][P] gradient
+    const int64_t ld = 3 * I;
+    DM_TRY(attention_core_bwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), dAO, DM_BJI, q, k, v,
+                              prob, alpha, gamma, prm->wo, g->dwo, dgamma, dalpha, dbeta, dqkv, ld,
+                              B8(dqkv, (size_t)es * I), ld, B8(dqkv, (size_t)es * 2 * I), ld, st));
+    // Q, K, V dX (fused) + encoder-input residual; Q, K, V dW (fused)
+    DM_TRY(project_fused_bwd(x, DM_BJI, x_in, dqkv, prm, dx, g, dS1, st));
+    // input-bias grads
+    TraceScope t20("B20 qkv_bias_grad", st);
+    run_colsum_partial(dt, T, (int)(3 * I), dqkv, part, st);
+    run_colsum_finish_qkv(T, (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
+    return check_launch("input-bias backward");
+}
+
+// ------------------------------------------------------------ attention only
+int mha_sizes(const dm_layer_desc* d, size_t* saved_bytes, size_t* fwd_ws_bytes, size_t* bwd_ws_bytes) {
+    DM_TRY(check_desc(d, false));
+    MhaSizes s = plan_mha(dims_of(d), d->self_attention != 0);
+    if (saved_bytes) *saved_bytes = s.saved;
+    if (fwd_ws_bytes) *fwd_ws_bytes = s.fwd;
+    if (bwd_ws_bytes) *bwd_ws_bytes = s.bwd;
+    return DM_OK;
+}
+
+int mha_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin, const void* kin, const void* vin,
+            void* out, void* saved, void* ws, size_t ws_bytes, void* stream) {
+    DM_TRY(check_desc(d, false));
+    DM_TRY(check_params(prm, false));
+    const bool fused = d->self_attention != 0;
+    DM_TRY(need(qin, "q")); DM_TRY(need(out, "out")); DM_TRY(need(saved, "saved")); DM_TRY(need(ws, "ws"));
+    if (fused) {
+        if ((kin && kin != qin) || (vin && vin != qin))
+            return set_error(DM_ERR_ARG, "self-attention needs k and v NULL or equal to q");
+    } else {
+        DM_TRY(need(kin, "k")); DM_TRY(need(vin, "v"));
+    }
+    const Dims x = dims_of(d);
+    const MhaSizes s = plan_mha(x, fused);
+    if (ws_bytes < s.fwd) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);
+    if (fused) {
+        TraceScope t_("F1 qkv", st);
+        DM_TRY(project_fused(x, x.layout, qin, prm, q, k, v, st));
+    } else {
+        TraceScope t_("F1 q,k,v", st);
+        DM_TRY(project(x, x.layout, qin, x.J, x.P, prm->wq, prm->bq, q, st));
+        DM_TRY(project(x, x.layout, kin, x.K, x.P, prm->wk, prm->bk, k, st));
+        DM_TRY(project(x, x.layout, vin, x.K, x.W, prm->wv, prm->bv, v, st));
+    }
+    DM_TRY(attention_core_fwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), q, k, v,
+                              B8(ws, s.p.beta), B8(saved, s.p.prob), B8(saved, s.p.alpha), B8(saved, s.p.gamma),
+                              st));
+    return out_projection(x, B8(saved, s.p.gamma), prm->wo, prm->bo, out, x.layout, st);
+}
+
+int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin, const void* kin, const void* vin,
+            const void* saved, const void* dout, void* dq, void* dk, void* dv, const dm_layer_grads* g, void* ws,
+            size_t ws_bytes, void* stream) {
+    DM_TRY(check_desc(d, false));
+    DM_TRY(check_params(prm, false));
+    DM_TRY(check_grads(g, false));
+    const bool fused = d->self_attention != 0;
+    DM_TRY(need(qin, "q")); DM_TRY(need(saved, "saved")); DM_TRY(need(dout, "dout")); DM_TRY(need(dq, "dq"));
+    DM_TRY(need(ws, "ws"));
+    if (fused) {
+        if (dk || dv) return set_error(DM_ERR_ARG, "self-attention writes the total input gradient to dq; dk, dv must be NULL");
+        if ((kin && kin != qin) || (vin && vin != qin))
+            return set_error(DM_ERR_ARG, "self-attention needs k and v NULL or equal to q");
+    } else {
+        DM_TRY(need(kin, "k")); DM_TRY(need(vin, "v")); DM_TRY(need(dk, "dk")); DM_TRY(need(dv, "dv"));
+    }
+    const Dims x = dims_of(d);
+    const MhaSizes s = plan_mha(x, fused);
+    if (ws_bytes < s.bwd) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const int dt = x.dtype;
+    const int es = x.es;
+    const void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);
+    void* bq = B8(ws, s.p.dq);
+    void* bk = fused ? B8(ws, s.p.dq + (size_t)es * x.H * x.P) : B8(ws, s.p.dk);
+    void* bv = fused ? B8(ws, s.p.dq + (size_t)es * 2 * x.H * x.P) : B8(ws, s.p.dv);
+    float* part = (float*)B8(ws, s.p.part);
+
+    // output-bias grad
+    TraceScope t10("B10 out_bias_grad", st);
+    if (x.layout == DM_BJI) {
+        run_colsum_partial(dt, x.Tq, (int)x.I, dout, part, st);
+        run_colsum_finish(x.Tq, (int)x.I, part, g->dbo, st);
+    } else {
+        run_rowsum(dt, x.I, (int)x.Tq, dout, g->dbo, st);
+    }
+    DM_TRY(check_launch("output-bias backward"));
+    t10.stop();
+    DM_TRY(attention_core_bwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), dout, x.layout, q, k, v,
+                              B8(saved, s.p.prob), B8(saved, s.p.alpha), B8(saved, s.p.gamma), prm->wo, g->dwo,
+                              B8(ws, s.p.dgamma), B8(ws, s.p.dalpha), B8(ws, s.p.dbeta), bq, s.p.ldq, bk, s.p.ldk, bv,
+                              s.p.ldv, st));
+    if (fused) {
+        DM_TRY(project_fused_bwd(x, x.layout, qin, bq, prm, dq, g, nullptr, st));
+        TraceScope t_("B20 qkv_bias_grad", st);
+        run_colsum_partial(dt, x.Tq, (int)(3 * x.H * x.P), bq, part, st);
+        run_colsum_finish_qkv(x.Tq, (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
+    } else {
+        TraceScope t_("B18-20 q,k,v_bwd", st);
+        DM_TRY(project_bwd(x, x.layout, qin, x.Tq, x.P, bq, s.p.ldq, prm->wq, dq, g->dwq, nullptr, st));
+        DM_TRY(project_bwd(x, x.layout, kin, x.Tk, x.P, bk, s.p.ldk, prm->wk, dk, g->dwk, nullptr, st));
+        DM_TRY(project_bwd(x, x.layout, vin, x.Tk, x.W, bv, s.p.ldv, prm->wv, dv, g->dwv, nullptr, st));
+        run_colsum_partial(dt, x.Tq, (int)(x.H * x.P), bq, part, st);
+        run_colsum_finish_qkv(x.Tq, (int)x.H, (int)x.P, 1, part, g->dbq, nullptr, nullptr, st);
+        run_colsum_partial(dt, x.Tk, (int)(x.H * x.P), bk, part, st);
+        run_colsum_finish_qkv(x.Tk, (int)x.H, (int)x.P, 1, part, g->dbk, nullptr, nullptr, st);
+        run_colsum_partial(dt, x.Tk, (int)(x.H * x.W), bv, part, st);
+        run_colsum_finish_qkv(x.Tk, (int)x.H, (int)x.W, 1, part, g->dbv, nullptr, nullptr, st);
+    }
+    return check_launch("input-bias backward");
+}
+
+}  // extern "C"

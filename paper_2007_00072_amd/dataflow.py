@@ -1,0 +1,106 @@
+"""Algorithmic work of every launch in the encoder layer (the analogue of
+the paper's per-operator flop / I/O analysis, Table 3).
+
+For each operator the model counts flop (2 per multiply-add of a
+contraction; element-wise work is not counted as flop) and the minimum
+bytes it must move: every input read once and every output written once,
+in the storage dtype (float32 for statistics and parameter gradients).
+Dropout masks cost no bytes (they are regenerated).  Scratch traffic of
+the two-stage column reductions is not algorithmic and appears as zero.
+
+Labels equal those the library records in its per-launch timing.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict
+
+from .inputs import Shape
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_PEAK_TFLOPS = {"f16": 2516.6, "bf16": 2516.6, "f32": 157.3}   # dense MFMA / fp32 vector
+
+
+@dataclass
+class Work:
+    flop: float
+    bytes: float
+    bound: str     # "mfma" or "hbm"
+
+
+def ridge(dtype: str) -> float:
+    return MFMA_PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def _gemm(M, N, K, a_el, b_el, c_el, es, c_es=None, dtype="f16", extra=0.0) -> Work:
+    c_es = es if c_es is None else c_es
+    flop = 2.0 * M * N * K
+    byt = (a_el + b_el) * es + c_el * c_es + extra
+    return Work(flop, byt, "mfma" if flop / byt > ridge(dtype) else "hbm")
+
+
+def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
+    """Work of each labelled launch group of one encoder-layer forward + backward."""
+    es = 4 if dtype == "f32" else 2
+    T, I, F, H, P, W = s.B * s.J, s.I, s.F, s.H, s.P, s.W
+    Z, J, K = s.B * s.H, s.J, s.K
+    N, S, Fh = T * I, s.B * s.H * s.J * s.K, T * F
+    g = lambda *a, **k: _gemm(*a, es=es, dtype=dtype, **k)
+    m = lambda b: Work(0.0, float(b), "hbm")
+    w = {}
+    # forward
+    w["F1 qkv"] = g(T, 3 * I, I, N, 3 * I * I, 3 * N, extra=3 * I * es)
+    w["F2 qkt"] = _att(Z, J, K, P, es, dtype, S, N)
+    w["F3 softmax"] = m(3 * S * es)
+    w["F4 gamma"] = _att(Z, J, W, K, es, dtype, S, N)
+    w["F5 out"] = g(T, I, I, N, I * I, N)
+    w["F6 bdrln1"] = m(4 * N * es + 4 * T + 3 * I * es)
+    w["F7 linear1"] = g(T, F, I, N, F * I, Fh)
+    w["F8 bias_act"] = m(2 * Fh * es + F * es)
+    w["F9 linear2"] = g(T, I, F, Fh, I * F, N)
+    w["F10 bdrln2"] = m(4 * N * es + 4 * T + 3 * I * es)
+    # backward
+    w["B1-2 ln2_bwd"] = m(4 * N * es + 4 * T + I * es + 3 * I * 4)
+    w["B1-2 colsum"] = m(0)
+    w["B3 linear2_dx"] = g(T, F, I, N, I * F, Fh)
+    w["B4 linear2_dw"] = g(I, F, T, N, Fh, I * F, c_es=4)
+    w["B5 act_bwd"] = m(3 * Fh * es + F * es + F * 4)
+    w["B5 colsum"] = m(0)
+    w["B6 linear1_dx"] = g(T, I, F, Fh, F * I, N)
+    w["B7 linear1_dw"] = g(F, I, T, Fh, N, F * I, c_es=4)
+    w["B8-10 ln1_bwd"] = m(5 * N * es + 4 * T + I * es + 3 * I * 4)
+    w["B8-10 colsum"] = m(0)
+    w["B11 out_dx"] = g(T, I, I, N, I * I, N)
+    w["B12 out_dw"] = g(I, I, T, N, N, I * I, c_es=4)
+    w["B13 gamma_dx1"] = _att(Z, J, K, W, es, dtype, S, N)
+    w["B14 gamma_dx2"] = _att(Z, K, W, J, es, dtype, S, N)
+    w["B15 softmax_bwd"] = m(3 * S * es)
+    w["B16 qkt_dx1"] = _att(Z, J, P, K, es, dtype, S, N)
+    w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
+    w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read
+    w["B19 qkv_dw"] = g(3 * I, I, T, 3 * N, N, 3 * I * I, c_es=4)
+    w["B20 qkv_bias_grad"] = m(3 * N * es + 3 * I * 4)
+    return w
+
+
+def _att(Z, M, N, K, es, dtype, S, Ntok) -> Work:
+    """Batched attention contraction: one S-sized operand and two N-sized ones."""
+    flop = 2.0 * Z * M * N * K
+    byt = (S + 2 * Ntok) * es
+    return Work(flop, byt, "mfma" if flop / byt > ridge(dtype) else "hbm")
+
+
+def contraction_gflop(s: Shape) -> Dict[str, float]:
+    """Per-row contraction Gflop in the order of the paper's Table 3 rows."""
+    T, I, F = s.B * s.J, s.I, s.F
+    att = 2.0 * s.B * s.H * s.J * s.K * s.P / 1e9
+    qkv = 2.0 * T * 3 * I * I / 1e9
+    out = 2.0 * T * I * I / 1e9
+    lin = 2.0 * T * F * I / 1e9
+    return {
+        "fwd Q,K,V": qkv, "fwd QK^T": att, "fwd Gamma": att, "fwd Out": out,
+        "fwd Linear1": lin, "fwd Linear2": lin,
+        "bwd Linear2 dX": lin, "bwd Linear2 dW": lin, "bwd Linear1 dX": lin, "bwd Linear1 dW": lin,
+        "bwd Out dX": out, "bwd Out dW": out, "bwd Gamma dX1": att, "bwd Gamma dX2": att,
+        "bwd QK^T dX1": att, "bwd QK^T dX2": att, "bwd Q,K,V dX": qkv, "bwd Q,K,V dW": qkv,
+    }

@@ -1,0 +1,136 @@
+"""The C ABI on a machine without a GPU: the library loads, exports every
+function include/dmtx.h declares, and rejects bad arguments before any
+launch (validation is host code, so these calls never reach the device)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dmtx.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    so = os.path.join(ROOT, "paper_2007_00072_amd", "libdmtx.so")
+    if not os.path.exists(so):
+        from paper_2007_00072_amd import build
+        build.build()
+    from paper_2007_00072_amd import lib as L
+    return L
+
+
+def header_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w]*\s*\*?\s*([A-Za-z_]\w*)\s*\(", txt, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "while", "sizeof")))
+
+
+def test_header_declares_expected_entry_points():
+    names = header_functions()
+    for n in ("encoder_layer_fwd", "encoder_layer_bwd", "mha_fwd", "mha_bwd", "bdrln_fwd",
+              "softmax_dropout_fwd", "softmax_dropout_bwd", "dropout_mask", "dm_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_header_symbol(lib):
+    so = C.CDLL(lib.LIB_PATH)
+    missing = [n for n in header_functions() if not hasattr(so, n)]
+    assert not missing, missing
+    assert sorted(lib.EXPORTED) == header_functions()
+
+
+def _desc(lib, **kw):
+    from paper_2007_00072_amd.inputs import WORKLOADS
+    d = lib.make_desc(WORKLOADS["bert_large_f16"].shape, "f16", p_attn=0.1, p_attn_out=0.1, p_ffn_out=0.1)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+def test_sizes_valid(lib):
+    d = _desc(lib)
+    saved, fwd, bwd = lib.encoder_layer_sizes(d)
+    N, S, Fh = 8 * 512 * 1024, 8 * 16 * 512 * 512, 8 * 512 * 4096
+    assert saved >= 2 * (7 * N + 2 * S + 2 * Fh)       # Q,K,V,gamma,xhat1,y1,xhat2 + prob,alpha + H,A
+    assert fwd >= 2 * (S + 2 * N)
+    assert bwd >= 2 * (2 * S + 9 * N + 2 * Fh)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("I", 1004, 2), ("I", 1000, 1), ("W", 32, 1), ("K", 256, 1), ("dtype", 7, 2), ("layout", 1, 2),
+    ("p_attn", 1.0, 1), ("p_ffn_out", -0.1, 1), ("ln_eps", 0.0, 1), ("F", 100, 2), ("B", 0, 1),
+    ("act", 9, 2), ("I", 4096, 2)])
+def test_sizes_reject_bad_descriptors(lib, field, value, code):
+    d = _desc(lib, **{field: value})
+    if field == "I" and value == 4096:
+        d.H, d.P, d.W = 64, 64, 64
+    with pytest.raises(lib.DmError) as e:
+        lib.encoder_layer_sizes(d)
+    assert e.value.code == code
+    assert lib.dm_last_error()
+
+
+def test_forward_rejects_null_misaligned_and_small_workspace(lib):
+    d = _desc(lib)
+    prm = lib.make_params({n: 0x10000 for n in lib._PNAMES})
+    saved, fwd, _ = lib.encoder_layer_sizes(d)
+    with pytest.raises(lib.DmError) as e:
+        lib.encoder_layer_fwd(d, prm, None, 0x20000, 0x30000, 0x40000, fwd, stream=None)
+    assert e.value.code == lib.DM_ERR_ARG and "x" in str(e.value)
+    with pytest.raises(lib.DmError) as e:
+        lib.encoder_layer_fwd(d, prm, 0x10008, 0x20000, 0x30000, 0x40000, fwd, stream=None)
+    assert e.value.code == lib.DM_ERR_ARG and "aligned" in str(e.value)
+    with pytest.raises(lib.DmError) as e:
+        lib.encoder_layer_fwd(d, prm, 0x10000, 0x20000, 0x30000, 0x40000, fwd - 1, stream=None)
+    assert e.value.code == lib.DM_ERR_WORKSPACE
+    bad = lib.make_params({n: (0x10000 if n != "w1" else None) for n in lib._PNAMES})
+    with pytest.raises(lib.DmError) as e:
+        lib.encoder_layer_fwd(d, bad, 0x10000, 0x20000, 0x30000, 0x40000, fwd, stream=None)
+    assert "w1" in str(e.value)
+
+
+def test_backward_rejects_missing_grads(lib):
+    d = _desc(lib)
+    prm = lib.make_params({n: 0x10000 for n in lib._PNAMES})
+    g = lib.make_grads({n: (0x10000 if n != "g2" else None) for n in lib._PNAMES})
+    _, _, bwd = lib.encoder_layer_sizes(d)
+    with pytest.raises(lib.DmError) as e:
+        lib.encoder_layer_bwd(d, prm, 0x10000, 0x20000, 0x30000, 0x40000, g, 0x50000, bwd, stream=None)
+    assert "dg2" in str(e.value)
+
+
+def test_mha_validation(lib):
+    from paper_2007_00072_amd.inputs import Shape
+    d = lib.make_desc(Shape(B=2, J=64, K=72, H=4, P=32, W=32, I=128), "f16", layout="ibj", self_attention=True)
+    with pytest.raises(lib.DmError):
+        lib.mha_sizes(d)          # self-attention needs J == K
+    d.self_attention = 0
+    lib.mha_sizes(d)
+    prm = lib.make_params({n: 0x10000 for n in lib._PNAMES[:8]})
+    s, f, b = lib.mha_sizes(d)
+    with pytest.raises(lib.DmError) as e:
+        lib.mha_fwd(d, prm, 0x10000, None, 0x10000, 0x20000, 0x30000, 0x40000, f, stream=None)
+    assert "k" in str(e.value)
+
+
+def test_fused_op_validation(lib):
+    with pytest.raises(lib.DmError) as e:
+        lib.bdrln_fwd(1, 16, 100, 0x10000, 0x10000, 0x10000, 0x10000, 0x10000, 1e-5, None, 0x10000, None, None,
+                      stream=None)
+    assert e.value.code == lib.DM_ERR_UNSUPPORTED
+    with pytest.raises(lib.DmError) as e:
+        lib.softmax_dropout_fwd(1, 1, 1, 8, 64, 1.0, 0x10000, (1.5, 0, 0, 0), 0x10000, 0x10000, stream=None)
+    assert e.value.code == lib.DM_ERR_ARG
+    with pytest.raises(lib.DmError) as e:
+        lib.bias_grad(1, 64, 64, 0x10000, 0x10000, 0x10000, 16, stream=None)
+    assert e.value.code == lib.DM_ERR_WORKSPACE
+    with pytest.raises(lib.DmError) as e:
+        lib.dropout_mask(0, 0, 0, 0.1, 3, 8, 0x10000, stream=None)
+    assert e.value.code == lib.DM_ERR_ARG
+    with pytest.raises(lib.DmError) as e:
+        lib.contract(2, 1, 12, 16, 16, 1.0, 0x10000, 0, 0, 0x10000, 0, 0, None, 0x10000, 0, 0, stream=None)
+    assert e.value.code == lib.DM_ERR_UNSUPPORTED
+    assert lib.colsum_ws_bytes(4096, 1024) == 3 * 256 * 1024 * 4

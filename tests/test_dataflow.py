@@ -1,0 +1,32 @@
+"""The work model used for roofline reporting, pinned to the paper's
+Table 3 contraction flop counts (tests/golden/table3_contraction_gflop.json)."""
+import json
+import os
+
+import pytest
+
+from paper_2007_00072_amd import dataflow
+from paper_2007_00072_amd.inputs import WORKLOADS
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "table3_contraction_gflop.json")
+
+
+def test_contraction_gflop_matches_table3():
+    gold = json.load(open(GOLD))
+    got = dataflow.contraction_gflop(WORKLOADS["bert_large_f16"].shape)
+    for k, v in gold["rows"].items():
+        assert got[k] == pytest.approx(v, abs=6e-4), k
+    assert sum(got.values()) == pytest.approx(gold["total_tensor_contractions"], abs=2e-3)
+
+
+def test_layer_model_flops_consistent():
+    s = WORKLOADS["bert_large_f16"].shape
+    w = dataflow.encoder_layer(s, "f16")
+    total = sum(x.flop for x in w.values()) / 1e9
+    assert total == pytest.approx(sum(dataflow.contraction_gflop(s).values()), rel=1e-12)
+    # the projection / feed-forward contractions are MFMA-bound, attention and fused ops HBM-bound
+    assert w["F7 linear1"].bound == "mfma" and w["F1 qkv"].bound == "mfma"
+    assert w["F2 qkt"].bound == "hbm" and w["F3 softmax"].bound == "hbm"
+    # fused-operator algorithmic bytes: softmax fwd moves 3 S elements
+    S = s.B * s.H * s.J * s.K
+    assert w["F3 softmax"].bytes == 3 * S * 2
