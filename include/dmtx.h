@@ -253,10 +253,15 @@ int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t
  * C[z][m][n] = alpha * sum_k A[z][m][k] * B[z][k][n] (+ bias[n]) with
  * row-major operands, `a_trans` / `b_trans` selecting A stored [K][M] /
  * B stored [N][K]; C dtype = dtype (out_f32 = 1: float C).  Strides in
- * elements between batches: sa, sb, sc. */
+ * elements between batches: sa, sb, sc.  tile_cfg selects the block tile
+ * (0: 256x256, 1: 256x128, 2: 128x128, 3: 256x64, 4: 128x64; -1: chosen
+ * from the shape); splits > 1 splits k, using `ws` (ws_bytes >=
+ * splits*batch*M*N*4) for partial sums; splits = 0 chooses (no split
+ * without ws). */
 int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, float alpha,
              const void* A, int32_t a_trans, int64_t sa, const void* B, int32_t b_trans,
-             int64_t sb, const void* bias, void* C, int32_t out_f32, int64_t sc, void* stream);
+             int64_t sb, const void* bias, void* C, int32_t out_f32, int64_t sc,
+             int32_t tile_cfg, int32_t splits, void* ws, size_t ws_bytes, void* stream);
 
 /* ----------------------------------------------------- kernel timing
  * Optional per-launch timing for measurement: while enabled, every kernel

@@ -348,7 +348,8 @@ int dropout_mask(uint64_t seed, uint32_t site, uint32_t layer, float p, uint64_t
 
 int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, float alpha, const void* A,
              int32_t a_trans, int64_t sa, const void* B, int32_t b_trans, int64_t sb, const void* bias, void* C,
-             int32_t out_f32, int64_t sc, void* stream) {
+             int32_t out_f32, int64_t sc, int32_t tile_cfg, int32_t splits, void* ws, size_t ws_bytes,
+             void* stream) {
     DM_TRY(check_dtype(dtype));
     if (batch < 0 || M < 0 || N < 0 || K <= 0) return set_error(DM_ERR_ARG, "bad contraction shape");
     if ((int64_t)batch * M * N == 0) return DM_OK;
@@ -356,8 +357,17 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
         return set_error(DM_ERR_UNSUPPORTED, "M, N, K must be multiples of 8");
     DM_TRY(check_ptr(A, "A")); DM_TRY(check_ptr(B, "B")); DM_TRY(check_ptr(C, "C"));
     if (bias) DM_TRY(check_ptr(bias, "bias"));
+    if (tile_cfg < -1 || tile_cfg > 4) return set_error(DM_ERR_ARG, "tile_cfg %d outside [-1, 4]", tile_cfg);
+    if (splits < 0 || splits > 64) return set_error(DM_ERR_ARG, "splits %d outside [0, 64]", splits);
+    if (splits > 1 && (!ws || ws_bytes < gemm_split_ws_bytes(M, N, batch, splits)))
+        return set_error(DM_ERR_WORKSPACE, "split-k workspace too small");
+    if (ws) DM_TRY(check_ptr(ws, "ws"));
     if (dtype == DM_F32 && !out_f32) out_f32 = 1;
     GemmArgs g{};
+    g.cfg = tile_cfg;
+    g.splits = splits;
+    g.split_ws = (float*)ws;
+    g.split_cap = (int64_t)(ws_bytes / sizeof(float));
     g.M = M; g.N = N; g.K = K; g.batch = batch;
     g.a.ptr[0] = A; g.a.nseg = 1;
     g.a.kcontig = a_trans ? 0 : 1;

@@ -1,17 +1,27 @@
 // MFMA contraction kernel for gfx950 (fp16 / bf16 storage, fp32
 // accumulation) and a plain fp32 kernel for float32 layers.
 //
-// Block tile BM x BN, k-step BK, 256 threads = 4 wave64s in a 2 x 2 grid of
-// wave tiles.  Both operands are staged in LDS as [outer][k] (k contiguous,
-// row padded by 8 elements so the 16-byte fragment reads of 16 consecutive
-// rows hit distinct banks).  A k-contiguous operand is copied with 16-byte
-// loads; an outer-contiguous operand is loaded 4 k-rows x 8 outer elements
-// per thread and transposed in registers on its way to LDS, so every einsum
-// layout reaches the same inner loop without a separate transpose pass.
-// The next k-step's global loads are issued before the current step's
-// MFMAs (register prefetch + LDS double buffer, one barrier per step).
-// The epilogue stages the fp32 tile through LDS and writes 16-byte vectors
-// along whichever output index is contiguous.
+// Block tile BM x BN (256x256 down to 128x64), k-step 64, 4 or 8 wave64s in
+// a WGM x WGN grid of wave tiles, v_mfma_f32_16x16x32 inner products.
+//
+// LDS holds both operands as [outer][k] rows of 64 elements (8 chunks of
+// 16 bytes).  Chunk c of row r sits at position c ^ ((r >> 1) & 7): the
+// 16-byte fragment reads of 16 consecutive rows then cover all 64 banks
+// exactly once, and no padding is needed.
+//
+// A k-contiguous operand is copied to that layout with 16-byte loads; an
+// outer-contiguous operand is copied in its own [k][outer] order and its
+// fragments are read with the gfx950 LDS transpose read, so every einsum
+// layout reaches the MFMAs without a transpose pass.  Global loads run one or
+// two k-steps ahead of the MFMAs (one or two register sets, LDS double
+// buffer, one barrier per step).
+//
+// Tiles are numbered so that each of the 8 XCDs gets a contiguous run of
+// tile indices, walked in groups of rows for L2 reuse.  A split-K mode
+// writes float partial sums that a second kernel adds in a fixed order
+// (deterministic), for contractions with few output tiles and a long k.
+// The epilogue stages the fp32 tile through LDS in 64-column passes and
+// writes 16-byte vectors along whichever output index is contiguous.
 #include "gemm.hpp"
 #include "internal.hpp"
 
@@ -34,8 +44,9 @@ IdxMap make_map(uint32_t r0, uint32_t r1, int64_t s0, int64_t s1, int64_t s2) {
 
 namespace {
 
-constexpr int NT = 256;
-constexpr int PAD = 8;
+constexpr int BK = 64;  // k per step = 8 chunks of 8 elements
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
 template <typename T> struct Mfma;
 template <> struct Mfma<half_t> {
@@ -51,141 +62,216 @@ template <> struct Mfma<bf16_t> {
     }
 };
 
-// Loads one operand tile (R outer x BK) of k-step k0 into registers.
-template <typename T, int R, int BK, bool KC>
-struct TileLoader;
+template <typename T, int R, int NT, bool KC>
+struct Loader;
 
-// k-contiguous: each thread owns NV 16-byte vectors; row pointers are fixed
-// for the whole k loop.
-template <typename T, int R, int BK>
-struct TileLoader<T, R, BK, true> {
-    static constexpr int VPR = BK / 8;
-    static constexpr int NV = R * VPR / NT;
-    static_assert(NV * NT == R * VPR, "tile / thread mismatch");
+// k-contiguous operand: thread t owns 16-byte chunk (t & 7) of rows
+// t/8, t/8 + NT/8, ...; row pointers are fixed for the whole k loop.  Rows
+// past the operand's end read its first row and are zeroed by select, and
+// k past the end reads k = 0, so every load is unconditional.
+template <typename T, int R, int NT>
+struct Loader<T, R, NT, true> {
+    static constexpr int NV = R * 8 / NT;
+    static_assert(NV >= 1 && NV * NT == R * 8, "tile / thread mismatch");
+    typedef u32x4 Regs[NV];
     const T* rowp[NV];
-    u32x4 reg[NV];
-    int kv;
+    uint32_t valid;  // bit i: row i in range
 
-    __device__ __forceinline__ void init(const Operand& op, int outer0, int outer_max, int64_t boff) {
-        int tid = threadIdx.x;
-        kv = tid % VPR;
+    __device__ __forceinline__ void init(const Operand& op, int o0, int omax, int64_t boff) {
+        const int tid = threadIdx.x;
+        valid = 0;
+        int seg0 = 0;
+        const int64_t off0 = map_off(op.row, (uint32_t)(o0 < omax ? o0 : 0), op.nseg, &seg0);
+        const T* first = reinterpret_cast<const T*>(op.ptr[seg0]) + boff + off0;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            int r = tid / VPR + i * (NT / VPR);
-            int o = outer0 + r;
-            rowp[i] = nullptr;
-            if (o < outer_max) {
+            const int o = o0 + (tid >> 3) + i * (NT / 8);
+            rowp[i] = first;
+            if (o < omax) {
                 int seg = 0;
-                int64_t off = map_off(op.row, (uint32_t)o, op.nseg, &seg);
+                const int64_t off = map_off(op.row, (uint32_t)o, op.nseg, &seg);
                 rowp[i] = reinterpret_cast<const T*>(op.ptr[seg]) + boff + off;
+                valid |= 1u << i;
             }
         }
     }
-    __device__ __forceinline__ void load(const Operand&, int k0, int K) {
-        int k = k0 + kv * 8;
+    // Loads never consume their data here (a select on it would make the
+    // load wait at once); out-of-range lanes are zeroed when stored.
+    __device__ __forceinline__ void load(const Operand&, int k0, int kend, Regs& reg) const {
+        const int k = k0 + (threadIdx.x & 7) * 8;
+        const int kk = k < kend ? k : 0;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            u32x4 z = {0u, 0u, 0u, 0u};
-            reg[i] = (rowp[i] && k < K) ? *reinterpret_cast<const u32x4*>(rowp[i] + k) : z;
-        }
+        for (int i = 0; i < NV; ++i) reg[i] = *reinterpret_cast<const u32x4*>(rowp[i] + kk);
     }
-    __device__ __forceinline__ void store(T* lds) {
-        int tid = threadIdx.x;
+    // fragment of outer rows ob .. ob+15, k = kk .. kk+31 of this LDS stage:
+    // lane l reads row ob + (l & 15), chunk kk/8 + l/16 (one 16-byte read;
+    // 16 consecutive rows cover all 64 banks once under the swizzle)
+    __device__ __forceinline__ u32x4 frag(const T* lds, int ob, int kk, int lane) const {
+        const int r = ob + (lane & 15);
+        const int c = (kk >> 3) + (lane >> 4);
+        return *reinterpret_cast<const u32x4*>(lds + r * BK + swz(r, c) * 8);
+    }
+    __device__ __forceinline__ void store(T* lds, const Regs& reg, int k0, int kend) const {
+        const int tid = threadIdx.x, c = tid & 7;
+        const bool kin = k0 + c * 8 < kend;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            int r = tid / VPR + i * (NT / VPR);
-            *reinterpret_cast<u32x4*>(lds + r * (BK + PAD) + kv * 8) = reg[i];
+            const int r = (tid >> 3) + i * (NT / 8);
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            const bool ok = kin && ((valid >> i) & 1u);
+            *reinterpret_cast<u32x4*>(lds + r * BK + swz(r, c) * 8) = ok ? reg[i] : z;
         }
     }
 };
 
-// outer-contiguous: each thread owns NB blocks of 4 k-rows x 8 outer
-// elements; row (k) addresses are evaluated per step.
-template <typename T, int R, int BK>
-struct TileLoader<T, R, BK, false> {
-    static constexpr int KB = 4;
-    static constexpr int OG = R / 8;
-    static constexpr int NB = (BK / KB) * OG / NT;
-    static_assert(NB * NT == (BK / KB) * OG, "tile / thread mismatch");
-    u32x4 reg[NB][KB];
-    int outer0, outer_max;
+// outer-contiguous operand: LDS keeps its natural [k][outer] order (rows
+// of R elements, 16-byte chunk c of row r at c ^ (2 * (r & 3))), filled by
+// plain 16-byte copies.  MFMA fragments are read with the gfx950 transpose
+// read ds_read_b64_tr_b16: within a group of 16 lanes, lane i receives
+// element i % 4 of the 8-byte pieces addressed by lanes i/4 + 4j, j = 0..3.
+// Lane s of group g addresses row k0 + 8g + s/4 (+4 for the second read),
+// outer elements 4(s % 4) .. +3, and so receives outer element s at k
+// values 8g .. 8g+7: exactly the k-contiguous fragment layout.
+template <typename T, int R, int NT>
+struct Loader<T, R, NT, false> {
+    static constexpr int CPR = R / 8;  // chunks per k-row
+    static constexpr int NV = BK * CPR / NT;
+    static_assert(NV >= 1 && NV * NT == BK * CPR && CPR >= 8, "tile / thread mismatch");
+    typedef u32x4 Regs[NV];
+    int o0, omax;
     int64_t boff;
 
-    __device__ __forceinline__ void init(const Operand&, int o0, int omax, int64_t b) {
-        outer0 = o0; outer_max = omax; boff = b;
+    __device__ __forceinline__ void init(const Operand&, int o0_, int omax_, int64_t b) {
+        o0 = o0_; omax = omax_; boff = b;
     }
-    __device__ __forceinline__ void load(const Operand& op, int k0, int K) {
-        int tid = threadIdx.x;
+    __device__ __forceinline__ void load(const Operand& op, int k0, int kend, Regs& reg) const {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            int blk = tid + b * NT;
-            int og = blk % OG, kb = blk / OG;
-            int o = outer0 + og * 8;
-#pragma unroll
-            for (int r = 0; r < KB; ++r) {
-                int k = k0 + kb * KB + r;
-                u32x4 z = {0u, 0u, 0u, 0u};
-                reg[b][r] = z;
-                if (k < K && o < outer_max) {
-                    int seg = 0;
-                    int64_t off = map_off(op.row, (uint32_t)k, op.nseg, &seg);
-                    const T* p = reinterpret_cast<const T*>(op.ptr[seg]) + boff + off + o;
-                    reg[b][r] = *reinterpret_cast<const u32x4*>(p);
-                }
-            }
+        for (int i = 0; i < NV; ++i) {
+            const int v = threadIdx.x + i * NT;
+            const int kr = v / CPR, c = v % CPR;
+            const int k = k0 + kr, o = o0 + c * 8;
+            const bool in = k < kend && o < omax;
+            int seg = 0;
+            const int64_t off = map_off(op.row, (uint32_t)(in ? k : 0), op.nseg, &seg);
+            reg[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(op.ptr[seg]) + boff + off +
+                                                     (in ? o : 0));
         }
     }
-    __device__ __forceinline__ void store(T* lds) {
-        int tid = threadIdx.x;
+    __device__ __forceinline__ void store(T* lds, const Regs& reg, int k0, int kend) const {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            int blk = tid + b * NT;
-            int og = blk % OG, kb = blk / OG;
-            // reg[b][r] holds outer elements og*8 .. og*8+7 of k-row r as 4
-            // dwords of 2 x 16 bits; emit, per outer element, its 4 k values.
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                uint32_t r0 = reg[b][0][w], r1 = reg[b][1][w], r2 = reg[b][2][w], r3 = reg[b][3][w];
-                u32x2 lo, hi;
-                lo[0] = (r0 & 0xFFFFu) | (r1 << 16);
-                lo[1] = (r2 & 0xFFFFu) | (r3 << 16);
-                hi[0] = (r0 >> 16) | (r1 & 0xFFFF0000u);
-                hi[1] = (r2 >> 16) | (r3 & 0xFFFF0000u);
-                int o = og * 8 + 2 * w;
-                *reinterpret_cast<u32x2*>(lds + o * (BK + PAD) + kb * KB) = lo;
-                *reinterpret_cast<u32x2*>(lds + (o + 1) * (BK + PAD) + kb * KB) = hi;
-            }
+        for (int i = 0; i < NV; ++i) {
+            const int v = threadIdx.x + i * NT;
+            const int kr = v / CPR, c = v % CPR;
+            const bool in = k0 + kr < kend && o0 + c * 8 < omax;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            *reinterpret_cast<u32x4*>(lds + kr * R + ((c ^ (2 * (kr & 3))) * 8)) = in ? reg[i] : z;
         }
+    }
+    // fragment of outer rows ob .. ob+15, k = kk .. kk+31 of this LDS stage
+    __device__ __forceinline__ u32x4 frag(const T* lds, int ob, int kk, int lane) const {
+        typedef short s4 __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) s4 lds_s4;
+        const int g = lane >> 4, sl = lane & 15;
+        const int r = kk + 8 * g + (sl >> 2);
+        const int c = (ob >> 3) + ((sl & 3) >> 1);
+        const T* p = lds + r * R + ((c ^ (2 * (sl >> 2))) * 8) + (sl & 1) * 4;
+        const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)p);
+        const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p + 4 * R));
+        u32x4 out;
+        out[0] = (uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
+        out[1] = (uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
+        out[2] = (uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
+        out[3] = (uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
+        return out;
     }
 };
 
-template <typename T, int BM, int BN, int BK, bool AKC, bool BKC>
-__global__ __launch_bounds__(NT) void gemm_mfma(GemmArgs g) {
-    constexpr int WM = BM / 2, WN = BN / 2;
+// ------------------------------------------------------------------ epilogue
+// Stores 8 outputs (along n if contig_n, else along m) starting at (m, n)
+// of batch z: alpha already applied; adds bias and resid, converts, maps.
+template <typename T>
+__device__ __forceinline__ void store_vec(const GemmArgs& g, int64_t coff, int m, int n, float vals[8]) {
+    const Epilogue& e = g.c;
+    if (e.bias[0]) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const uint32_t idx = e.bias_on_m ? (uint32_t)(e.contig_n ? m : m + q) : (uint32_t)(e.contig_n ? n + q : n);
+            int bseg = 0;
+            const int64_t bo = map_off(e.bias_map, idx, e.bias_nseg, &bseg);
+            vals[q] += to_f(reinterpret_cast<const T*>(e.bias[bseg])[bo]);
+        }
+    }
+    int sm = 0, sn = 0;
+    const int64_t off = coff + map_off(e.mmap, (uint32_t)m, e.seg_on_m ? e.nseg : 1, &sm) +
+                        map_off(e.nmap, (uint32_t)n, e.seg_on_m ? 1 : e.nseg, &sn);
+    const int seg = e.seg_on_m ? sm : sn;
+    if (e.out_f32) {
+        if (e.resid) {
+            float rv[8];
+            V8<float>::load(reinterpret_cast<const float*>(e.resid) + off, rv);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] += rv[q];
+        }
+        V8<float>::store(reinterpret_cast<float*>(e.ptr[seg]) + off, vals);
+    } else {
+        if (e.resid) {
+            float rv[8];
+            V8<T>::load(reinterpret_cast<const T*>(e.resid) + off, rv);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] += rv[q];
+        }
+        V8<T>::store(reinterpret_cast<T*>(e.ptr[seg]) + off, vals);
+    }
+}
+
+// Tile index of block `bid` among nt tiles: each XCD (blocks are dealt to
+// the 8 XCDs round-robin) gets a contiguous run of tile indices, and runs
+// are walked GM tile-rows at a time so neighbouring blocks share operands.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+    const int nt = tiles_m * tiles_n;
+    int t = bid;
+    if ((nt & 7) == 0) t = (bid & 7) * (nt >> 3) + (bid >> 3);
+    constexpr int GM = 4;
+    const int per_group = GM * tiles_n;
+    const int grp = t / per_group;
+    const int first = grp * GM;
+    const int gm = min(tiles_m - first, GM);
+    const int r = t - grp * per_group;
+    tm = first + r % gm;
+    tn = r / gm;
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH, bool AKC, bool BKC>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma(GemmArgs g) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int FM = WM / 16, FN = WN / 16;
-    constexpr int LDA = BK + PAD;
-    constexpr int AS = BM * LDA, BS = BN * LDA;
-    constexpr int CLD = BN + 4;
+    constexpr int AS = BM * BK, BS = BN * BK;
     constexpr int SMEM_AB = 2 * (AS + BS) * (int)sizeof(T);
-    constexpr int SMEM_C = BM * CLD * 4;
-    constexpr int SMEM = SMEM_AB > SMEM_C ? SMEM_AB : SMEM_C;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
+    constexpr int PW = 64, CLD = PW + 4;
+    static_assert(BM * CLD * 4 <= SMEM_AB, "epilogue staging does not fit");
+    static_assert(WM % 16 == 0 && WN % 16 == 0 && BN % PW == 0, "bad tile");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM_AB];
     T* As = reinterpret_cast<T*>(smem);
     T* Bs = As + 2 * AS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int tile = blockIdx.x;
-    const int tm = tile / g.tiles_n, tn = tile - tm * g.tiles_n;
+    const int wm = wave / WGN, wn = wave % WGN;
+    int tm, tn;
+    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
-    const uint32_t z = blockIdx.y;
+    const int splits = g.splits > 1 ? g.splits : 1;
+    const uint32_t z = blockIdx.y / splits;
+    const int sidx = blockIdx.y - (int)z * splits;
+    const int kb = splits > 1 ? sidx * g.kper : 0;
+    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
 
     int dummy = 0;
-    int64_t aoff = map_off(g.a.batch, z, 1, &dummy);
-    int64_t boff = map_off(g.b.batch, z, 1, &dummy);
+    const int64_t aoff = map_off(g.a.batch, z, 1, &dummy);
+    const int64_t boff = map_off(g.b.batch, z, 1, &dummy);
 
-    TileLoader<T, BM, BK, AKC> la;
-    TileLoader<T, BN, BK, BKC> lb;
+    Loader<T, BM, NT, AKC> la;
+    Loader<T, BN, NT, BKC> lb;
     la.init(g.a, m0, g.M, aoff);
     lb.init(g.b, n0, g.N, boff);
 
@@ -195,111 +281,179 @@ __global__ __launch_bounds__(NT) void gemm_mfma(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = (g.K + BK - 1) / BK;
-    la.load(g.a, 0, g.K);
-    lb.load(g.b, 0, g.K);
-    la.store(As);
-    lb.store(Bs);
-    __syncthreads();
-
     typedef typename Mfma<T>::frag frag;
-    const int lr = lane & 15, lk = (lane >> 4) * 8;
-    for (int s = 0; s < nk; ++s) {
-        const int buf = s & 1;
-        if (s + 1 < nk) {
-            la.load(g.a, (s + 1) * BK, g.K);
-            lb.load(g.b, (s + 1) * BK, g.K);
-        }
-        const T* Ab = As + buf * AS + (wm * WM + lr) * LDA + lk;
-        const T* Bb = Bs + buf * BS + (wn * WN + lr) * LDA + lk;
+    const int lr = lane & 15, lc = lane >> 4;
+    auto compute = [&](int buf) {
+        const T* Ab = As + buf * AS;
+        const T* Bb = Bs + buf * BS;
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 32) {
             frag af[FM], bf[FN];
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-                af[i] = __builtin_bit_cast(frag, *reinterpret_cast<const u32x4*>(Ab + i * 16 * LDA + kk));
+            for (int i = 0; i < FM; ++i) af[i] = __builtin_bit_cast(frag, la.frag(Ab, wm * WM + i * 16, kk, lane));
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                bf[j] = __builtin_bit_cast(frag, *reinterpret_cast<const u32x4*>(Bb + j * 16 * LDA + kk));
+            for (int j = 0; j < FN; ++j) bf[j] = __builtin_bit_cast(frag, lb.frag(Bb, wn * WN + j * 16, kk, lane));
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(af[i], bf[j], acc[i][j]);
         }
-        if (s + 1 < nk) {
-            la.store(As + (buf ^ 1) * AS);
-            lb.store(Bs + (buf ^ 1) * BS);
+    };
+
+    const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+    if constexpr (DEPTH == 2) {
+        // Two register sets hold the k-steps in flight: step s+1 was
+        // requested one step ago and is written to LDS at the end of step
+        // s, while step s+2 is requested at the start of step s (loop
+        // unrolled by two so the sets have fixed registers).
+        typename Loader<T, BM, NT, AKC>::Regs ra0, ra1;
+        typename Loader<T, BN, NT, BKC>::Regs rb0, rb1;
+        if (nk > 0) {
+            la.load(g.a, kb, ke, ra0);
+            lb.load(g.b, kb, ke, rb0);
+            la.store(As, ra0, kb, ke);
+            lb.store(Bs, rb0, kb, ke);
+            if (nk > 1) {
+                la.load(g.a, kb + BK, ke, ra1);
+                lb.load(g.b, kb + BK, ke, rb1);
+            }
+        }
+        __syncthreads();
+        for (int s = 0; s < nk; s += 2) {
+            // even step: LDS buffer 0 holds step s, set 1 holds step s+1
+            if (s + 2 < nk) {
+                la.load(g.a, kb + (s + 2) * BK, ke, ra0);
+                lb.load(g.b, kb + (s + 2) * BK, ke, rb0);
+            }
+            compute(0);
+            if (s + 1 < nk) {
+                la.store(As + AS, ra1, kb + (s + 1) * BK, ke);
+                lb.store(Bs + BS, rb1, kb + (s + 1) * BK, ke);
+            }
+            __syncthreads();
+            if (s + 1 >= nk) break;
+            // odd step: LDS buffer 1 holds step s+1, set 0 holds step s+2
+            if (s + 3 < nk) {
+                la.load(g.a, kb + (s + 3) * BK, ke, ra1);
+                lb.load(g.b, kb + (s + 3) * BK, ke, rb1);
+            }
+            compute(1);
+            if (s + 2 < nk) {
+                la.store(As, ra0, kb + (s + 2) * BK, ke);
+                lb.store(Bs, rb0, kb + (s + 2) * BK, ke);
+            }
+            __syncthreads();
+        }
+    } else {
+        // One register set: step s+1 is requested at the start of step s.
+        typename Loader<T, BM, NT, AKC>::Regs ra;
+        typename Loader<T, BN, NT, BKC>::Regs rb;
+        if (nk > 0) {
+            la.load(g.a, kb, ke, ra);
+            lb.load(g.b, kb, ke, rb);
+            la.store(As, ra, kb, ke);
+            lb.store(Bs, rb, kb, ke);
+        }
+        __syncthreads();
+        for (int s = 0; s < nk; ++s) {
+            const int buf = s & 1;
+            if (s + 1 < nk) {
+                la.load(g.a, kb + (s + 1) * BK, ke, ra);
+                lb.load(g.b, kb + (s + 1) * BK, ke, rb);
+            }
+            compute(buf);
+            if (s + 1 < nk) {
+                la.store(As + (buf ^ 1) * AS, ra, kb + (s + 1) * BK, ke);
+                lb.store(Bs + (buf ^ 1) * BS, rb, kb + (s + 1) * BK, ke);
+            }
+            __syncthreads();
+        }
+    }
+
+    // ---- epilogue: 64-column passes of the fp32 tile through LDS
+    float* Cs = reinterpret_cast<float*>(smem);
+    const bool partial = splits > 1;
+    const float alpha = partial ? 1.0f : g.c.alpha;
+    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
+    const bool contig_n = partial ? true : g.c.contig_n != 0;
+#pragma unroll
+    for (int p = 0; p < BN / PW; ++p) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int col = wn * WN + j * 16;
+            if (col < p * PW || col >= (p + 1) * PW) continue;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = wm * WM + i * 16 + lc * 4 + r;
+                    Cs[row * CLD + col - p * PW + lr] = acc[i][j][r] * alpha;
+                }
+        }
+        __syncthreads();
+        constexpr int NVEC = BM * PW / 8;
+        for (int v = tid; v < NVEC; v += NT) {
+            int m, n, lm, ln;
+            float vals[8];
+            if (contig_n) {
+                lm = v / (PW / 8); ln = (v % (PW / 8)) * 8;
+                m = m0 + lm; n = n0 + p * PW + ln;
+                if (m >= g.M || n >= g.N) continue;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) vals[q] = Cs[lm * CLD + ln + q];
+            } else {
+                ln = v / (BM / 8); lm = (v % (BM / 8)) * 8;
+                m = m0 + lm; n = n0 + p * PW + ln;
+                if (m >= g.M || n >= g.N) continue;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm + q) * CLD + ln];
+            }
+            if (partial) {
+                float* dst = g.split_ws + (((int64_t)sidx * g.batch + z) * g.M + m) * (int64_t)g.N + n;
+                V8<float>::store(dst, vals);
+            } else {
+                store_vec<T>(g, coff, m, n, vals);
+            }
         }
         __syncthreads();
     }
+}
 
-    // ---- epilogue: fp32 tile through LDS, then 8-wide vector stores
-    float* Cs = reinterpret_cast<float*>(smem);
-    const float alpha = g.c.alpha;
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                int row = wm * WM + i * 16 + (lane >> 4) * 4 + r;
-                int col = wn * WN + j * 16 + lr;
-                Cs[row * CLD + col] = acc[i][j][r] * alpha;
-            }
-    __syncthreads();
-
-    const Epilogue& e = g.c;
-    int64_t coff = map_off(e.batch, z, 1, &dummy);
-    constexpr int NVEC = BM * BN / 8;
-    for (int v = tid; v < NVEC; v += NT) {
-        int m, n, lm, ln;
+// Sum of the split-K partials in split order, then the regular epilogue.
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_reduce(GemmArgs g) {
+    const int64_t MN8 = (int64_t)g.M * g.N / 8;
+    const int64_t total = MN8 * g.batch;
+    const int64_t plane = (int64_t)g.batch * g.M * g.N;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < total; v += (int64_t)gridDim.x * 256) {
+        const int64_t z = v / MN8;
+        const int64_t r = v - z * MN8;
+        int m, n;
         float vals[8];
-        if (e.contig_n) {
-            lm = v / (BN / 8); ln = (v % (BN / 8)) * 8;
-            m = m0 + lm; n = n0 + ln;
-            if (m >= g.M || n >= g.N) continue;
+        if (g.c.contig_n) {
+            const int nv = g.N / 8;
+            m = (int)(r / nv); n = (int)(r % nv) * 8;
+            V8<float>::load(g.split_ws + (z * g.M + m) * (int64_t)g.N + n, vals);
+            for (int s = 1; s < g.splits; ++s) {
+                float t[8];
+                V8<float>::load(g.split_ws + s * plane + (z * g.M + m) * (int64_t)g.N + n, t);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) vals[q] = Cs[lm * CLD + ln + q];
+                for (int q = 0; q < 8; ++q) vals[q] += t[q];
+            }
         } else {
-            ln = v / (BM / 8); lm = (v % (BM / 8)) * 8;
-            m = m0 + lm; n = n0 + ln;
-            if (m >= g.M || n >= g.N) continue;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm + q) * CLD + ln];
-        }
-        if (e.bias[0]) {
+            const int mv = g.M / 8;
+            n = (int)(r / mv); m = (int)(r % mv) * 8;
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
-                uint32_t idx = e.bias_on_m ? (uint32_t)(e.contig_n ? m : m + q)
-                                           : (uint32_t)(e.contig_n ? n + q : n);
-                int bseg = 0;
-                int64_t bo = map_off(e.bias_map, idx, e.bias_nseg, &bseg);
-                vals[q] += to_f(reinterpret_cast<const T*>(e.bias[bseg])[bo]);
+                float acc = 0.f;
+                for (int s = 0; s < g.splits; ++s) acc += g.split_ws[s * plane + (z * g.M + m + q) * (int64_t)g.N + n];
+                vals[q] = acc;
             }
         }
-        int sm = 0, sn = 0;
-        int64_t off = coff + map_off(e.mmap, (uint32_t)m, e.seg_on_m ? e.nseg : 1, &sm) +
-                      map_off(e.nmap, (uint32_t)n, e.seg_on_m ? 1 : e.nseg, &sn);
-        int seg = e.seg_on_m ? sm : sn;
-        if (e.out_f32) {
-            float* p = reinterpret_cast<float*>(e.ptr[seg]) + off;
-            if (e.resid) {
-                float rv[8];
-                V8<float>::load(reinterpret_cast<const float*>(e.resid) + off, rv);
 #pragma unroll
-                for (int q = 0; q < 8; ++q) vals[q] += rv[q];
-            }
-            V8<float>::store(p, vals);
-        } else {
-            T* p = reinterpret_cast<T*>(e.ptr[seg]) + off;
-            if (e.resid) {
-                float rv[8];
-                V8<T>::load(reinterpret_cast<const T*>(e.resid) + off, rv);
-#pragma unroll
-                for (int q = 0; q < 8; ++q) vals[q] += rv[q];
-            }
-            V8<T>::store(p, vals);
-        }
+        for (int q = 0; q < 8; ++q) vals[q] *= g.c.alpha;
+        int dummy = 0;
+        store_vec<T>(g, map_off(g.c.batch, (uint32_t)z, 1, &dummy), m, n, vals);
     }
 }
 
@@ -340,20 +494,80 @@ __global__ __launch_bounds__(256) void gemm_f32(GemmArgs g) {
     reinterpret_cast<float*>(e.ptr[seg])[off] = v;
 }
 
-template <typename T, int BM, int BN, int BK>
-int launch_t(GemmArgs g, hipStream_t st) {
-    g.tiles_m = (g.M + BM - 1) / BM;
-    g.tiles_n = (g.N + BN - 1) / BN;
-    dim3 grid(g.tiles_m * g.tiles_n, g.batch);
+// Tile configurations: (BM, BN, waves along m, waves along n).
+struct TileCfg {
+    int bm, bn, wgm, wgn;
+};
+constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2}};
+constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
+
+template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH>
+void launch_cfg(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
     if (g.a.kcontig && g.b.kcontig)
-        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, BK, true, true>), grid, dim3(NT), 0, st, g);
+        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, WGM, WGN, DEPTH, true, true>), grid, block, 0, st, g);
     else if (g.a.kcontig)
-        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, BK, true, false>), grid, dim3(NT), 0, st, g);
+        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, WGM, WGN, DEPTH, true, false>), grid, block, 0, st, g);
     else if (g.b.kcontig)
-        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, BK, false, true>), grid, dim3(NT), 0, st, g);
+        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, WGM, WGN, DEPTH, false, true>), grid, block, 0, st, g);
     else
-        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, BK, false, false>), grid, dim3(NT), 0, st, g);
-    return 0;
+        hipLaunchKernelGGL((gemm_mfma<T, BM, BN, WGM, WGN, DEPTH, false, false>), grid, block, 0, st, g);
+}
+
+template <typename T>
+void launch_t(const GemmArgs& g, hipStream_t st) {
+    switch (g.cfg) {
+        case 0: launch_cfg<T, 256, 256, 2, 4, 1>(g, st); break;
+        case 1: launch_cfg<T, 256, 128, 2, 2, 1>(g, st); break;
+        case 2: launch_cfg<T, 128, 128, 2, 2, 1>(g, st); break;
+        case 3: launch_cfg<T, 256, 64, 4, 1, 1>(g, st); break;
+        default: launch_cfg<T, 128, 64, 2, 2, 1>(g, st); break;
+    }
+    if (g.splits > 1) {
+        const int64_t total = (int64_t)g.batch * g.M * g.N / 8;
+        int64_t blocks = (total + 255) / 256;
+        if (blocks > 4096) blocks = 4096;
+        hipLaunchKernelGGL((splitk_reduce<T>), dim3((unsigned)blocks), dim3(256), 0, st, g);
+    }
+}
+
+int64_t ntiles(const TileCfg& c, const GemmArgs& g) {
+    return (int64_t)((g.M + c.bm - 1) / c.bm) * ((g.N + c.bn - 1) / c.bn) * g.batch;
+}
+
+// Largest tile that still gives every CU a block; split k when even the
+// smallest suitable tile leaves CUs idle and k is long.
+void choose(GemmArgs& g) {
+    constexpr int64_t CUS = 256;
+    if (g.cfg < 0 || g.cfg >= NCFG) {
+        const bool narrow = g.N <= 64;
+        const int order_wide[] = {0, 1, 2, 4};
+        const int order_narrow[] = {3, 4};
+        const int* ord = narrow ? order_narrow : order_wide;
+        const int nord = narrow ? 2 : 4;
+        g.cfg = ord[nord - 1];
+        for (int i = 0; i < nord; ++i)
+            if (ntiles(CFGS[ord[i]], g) >= CUS) { g.cfg = ord[i]; break; }
+    }
+    const TileCfg& c = CFGS[g.cfg];
+    g.tiles_m = (g.M + c.bm - 1) / c.bm;
+    g.tiles_n = (g.N + c.bn - 1) / c.bn;
+    if (g.splits <= 0) {
+        g.splits = 1;
+        const int64_t t = ntiles(c, g);
+        if (g.split_ws && t < CUS && g.K >= 1024) {
+            int s = (int)((CUS + t - 1) / t);
+            if (s > 8) s = 8;
+            while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
+            g.splits = s;
+        }
+    }
+    if (g.splits > 1) {
+        const int ksteps = (g.K + BK - 1) / BK;
+        g.kper = (ksteps + g.splits - 1) / g.splits * BK;
+        g.splits = (g.K + g.kper - 1) / g.kper;
+    }
 }
 
 }  // namespace
@@ -373,8 +587,13 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     } else {
         if (g.K % 8 || g.M % 8 || g.N % 8)
             return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
-        if (dtype == G_F16) launch_t<half_t, 128, 128, 64>(g, st);
-        else launch_t<bf16_t, 128, 128, 64>(g, st);
+        if (!g.split_ws) g.splits = 1;
+        choose(g);
+        if (g.splits > 1 && (int64_t)g.splits * g.batch * g.M * g.N > g.split_cap)
+            return set_error(DM_ERR_WORKSPACE, "split-k scratch too small");
+        if ((int64_t)g.batch * g.splits > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction grid too large");
+        if (dtype == G_F16) launch_t<half_t>(g, st);
+        else launch_t<bf16_t>(g, st);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return set_error(DM_ERR_DEVICE, "contraction launch: %s", hipGetErrorString(err));

@@ -73,8 +73,18 @@ struct GemmArgs {
     int M, N, K, batch;
     Operand a, b;
     Epilogue c;
-    int tiles_m, tiles_n;
+    int tiles_m, tiles_n;  // set by the launcher
+    int splits;            // split-K factor; > 1 needs split_ws (0 or 1: none)
+    float* split_ws;       // splits * batch * M * N floats of partial sums
+    int64_t split_cap;     // floats available at split_ws
+    int kper;              // k range per split (set by the launcher)
+    int cfg;               // tile configuration index; < 0 lets the launcher choose
 };
+
+// Scratch bytes for a split-K contraction.
+inline size_t gemm_split_ws_bytes(int64_t M, int64_t N, int64_t batch, int splits) {
+    return splits > 1 ? (size_t)splits * batch * M * N * sizeof(float) : 0;
+}
 
 // Host-side construction helpers.
 IdxMap make_map(uint32_t r0, uint32_t r1, int64_t s0, int64_t s1, int64_t s2);

@@ -60,8 +60,22 @@ struct MhaPlan {
 struct EncPlan {
     MhaPlan m;
     size_t xhat1, rstd1, y1, h, a, xhat2, rstd2, saved_total;
-    size_t ao, o, fwd_total;
-    size_t dS2, dO, dA, dH, dY1f, dS1, dAO, bwd_total;
+    size_t ao, o, fwd_split, fwd_total;
+    size_t dS2, dO, dA, dH, dY1f, dS1, dAO, bwd_split, bwd_total;
+    int64_t split_floats;
+};
+
+// Split-k scratch for the contractions of one call: room for four partial
+// sums of the largest weight-sized output.
+int64_t split_floats_for(int64_t a, int64_t b, int64_t c) { return 4 * (a > b ? (a > c ? a : c) : (b > c ? b : c)); }
+
+// The contraction launches of one entry-point call take their split-k
+// scratch from here (set for the duration of the call on this thread).
+thread_local float* t_split_ws = nullptr;
+thread_local int64_t t_split_cap = 0;
+struct SplitScope {
+    SplitScope(void* p, int64_t cap) { t_split_ws = reinterpret_cast<float*>(p); t_split_cap = cap; }
+    ~SplitScope() { t_split_ws = nullptr; t_split_cap = 0; }
 };
 
 int64_t max3(int64_t a, int64_t b, int64_t c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
@@ -106,6 +120,8 @@ EncPlan plan_encoder(const Dims& x) {
     e.saved_total = sv.total;
     e.ao = fw.take(es * x.N);
     e.o = fw.take(es * x.N);
+    e.split_floats = split_floats_for(3 * x.I * x.I, x.I * x.F, x.Tq * x.I);
+    e.fwd_split = fw.take(4 * e.split_floats);
     e.fwd_total = fw.total;
     e.dS2 = bw.take(es * x.N);
     e.dO = bw.take(es * x.N);
@@ -115,17 +131,21 @@ EncPlan plan_encoder(const Dims& x) {
     e.dS1 = bw.take(es * x.N);
     e.dAO = bw.take(es * x.N);
     e.m.part = bw.take(colsum_ws_bytes(T, (int32_t)max3(3 * x.I, x.F, x.I)));
+    e.bwd_split = bw.take(4 * e.split_floats);
     e.bwd_total = bw.total;
     return e;
 }
 
-struct MhaSizes { MhaPlan p; size_t saved, fwd, bwd; };
+struct MhaSizes { MhaPlan p; size_t saved, fwd, bwd, fwd_split, bwd_split; int64_t split_floats; };
 MhaSizes plan_mha(const Dims& x, bool fused) {
     MhaSizes s{};
     Carver sv, fw, bw;
     plan_attention(x, fused, sv, fw, bw, s.p);
     int64_t cols = max3(fused ? 3 * x.H * x.P : x.H * x.P, x.H * x.W, x.I);
     s.p.part = bw.take(colsum_ws_bytes(x.Tq > x.Tk ? x.Tq : x.Tk, (int32_t)cols) + 4 * x.I);
+    s.split_floats = split_floats_for(3 * x.H * x.P * x.I, x.H * x.W * x.I, x.Tq * x.I);
+    s.fwd_split = fw.take(4 * s.split_floats);
+    s.bwd_split = bw.take(4 * s.split_floats);
     s.saved = sv.total; s.fwd = fw.total; s.bwd = bw.total;
     return s;
 }
@@ -227,6 +247,10 @@ GemmArgs gemm(int64_t M, int64_t N, int64_t K, int64_t batch, const Operand& a, 
     GemmArgs g{};
     g.M = (int)M; g.N = (int)N; g.K = (int)K; g.batch = (int)batch;
     g.a = a; g.b = b; g.c = c;
+    g.cfg = -1;
+    g.splits = t_split_ws ? 0 : 1;
+    g.split_ws = t_split_ws;
+    g.split_cap = t_split_cap;
     return g;
 }
 
@@ -470,6 +494,7 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     const EncPlan e = plan_encoder(x);
     if (ws_bytes < e.fwd_total) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    SplitScope split_(B8(ws, e.fwd_split), e.split_floats);
     const int dt = x.dtype;
     const int64_t T = x.Tq;
     void *q = B8(saved, e.m.q), *k = B8(saved, e.m.k), *v = B8(saved, e.m.v);
@@ -539,6 +564,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     const EncPlan e = plan_encoder(x);
     if (ws_bytes < e.bwd_total) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    SplitScope split_(B8(ws, e.bwd_split), e.split_floats);
     const int dt = x.dtype;
     const int64_t T = x.Tq, I = x.I, F = x.F;
     const int es = x.es;
@@ -667,6 +693,7 @@ int mha_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     const MhaSizes s = plan_mha(x, fused);
     if (ws_bytes < s.fwd) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    SplitScope split_(B8(ws, s.fwd_split), s.split_floats);
     void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);
     if (fused) {
         TraceScope t_("F1 qkv", st);
@@ -703,6 +730,7 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     const MhaSizes s = plan_mha(x, fused);
     if (ws_bytes < s.bwd) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    SplitScope split_(B8(ws, s.bwd_split), s.split_floats);
     const int dt = x.dtype;
     const int es = x.es;
     const void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);

@@ -110,7 +110,8 @@ _f["attn_input_bias_grad"] = _sig("attn_input_bias_grad", I32, I32, I64, I32, I3
 _f["residual_add"] = _sig("residual_add", I32, I32, I64, P_, P_, P_, P_)
 _f["dropout_mask"] = _sig("dropout_mask", I32, U64, U32, U32, F32, U64, U64, P_, P_)
 _f["saved_tensor_view"] = _sig("saved_tensor_view", I32, PDESC, I32, PSZ, PSZ)
-_f["contract"] = _sig("contract", I32, I32, I32, I32, I32, I32, F32, P_, I32, I64, P_, I32, I64, P_, P_, I32, I64, P_)
+_f["contract"] = _sig("contract", I32, I32, I32, I32, I32, I32, F32, P_, I32, I64, P_, I32, I64, P_, P_, I32, I64,
+                      I32, I32, P_, SZ, P_)
 _f["dm_last_error"] = _sig("dm_last_error", C.c_char_p)
 _f["dm_trace_enable"] = _sig("dm_trace_enable", I32, I32)
 _f["dm_trace_count"] = _sig("dm_trace_count", I32)
@@ -275,9 +276,10 @@ def dropout_mask(seed, site, layer, p, offset, n, out, stream=None):
     return _call("dropout_mask", seed, site, layer, p, offset, n, ptr(out), _st(stream))
 
 
-def contract(dtype, batch, M, N, K, alpha, A, a_trans, sa, B, b_trans, sb, bias, Cout, out_f32, sc, stream=None):
+def contract(dtype, batch, M, N, K, alpha, A, a_trans, sa, B, b_trans, sb, bias, Cout, out_f32, sc,
+             tile_cfg=-1, splits=0, ws=None, ws_bytes=0, stream=None):
     return _call("contract", dtype, batch, M, N, K, alpha, ptr(A), a_trans, sa, ptr(B), b_trans, sb, ptr(bias),
-                 ptr(Cout), out_f32, sc, _st(stream))
+                 ptr(Cout), out_f32, sc, tile_cfg, splits, ptr(ws), ws_bytes, _st(stream))
 
 
 def dm_trace_enable(on: bool) -> None:

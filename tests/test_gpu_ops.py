@@ -244,17 +244,20 @@ def test_bias_grads_and_residual(lib, dt):
 
 
 # --------------------------------------------------------------- contraction
-@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
-@pytest.mark.parametrize("a_trans,b_trans", [(0, 0), (0, 1), (1, 0), (1, 1)])
-@pytest.mark.parametrize("batch,M,N,K", [(1, 128, 128, 64), (3, 136, 200, 72), (2, 264, 40, 520), (1, 8, 8, 8)])
-def test_contract_modes(lib, dt, a_trans, b_trans, batch, M, N, K):
+def _contract_case(lib, dt, a_trans, b_trans, batch, M, N, K, cfg=-1, splits=0):
     A = make_tensor((batch, K, M) if a_trans else (batch, M, K), dt, 101)
     B = make_tensor((batch, N, K) if b_trans else (batch, K, N), dt, 102)
     bias = make_tensor((N,), dt, 103)
     C = torch.empty((batch, M, N), dtype=A.dtype, device=DEV)
     Cf = torch.empty((batch, M, N), dtype=torch.float32, device=DEV)
-    lib.contract(DT[dt], batch, M, N, K, 0.5, dev(A), a_trans, M * K, dev(B), b_trans, N * K, dev(bias), C, 0, M * N)
-    lib.contract(DT[dt], batch, M, N, K, 1.0, dev(A), a_trans, M * K, dev(B), b_trans, N * K, None, Cf, 1, M * N)
+    ws, wsb = None, 0
+    if splits > 1:
+        wsb = splits * batch * M * N * 4
+        ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    lib.contract(DT[dt], batch, M, N, K, 0.5, dev(A), a_trans, M * K, dev(B), b_trans, N * K, dev(bias), C, 0,
+                 M * N, cfg, splits, ws, wsb)
+    lib.contract(DT[dt], batch, M, N, K, 1.0, dev(A), a_trans, M * K, dev(B), b_trans, N * K, None, Cf, 1, M * N,
+                 cfg, splits, ws, wsb)
     torch.cuda.synchronize()
     a = f64(A).transpose(0, 2, 1) if a_trans else f64(A)
     b = f64(B).transpose(0, 2, 1) if b_trans else f64(B)
@@ -262,3 +265,25 @@ def test_contract_modes(lib, dt, a_trans, b_trans, batch, M, N, K):
     scale = float(np.sqrt(K))
     assert_close("C", C, rnd(0.5 * ref + f64(bias), dt), dt, scale=scale)
     assert_close("Cf", Cf, ref, "f32" if dt == "f32" else dt, scale=scale)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("a_trans,b_trans", [(0, 0), (0, 1), (1, 0), (1, 1)])
+@pytest.mark.parametrize("batch,M,N,K", [(1, 128, 128, 64), (3, 136, 200, 72), (2, 264, 40, 520), (1, 8, 8, 8)])
+def test_contract_modes(lib, dt, a_trans, b_trans, batch, M, N, K):
+    _contract_case(lib, dt, a_trans, b_trans, batch, M, N, K)
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (0, 0), (1, 0), (1, 1)])
+def test_contract_tile_configs(lib, dt, cfg, a_trans, b_trans):
+    # ragged in every dimension for every block tile
+    _contract_case(lib, dt, a_trans, b_trans, 2, 264, 328, 200, cfg=cfg)
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("cfg,splits", [(2, 2), (4, 3), (0, 4), (3, 5)])
+@pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (1, 0)])
+def test_contract_split_k(lib, dt, cfg, splits, a_trans, b_trans):
+    _contract_case(lib, dt, a_trans, b_trans, 2, 136, 264, 1096, cfg=cfg, splits=splits)
