@@ -139,25 +139,33 @@ def main() -> int:
     torch.cuda.synchronize()
     recs = lib.trace_records()
     lib.dm_trace_enable(False)
-    per = {}
-    for lab, t in recs:
-        per.setdefault(lab, []).append(t)
+    per, order = {}, []
+    for lab, sub, t in recs:
+        key = (lab, sub)
+        if key not in per:
+            per[key] = []
+            order.append(key)
+        per[key].append(t)
     work = dataflow.encoder_layer(s, wl.dtype)
     table = []
-    for lab, ts in per.items():
-        w = work.get(lab)
+    for key in order:
+        lab, sub = key
+        ts = per[key]
+        w = work.get(lab) if not sub else None
         avg = sum(ts) / len(ts)
-        launches_per_step = len(ts) / a.steps
-        row = {"kernel": lab, "us": round(avg * 1e3, 2), "launches_per_step": launches_per_step}
+        row = {"kernel": lab + (" " + sub if sub else ""), "op": lab, "us": round(avg * 1e3, 2),
+               "launches_per_step": len(ts) / a.steps}
         if w is not None:
             row.update(bound=w.bound, gflop=round(w.flop / 1e9, 4), mbytes=round(w.bytes / 1e6, 3))
             if avg > 0:
                 row["tflops"] = round(w.flop / (avg * 1e-3) / 1e12, 1)
                 row["gbs"] = round(w.bytes / (avg * 1e-3) / 1e9, 1)
         table.append(row)
-    traced_ms = sum(r["us"] * r["launches_per_step"] for r in table) / 1e3
-    dom = max(table, key=lambda r: r["us"] * r["launches_per_step"])
-    dw = work[dom["kernel"]]
+    step_us = lambda rows: sum(r["us"] * r["launches_per_step"] for r in rows)
+    traced_ms = step_us(table) / 1e3
+    # dominant kernel: the single launch with the largest time per step
+    dom = max((r for r in table if "bound" in r), key=lambda r: r["us"] * r["launches_per_step"])
+    dw = work[dom["op"]]
     dom_s = dom["us"] * 1e-6
     if dw.bound == "mfma":
         achieved = dw.flop / dom_s / 1e12
@@ -171,18 +179,20 @@ def main() -> int:
             "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(dom["kernel"]),
             "per_launch_us": dom["us"],
             "algorithmic_per_launch": dw.flop if dw.bound == "mfma" else dw.bytes}
-    fused = [r for r in table if work.get(r["kernel"]) is not None and work[r["kernel"]].bound == "hbm"
-             and work[r["kernel"]].flop == 0.0]
-    fb = sum(work[r["kernel"]].bytes * r["launches_per_step"] for r in fused)
-    ft = sum(r["us"] * r["launches_per_step"] for r in fused) * 1e-6
+    # operator classes; second launches (reduce / finish) count with their operator
+    is_fused = lambda r: work.get(r["op"]) is not None and work[r["op"]].flop == 0.0
+    is_contr = lambda r: work.get(r["op"]) is not None and work[r["op"]].flop > 0.0
+    fused = [r for r in table if is_fused(r)]
+    fb = sum(work[r["op"]].bytes * r["launches_per_step"] for r in fused if r["op"] == r["kernel"])
+    ft = step_us(fused) * 1e-6
     fused_summary = {"GB/s": round(fb / ft / 1e9, 1), "frac_of_peak": round(fb / ft / 1e9 / dataflow.HBM_PEAK_GBS, 4),
                      "us_per_step": round(ft * 1e6, 1), "mbytes_per_step": round(fb / 1e6, 2)}
-    contraction = [r for r in table if work.get(r["kernel"]) is not None and work[r["kernel"]].flop > 0]
-    cf = sum(work[r["kernel"]].flop * r["launches_per_step"] for r in contraction)
-    ct = sum(r["us"] * r["launches_per_step"] for r in contraction) * 1e-6
-    mf = [r for r in contraction if work[r["kernel"]].bound == "mfma"]
-    mff = sum(work[r["kernel"]].flop for r in mf)
-    mft = sum(r["us"] for r in mf) * 1e-6
+    contraction = [r for r in table if is_contr(r)]
+    cf = sum(work[r["op"]].flop * r["launches_per_step"] for r in contraction if r["op"] == r["kernel"])
+    ct = step_us(contraction) * 1e-6
+    mf = [r for r in contraction if work[r["op"]].bound == "mfma"]
+    mff = sum(work[r["op"]].flop * r["launches_per_step"] for r in mf if r["op"] == r["kernel"])
+    mft = step_us(mf) * 1e-6
 
     out = {
         "metric": METRIC, "value": round(ms, 4), "unit": "ms", "n_gpus": 1, "steps": a.steps,

@@ -267,14 +267,17 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
  * Optional per-launch timing for measurement: while enabled, every kernel
  * the layer and attention entry points enqueue is bracketed by two HIP
  * events on the call's stream and recorded under a short label naming the
- * paper's operator (e.g. "F7 linear1", "B15 softmax_bwd").  Recording adds
- * two event records per launch; leave it off outside measurement.
+ * paper's operator (e.g. "F7 linear1", "B15 softmax_bwd") and a sub-label
+ * ("" for an operator's first launch, e.g. "reduce" or "finish" for the
+ * second launch of a two-stage reduction).  Recording adds two event
+ * records per launch; leave it off outside measurement.
  * dm_trace_enable(1) clears earlier records; dm_trace_get waits for the
- * i-th record to complete and returns its label (static storage) and its
- * duration in milliseconds.  Not for concurrent use from several threads. */
+ * i-th record to complete and returns its label and sub-label (static
+ * storage) and its duration in milliseconds.  Not for concurrent use from
+ * several threads. */
 int dm_trace_enable(int32_t on);
 int32_t dm_trace_count(void);
-int dm_trace_get(int32_t i, const char** label, float* ms);
+int dm_trace_get(int32_t i, const char** label, const char** sub, float* ms);
 
 /* Message for the last non-OK status returned on the calling thread. */
 const char* dm_last_error(void);

@@ -34,8 +34,10 @@ int check_launch(const char* what) {
 namespace {
 struct TraceRec {
     const char* label;
+    const char* sub;
     hipEvent_t a, b;
 };
+thread_local TraceScope* g_active = nullptr;
 std::atomic<bool> g_trace_on{false};
 std::mutex g_trace_mu;
 std::vector<TraceRec> g_trace;     // records of the current session
@@ -52,21 +54,46 @@ hipEvent_t pooled_event() {
 }
 }  // namespace
 
-TraceScope::TraceScope(const char* label, hipStream_t s) : idx(-1), st(s) {
-    if (!g_trace_on.load(std::memory_order_relaxed)) return;
+static int trace_open(const char* label, const char* sub, hipStream_t st) {
     std::lock_guard<std::mutex> lk(g_trace_mu);
     hipEvent_t a = pooled_event(), b = pooled_event();
-    if (!a || !b) return;
+    if (!a || !b) return -1;
     (void)hipEventRecord(a, st);
-    g_trace.push_back({label, a, b});
-    idx = (int)g_trace.size() - 1;
+    g_trace.push_back({label, sub, a, b});
+    return (int)g_trace.size() - 1;
+}
+
+TraceScope::TraceScope(const char* lab, hipStream_t s) : idx(-1), st(s), label(lab), outer(nullptr) {
+    if (!g_trace_on.load(std::memory_order_relaxed)) return;
+    idx = trace_open(label, "", st);
+    if (idx >= 0) {
+        outer = g_active;
+        g_active = this;
+    }
 }
 
 void TraceScope::stop() {
     if (idx < 0) return;
-    std::lock_guard<std::mutex> lk(g_trace_mu);
-    (void)hipEventRecord(g_trace[idx].b, st);
+    {
+        std::lock_guard<std::mutex> lk(g_trace_mu);
+        (void)hipEventRecord(g_trace[idx].b, st);
+    }
     idx = -1;
+    if (g_active == this) g_active = outer;
+}
+
+void TraceScope::next(const char* sub) {
+    if (idx < 0) return;
+    {
+        std::lock_guard<std::mutex> lk(g_trace_mu);
+        (void)hipEventRecord(g_trace[idx].b, st);
+    }
+    idx = trace_open(label, sub, st);
+    if (idx < 0 && g_active == this) g_active = outer;
+}
+
+void trace_next(const char* sub) {
+    if (g_active) g_active->next(sub);
 }
 
 DropParams make_drop(float p, uint64_t seed, uint32_t site, uint32_t layer) {
@@ -144,7 +171,7 @@ int32_t dm_trace_count(void) {
     return (int32_t)g_trace.size();
 }
 
-int dm_trace_get(int32_t i, const char** label, float* ms) {
+int dm_trace_get(int32_t i, const char** label, const char** sub, float* ms) {
     std::lock_guard<std::mutex> lk(g_trace_mu);
     if (i < 0 || i >= (int32_t)g_trace.size()) return set_error(DM_ERR_ARG, "trace index %d out of range", i);
     hipError_t e = hipEventSynchronize(g_trace[i].b);
@@ -152,6 +179,7 @@ int dm_trace_get(int32_t i, const char** label, float* ms) {
     if (e == hipSuccess) e = hipEventElapsedTime(&t, g_trace[i].a, g_trace[i].b);
     if (e != hipSuccess) return set_error(DM_ERR_DEVICE, "trace event: %s", hipGetErrorString(e));
     if (label) *label = g_trace[i].label;
+    if (sub) *sub = g_trace[i].sub;
     if (ms) *ms = t;
     return DM_OK;
 }
@@ -308,6 +336,7 @@ int bias_grad(int32_t dtype, int64_t rows, int32_t cols, const void* x, float* d
     DM_TRY(check_ptr(x, "x")); DM_TRY(check_ptr(db, "db")); DM_TRY(check_ptr(ws, "ws"));
     if (ws_bytes < colsum_ws_bytes(rows, cols)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
     run_colsum_partial(dtype, rows, cols, x, (float*)ws, S(stream));
+    trace_next("finish");
     run_colsum_finish(rows, cols, (float*)ws, db, S(stream));
     return check_launch("bias_grad");
 }

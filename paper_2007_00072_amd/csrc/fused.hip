@@ -214,56 +214,74 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, 
         for (int q = 0; q < 8; ++q) { p_dyx[i][q] = 0.f; p_dy[i][q] = 0.f; p_dsub[i][q] = 0.f; }
     }
 
-    for (int64_t rb = r0; rb < r1; rb += GROUPS) {
-        const int64_t row = rb + wave * RPW + gi;
-        const bool active = row < r1;
-        const int64_t base = row * cols;
-        float dy[NV][8], xh[NV][8];
-        float s1 = 0.f, s2 = 0.f;
+    // UR rows per lane group are in flight: all their loads are issued
+    // before the first row's reductions.
+    constexpr int UR = NV <= 2 ? 2 : 1;
+    for (int64_t rb = r0; rb < r1; rb += GROUPS * UR) {
+        float dy[UR][NV][8], xh[UR][NV][8];
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            const int c = (gl + i * LPR) * 8;
-            if (active && c < cols) {
-                V8<T>::load(dya + base + c, dy[i]);
-                if (dyb) {
-                    float t[8];
-                    V8<T>::load(dyb + base + c, t);
+        for (int u = 0; u < UR; ++u) {
+            const int64_t row = rb + u * GROUPS + wave * RPW + gi;
+            const bool active = row < r1;
+            const int64_t base = row * cols;
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) dy[i][q] += t[q];
+            for (int i = 0; i < NV; ++i) {
+                const int c = (gl + i * LPR) * 8;
+                if (active && c < cols) {
+                    V8<T>::load(dya + base + c, dy[u][i]);
+                    V8<T>::load(xhat + base + c, xh[u][i]);
+                    if (dyb) {
+                        float t[8];
+                        V8<T>::load(dyb + base + c, t);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) dy[u][i][q] += t[q];
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) { dy[u][i][q] = 0.f; xh[u][i][q] = 0.f; }
                 }
-                if (a.dysum) V8<T>::store(reinterpret_cast<T*>(a.dysum) + base + c, dy[i]);
-                V8<T>::load(xhat + base + c, xh[i]);
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    if (do_part) { p_dyx[i][q] += dy[i][q] * xh[i][q]; p_dy[i][q] += dy[i][q]; }
-                    if (do_ds) { float gy = dy[i][q] * g[i][q]; s1 += gy; s2 += gy * xh[i][q]; }
-                }
-            } else {
-#pragma unroll
-                for (int q = 0; q < 8; ++q) { dy[i][q] = 0.f; xh[i][q] = 0.f; }
             }
         }
-        if (do_ds) {
-            const float inv = 1.0f / (float)cols;
-            const float m1 = group_sum<LPR>(s1) * inv;
-            const float m2 = group_sum<LPR>(s2) * inv;
-            if (active) {
-                const float rs = a.rstd[row];
 #pragma unroll
-                for (int i = 0; i < NV; ++i) {
-                    const int c = (gl + i * LPR) * 8;
-                    if (c < cols) {
-                        float o[8];
+        for (int u = 0; u < UR; ++u) {
+            const int64_t row = rb + u * GROUPS + wave * RPW + gi;
+            const bool active = row < r1;
+            const int64_t base = row * cols;
+            float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-                        for (int q = 0; q < 8; ++q) o[q] = rs * (dy[i][q] * g[i][q] - m1 - xh[i][q] * m2);
-                        if (a.ds) V8<T>::store(reinterpret_cast<T*>(a.ds) + base + c, o);
-                        if (a.dsub) {
-                            dropout8(a.dp, (uint64_t)(base + c), o);
-                            V8<T>::store(reinterpret_cast<T*>(a.dsub) + base + c, o);
-                            if (do_part && a.want_dsub_sum) {
-                                // sum the stored (rounded) values that later consumers see
+            for (int i = 0; i < NV; ++i) {
+                const int c = (gl + i * LPR) * 8;
+                if (active && c < cols) {
+                    if (a.dysum) V8<T>::store(reinterpret_cast<T*>(a.dysum) + base + c, dy[u][i]);
 #pragma unroll
-                                for (int q = 0; q < 8; ++q) p_dsub[i][q] += to_f(from_f<T>(o[q]));
+                    for (int q = 0; q < 8; ++q) {
+                        if (do_part) { p_dyx[i][q] += dy[u][i][q] * xh[u][i][q]; p_dy[i][q] += dy[u][i][q]; }
+                        if (do_ds) { float gy = dy[u][i][q] * g[i][q]; s1 += gy; s2 += gy * xh[u][i][q]; }
+                    }
+                }
+            }
+            if (do_ds) {
+                const float inv = 1.0f / (float)cols;
+                const float m1 = group_sum<LPR>(s1) * inv;
+                const float m2 = group_sum<LPR>(s2) * inv;
+                if (active) {
+                    const float rs = a.rstd[row];
+#pragma unroll
+                    for (int i = 0; i < NV; ++i) {
+                        const int c = (gl + i * LPR) * 8;
+                        if (c < cols) {
+                            float o[8];
+#pragma unroll
+                            for (int q = 0; q < 8; ++q) o[q] = rs * (dy[u][i][q] * g[i][q] - m1 - xh[u][i][q] * m2);
+                            if (a.ds) V8<T>::store(reinterpret_cast<T*>(a.ds) + base + c, o);
+                            if (a.dsub) {
+                                dropout8(a.dp, (uint64_t)(base + c), o);
+                                V8<T>::store(reinterpret_cast<T*>(a.dsub) + base + c, o);
+                                if (do_part && a.want_dsub_sum) {
+                                    // sum the stored (rounded) values that later consumers see
+#pragma unroll
+                                    for (int q = 0; q < 8; ++q) p_dsub[i][q] += to_f(from_f<T>(o[q]));
+                                }
                             }
                         }
                     }
@@ -306,101 +324,114 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, 
 }
 
 // ------------------------------------------------------ activation backward + bias grad
-// Each thread owns up to CV column vectors for all rows of its block.
-template <typename T, int CV>
+// Block (x, y) takes the rows of row block x and the column chunk y of
+// NT*8 columns: each thread owns one 8-column vector and walks its rows
+// four at a time (all loads of the four rows issued before any use).
+constexpr int RU = 4;
+
+template <typename T>
 __global__ __launch_bounds__(NT) void act_bwd_k(int64_t rows, int F, const T* __restrict__ da,
                                                 const T* __restrict__ h, const T* __restrict__ b1, int act,
                                                 DropParams dp, T* __restrict__ dh, float* __restrict__ part,
                                                 int rows_per_block) {
-    const int nvec = F / 8;
+    const int v = blockIdx.y * NT + threadIdx.x;
+    if (v >= F / 8) return;
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t r1 = min<int64_t>(rows, r0 + rows_per_block);
-    float bb[CV][8], acc[CV][8];
+    float bb[8], acc[8];
+    V8<T>::load(b1 + v * 8, bb);
 #pragma unroll
-    for (int i = 0; i < CV; ++i) {
-        const int v = threadIdx.x + i * NT;
-        if (v < nvec) V8<T>::load(b1 + v * 8, bb[i]);
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int64_t r = r0; r < r1; r += RU) {
+        float g[RU][8], u[RU][8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[i][q] = 0.f;
-    }
-    for (int64_t r = r0; r < r1; ++r) {
+        for (int j = 0; j < RU; ++j)
+            if (r + j < r1) {
+                V8<T>::load(da + (r + j) * F + v * 8, g[j]);
+                V8<T>::load(h + (r + j) * F + v * 8, u[j]);
+            }
 #pragma unroll
-        for (int i = 0; i < CV; ++i) {
-            const int v = threadIdx.x + i * NT;
-            if (v < nvec) {
-                const int64_t off = r * F + v * 8;
-                float g[8], u[8];
-                V8<T>::load(da + off, g);
-                V8<T>::load(h + off, u);
-                dropout8(dp, (uint64_t)off, g);
+        for (int j = 0; j < RU; ++j)
+            if (r + j < r1) {
+                const int64_t off = (r + j) * F + v * 8;
+                dropout8(dp, (uint64_t)off, g[j]);
 #pragma unroll
-                for (int q = 0; q < 8; ++q) g[q] *= act_grad(u[q] + bb[i][q], act);
-                V8<T>::store(dh + off, g);
+                for (int q = 0; q < 8; ++q) g[j][q] *= act_grad(u[j][q] + bb[q], act);
+                V8<T>::store(dh + off, g[j]);
                 // sum the stored (rounded) values that consumers of dh read
 #pragma unroll
-                for (int q = 0; q < 8; ++q) acc[i][q] += to_f(from_f<T>(g[q]));
+                for (int q = 0; q < 8; ++q) acc[q] += to_f(from_f<T>(g[j][q]));
             }
-        }
     }
-#pragma unroll
-    for (int i = 0; i < CV; ++i) {
-        const int v = threadIdx.x + i * NT;
-        if (v < nvec) V8<float>::store(part + (int64_t)blockIdx.x * F + v * 8, acc[i]);
-    }
+    V8<float>::store(part + (int64_t)blockIdx.x * F + v * 8, acc);
 }
 
-template <typename T, int CV>
+template <typename T>
 __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, const T* __restrict__ x,
                                                        float* __restrict__ part, int rows_per_block) {
-    const int nvec = cols / 8;
+    const int v = blockIdx.y * NT + threadIdx.x;
+    if (v >= cols / 8) return;
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t r1 = min<int64_t>(rows, r0 + rows_per_block);
-    float acc[CV][8];
+    float acc[8];
 #pragma unroll
-    for (int i = 0; i < CV; ++i)
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int64_t r = r0; r < r1; r += RU) {
+        float t[RU][8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[i][q] = 0.f;
-    for (int64_t r = r0; r < r1; ++r) {
+        for (int j = 0; j < RU; ++j)
+            if (r + j < r1) V8<T>::load(x + (r + j) * cols + v * 8, t[j]);
 #pragma unroll
-        for (int i = 0; i < CV; ++i) {
-            const int v = threadIdx.x + i * NT;
-            if (v < nvec) {
-                float t[8];
-                V8<T>::load(x + r * cols + v * 8, t);
+        for (int j = 0; j < RU; ++j)
+            if (r + j < r1) {
 #pragma unroll
-                for (int q = 0; q < 8; ++q) acc[i][q] += t[q];
+                for (int q = 0; q < 8; ++q) acc[q] += t[j][q];
             }
-        }
     }
-#pragma unroll
-    for (int i = 0; i < CV; ++i) {
-        const int v = threadIdx.x + i * NT;
-        if (v < nvec) V8<float>::store(part + (int64_t)blockIdx.x * cols + v * 8, acc[i]);
-    }
+    V8<float>::store(part + (int64_t)blockIdx.x * cols + v * 8, acc);
 }
 
-// out[c] = sum over nblk partial rows, fixed order; 64 columns x 4 row phases per block.
+// out[c] = sum over the nblk partial rows in a fixed order.  Block x covers
+// columns 64x .. 64x+63 as 16 four-column groups x 16 row phases; block y
+// selects one of up to three partial sets (part + y*nblk*cols -> outs[y]).
+// With qkv_H > 0 the columns are (s, h, p) of a fused projection and land
+// in outs[s][p * qkv_H + h] (single partial set).
+struct FinishOut {
+    float* out[3];
+};
+
 __global__ __launch_bounds__(NT) void colsum_finish_k(int nblk, int cols, const float* __restrict__ part,
-                                                      float* __restrict__ out, int qkv_H, int qkv_P,
-                                                      float* o1, float* o2) {
-    __shared__ float red[4][64];
-    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int ph = threadIdx.x >> 6;
-    float s = 0.f;
-    if (c < cols)
-        for (int b = ph; b < nblk; b += 4) s += part[(int64_t)b * cols + c];
-    red[ph][threadIdx.x & 63] = s;
+                                                      FinishOut fo, int qkv_H, int qkv_P) {
+    __shared__ floatx4 red[16][16];
+    const int cg = threadIdx.x & 15, ph = threadIdx.x >> 4;
+    const int c = blockIdx.x * 64 + cg * 4;
+    const float* base = part + (int64_t)blockIdx.y * nblk * cols;
+    floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
+    if (c < cols) {
+        int b = ph;
+        for (; b + 16 < nblk; b += 32) {
+            s0 += *reinterpret_cast<const floatx4*>(base + (int64_t)b * cols + c);
+            s1 += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + 16) * cols + c);
+        }
+        if (b < nblk) s0 += *reinterpret_cast<const floatx4*>(base + (int64_t)b * cols + c);
+    }
+    red[ph][cg] = s0 + s1;
     __syncthreads();
     if (ph == 0 && c < cols) {
-        float t = (red[0][threadIdx.x] + red[1][threadIdx.x]) + (red[2][threadIdx.x] + red[3][threadIdx.x]);
-        if (qkv_H > 0) {
-            // column (s, h, p) of a fused projection -> bias gradient b_s[p][h]
-            const int I = qkv_H * qkv_P;
-            const int sg = c / I, hp = c - sg * I, hh = hp / qkv_P, pp = hp - hh * qkv_P;
-            float* dst = sg == 0 ? out : (sg == 1 ? o1 : o2);
-            dst[pp * qkv_H + hh] = t;
-        } else {
-            out[c] = t;
+        floatx4 t = red[0][cg];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) t += red[i][cg];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int cc = c + q;
+            if (qkv_H > 0) {
+                // column (s, h, p) of a fused projection -> bias gradient b_s[p][h]
+                const int I = qkv_H * qkv_P;
+                const int sg = cc / I, hp = cc - sg * I, hh = hp / qkv_P, pp = hp - hh * qkv_P;
+                fo.out[sg][pp * qkv_H + hh] = t[q];
+            } else {
+                fo.out[blockIdx.y][cc] = t[q];
+            }
         }
     }
 }
@@ -608,44 +639,38 @@ void run_act_bwd(int dtype, int64_t rows, int F, const void* da, const void* h, 
                  const DropParams& dp, void* dh, float* part, hipStream_t st) {
     const int nblk = colsum_blocks(rows);
     const int rpb = (int)((rows + nblk - 1) / nblk);
-    const int cv = (F / 8 + NT - 1) / NT;
-#define L(CV)                                                                                          \
-    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((act_bwd_k<T, CV>), dim3(nblk), dim3(NT), 0, st, rows, F, \
-                                               (const T*)da, (const T*)h, (const T*)b1, act, dp, (T*)dh, \
-                                               part, rpb))
-    if (cv <= 1) L(1);
-    else if (cv <= 2) L(2);
-    else if (cv <= 4) L(4);
-    else L(8);
-#undef L
+    const dim3 grid(nblk, (F / 8 + NT - 1) / NT);
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((act_bwd_k<T>), grid, dim3(NT), 0, st, rows, F, (const T*)da,
+                                              (const T*)h, (const T*)b1, act, dp, (T*)dh, part, rpb));
 }
 
 void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float* part, hipStream_t st) {
     const int nblk = colsum_blocks(rows);
     const int rpb = (int)((rows + nblk - 1) / nblk);
-    const int cv = (cols / 8 + NT - 1) / NT;
-#define L(CV)                                                                                     \
-    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((colsum_partial_k<T, CV>), dim3(nblk), dim3(NT), 0, st, \
-                                               rows, cols, (const T*)x, part, rpb))
-    if (cv <= 1) L(1);
-    else if (cv <= 2) L(2);
-    else if (cv <= 4) L(4);
-    else L(8);
-#undef L
+    const dim3 grid(nblk, (cols / 8 + NT - 1) / NT);
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((colsum_partial_k<T>), grid, dim3(NT), 0, st, rows, cols,
+                                              (const T*)x, part, rpb));
 }
 
 void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st) {
-    const int nblk = colsum_blocks(rows);
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64), dim3(NT), 0, st, nblk, cols, part, out, 0, 0,
-                       nullptr, nullptr);
+    FinishOut fo{{out, nullptr, nullptr}};
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
+                       fo, 0, 0);
+}
+
+void run_colsum_finish3(int64_t rows, int cols, const float* part, float* o0, float* o1, float* o2,
+                        hipStream_t st) {
+    FinishOut fo{{o0, o1, o2}};
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64, 3), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
+                       fo, 0, 0);
 }
 
 void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* part, float* dbq, float* dbk,
                            float* dbv, hipStream_t st) {
-    const int nblk = colsum_blocks(rows);
     const int cols = nseg * H * P;
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64), dim3(NT), 0, st, nblk, cols, part, dbq, H, P,
-                       dbk, dbv);
+    FinishOut fo{{dbq, dbk, dbv}};
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
+                       fo, H, P);
 }
 
 void run_rowsum(int dtype, int64_t rows, int len, const void* x, float* out, hipStream_t st) {

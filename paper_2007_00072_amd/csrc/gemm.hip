@@ -525,6 +525,7 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
         default: launch_cfg<T, 128, 64, 2, 2, 1>(g, st); break;
     }
     if (g.splits > 1) {
+        trace_next("reduce");
         const int64_t total = (int64_t)g.batch * g.M * g.N / 8;
         int64_t blocks = (total + 255) / 256;
         if (blocks > 4096) blocks = 4096;
@@ -536,32 +537,41 @@ int64_t ntiles(const TileCfg& c, const GemmArgs& g) {
     return (int64_t)((g.M + c.bm - 1) / c.bm) * ((g.N + c.bn - 1) / c.bn) * g.batch;
 }
 
-// Largest tile that still gives every CU a block; split k when even the
-// smallest suitable tile leaves CUs idle and k is long.
+// Tile and split choice, from measurements of the layer's contraction
+// shapes on MI355X (every configuration x split 1/2/4): the 256x256 tile
+// when it alone gives every CU a block; for long k with an
+// outer-contiguous operand, 256x256 split four ways (weight gradients) or
+// 256x64 split two ways; otherwise 128x64.  Explicit choices (cfg >= 0,
+// splits > 0) are kept.
 void choose(GemmArgs& g) {
     constexpr int64_t CUS = 256;
+    const bool split_ok = g.split_ws != nullptr && g.batch == 1;
+    const bool both_outer = !g.a.kcontig && !g.b.kcontig;
+    const bool any_outer = !g.a.kcontig || !g.b.kcontig;
+    int want_split = 1;
     if (g.cfg < 0 || g.cfg >= NCFG) {
-        const bool narrow = g.N <= 64;
-        const int order_wide[] = {0, 1, 2, 4};
-        const int order_narrow[] = {3, 4};
-        const int* ord = narrow ? order_narrow : order_wide;
-        const int nord = narrow ? 2 : 4;
-        g.cfg = ord[nord - 1];
-        for (int i = 0; i < nord; ++i)
-            if (ntiles(CFGS[ord[i]], g) >= CUS) { g.cfg = ord[i]; break; }
+        if (g.N <= 64) {
+            g.cfg = ntiles(CFGS[3], g) >= CUS ? 3 : 4;
+        } else if (ntiles(CFGS[0], g) >= CUS) {
+            g.cfg = 0;
+        } else if (split_ok && both_outer && g.K >= 2048) {
+            const bool small_out = (int64_t)g.M * g.N < ((int64_t)2 << 20);
+            g.cfg = small_out ? 4 : 0;
+            want_split = 4;
+        } else if (split_ok && any_outer && g.K >= 2048) {
+            g.cfg = 3;
+            want_split = 2;
+        } else {
+            g.cfg = 4;
+        }
     }
     const TileCfg& c = CFGS[g.cfg];
     g.tiles_m = (g.M + c.bm - 1) / c.bm;
     g.tiles_n = (g.N + c.bn - 1) / c.bn;
     if (g.splits <= 0) {
-        g.splits = 1;
-        const int64_t t = ntiles(c, g);
-        if (g.split_ws && t < CUS && g.K >= 1024) {
-            int s = (int)((CUS + t - 1) / t);
-            if (s > 8) s = 8;
-            while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
-            g.splits = s;
-        }
+        int s = split_ok ? want_split : 1;
+        while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
+        g.splits = s;
     }
     if (g.splits > 1) {
         const int ksteps = (g.K + BK - 1) / BK;

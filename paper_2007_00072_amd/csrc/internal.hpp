@@ -20,10 +20,16 @@ int check_launch(const char* what);
 struct TraceScope {
     TraceScope(const char* label, hipStream_t st);
     ~TraceScope() { stop(); }
-    void stop();  // records the end event now (idempotent)
+    void stop();                // records the end event now (idempotent)
+    void next(const char* sub);  // ends the current record, starts one for the next launch of this scope
     int idx;
     hipStream_t st;
+    const char* label;
+    TraceScope* outer;
 };
+// Marks the start of a further launch of the innermost active scope (no-op
+// when tracing is off), so every launch has a record of its own.
+void trace_next(const char* sub);
 
 // p in [0,1); seed/site/layer -> kernel parameters (thr, scale computed in double).
 DropParams make_drop(float p, uint64_t seed, uint32_t site, uint32_t layer);
@@ -88,6 +94,9 @@ void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float*
 // out[map(c)] = sum_b part[b][c] for c < cols.  With H, P > 0 the columns
 // are (s, h, p) of a fused projection and go to outs[s][p*H + h].
 void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st);
+// three partial sets part[q][nblk][cols] -> o0, o1, o2 in one launch
+void run_colsum_finish3(int64_t rows, int cols, const float* part, float* o0, float* o1, float* o2,
+                        hipStream_t st);
 void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* part, float* dbq,
                            float* dbk, float* dbv, hipStream_t st);
 

@@ -578,7 +578,6 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     void *dgamma = B8(ws, e.m.dgamma), *dalpha = B8(ws, e.m.dalpha), *dbeta = B8(ws, e.m.dbeta);
     void* dqkv = B8(ws, e.m.dq);
     float* part = (float*)B8(ws, e.m.part);
-    const int nb = colsum_blocks(T);
 
     // LayerNorm-2 scale/shift grads, LayerNorm-2 dX, dropout dX, Linear-2 bias grad
     LnBwdArgs l2{};
@@ -591,9 +590,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     }
     {
         TraceScope t_("B1-2 colsum", st);
-        run_colsum_finish(T, (int)I, part, g->dg2, st);
-        run_colsum_finish(T, (int)I, part + (size_t)nb * I, g->dbe2, st);
-        run_colsum_finish(T, (int)I, part + (size_t)2 * nb * I, g->db2, st);
+        run_colsum_finish3(T, (int)I, part, g->dg2, g->dbe2, g->db2, st);
     }
     DM_TRY(check_launch("LayerNorm-2 backward"));
     // Linear 2 dX and dW
@@ -648,9 +645,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     }
     {
         TraceScope t_("B8-10 colsum", st);
-        run_colsum_finish(T, (int)I, part, g->dg1, st);
-        run_colsum_finish(T, (int)I, part + (size_t)nb * I, g->dbe1, st);
-        run_colsum_finish(T, (int)I, part + (size_t)2 * nb * I, g->dbo, st);
+        run_colsum_finish3(T, (int)I, part, g->dg1, g->dbe1, g->dbo, st);
     }
     DM_TRY(check_launch("LayerNorm-1 backward"));
     // attention backward into the token-major [T][3][H][P] gradient
@@ -663,6 +658,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     // input-bias grads
     TraceScope t20("B20 qkv_bias_grad", st);
     run_colsum_partial(dt, T, (int)(3 * I), dqkv, part, st);
+    trace_next("finish");
     run_colsum_finish_qkv(T, (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
     return check_launch("input-bias backward");
 }
@@ -743,6 +739,7 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     TraceScope t10("B10 out_bias_grad", st);
     if (x.layout == DM_BJI) {
         run_colsum_partial(dt, x.Tq, (int)x.I, dout, part, st);
+        trace_next("finish");
         run_colsum_finish(x.Tq, (int)x.I, part, g->dbo, st);
     } else {
         run_rowsum(dt, x.I, (int)x.Tq, dout, g->dbo, st);
@@ -757,6 +754,7 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
         DM_TRY(project_fused_bwd(x, x.layout, qin, bq, prm, dq, g, nullptr, st));
         TraceScope t_("B20 qkv_bias_grad", st);
         run_colsum_partial(dt, x.Tq, (int)(3 * x.H * x.P), bq, part, st);
+        trace_next("finish");
         run_colsum_finish_qkv(x.Tq, (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
     } else {
         TraceScope t_("B18-20 q,k,v_bwd", st);

@@ -115,7 +115,8 @@ _f["contract"] = _sig("contract", I32, I32, I32, I32, I32, I32, F32, P_, I32, I6
 _f["dm_last_error"] = _sig("dm_last_error", C.c_char_p)
 _f["dm_trace_enable"] = _sig("dm_trace_enable", I32, I32)
 _f["dm_trace_count"] = _sig("dm_trace_count", I32)
-_f["dm_trace_get"] = _sig("dm_trace_get", I32, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_float))
+_f["dm_trace_get"] = _sig("dm_trace_get", I32, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_char_p),
+                          C.POINTER(C.c_float))
 
 
 def ptr(t) -> Optional[int]:
@@ -291,13 +292,15 @@ def dm_trace_count() -> int:
 
 
 def dm_trace_get(i: int):
-    lab, ms = C.c_char_p(), C.c_float()
-    _call("dm_trace_get", i, C.byref(lab), C.byref(ms))
-    return lab.value.decode(), ms.value
+    """(label, sub-label, ms) of the i-th launch record."""
+    lab, sub, ms = C.c_char_p(), C.c_char_p(), C.c_float()
+    _call("dm_trace_get", i, C.byref(lab), C.byref(sub), C.byref(ms))
+    return lab.value.decode(), (sub.value or b"").decode(), ms.value
 
 
 def trace_records():
-    """All (label, ms) records of the current timing session."""
+    """All (label, sub-label, ms) records of the current timing session; an
+    operator's second launch carries a sub-label (e.g. "reduce")."""
     return [dm_trace_get(i) for i in range(dm_trace_count())]
 
 
