@@ -48,6 +48,13 @@ constexpr int BK = 64;  // k per step = 8 chunks of 8 elements
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
+// Pointer of segment `seg` without indexing the kernel-argument array at
+// run time (a dynamic index would turn it into a memory load).
+template <typename P>
+__device__ __forceinline__ P seg_ptr(P const (&p)[3], int seg) {
+    return seg == 0 ? p[0] : (seg == 1 ? p[1] : p[2]);
+}
+
 template <typename T> struct Mfma;
 template <> struct Mfma<half_t> {
     typedef half8 frag;
@@ -82,7 +89,7 @@ struct Loader<T, R, NT, true> {
         valid = 0;
         int seg0 = 0;
         const int64_t off0 = map_off(op.row, (uint32_t)(o0 < omax ? o0 : 0), op.nseg, &seg0);
-        const T* first = reinterpret_cast<const T*>(op.ptr[seg0]) + boff + off0;
+        const T* first = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg0)) + boff + off0;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int o = o0 + (tid >> 3) + i * (NT / 8);
@@ -90,7 +97,7 @@ struct Loader<T, R, NT, true> {
             if (o < omax) {
                 int seg = 0;
                 const int64_t off = map_off(op.row, (uint32_t)o, op.nseg, &seg);
-                rowp[i] = reinterpret_cast<const T*>(op.ptr[seg]) + boff + off;
+                rowp[i] = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off;
                 valid |= 1u << i;
             }
         }
@@ -153,7 +160,7 @@ struct Loader<T, R, NT, false> {
             const bool in = k < kend && o < omax;
             int seg = 0;
             const int64_t off = map_off(op.row, (uint32_t)(in ? k : 0), op.nseg, &seg);
-            reg[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(op.ptr[seg]) + boff + off +
+            reg[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off +
                                                      (in ? o : 0));
         }
     }
@@ -198,7 +205,7 @@ __device__ __forceinline__ void store_vec(const GemmArgs& g, int64_t coff, int m
             const uint32_t idx = e.bias_on_m ? (uint32_t)(e.contig_n ? m : m + q) : (uint32_t)(e.contig_n ? n + q : n);
             int bseg = 0;
             const int64_t bo = map_off(e.bias_map, idx, e.bias_nseg, &bseg);
-            vals[q] += to_f(reinterpret_cast<const T*>(e.bias[bseg])[bo]);
+            vals[q] += to_f(reinterpret_cast<const T*>(seg_ptr(e.bias, bseg))[bo]);
         }
     }
     int sm = 0, sn = 0;
@@ -212,7 +219,7 @@ __device__ __forceinline__ void store_vec(const GemmArgs& g, int64_t coff, int m
 #pragma unroll
             for (int q = 0; q < 8; ++q) vals[q] += rv[q];
         }
-        V8<float>::store(reinterpret_cast<float*>(e.ptr[seg]) + off, vals);
+        V8<float>::store(reinterpret_cast<float*>(seg_ptr(e.ptr, seg)) + off, vals);
     } else {
         if (e.resid) {
             float rv[8];
@@ -220,7 +227,70 @@ __device__ __forceinline__ void store_vec(const GemmArgs& g, int64_t coff, int m
 #pragma unroll
             for (int q = 0; q < 8; ++q) vals[q] += rv[q];
         }
-        V8<T>::store(reinterpret_cast<T*>(e.ptr[seg]) + off, vals);
+        V8<T>::store(reinterpret_cast<T*>(seg_ptr(e.ptr, seg)) + off, vals);
+    }
+}
+
+// ------------------------------------------------------------------ epilogue
+// 64-column passes of the fp32 tile through LDS (smem, at least
+// BM * 68 floats), then 16-byte stores along the contiguous output index;
+// with split k, float partial sums go to the split workspace instead.
+template <typename T, int BM, int BN, int WGM, int WGN>
+__device__ __forceinline__ void epilogue(const GemmArgs& g, const floatx4 (&acc)[BM / WGM / 16][BN / WGN / 16],
+                                         unsigned char* smem, int m0, int n0, uint32_t z, int sidx, int splits) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    constexpr int PW = 64, CLD = PW + 4;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    const int lr = lane & 15, lc = lane >> 4;
+    int dummy = 0;
+    float* Cs = reinterpret_cast<float*>(smem);
+    const bool partial = splits > 1;
+    const float alpha = partial ? 1.0f : g.c.alpha;
+    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
+    const bool contig_n = partial ? true : g.c.contig_n != 0;
+#pragma unroll
+    for (int p = 0; p < BN / PW; ++p) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int col = wn * WN + j * 16;
+            if (col < p * PW || col >= (p + 1) * PW) continue;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = wm * WM + i * 16 + lc * 4 + r;
+                    Cs[row * CLD + col - p * PW + lr] = acc[i][j][r] * alpha;
+                }
+        }
+        __syncthreads();
+        constexpr int NVEC = BM * PW / 8;
+        for (int v = tid; v < NVEC; v += NT) {
+            int m, n, lm, ln;
+            float vals[8];
+            if (contig_n) {
+                lm = v / (PW / 8); ln = (v % (PW / 8)) * 8;
+                m = m0 + lm; n = n0 + p * PW + ln;
+                if (m >= g.M || n >= g.N) continue;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) vals[q] = Cs[lm * CLD + ln + q];
+            } else {
+                ln = v / (BM / 8); lm = (v % (BM / 8)) * 8;
+                m = m0 + lm; n = n0 + p * PW + ln;
+                if (m >= g.M || n >= g.N) continue;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm + q) * CLD + ln];
+            }
+            if (partial) {
+                float* dst = g.split_ws + (((int64_t)sidx * g.batch + z) * g.M + m) * (int64_t)g.N + n;
+                V8<float>::store(dst, vals);
+            } else {
+                store_vec<T>(g, coff, m, n, vals);
+            }
+        }
+        __syncthreads();
     }
 }
 
@@ -370,53 +440,180 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma(GemmArgs g) {
         }
     }
 
-    // ---- epilogue: 64-column passes of the fp32 tile through LDS
-    float* Cs = reinterpret_cast<float*>(smem);
-    const bool partial = splits > 1;
-    const float alpha = partial ? 1.0f : g.c.alpha;
-    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
-    const bool contig_n = partial ? true : g.c.contig_n != 0;
+    epilogue<T, BM, BN, WGM, WGN>(g, acc, smem, m0, n0, z, sidx, splits);
+}
+
+
+// ------------------------------------------------------ asynchronous variant
+// Same LDS layouts and fragment reads as gemm_mfma, but operands move from
+// global memory straight into LDS (global_load_lds_dwordx4: lane l of a
+// wave writes 16 bytes at M0 + 16 l), through a ring of three LDS stages
+// with two k-steps in flight.  The copies are issued from inline assembly
+// so that the compiler neither waits for them early nor reorders LDS
+// accesses around them; each thread waits for its own copies of a stage
+// with s_waitcnt vmcnt before the barrier that publishes the stage.
+__device__ __attribute__((aligned(16))) uint32_t g_zero16[4] = {0u, 0u, 0u, 0u};
+
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_byte) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src),
+                 "s"(__builtin_amdgcn_readfirstlane(lds_byte))
+                 : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+template <typename T, int R, int NT, bool KC>
+struct Dma;
+
+// k-contiguous: slot q = i*NT + tid of a stage holds row q/8, physical
+// chunk q%8, i.e. logical chunk (q%8) ^ ((row>>1)&7).
+template <typename T, int R, int NT>
+struct Dma<T, R, NT, true> {
+    static constexpr int NV = R * 8 / NT;
+    static_assert(NV >= 1 && NV * NT == R * 8, "tile / thread mismatch");
+    const T* src[NV];  // element pointer of the thread's chunk at k = 0
+    int cofs[NV];      // k offset of that chunk
+
+    __device__ __forceinline__ void init(const Operand& op, int o0, int omax, int64_t boff) {
+        const int tid = threadIdx.x;
 #pragma unroll
-    for (int p = 0; p < BN / PW; ++p) {
+        for (int i = 0; i < NV; ++i) {
+            const int q = i * NT + tid, r = q >> 3, c = (q & 7) ^ ((r >> 1) & 7);
+            const int o = o0 + r < omax ? o0 + r : (omax > 0 ? omax - 1 : 0);
+            int seg = 0;
+            const int64_t off = map_off(op.row, (uint32_t)o, op.nseg, &seg);
+            src[i] = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off;
+            cofs[i] = c * 8;
+        }
+    }
+    __device__ __forceinline__ void issue(const Operand&, int k0, int kend, uint32_t stage_lds) const {
+        const int w = threadIdx.x >> 6;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int col = wn * WN + j * 16;
-            if (col < p * PW || col >= (p + 1) * PW) continue;
+        for (int i = 0; i < NV; ++i) {
+            const int k = k0 + cofs[i];
+            const void* p = k < kend ? (const void*)(src[i] + k) : (const void*)g_zero16;
+            lds_dma16(p, stage_lds + (uint32_t)(i * NT + w * 64) * 16u);
+        }
+    }
+};
+
+// outer-contiguous: slot q holds k-row q/CPR, physical chunk q%CPR, i.e.
+// logical chunk (q%CPR) ^ (2*(row&3)).
+template <typename T, int R, int NT>
+struct Dma<T, R, NT, false> {
+    static constexpr int CPR = R / 8;
+    static constexpr int NV = 64 * CPR / NT;
+    static_assert(NV >= 1 && NV * NT == 64 * CPR && CPR >= 8, "tile / thread mismatch");
+    int kr[NV];
+    int oofs[NV];
+    int64_t boff;
+
+    __device__ __forceinline__ void init(const Operand&, int o0, int omax, int64_t b) {
+        const int tid = threadIdx.x;
+        boff = b;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int q = i * NT + tid;
+            kr[i] = q / CPR;
+            const int c = (q % CPR) ^ (2 * (kr[i] & 3));
+            const int o = o0 + c * 8;
+            oofs[i] = o < omax ? o : 0;
+        }
+    }
+    __device__ __forceinline__ void issue(const Operand& op, int k0, int kend, uint32_t stage_lds) const {
+        const int w = threadIdx.x >> 6;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            // k0 < kend always holds here, so k0 is a valid row for the
+            // lanes whose own row is past the end (they read zeros instead)
+            const int k = k0 + kr[i];
+            const bool in = k < kend;
+            int seg = 0;
+            const int64_t off = map_off(op.row, (uint32_t)(in ? k : k0), op.nseg, &seg);
+            const T* src = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off + oofs[i];
+            lds_dma16(in ? (const void*)src : (const void*)g_zero16, stage_lds + (uint32_t)(i * NT + w * 64) * 16u);
+        }
+    }
+};
+
+template <typename T, int BM, int BN, int WGM, int WGN, bool AKC, bool BKC>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma(GemmArgs g) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    constexpr int AS = BM * BK, BS = BN * BK;       // elements per stage
+    constexpr int STAGE = (AS + BS) * (int)sizeof(T);  // bytes per stage
+    constexpr int SMEM = 3 * STAGE;
+    static_assert(BM * 68 * 4 <= SMEM, "epilogue staging does not fit");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
+    typedef Dma<T, BM, NT, AKC> DA;
+    typedef Dma<T, BN, NT, BKC> DB;
+    constexpr int NLOADS = DA::NV + DB::NV;  // copies per thread per stage
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    int tm, tn;
+    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int splits = g.splits > 1 ? g.splits : 1;
+    const uint32_t z = blockIdx.y / splits;
+    const int sidx = blockIdx.y - (int)z * splits;
+    const int kb = splits > 1 ? sidx * g.kper : 0;
+    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
+    int dummy = 0;
+    DA da;
+    DB db;
+    da.init(g.a, m0, g.M, map_off(g.a.batch, z, 1, &dummy));
+    db.init(g.b, n0, g.N, map_off(g.b.batch, z, 1, &dummy));
+    // only the fragment readers of the staged loaders are used
+    const Loader<T, BM, 64 * WGM * WGN, AKC> fa{};
+    const Loader<T, BN, 64 * WGM * WGN, BKC> fb{};
+    const uint32_t base = lds_addr(smem);
+
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    typedef typename Mfma<T>::frag frag;
+    const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+    auto issue = [&](int s) {
+        const uint32_t st = base + (uint32_t)((s % 3) * STAGE);
+        da.issue(g.a, kb + s * BK, ke, st);
+        db.issue(g.b, kb + s * BK, ke, st + (uint32_t)(AS * sizeof(T)));
+    };
+    if (nk > 0) issue(0);
+    if (nk > 1) issue(1);
+    for (int s = 0; s < nk; ++s) {
+        if (s + 1 < nk) wait_vm<NLOADS>();
+        else wait_vm<0>();
+        __builtin_amdgcn_s_barrier();
+        if (s + 2 < nk) issue(s + 2);
+        const T* Ab = reinterpret_cast<const T*>(smem + (s % 3) * STAGE);
+        const T* Bb = Ab + AS;
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 32) {
+            frag af[FM], bf[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) af[i] = __builtin_bit_cast(frag, fa.frag(Ab, wm * WM + i * 16, kk, lane));
+#pragma unroll
+            for (int j = 0; j < FN; ++j) bf[j] = __builtin_bit_cast(frag, fb.frag(Bb, wn * WN + j * 16, kk, lane));
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = wm * WM + i * 16 + lc * 4 + r;
-                    Cs[row * CLD + col - p * PW + lr] = acc[i][j][r] * alpha;
-                }
+                for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(af[i], bf[j], acc[i][j]);
         }
-        __syncthreads();
-        constexpr int NVEC = BM * PW / 8;
-        for (int v = tid; v < NVEC; v += NT) {
-            int m, n, lm, ln;
-            float vals[8];
-            if (contig_n) {
-                lm = v / (PW / 8); ln = (v % (PW / 8)) * 8;
-                m = m0 + lm; n = n0 + p * PW + ln;
-                if (m >= g.M || n >= g.N) continue;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) vals[q] = Cs[lm * CLD + ln + q];
-            } else {
-                ln = v / (BM / 8); lm = (v % (BM / 8)) * 8;
-                m = m0 + lm; n = n0 + p * PW + ln;
-                if (m >= g.M || n >= g.N) continue;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm + q) * CLD + ln];
-            }
-            if (partial) {
-                float* dst = g.split_ws + (((int64_t)sidx * g.batch + z) * g.M + m) * (int64_t)g.N + n;
-                V8<float>::store(dst, vals);
-            } else {
-                store_vec<T>(g, coff, m, n, vals);
-            }
-        }
-        __syncthreads();
     }
+    __syncthreads();
+    epilogue<T, BM, BN, WGM, WGN>(g, acc, smem, m0, n0, z, sidx, splits);
 }
 
 // Sum of the split-K partials in split order, then the regular epilogue.
@@ -498,7 +695,9 @@ __global__ __launch_bounds__(256) void gemm_f32(GemmArgs g) {
 struct TileCfg {
     int bm, bn, wgm, wgn;
 };
-constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2}};
+// 0-4: register-staged kernel; 5-8: asynchronous (global -> LDS) kernel.
+constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
+                            {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2}};
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
 template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH>
@@ -515,9 +714,27 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_mfma<T, BM, BN, WGM, WGN, DEPTH, false, false>), grid, block, 0, st, g);
 }
 
+template <typename T, int BM, int BN, int WGM, int WGN>
+void launch_dma(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig && g.b.kcontig)
+        hipLaunchKernelGGL((gemm_dma<T, BM, BN, WGM, WGN, true, true>), grid, block, 0, st, g);
+    else if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_dma<T, BM, BN, WGM, WGN, true, false>), grid, block, 0, st, g);
+    else if (g.b.kcontig)
+        hipLaunchKernelGGL((gemm_dma<T, BM, BN, WGM, WGN, false, true>), grid, block, 0, st, g);
+    else
+        hipLaunchKernelGGL((gemm_dma<T, BM, BN, WGM, WGN, false, false>), grid, block, 0, st, g);
+}
+
 template <typename T>
 void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
+        case 5: launch_dma<T, 256, 128, 2, 2>(g, st); break;
+        case 6: launch_dma<T, 128, 128, 2, 2>(g, st); break;
+        case 7: launch_dma<T, 256, 64, 4, 1>(g, st); break;
+        case 8: launch_dma<T, 128, 64, 2, 2>(g, st); break;
         case 0: launch_cfg<T, 256, 256, 2, 4, 1>(g, st); break;
         case 1: launch_cfg<T, 256, 128, 2, 2, 1>(g, st); break;
         case 2: launch_cfg<T, 128, 128, 2, 2, 1>(g, st); break;
@@ -539,15 +756,15 @@ int64_t ntiles(const TileCfg& c, const GemmArgs& g) {
 
 // Tile and split choice, from measurements of the layer's contraction
 // shapes on MI355X (every configuration x split 1/2/4): the 256x256 tile
-// when it alone gives every CU a block; for long k with an
-// outer-contiguous operand, 256x256 split four ways (weight gradients) or
-// 256x64 split two ways; otherwise 128x64.  Explicit choices (cfg >= 0,
-// splits > 0) are kept.
+// when it alone gives every CU a block; for weight gradients (both operands
+// outer-contiguous, long k) the 256x256 tile split four ways, or the
+// asynchronous 128x64 tile split four ways for small outputs; otherwise the
+// asynchronous 128x64 tile.  Explicit choices (cfg >= 0, splits > 0) are
+// kept.
 void choose(GemmArgs& g) {
     constexpr int64_t CUS = 256;
     const bool split_ok = g.split_ws != nullptr && g.batch == 1;
     const bool both_outer = !g.a.kcontig && !g.b.kcontig;
-    const bool any_outer = !g.a.kcontig || !g.b.kcontig;
     int want_split = 1;
     if (g.cfg < 0 || g.cfg >= NCFG) {
         if (g.N <= 64) {
@@ -556,13 +773,10 @@ void choose(GemmArgs& g) {
             g.cfg = 0;
         } else if (split_ok && both_outer && g.K >= 2048) {
             const bool small_out = (int64_t)g.M * g.N < ((int64_t)2 << 20);
-            g.cfg = small_out ? 4 : 0;
+            g.cfg = small_out ? 8 : 0;
             want_split = 4;
-        } else if (split_ok && any_outer && g.K >= 2048) {
-            g.cfg = 3;
-            want_split = 2;
         } else {
-            g.cfg = 4;
+            g.cfg = 8;
         }
     }
     const TileCfg& c = CFGS[g.cfg];
