@@ -24,6 +24,11 @@ def short_name(sym: str) -> str:
         dt = "f16" if m.group(1) == "DF16_" else "bf16"
         mode = lambda b: "k" if b == "1" else "o"
         return f"gemm_mfma<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},A:{mode(m.group(7))},B:{mode(m.group(8))}>"
+    m = re.search(r"gemm_dmaI(DF16_|DF16b)Li(\d+)ELi(\d+)ELi(\d)ELi(\d)ELb(\d)ELb(\d)", sym)
+    if m:
+        dt = "f16" if m.group(1) == "DF16_" else "bf16"
+        mode = lambda b: "k" if b == "1" else "o"
+        return f"gemm_dma<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},A:{mode(m.group(6))},B:{mode(m.group(7))}>"
     m = re.search(r"_ZN2dm12_GLOBAL__N_1\d+(\w+?)I", sym)
     if m:
         return m.group(1)
