@@ -253,9 +253,15 @@ int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t
  * C[z][m][n] = alpha * sum_k A[z][m][k] * B[z][k][n] (+ bias[n]) with
  * row-major operands, `a_trans` / `b_trans` selecting A stored [K][M] /
  * B stored [N][K]; C dtype = dtype (out_f32 = 1: float C).  Strides in
- * elements between batches: sa, sb, sc.  tile_cfg selects the block tile
- * (0: 256x256, 1: 256x128, 2: 128x128, 3: 256x64, 4: 128x64; -1: chosen
- * from the shape); splits > 1 splits k, using `ws` (ws_bytes >=
+ * elements between batches: sa, sb, sc.  tile_cfg selects kernel and block
+ * tile (register-staged 16x16x32 MFMA kernel: 0: 256x256, 1: 256x128,
+ * 2: 128x128, 3: 256x64, 4: 128x64; asynchronous-copy 16x16x32 kernel:
+ * 5: 256x128, 6: 128x128, 7: 256x64, 8: 128x64; asynchronous-copy
+ * 32x32x16 kernel: 9: 256x256, 10: 256x128 (4 waves), 11: 128x128,
+ * 12: 256x128 (8 waves), 13: 256x256 with 4 waves of 128x128, 14: 256x256
+ * with 8 waves of 128x64; -1:
+ * chosen from the shape; other values are
+ * DM_ERR_ARG); splits > 1 splits k, using `ws` (ws_bytes >=
  * splits*batch*M*N*4) for partial sums; splits = 0 chooses (no split
  * without ws). */
 int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, float alpha,

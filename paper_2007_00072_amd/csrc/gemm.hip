@@ -48,6 +48,11 @@ constexpr int BK = 64;  // k per step = 8 chunks of 8 elements
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
+// Barrier for hand-offs through LDS: waits for this thread's LDS accesses
+// only.  (__syncthreads would also wait for every outstanding global store,
+// which in the epilogue serialises the passes on the store latency.)
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Pointer of segment `seg` without indexing the kernel-argument array at
 // run time (a dynamic index would turn it into a memory load).
 template <typename P>
@@ -231,6 +236,110 @@ __device__ __forceinline__ void store_vec(const GemmArgs& g, int64_t coff, int m
     }
 }
 
+// Writes one 64-column pass of the output tile, staged in LDS as fp32 rows
+// of 68 floats: 16-byte stores along whichever output index is contiguous
+// (or float partial sums to the split workspace).
+template <typename T, int BM, int NT>
+__device__ __forceinline__ void store_pass(const GemmArgs& g, const float* Cs, int m0, int n0, uint32_t z, int sidx,
+                                           bool partial, int64_t coff, bool contig_n) {
+    constexpr int PW = 64, CLD = PW + 4;
+    constexpr int NVEC = BM * PW / 8;
+    for (int v = threadIdx.x; v < NVEC; v += NT) {
+        int m, n, lm, ln;
+        float vals[8];
+        if (contig_n) {
+            lm = v / (PW / 8); ln = (v % (PW / 8)) * 8;
+            m = m0 + lm; n = n0 + ln;
+            if (m >= g.M || n >= g.N) continue;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] = Cs[lm * CLD + ln + q];
+        } else {
+            ln = v / (BM / 8); lm = (v % (BM / 8)) * 8;
+            m = m0 + lm; n = n0 + ln;
+            if (m >= g.M || n >= g.N) continue;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm + q) * CLD + ln];
+        }
+        if (partial) {
+            float* dst = g.split_ws + (((int64_t)sidx * g.batch + z) * g.M + m) * (int64_t)g.N + n;
+            V8<float>::store(dst, vals);
+        } else {
+            store_vec<T>(g, coff, m, n, vals);
+        }
+    }
+}
+
+// Store pass for affine outputs (one pointer, unit stride along the
+// contiguous index, bias along either index): residual and bias loads for
+// all of a thread's vectors are issued before its stores.
+template <typename T, int BM, int NT>
+__device__ __forceinline__ void store_pass_affine(const GemmArgs& g, const float* Cs, int m0, int n0, int64_t coff,
+                                                  bool contig_n) {
+    constexpr int PW = 64, CLD = PW + 4;
+    constexpr int NVEC = BM * PW / 8;
+    constexpr int VPT = NVEC / NT;
+    static_assert(VPT * NT == NVEC, "pass / thread mismatch");
+    const Epilogue& e = g.c;
+    const int tid = threadIdx.x;
+    int lm[VPT], ln[VPT];
+    bool ok[VPT];
+    int64_t off[VPT];
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int v = tid + i * NT;
+        if (contig_n) { lm[i] = v / (PW / 8); ln[i] = (v % (PW / 8)) * 8; }
+        else { ln[i] = v / (BM / 8); lm[i] = (v % (BM / 8)) * 8; }
+        const int m = m0 + lm[i], n = n0 + ln[i];
+        ok[i] = m < g.M && n < g.N;
+        off[i] = coff + (contig_n ? (int64_t)m * g.ldc + n : (int64_t)m + (int64_t)n * g.ldc);
+    }
+    float add[VPT][8];
+#pragma unroll
+    for (int i = 0; i < VPT; ++i)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) add[i][q] = 0.f;
+    if (g.bias_mode == 1) {
+        const T* b = reinterpret_cast<const T*>(e.bias[0]);
+#pragma unroll
+        for (int i = 0; i < VPT; ++i)
+            if (ok[i]) V8<T>::load(b + (contig_n ? n0 + ln[i] : m0 + lm[i]), add[i]);
+    } else if (g.bias_mode == 2) {
+        const T* b = reinterpret_cast<const T*>(e.bias[0]);
+#pragma unroll
+        for (int i = 0; i < VPT; ++i)
+            if (ok[i]) {
+                const float bv = to_f(b[contig_n ? m0 + lm[i] : n0 + ln[i]]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) add[i][q] = bv;
+            }
+    }
+    if (e.resid) {
+#pragma unroll
+        for (int i = 0; i < VPT; ++i)
+            if (ok[i]) {
+                float rv[8];
+                if (e.out_f32) V8<float>::load(reinterpret_cast<const float*>(e.resid) + off[i], rv);
+                else V8<T>::load(reinterpret_cast<const T*>(e.resid) + off[i], rv);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) add[i][q] += rv[q];
+            }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        float vals[8];
+        if (contig_n) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] = Cs[lm[i] * CLD + ln[i] + q] + add[i][q];
+        } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm[i] + q) * CLD + ln[i]] + add[i][q];
+        }
+        if (!ok[i]) continue;
+        if (e.out_f32) V8<float>::store(reinterpret_cast<float*>(e.ptr[0]) + off[i], vals);
+        else V8<T>::store(reinterpret_cast<T*>(e.ptr[0]) + off[i], vals);
+    }
+}
+
 // ------------------------------------------------------------------ epilogue
 // 64-column passes of the fp32 tile through LDS (smem, at least
 // BM * 68 floats), then 16-byte stores along the contiguous output index;
@@ -265,32 +374,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& g, const floatx4 (&acc)
                     Cs[row * CLD + col - p * PW + lr] = acc[i][j][r] * alpha;
                 }
         }
-        __syncthreads();
-        constexpr int NVEC = BM * PW / 8;
-        for (int v = tid; v < NVEC; v += NT) {
-            int m, n, lm, ln;
-            float vals[8];
-            if (contig_n) {
-                lm = v / (PW / 8); ln = (v % (PW / 8)) * 8;
-                m = m0 + lm; n = n0 + p * PW + ln;
-                if (m >= g.M || n >= g.N) continue;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) vals[q] = Cs[lm * CLD + ln + q];
-            } else {
-                ln = v / (BM / 8); lm = (v % (BM / 8)) * 8;
-                m = m0 + lm; n = n0 + p * PW + ln;
-                if (m >= g.M || n >= g.N) continue;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) vals[q] = Cs[(lm + q) * CLD + ln];
-            }
-            if (partial) {
-                float* dst = g.split_ws + (((int64_t)sidx * g.batch + z) * g.M + m) * (int64_t)g.N + n;
-                V8<float>::store(dst, vals);
-            } else {
-                store_vec<T>(g, coff, m, n, vals);
-            }
-        }
-        __syncthreads();
+        lds_barrier();
+        if (g.affine && !partial) store_pass_affine<T, BM, NT>(g, Cs, m0, n0 + p * PW, coff, contig_n);
+        else store_pass<T, BM, NT>(g, Cs, m0, n0 + p * PW, z, sidx, partial, coff, contig_n);
+        lds_barrier();
     }
 }
 
@@ -469,13 +556,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
 
-template <typename T, int R, int NT, bool KC>
+template <typename T, int R, int NT, bool KC, int SW = 2>
 struct Dma;
 
 // k-contiguous: slot q = i*NT + tid of a stage holds row q/8, physical
 // chunk q%8, i.e. logical chunk (q%8) ^ ((row>>1)&7).
-template <typename T, int R, int NT>
-struct Dma<T, R, NT, true> {
+template <typename T, int R, int NT, int SW>
+struct Dma<T, R, NT, true, SW> {
     static constexpr int NV = R * 8 / NT;
     static_assert(NV >= 1 && NV * NT == R * 8, "tile / thread mismatch");
     const T* src[NV];  // element pointer of the thread's chunk at k = 0
@@ -505,12 +592,12 @@ struct Dma<T, R, NT, true> {
 };
 
 // outer-contiguous: slot q holds k-row q/CPR, physical chunk q%CPR, i.e.
-// logical chunk (q%CPR) ^ (2*(row&3)).
-template <typename T, int R, int NT>
-struct Dma<T, R, NT, false> {
+// logical chunk (q%CPR) ^ (SW*(row&3)).
+template <typename T, int R, int NT, int SW>
+struct Dma<T, R, NT, false, SW> {
     static constexpr int CPR = R / 8;
     static constexpr int NV = 64 * CPR / NT;
-    static_assert(NV >= 1 && NV * NT == 64 * CPR && CPR >= 8, "tile / thread mismatch");
+    static_assert(NV >= 1 && NV * NT == 64 * CPR && CPR >= 8 && 3 * SW < CPR, "tile / thread mismatch");
     int kr[NV];
     int oofs[NV];
     int64_t boff;
@@ -522,7 +609,7 @@ struct Dma<T, R, NT, false> {
         for (int i = 0; i < NV; ++i) {
             const int q = i * NT + tid;
             kr[i] = q / CPR;
-            const int c = (q % CPR) ^ (2 * (kr[i] & 3));
+            const int c = (q % CPR) ^ (SW * (kr[i] & 3));
             const int o = o0 + c * 8;
             oofs[i] = o < omax ? o : 0;
         }
@@ -616,6 +703,426 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma(GemmArgs g) {
     epilogue<T, BM, BN, WGM, WGN>(g, acc, smem, m0, n0, z, sidx, splits);
 }
 
+// ------------------------------------------------- 32x32x16 MFMA variant
+// v_mfma_f32_32x32x16: lane l holds A row l%32 (B column l%32) at k values
+// 8(l/32) .. +7; result element r of lane l is row 8(r/4) + 4(l/32) + r%4,
+// column l%32.  This instruction runs at the full MFMA rate with only a few
+// independent accumulators, where the 16x16x32 form needs many more.
+template <typename T> struct Mfma32;
+template <> struct Mfma32<half_t> {
+    typedef half8 frag;
+    __device__ __forceinline__ static floatx16 run(frag a, frag b, floatx16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+};
+template <> struct Mfma32<bf16_t> {
+    typedef bf16x8 frag;
+    __device__ __forceinline__ static floatx16 run(frag a, frag b, floatx16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <typename T, int R, bool KC>
+struct Frag32;
+
+// k-contiguous LDS rows (BK elements, chunks swizzled by swz): lane l reads
+// row ob + l%32, chunk kk/8 + l/32.
+template <typename T, int R>
+struct Frag32<T, R, true> {
+    __device__ __forceinline__ static u32x4 read(const T* lds, int ob, int kk, int lane) {
+        const int r = ob + (lane & 31);
+        const int c = (kk >> 3) + (lane >> 5);
+        return *reinterpret_cast<const u32x4*>(lds + r * BK + swz(r, c) * 8);
+    }
+};
+
+// [k][outer] LDS rows of R elements, chunk c of row r stored at
+// c ^ (4 (r & 3)): lanes 16g .. 16g+15 take outer ob + 16 (g % 2) + l%16 at
+// k = kk + 8 (g / 2) .. +7 with two transposing reads (the lane pattern of
+// ds_read_b64_tr_b16 is described at Loader<T, R, NT, false>).  The four
+// k-rows one read touches land on four different 64-byte bank groups.
+template <typename T, int R>
+struct Frag32<T, R, false> {
+    static_assert(R >= 128, "outer tile too narrow for the swizzle");
+    __device__ __forceinline__ static u32x4 read(const T* lds, int ob, int kk, int lane) {
+        typedef short s4 __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) s4 lds_s4;
+        const int g = lane >> 4, sl = lane & 15;
+        const int r = kk + 8 * (g >> 1) + (sl >> 2);
+        const int c = ((ob + 16 * (g & 1)) >> 3) + ((sl & 3) >> 1);
+        const T* p = lds + r * R + ((c ^ (4 * (sl >> 2))) * 8) + (sl & 1) * 4;
+        const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)p);
+        const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p + 4 * R));
+        u32x4 out;
+        out[0] = (uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
+        out[1] = (uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
+        out[2] = (uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
+        out[3] = (uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
+        return out;
+    }
+};
+
+template <typename T, int BM, int BN, int WGM, int WGN>
+__device__ __forceinline__ void epilogue32(const GemmArgs& g, const floatx16 (&acc)[BM / WGM / 32][BN / WGN / 32],
+                                           unsigned char* smem, int m0, int n0, uint32_t z, int sidx, int splits) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int FM = WM / 32, FN = WN / 32;
+    constexpr int PW = 64, CLD = PW + 4;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    int dummy = 0;
+    float* Cs = reinterpret_cast<float*>(smem);
+    const bool partial = splits > 1;
+    const float alpha = partial ? 1.0f : g.c.alpha;
+    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
+    const bool contig_n = partial ? true : g.c.contig_n != 0;
+#pragma unroll
+    for (int p = 0; p < BN / PW; ++p) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int col = wn * WN + j * 32;
+            if (col < p * PW || col >= (p + 1) * PW) continue;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    Cs[row * CLD + col - p * PW + (lane & 31)] = acc[i][j][r] * alpha;
+                }
+        }
+        lds_barrier();
+        if (g.affine && !partial) store_pass_affine<T, BM, NT>(g, Cs, m0, n0 + p * PW, coff, contig_n);
+        else store_pass<T, BM, NT>(g, Cs, m0, n0 + p * PW, z, sidx, partial, coff, contig_n);
+        lds_barrier();
+    }
+}
+
+// Waits until at most `after` stages of this thread's copies are still in
+// flight (the copies of one stage are NL instructions).
+template <int NL, int STAGES>
+__device__ __forceinline__ void wait_stages(int after) {
+    if (STAGES >= 4 && after >= 2) wait_vm<2 * NL>();
+    else if (STAGES >= 3 && after >= 1) wait_vm<NL>();
+    else wait_vm<0>();
+}
+
+// Asynchronous-copy contraction on 32x32x16 MFMAs: a ring of STAGES LDS
+// stages (BK = 64 each) with STAGES - 1 k-steps in flight; inside a stage
+// the fragments of the next 16-wide k slice are read while the current
+// slice's MFMAs run.
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool AKC, bool BKC>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_x32(GemmArgs g) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int FM = WM / 32, FN = WN / 32;
+    constexpr int AS = BM * BK, BS = BN * BK;
+    constexpr int STAGE = (AS + BS) * (int)sizeof(T);
+    constexpr int RING = STAGES * STAGE;
+    constexpr int SMEM = RING > BM * 68 * 4 ? RING : BM * 68 * 4;
+    static_assert(STAGES >= 2 && STAGES <= 4 && FM >= 1 && FN >= 1, "configuration");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
+    typedef Dma<T, BM, NT, AKC, 4> DA;
+    typedef Dma<T, BN, NT, BKC, 4> DB;
+    constexpr int NLOADS = DA::NV + DB::NV;
+    typedef typename Mfma32<T>::frag frag;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    int tm, tn;
+    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int splits = g.splits > 1 ? g.splits : 1;
+    const uint32_t z = blockIdx.y / splits;
+    const int sidx = blockIdx.y - (int)z * splits;
+    const int kb = splits > 1 ? sidx * g.kper : 0;
+    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
+    int dummy = 0;
+    DA da;
+    DB db;
+    da.init(g.a, m0, g.M, map_off(g.a.batch, z, 1, &dummy));
+    db.init(g.b, n0, g.N, map_off(g.b.batch, z, 1, &dummy));
+    const uint32_t base = lds_addr(smem);
+
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+    auto issue = [&](int s) {
+        const uint32_t st = base + (uint32_t)((s % STAGES) * STAGE);
+        da.issue(g.a, kb + s * BK, ke, st);
+        db.issue(g.b, kb + s * BK, ke, st + (uint32_t)(AS * sizeof(T)));
+    };
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nk) issue(s);
+    for (int s = 0; s < nk; ++s) {
+        const int after = min(STAGES - 2, nk - 1 - s);
+        wait_stages<NLOADS, STAGES>(after);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (s + STAGES - 1 < nk) issue(s + STAGES - 1);
+        const T* Ab = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
+        const T* Bb = Ab + AS;
+        frag af[2][FM], bf[2][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[0][i] = __builtin_bit_cast(frag, Frag32<T, BM, AKC>::read(Ab, wm * WM + i * 32, 0, lane));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bf[0][j] = __builtin_bit_cast(frag, Frag32<T, BN, BKC>::read(Bb, wn * WN + j * 32, 0, lane));
+#pragma unroll
+        for (int q = 0; q < BK / 16; ++q) {
+            const int cur = q & 1, nxt = cur ^ 1;
+            if (q + 1 < BK / 16) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    af[nxt][i] = __builtin_bit_cast(frag, Frag32<T, BM, AKC>::read(Ab, wm * WM + i * 32, (q + 1) * 16, lane));
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    bf[nxt][j] = __builtin_bit_cast(frag, Frag32<T, BN, BKC>::read(Bb, wn * WN + j * 32, (q + 1) * 16, lane));
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = Mfma32<T>::run(af[cur][i], bf[cur][j], acc[i][j]);
+        }
+    }
+    __syncthreads();
+    epilogue32<T, BM, BN, WGM, WGN>(g, acc, smem, m0, n0, z, sidx, splits);
+}
+
+// -------------------------------------------- 256x256 kernel, 4 waves
+// Each wave owns a 128x128 quarter of the block tile (4x4 tiles of
+// 32x32x16 MFMAs, 256 accumulators), which halves the LDS fragment traffic
+// per MFMA against 128x64 wave tiles.  k-step 32, a ring of four LDS stages
+// fed by asynchronous copies three k-steps ahead.  Fragments of the next
+// 16-wide k slice are read while the current slice's MFMAs run, across the
+// stage boundary too: the one barrier per k-step sits between the two
+// slices of a step, after every wave has read all of that step's
+// fragments.
+constexpr int BK2 = 32;  // k per stage of the 4-wave kernel = 4 chunks of 8
+
+// k-contiguous rows of 32 elements; chunk c of row r at c ^ ((r >> 2) & 3):
+// 16 consecutive rows then cover all 64 banks with one 16-byte read each.
+__device__ __forceinline__ int swz4(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+
+template <typename T, int R, int NT, bool KC>
+struct Dma2;
+
+// k-contiguous: slot q = i*NT + tid of a stage holds row q/4, physical
+// chunk q%4.
+template <typename T, int R, int NT>
+struct Dma2<T, R, NT, true> {
+    static constexpr int NV = R * 4 / NT;
+    static_assert(NV >= 1 && NV * NT == R * 4, "tile / thread mismatch");
+    const T* src[NV];
+    int cofs[NV];
+
+    __device__ __forceinline__ void init(const Operand& op, int o0, int omax, int64_t boff) {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int q = i * NT + tid, r = q >> 2, c = swz4(r, q & 3);
+            const int o = o0 + r < omax ? o0 + r : (omax > 0 ? omax - 1 : 0);
+            int seg = 0;
+            const int64_t off = map_off(op.row, (uint32_t)o, op.nseg, &seg);
+            src[i] = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off;
+            cofs[i] = c * 8;
+        }
+    }
+    __device__ __forceinline__ void issue(const Operand&, int k0, int kend, uint32_t stage_lds) const {
+        const int w = threadIdx.x >> 6;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int k = k0 + cofs[i];
+            const void* p = k < kend ? (const void*)(src[i] + k) : (const void*)g_zero16;
+            lds_dma16(p, stage_lds + (uint32_t)(i * NT + w * 64) * 16u);
+        }
+    }
+    // lane l: row ob + l%32, k = kk + 8 (l / 32) .. +7
+    __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
+        const int r = ob + (lane & 31);
+        const int c = (kk >> 3) + (lane >> 5);
+        return *reinterpret_cast<const u32x4*>(lds + r * BK2 + swz4(r, c) * 8);
+    }
+};
+
+// outer-contiguous: [k][outer] rows of R elements, slot q holds k-row q/CPR,
+// physical chunk q%CPR = logical chunk ^ (4 (row & 3)); fragments as in
+// Frag32<T, R, false>.
+template <typename T, int R, int NT>
+struct Dma2<T, R, NT, false> {
+    static constexpr int CPR = R / 8;
+    static constexpr int NV = BK2 * CPR / NT;
+    static_assert(NV >= 1 && NV * NT == BK2 * CPR && CPR >= 16, "tile / thread mismatch");
+    int kr[NV];
+    int oofs[NV];
+    int64_t boff;
+
+    __device__ __forceinline__ void init(const Operand&, int o0, int omax, int64_t b) {
+        const int tid = threadIdx.x;
+        boff = b;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int q = i * NT + tid;
+            kr[i] = q / CPR;
+            const int c = (q % CPR) ^ (4 * (kr[i] & 3));
+            const int o = o0 + c * 8;
+            oofs[i] = o < omax ? o : 0;
+        }
+    }
+    __device__ __forceinline__ void issue(const Operand& op, int k0, int kend, uint32_t stage_lds) const {
+        const int w = threadIdx.x >> 6;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            // k0 < kend here, so k0 is a valid row for lanes past the end
+            const int k = k0 + kr[i];
+            const bool in = k < kend;
+            int seg = 0;
+            const int64_t off = map_off(op.row, (uint32_t)(in ? k : k0), op.nseg, &seg);
+            const T* src = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off + oofs[i];
+            lds_dma16(in ? (const void*)src : (const void*)g_zero16, stage_lds + (uint32_t)(i * NT + w * 64) * 16u);
+        }
+    }
+    __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
+        return Frag32<T, R, false>::read(lds, ob, kk, lane);
+    }
+};
+
+template <typename T, int WGM, int WGN, bool AKC, bool BKC>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_big(GemmArgs g) {
+    constexpr int BM = 256, BN = 256, NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32, STAGES = 4;
+    static_assert(WN % 64 == 0, "wave tile must cover whole 64-column passes");
+    constexpr int AS = BM * BK2, BS = BN * BK2;
+    constexpr int STAGE = (AS + BS) * (int)sizeof(T);
+    constexpr int SMEM = STAGES * STAGE;
+    static_assert(BM * 68 * 4 <= SMEM, "epilogue staging does not fit");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
+    typedef Dma2<T, BM, NT, AKC> DA;
+    typedef Dma2<T, BN, NT, BKC> DB;
+    constexpr int NL = DA::NV + DB::NV;  // copies per thread per stage
+    typedef typename Mfma32<T>::frag frag;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    int tm, tn;
+    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int splits = g.splits > 1 ? g.splits : 1;
+    const uint32_t z = blockIdx.y / splits;
+    const int sidx = blockIdx.y - (int)z * splits;
+    const int kb = splits > 1 ? sidx * g.kper : 0;
+    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
+    int dummy = 0;
+    DA da;
+    DB db;
+    da.init(g.a, m0, g.M, map_off(g.a.batch, z, 1, &dummy));
+    db.init(g.b, n0, g.N, map_off(g.b.batch, z, 1, &dummy));
+    const uint32_t base = lds_addr(smem);
+
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int nk = ke > kb ? (ke - kb + BK2 - 1) / BK2 : 0;
+    auto issue = [&](int s) {
+        const uint32_t st = base + (uint32_t)((s & 3) * STAGE);
+        da.issue(g.a, kb + s * BK2, ke, st);
+        db.issue(g.b, kb + s * BK2, ke, st + (uint32_t)(AS * sizeof(T)));
+    };
+    auto stage_a = [&](int s) { return reinterpret_cast<const T*>(smem + (s & 3) * STAGE); };
+    frag a0[FM], b0[FN], a1[FM], b1[FN];
+    auto read = [&](frag (&a)[FM], frag (&b)[FN], int s, int kk) {
+        const T* A = stage_a(s);
+        const T* B = A + AS;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, kk, lane));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[j] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + j * 32, kk, lane));
+    };
+    auto mma = [&](const frag (&a)[FM], const frag (&b)[FN]) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = Mfma32<T>::run(a[i], b[j], acc[i][j]);
+    };
+
+    if (nk > 0) {
+        issue(0);
+        if (nk > 1) issue(1);
+        if (nk > 2) issue(2);
+        if (nk > 2) wait_vm<2 * NL>();
+        else if (nk > 1) wait_vm<NL>();
+        else wait_vm<0>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        read(a0, b0, 0, 0);
+    }
+    // The fences keep each fragment read ahead of the MFMAs it overlaps (the
+    // compiler would otherwise sink the reads to their first use).
+    for (int s = 0; s < nk; ++s) {
+        // slice 0 of step s; fragments of slice 1 meanwhile
+        read(a1, b1, s, 16);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a0, b0);
+        // step s+1 must have landed (copies of s+2 may still fly), and this
+        // wave's reads of step s are complete before any wave refills a slot
+        if (s + 2 < nk) wait_vm<NL>();
+        else wait_vm<0>();
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (s + 3 < nk) issue(s + 3);
+        // slice 1 of step s; fragments of slice 0 of step s+1 meanwhile
+        // (after the last step this reads a stale slot, unused; keeping the
+        // read unconditional keeps the LDS wait counts exact)
+        read(a0, b0, s + 1, 0);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+
+    // epilogue: 64-column passes through LDS
+    constexpr int PW = 64, CLD = PW + 4;
+    float* Cs = reinterpret_cast<float*>(smem);
+    const bool partial = splits > 1;
+    const float alpha = partial ? 1.0f : g.c.alpha;
+    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
+    const bool contig_n = partial ? true : g.c.contig_n != 0;
+#pragma unroll
+    for (int p = 0; p < BN / PW; ++p) {
+        if (wn == p / (WN / PW)) {
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj) {
+                const int j = (p % (WN / PW)) * 2 + jj;
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                        Cs[row * CLD + jj * 32 + (lane & 31)] = acc[i][j][r] * alpha;
+                    }
+            }
+        }
+        lds_barrier();
+        if (g.affine && !partial) store_pass_affine<T, BM, NT>(g, Cs, m0, n0 + p * PW, coff, contig_n);
+        else store_pass<T, BM, NT>(g, Cs, m0, n0 + p * PW, z, sidx, partial, coff, contig_n);
+        lds_barrier();
+    }
+}
+
 // Sum of the split-K partials in split order, then the regular epilogue.
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_reduce(GemmArgs g) {
@@ -695,9 +1202,13 @@ __global__ __launch_bounds__(256) void gemm_f32(GemmArgs g) {
 struct TileCfg {
     int bm, bn, wgm, wgn;
 };
-// 0-4: register-staged kernel; 5-8: asynchronous (global -> LDS) kernel.
+// 0-4: register-staged kernel; 5-8: asynchronous (global -> LDS) kernel;
+// 9-12: asynchronous kernel on 32x32x16 MFMAs; 13, 14: 256x256 kernel with
+// a four-stage ring of 32-wide k-steps, 4 waves of 128x128 or 8 of 128x64.
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
-                            {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2}};
+                            {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
+                            {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
+                            {256, 256, 2, 2}, {256, 256, 2, 4}};
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
 template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH>
@@ -728,9 +1239,39 @@ void launch_dma(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_dma<T, BM, BN, WGM, WGN, false, false>), grid, block, 0, st, g);
 }
 
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+void launch_x32(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig && g.b.kcontig)
+        hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, true, true>), grid, block, 0, st, g);
+    else if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, true, false>), grid, block, 0, st, g);
+    else if (g.b.kcontig)
+        hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, false, true>), grid, block, 0, st, g);
+    else
+        hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, false, false>), grid, block, 0, st, g);
+}
+
+template <typename T, int WGM, int WGN>
+void launch_big(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig && g.b.kcontig) hipLaunchKernelGGL((gemm_big<T, WGM, WGN, true, true>), grid, block, 0, st, g);
+    else if (g.a.kcontig) hipLaunchKernelGGL((gemm_big<T, WGM, WGN, true, false>), grid, block, 0, st, g);
+    else if (g.b.kcontig) hipLaunchKernelGGL((gemm_big<T, WGM, WGN, false, true>), grid, block, 0, st, g);
+    else hipLaunchKernelGGL((gemm_big<T, WGM, WGN, false, false>), grid, block, 0, st, g);
+}
+
 template <typename T>
 void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
+        case 13: launch_big<T, 2, 2>(g, st); break;
+        case 14: launch_big<T, 2, 4>(g, st); break;
+        case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
+        case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
+        case 11: launch_x32<T, 128, 128, 2, 2, 4>(g, st); break;
+        case 12: launch_x32<T, 256, 128, 4, 2, 3>(g, st); break;
         case 5: launch_dma<T, 256, 128, 2, 2>(g, st); break;
         case 6: launch_dma<T, 128, 128, 2, 2>(g, st); break;
         case 7: launch_dma<T, 256, 64, 4, 1>(g, st); break;
@@ -755,12 +1296,12 @@ int64_t ntiles(const TileCfg& c, const GemmArgs& g) {
 }
 
 // Tile and split choice, from measurements of the layer's contraction
-// shapes on MI355X (every configuration x split 1/2/4): the 256x256 tile
-// when it alone gives every CU a block; for weight gradients (both operands
-// outer-contiguous, long k) the 256x256 tile split four ways, or the
-// asynchronous 128x64 tile split four ways for small outputs; otherwise the
-// asynchronous 128x64 tile.  Explicit choices (cfg >= 0, splits > 0) are
-// kept.
+// shapes on MI355X (every configuration x split 1/2/4): the 256x256
+// 32x32x16-MFMA tile when it alone gives (nearly) every CU a block; for
+// weight gradients (both operands outer-contiguous, long k) that tile split
+// four ways, or the asynchronous 128x64 tile split four ways for small
+// outputs; otherwise the asynchronous 128x64 tile.  Explicit choices
+// (cfg >= 0, splits > 0) are kept.
 void choose(GemmArgs& g) {
     constexpr int64_t CUS = 256;
     const bool split_ok = g.split_ws != nullptr && g.batch == 1;
@@ -768,12 +1309,12 @@ void choose(GemmArgs& g) {
     int want_split = 1;
     if (g.cfg < 0 || g.cfg >= NCFG) {
         if (g.N <= 64) {
-            g.cfg = ntiles(CFGS[3], g) >= CUS ? 3 : 4;
-        } else if (ntiles(CFGS[0], g) >= CUS) {
-            g.cfg = 0;
+            g.cfg = 8;
+        } else if (ntiles(CFGS[9], g) * 4 >= CUS * 3) {
+            g.cfg = 9;
         } else if (split_ok && both_outer && g.K >= 2048) {
             const bool small_out = (int64_t)g.M * g.N < ((int64_t)2 << 20);
-            g.cfg = small_out ? 8 : 0;
+            g.cfg = small_out ? 8 : 9;
             want_split = 4;
         } else {
             g.cfg = 8;
@@ -792,6 +1333,23 @@ void choose(GemmArgs& g) {
         g.kper = (ksteps + g.splits - 1) / g.splits * BK;
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
+}
+
+// Classifies the output addressing for the fast store pass.
+void set_affine(GemmArgs& g) {
+    const Epilogue& e = g.c;
+    const bool cn = e.contig_n != 0;
+    g.affine = 0;
+    g.bias_mode = 0;
+    g.ldc = 0;
+    if (e.nseg != 1 || e.mmap.r0 != 0 || e.nmap.r0 != 0) return;
+    if (cn ? e.nmap.s0 != 1 : e.mmap.s0 != 1) return;
+    if (e.bias[0]) {
+        if (e.bias_nseg != 1 || e.bias_map.r0 != 0 || e.bias_map.s0 != 1) return;
+        g.bias_mode = (e.bias_on_m != 0) == !cn ? 1 : 2;
+    }
+    g.ldc = cn ? e.mmap.s0 : e.nmap.s0;
+    g.affine = 1;
 }
 
 }  // namespace
@@ -813,6 +1371,7 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
             return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
         if (!g.split_ws) g.splits = 1;
         choose(g);
+        set_affine(g);
         if (g.splits > 1 && (int64_t)g.splits * g.batch * g.M * g.N > g.split_cap)
             return set_error(DM_ERR_WORKSPACE, "split-k scratch too small");
         if ((int64_t)g.batch * g.splits > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction grid too large");

@@ -79,6 +79,11 @@ struct GemmArgs {
     int64_t split_cap;     // floats available at split_ws
     int kper;              // k range per split (set by the launcher)
     int cfg;               // tile configuration index; < 0 lets the launcher choose
+    // set by the launcher: outputs at coff(z) + m * ldc + n (contig_n) or
+    // coff(z) + m + n * ldc, one pointer; bias_mode 0 none, 1 along the
+    // contiguous output index (unit stride), 2 along the other index
+    int affine, bias_mode;
+    int64_t ldc;
 };
 
 // Scratch bytes for a split-K contraction.

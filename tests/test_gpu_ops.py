@@ -275,7 +275,7 @@ def test_contract_modes(lib, dt, a_trans, b_trans, batch, M, N, K):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("cfg", list(range(15)))
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (0, 0), (1, 0), (1, 1)])
 def test_contract_tile_configs(lib, dt, cfg, a_trans, b_trans):
     # ragged in every dimension for every block tile
@@ -283,7 +283,7 @@ def test_contract_tile_configs(lib, dt, cfg, a_trans, b_trans):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("cfg,splits", [(2, 2), (4, 3), (0, 4), (3, 5), (5, 2), (6, 3), (7, 4), (8, 2)])
+@pytest.mark.parametrize("cfg,splits", [(2, 2), (4, 3), (0, 4), (3, 5), (5, 2), (6, 3), (7, 4), (8, 2), (9, 2), (10, 3), (11, 4), (12, 2), (13, 3), (14, 2)])
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (1, 0)])
 def test_contract_split_k(lib, dt, cfg, splits, a_trans, b_trans):
     _contract_case(lib, dt, a_trans, b_trans, 2, 136, 264, 1096, cfg=cfg, splits=splits)
