@@ -258,7 +258,8 @@ int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t
  * 2: 128x128, 3: 256x64, 4: 128x64; asynchronous-copy 16x16x32 kernel:
  * 5: 256x128, 6: 128x128, 7: 256x64, 8: 128x64; asynchronous-copy
  * 32x32x16 kernel: 9: 256x256, 10: 256x128 (4 waves), 11: 128x128,
- * 12: 256x128 (8 waves), 13: 256x256 with 4 waves of 128x128, 14: 256x256
+ * 12: 256x128 (8 waves), 13: 256x256 with 4 waves of 128x128 (plain
+ * strided operands, K a multiple of 32; otherwise run as 14), 14: 256x256
  * with 8 waves of 128x64; -1:
  * chosen from the shape; other values are
  * DM_ERR_ARG); splits > 1 splits k, using `ws` (ws_bytes >=

@@ -33,11 +33,14 @@ template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float x) { return (
 template <typename T> struct V8;
 
 template <> struct V8<half_t> {
-    __device__ __forceinline__ static void load(const half_t* p, float v[8]) {
-        u32x4 r = *reinterpret_cast<const u32x4*>(p);
+    // 8 elements already loaded as 16 raw bytes
+    __device__ __forceinline__ static void unpack(u32x4 r, float v[8]) {
         half8 h = __builtin_bit_cast(half8, r);
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = (float)h[i];
+    }
+    __device__ __forceinline__ static void load(const half_t* p, float v[8]) {
+        unpack(*reinterpret_cast<const u32x4*>(p), v);
     }
     __device__ __forceinline__ static void store(half_t* p, const float v[8]) {
         half8 h;
@@ -48,14 +51,17 @@ template <> struct V8<half_t> {
 };
 
 template <> struct V8<bf16_t> {
-    __device__ __forceinline__ static void load(const bf16_t* p, float v[8]) {
-        u32x4 r = *reinterpret_cast<const u32x4*>(p);
-        // bf16 -> fp32 is a 16-bit shift of the bit pattern
+    // 8 elements already loaded as 16 raw bytes; bf16 -> fp32 is a 16-bit
+    // shift of the bit pattern
+    __device__ __forceinline__ static void unpack(u32x4 r, float v[8]) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             v[2 * i] = __builtin_bit_cast(float, r[i] << 16);
             v[2 * i + 1] = __builtin_bit_cast(float, r[i] & 0xFFFF0000u);
         }
+    }
+    __device__ __forceinline__ static void load(const bf16_t* p, float v[8]) {
+        unpack(*reinterpret_cast<const u32x4*>(p), v);
     }
     __device__ __forceinline__ static void store(bf16_t* p, const float v[8]) {
         bf16x8 h;

@@ -205,12 +205,24 @@ template <typename T>
 __device__ __forceinline__ void store_vec(const GemmArgs& g, int64_t coff, int m, int n, float vals[8]) {
     const Epilogue& e = g.c;
     if (e.bias[0]) {
+        // The 8 outputs share one bias index when the bias runs along the
+        // other output index; along the contiguous index they are 8
+        // consecutive indices, which stay inside one digit of the bias map
+        // (vectors start at multiples of 8 and the launcher checks that the
+        // map's lowest radix is a multiple of 8), so one map evaluation and
+        // a stride give all of them.
+        const bool along = (e.bias_on_m != 0) == (e.contig_n == 0);
+        const uint32_t idx = (uint32_t)(e.bias_on_m ? m : n);
+        int bseg = 0;
+        const int64_t bo = map_off(e.bias_map, idx, e.bias_nseg, &bseg);
+        const T* bp = reinterpret_cast<const T*>(seg_ptr(e.bias, bseg)) + bo;
+        if (along) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const uint32_t idx = e.bias_on_m ? (uint32_t)(e.contig_n ? m : m + q) : (uint32_t)(e.contig_n ? n + q : n);
-            int bseg = 0;
-            const int64_t bo = map_off(e.bias_map, idx, e.bias_nseg, &bseg);
-            vals[q] += to_f(reinterpret_cast<const T*>(seg_ptr(e.bias, bseg))[bo]);
+            for (int q = 0; q < 8; ++q) vals[q] += to_f(bp[(int64_t)q * e.bias_map.s0]);
+        } else {
+            const float bv = to_f(bp[0]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) vals[q] += bv;
         }
     }
     int sm = 0, sn = 0;
@@ -762,39 +774,129 @@ struct Frag32<T, R, false> {
     }
 };
 
-template <typename T, int BM, int BN, int WGM, int WGN>
-__device__ __forceinline__ void epilogue32(const GemmArgs& g, const floatx16 (&acc)[BM / WGM / 32][BN / WGN / 32],
-                                           unsigned char* smem, int m0, int n0, uint32_t z, int sidx, int splits) {
-    constexpr int NT = 64 * WGM * WGN;
-    constexpr int WM = BM / WGM, WN = BN / WGN;
+// True when map m is affine over every aligned block of 32 indices (its
+// lowest radix is unbounded or a multiple of 32), so offset(x + d) =
+// offset(x) + d * s0 and the segment stay fixed for x % 32 == 0, d < 32.
+inline bool block32_linear(const IdxMap& m) { return m.r0 == 0 || m.r0 % 32 == 0; }
+
+// Epilogue of the 32x32x16 kernels, straight from the accumulators: no LDS
+// staging and no barrier, so each wave stores as soon as its own tile is
+// done.  In a 32x32 result, lane l holds column l % 32 at rows 8 (r / 4) +
+// 4 (l / 32) + r % 4, r = 0..15: with the output contiguous along n, the
+// 32 lanes of a half-wave write 32 consecutive elements of one row (the
+// memory system merges them into one run); contiguous along m, each lane
+// writes the 4 consecutive rows of one r / 4 group as one 8-byte (16-byte
+// for fp32) store.  Output offsets are evaluated once per 32-wide block of
+// rows and columns: the launcher keeps contractions whose output maps are
+// not affine over such blocks (g.blk32), or that take a residual operand or
+// a bias along m, on the 16x16x32 kernels.  Biases are loaded before the
+// first store: vector-memory waits count loads and stores together, so a
+// load between stores would wait for all of them.  With split k the values
+// are float partial sums into the split workspace.
+// Stores of one wave's WM x WN tile for one output type and orientation
+// (the dispatcher below picks the instance once, so the unrolled stores
+// carry no per-element branches).  Per 32-row block i: ubase = uniform
+// byte address of row mb (segment on m, batch), per 32x32 block j: the
+// lane's column offset; inside the block, rows step by rsb bytes.  M is a
+// multiple of 8, so each group of 4 rows is either wholly inside or
+// wholly outside.
+template <typename OutT, bool CN, int WM, int WN>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, const floatx16 (&acc)[WM / 32][WN / 32], int mw,
+                                           int nw, int64_t coff, const float (&bn)[WN / 32]) {
     constexpr int FM = WM / 32, FN = WN / 32;
-    constexpr int PW = 64, CLD = PW + 4;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WGN, wn = wave % WGN;
-    int dummy = 0;
-    float* Cs = reinterpret_cast<float*>(smem);
-    const bool partial = splits > 1;
-    const float alpha = partial ? 1.0f : g.c.alpha;
-    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
-    const bool contig_n = partial ? true : g.c.contig_n != 0;
+    const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
+    const Epilogue& e = g.c;
+    const float alpha = e.alpha;
+    const int64_t rs = g.affine ? (CN ? g.ldc : 1) : e.mmap.s0;
+    const uint32_t rsb = (uint32_t)(rs * (int64_t)sizeof(OutT));
 #pragma unroll
-    for (int p = 0; p < BN / PW; ++p) {
+    for (int i = 0; i < FM; ++i) {
+        const int mb = mw + i * 32;
+        if (mb >= g.M) break;
+        int64_t rbase;
+        int mseg = 0;
+        if (g.affine) rbase = (int64_t)mb * rs;
+        else rbase = map_off(e.mmap, (uint32_t)mb, e.seg_on_m ? e.nseg : 1, &mseg);
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int col = wn * WN + j * 32;
-            if (col < p * PW || col >= (p + 1) * PW) continue;
+            const int n = nw + j * 32 + c;
+            int nsg = 0;
+            int64_t ncol;
+            if (g.affine) ncol = CN ? (int64_t)n : (int64_t)n * g.ldc;
+            else ncol = map_off(e.nmap, (uint32_t)(n < g.N ? n : 0), e.seg_on_m ? 1 : e.nseg, &nsg);
+            char* pb = reinterpret_cast<char*>(seg_ptr(e.ptr, e.seg_on_m ? mseg : nsg)) +
+                       (coff + rbase + ncol) * (int64_t)sizeof(OutT) + (CN ? (uint32_t)(4 * h) * rsb
+                                                                          : (uint32_t)(4 * h) * sizeof(OutT));
+            const bool col_ok = n < g.N;
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
+            for (int rg = 0; rg < 4; ++rg) {
+                if (!col_ok || mb + 8 * rg + 4 * h >= g.M) continue;
+                float v[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = acc[i][j][4 * rg + k] * alpha + bn[j];
+                if (CN) {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        *reinterpret_cast<OutT*>(pb + (uint32_t)(8 * rg + k) * rsb) = from_f<OutT>(v[k]);
+                } else {
+                    char* q = pb + 8 * rg * (int)sizeof(OutT);
+                    if constexpr (sizeof(OutT) == 4) {
+                        floatx4 o = {v[0], v[1], v[2], v[3]};
+                        *reinterpret_cast<floatx4*>(q) = o;
+                    } else {
+                        OutT o4[4];
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) o4[k] = from_f<OutT>(v[k]);
+                        *reinterpret_cast<u32x2*>(q) = __builtin_bit_cast(u32x2, o4);
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <typename T, int WM, int WN>
+__device__ __forceinline__ void epilogue_direct(const GemmArgs& g, const floatx16 (&acc)[WM / 32][WN / 32],
+                                                int mw, int nw, uint32_t z, int sidx, int splits) {
+    constexpr int FM = WM / 32, FN = WN / 32;
+    const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
+    const Epilogue& e = g.c;
+    if (splits > 1) {
+        float* base = g.split_ws + ((int64_t)sidx * g.batch + z) * g.M * (int64_t)g.N;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int n = nw + j * 32 + c;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                    Cs[row * CLD + col - p * PW + (lane & 31)] = acc[i][j][r] * alpha;
+                    const int m = mw + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+                    if (m < g.M && n < g.N) base[(int64_t)m * g.N + n] = acc[i][j][r];
                 }
+            }
+        return;
+    }
+    int dummy = 0;
+    const int64_t coff = map_off(e.batch, z, 1, &dummy);
+    // bias along n (the launcher keeps bias-along-m contractions on the
+    // 16x16x32 kernels): one value per 32-column block, loaded before any store
+    float bn[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        bn[j] = 0.f;
+        if (e.bias[0]) {
+            const int n = nw + j * 32 + c;
+            int bseg = 0;
+            const int64_t bo = map_off(e.bias_map, (uint32_t)(n < g.N ? n : 0), e.bias_nseg, &bseg);
+            bn[j] = to_f(reinterpret_cast<const T*>(seg_ptr(e.bias, bseg))[bo]);
         }
-        lds_barrier();
-        if (g.affine && !partial) store_pass_affine<T, BM, NT>(g, Cs, m0, n0 + p * PW, coff, contig_n);
-        else store_pass<T, BM, NT>(g, Cs, m0, n0 + p * PW, z, sidx, partial, coff, contig_n);
-        lds_barrier();
+    }
+    if (e.contig_n) {
+        if (e.out_f32) store_tile<float, true, WM, WN>(g, acc, mw, nw, coff, bn);
+        else store_tile<T, true, WM, WN>(g, acc, mw, nw, coff, bn);
+    } else {
+        if (e.out_f32) store_tile<float, false, WM, WN>(g, acc, mw, nw, coff, bn);
+        else store_tile<T, false, WM, WN>(g, acc, mw, nw, coff, bn);
     }
 }
 
@@ -821,6 +923,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x32(GemmArgs g) {
     constexpr int RING = STAGES * STAGE;
     constexpr int SMEM = RING > BM * 68 * 4 ? RING : BM * 68 * 4;
     static_assert(STAGES >= 2 && STAGES <= 4 && FM >= 1 && FN >= 1, "configuration");
+    static_assert(WGM * WGN * 32 * (WN + 8) * 4 <= SMEM, "epilogue strips do not fit");
     __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
     typedef Dma<T, BM, NT, AKC, 4> DA;
     typedef Dma<T, BN, NT, BKC, 4> DB;
@@ -891,8 +994,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x32(GemmArgs g) {
                 for (int j = 0; j < FN; ++j) acc[i][j] = Mfma32<T>::run(af[cur][i], bf[cur][j], acc[i][j]);
         }
     }
-    __syncthreads();
-    epilogue32<T, BM, BN, WGM, WGN>(g, acc, smem, m0, n0, z, sidx, splits);
+    epilogue_direct<T, WM, WN>(g, acc, m0 + wm * WM, n0 + wn * WN, z, sidx, splits);
 }
 
 // -------------------------------------------- 256x256 kernel, 4 waves
@@ -1001,7 +1103,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_big(GemmArgs g) {
     constexpr int AS = BM * BK2, BS = BN * BK2;
     constexpr int STAGE = (AS + BS) * (int)sizeof(T);
     constexpr int SMEM = STAGES * STAGE;
-    static_assert(BM * 68 * 4 <= SMEM, "epilogue staging does not fit");
+    static_assert(WGM * WGN * 32 * (WN + 8) * 4 <= SMEM, "epilogue strips do not fit");
     __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
     typedef Dma2<T, BM, NT, AKC> DA;
     typedef Dma2<T, BN, NT, BKC> DB;
@@ -1092,35 +1194,253 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_big(GemmArgs g) {
         mma(a1, b1);
         __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
+    epilogue_direct<T, WM, WN>(g, acc, m0 + wm * WM, n0 + wn * WN, z, sidx, splits);
+}
 
-    // epilogue: 64-column passes through LDS
-    constexpr int PW = 64, CLD = PW + 4;
-    float* Cs = reinterpret_cast<float*>(smem);
-    const bool partial = splits > 1;
-    const float alpha = partial ? 1.0f : g.c.alpha;
-    const int64_t coff = partial ? 0 : map_off(g.c.batch, z, 1, &dummy);
-    const bool contig_n = partial ? true : g.c.contig_n != 0;
+// ------------------------------------------ lean 256x256 kernel, 4 waves
+// The same tile, wave layout, LDS layouts and pipeline as gemm_big, for the
+// contractions whose operands are plain strided matrices (row map a single
+// stride), whose k is a multiple of 32 and whose output is affine: a single
+// base pointer per operand row and a single pointer increment per k-step
+// replace the per-copy index arithmetic and bounds selects, and the
+// epilogue writes straight from the accumulators with one address per 32x32
+// block.  Rows and columns past M / N read a clamped valid row and their
+// results are never stored, so no copy needs a bounds test.
+
+// k-contiguous operand: slot q = i*NT + tid of a stage holds row q/4,
+// physical chunk q%4 = logical chunk ^ ((row >> 2) & 3).
+template <typename T, int NT>
+struct LeanK {
+    static constexpr int NV = 256 * 4 / NT;
+    const T* src[NV];
+    __device__ __forceinline__ void init(const T* base, int64_t ld, int o0, int omax) {
+        const int tid = threadIdx.x;
 #pragma unroll
-    for (int p = 0; p < BN / PW; ++p) {
-        if (wn == p / (WN / PW)) {
+        for (int i = 0; i < NV; ++i) {
+            const int q = i * NT + tid, r = q >> 2, c = swz4(r, q & 3);
+            const int o = o0 + r < omax ? o0 + r : omax - 1;
+            src[i] = base + (int64_t)o * ld + c * 8;
+        }
+    }
+    __device__ __forceinline__ void issue(int k0, uint32_t st) const {
+        const int w = threadIdx.x >> 6;
 #pragma unroll
-            for (int jj = 0; jj < 2; ++jj) {
-                const int j = (p % (WN / PW)) * 2 + jj;
+        for (int i = 0; i < NV; ++i) lds_dma16(src[i] + k0, st + (uint32_t)(i * NT + w * 64) * 16u);
+    }
+    __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
+        return Dma2<T, 256, NT, true>::frag(lds, ob, kk, lane);
+    }
+};
+
+// outer-contiguous operand ([k][outer] rows of 256 elements in LDS): slot q
+// holds k-row q/32, physical chunk q%32 = logical chunk ^ (4 (row & 3)).
+template <typename T, int NT>
+struct LeanO {
+    static constexpr int NV = BK2 * 32 / NT;
+    const T* src[NV];
+    int64_t step;  // elements per k-step
+    __device__ __forceinline__ void init(const T* base, int64_t ld, int o0, int omax) {
+        const int tid = threadIdx.x;
+        step = (int64_t)BK2 * ld;
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
+        for (int i = 0; i < NV; ++i) {
+            const int q = i * NT + tid, kr = q >> 5, c = (q & 31) ^ (4 * (kr & 3));
+            const int o = o0 + c * 8 < omax ? o0 + c * 8 : 0;
+            src[i] = base + (int64_t)kr * ld + o;
+        }
+    }
+    __device__ __forceinline__ void issue(int s, uint32_t st) const {
+        const int w = threadIdx.x >> 6;
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                        Cs[row * CLD + jj * 32 + (lane & 31)] = acc[i][j][r] * alpha;
-                    }
+        for (int i = 0; i < NV; ++i) lds_dma16(src[i] + s * step, st + (uint32_t)(i * NT + w * 64) * 16u);
+    }
+    __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
+        return Frag32<T, 256, false>::read(lds, ob, kk, lane);
+    }
+};
+
+template <typename T, bool KC, int NT>
+struct Lean;
+template <typename T, int NT>
+struct Lean<T, true, NT> : LeanK<T, NT> {
+    __device__ __forceinline__ void go(int s, uint32_t st) const { this->issue(s * BK2, st); }
+};
+template <typename T, int NT>
+struct Lean<T, false, NT> : LeanO<T, NT> {
+    __device__ __forceinline__ void go(int s, uint32_t st) const { this->issue(s, st); }
+};
+
+// Affine output straight from the accumulators (layout of a 32x32 result:
+// lane l holds column l % 32 at rows 8 (r / 4) + 4 (l / 32) + r % 4): along
+// n, the 32 lanes of a half-wave write 32 consecutive elements of a row;
+// along m, each lane writes the 4 consecutive rows of a group as one
+// vector.  Bias (along n) is loaded before the first store.
+template <typename OutT, bool CN, int FM, int FN>
+__device__ __forceinline__ void lean_store(const GemmArgs& g, const floatx16 (&acc)[FM][FN], OutT* C, int64_t ldc,
+                                           int mw, int nw, const float (&bn)[FN], float alpha) {
+    const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int mb = mw + i * 32;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int n = nw + j * 32 + c;
+            if (n >= g.N) continue;
+            OutT* pb = CN ? C + (int64_t)(mb + 4 * h) * ldc + n : C + (int64_t)n * ldc + mb + 4 * h;
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                if (mb + 8 * rg + 4 * h >= g.M) continue;
+                float v[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = acc[i][j][4 * rg + k] * alpha + bn[j];
+                if constexpr (CN) {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) pb[(int64_t)(8 * rg + k) * ldc] = from_f<OutT>(v[k]);
+                } else if constexpr (sizeof(OutT) == 4) {
+                    floatx4 o = {v[0], v[1], v[2], v[3]};
+                    *reinterpret_cast<floatx4*>(pb + 8 * rg) = o;
+                } else {
+                    OutT o4[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) o4[k] = from_f<OutT>(v[k]);
+                    *reinterpret_cast<u32x2*>(pb + 8 * rg) = __builtin_bit_cast(u32x2, o4);
+                }
             }
         }
-        lds_barrier();
-        if (g.affine && !partial) store_pass_affine<T, BM, NT>(g, Cs, m0, n0 + p * PW, coff, contig_n);
-        else store_pass<T, BM, NT>(g, Cs, m0, n0 + p * PW, z, sidx, partial, coff, contig_n);
-        lds_barrier();
     }
+}
+
+template <typename T, bool AKC, bool BKC>
+__global__ __launch_bounds__(256) void gemm_lean(GemmArgs g) {
+    constexpr int NT = 256, WM = 128, WN = 128, FM = 4, FN = 4, STAGES = 4;
+    constexpr int AS = 256 * BK2, BS = 256 * BK2;
+    constexpr int STAGE = (AS + BS) * (int)sizeof(T);
+    __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
+    typedef Lean<T, AKC, NT> DA;
+    typedef Lean<T, BKC, NT> DB;
+    constexpr int NL = DA::NV + DB::NV;
+    typedef typename Mfma32<T>::frag frag;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    int tm, tn;
+    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    const int m0 = tm * 256, n0 = tn * 256;
+    const int splits = g.splits > 1 ? g.splits : 1;
+    const uint32_t z = blockIdx.y / splits;
+    const int sidx = blockIdx.y - (int)z * splits;
+    const int kb = splits > 1 ? sidx * g.kper : 0;
+    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
+    int dummy = 0;
+    // operand bases at k = kb (row map: a single stride s0)
+    const T* abase = reinterpret_cast<const T*>(g.a.ptr[0]) + map_off(g.a.batch, z, 1, &dummy) +
+                     (AKC ? (int64_t)kb : (int64_t)kb * g.a.row.s0);
+    const T* bbase = reinterpret_cast<const T*>(g.b.ptr[0]) + map_off(g.b.batch, z, 1, &dummy) +
+                     (BKC ? (int64_t)kb : (int64_t)kb * g.b.row.s0);
+    DA da;
+    DB db;
+    da.init(abase, g.a.row.s0, m0, g.M);
+    db.init(bbase, g.b.row.s0, n0, g.N);
+    const uint32_t base = lds_addr(smem);
+
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int nk = (ke - kb) / BK2;
+    auto issue = [&](int s) {
+        const uint32_t st = base + (uint32_t)((s & 3) * STAGE);
+        da.go(s, st);
+        db.go(s, st + (uint32_t)(AS * sizeof(T)));
+    };
+    frag a[2][FM], b[2][FN];
+    auto read = [&](int buf, int s, int kk) {
+        const T* A = reinterpret_cast<const T*>(smem + (s & 3) * STAGE);
+        const T* B = A + AS;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[buf][i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, kk, lane));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[buf][j] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + j * 32, kk, lane));
+    };
+    auto mma = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = Mfma32<T>::run(a[buf][i], b[buf][j], acc[i][j]);
+    };
+
+    if (nk > 0) {
+        issue(0);
+        if (nk > 1) issue(1);
+        if (nk > 2) issue(2);
+        if (nk > 2) wait_vm<2 * NL>();
+        else if (nk > 1) wait_vm<NL>();
+        else wait_vm<0>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        read(0, 0, 0);
+    }
+    // per k-step: slice 0's MFMAs while slice 1's fragments are read; then
+    // (step s+1 landed, this wave done reading step s) barrier, refill the
+    // slot of step s-1 with step s+3, and slice 1's MFMAs while slice 0 of
+    // step s+1 is read (after the last step that read is of a stale slot,
+    // unused)
+    for (int s = 0; s < nk; ++s) {
+        read(1, s, 16);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        mma(0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (s + 2 < nk) wait_vm<NL>();
+        else wait_vm<0>();
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (s + 3 < nk) issue(s + 3);
+        read(0, s + 1, 0);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        mma(1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // split k: float partial sums, row-major [M][N] per split, through the
+    // same store routine as float outputs (one code path keeps registers few)
+    const int mw = m0 + wm * WM, nw = n0 + wn * WN, c = lane & 31;
+    const Epilogue& e = g.c;
+    const bool part = splits > 1;
+    float bn[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int n = nw + j * 32 + c;
+        bn[j] = (!part && e.bias[0]) ? to_f(reinterpret_cast<const T*>(e.bias[0])[n < g.N ? n : 0]) : 0.f;
+    }
+    const int64_t coff = map_off(e.batch, z, 1, &dummy);
+    if (part || (e.contig_n && e.out_f32)) {
+        float* C = part ? g.split_ws + ((int64_t)sidx * g.batch + z) * g.M * (int64_t)g.N
+                        : reinterpret_cast<float*>(e.ptr[0]) + coff;
+        lean_store<float, true, FM, FN>(g, acc, C, part ? (int64_t)g.N : g.ldc, mw, nw, bn, part ? 1.0f : e.alpha);
+    } else if (e.contig_n) {
+        lean_store<T, true, FM, FN>(g, acc, reinterpret_cast<T*>(e.ptr[0]) + coff, g.ldc, mw, nw, bn, e.alpha);
+    } else if (e.out_f32) {
+        lean_store<float, false, FM, FN>(g, acc, reinterpret_cast<float*>(e.ptr[0]) + coff, g.ldc, mw, nw, bn, e.alpha);
+    } else {
+        lean_store<T, false, FM, FN>(g, acc, reinterpret_cast<T*>(e.ptr[0]) + coff, g.ldc, mw, nw, bn, e.alpha);
+    }
+}
+
+// True when the lean kernel takes this contraction (see gemm_lean).
+bool lean_ok(const GemmArgs& g) {
+    const Epilogue& e = g.c;
+    if (g.K % BK2 || (g.splits > 1 && g.kper % BK2)) return false;
+    if (g.a.nseg != 1 || g.a.row.r0 != 0 || g.b.nseg != 1 || g.b.row.r0 != 0) return false;
+    if (!g.affine || e.resid) return false;
+    if (e.bias[0] && (e.bias_on_m || e.bias_nseg != 1 || e.bias_map.r0 != 0 || e.bias_map.s0 != 1)) return false;
+    return true;
 }
 
 // Sum of the split-K partials in split order, then the regular epilogue.
@@ -1204,7 +1524,8 @@ struct TileCfg {
 };
 // 0-4: register-staged kernel; 5-8: asynchronous (global -> LDS) kernel;
 // 9-12: asynchronous kernel on 32x32x16 MFMAs; 13, 14: 256x256 kernel with
-// a four-stage ring of 32-wide k-steps, 4 waves of 128x128 or 8 of 128x64.
+// a four-stage ring of 32-wide k-steps, 4 waves of 128x128 (the lean kernel;
+// contractions it does not take run as 14) or 8 of 128x64.
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
@@ -1253,6 +1574,15 @@ void launch_x32(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, false, false>), grid, block, 0, st, g);
 }
 
+template <typename T>
+void launch_lean(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    if (g.a.kcontig && g.b.kcontig) hipLaunchKernelGGL((gemm_lean<T, true, true>), grid, dim3(256), 0, st, g);
+    else if (g.a.kcontig) hipLaunchKernelGGL((gemm_lean<T, true, false>), grid, dim3(256), 0, st, g);
+    else if (g.b.kcontig) hipLaunchKernelGGL((gemm_lean<T, false, true>), grid, dim3(256), 0, st, g);
+    else hipLaunchKernelGGL((gemm_lean<T, false, false>), grid, dim3(256), 0, st, g);
+}
+
 template <typename T, int WGM, int WGN>
 void launch_big(const GemmArgs& g, hipStream_t st) {
     dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
@@ -1266,7 +1596,7 @@ void launch_big(const GemmArgs& g, hipStream_t st) {
 template <typename T>
 void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
-        case 13: launch_big<T, 2, 2>(g, st); break;
+        case 13: launch_lean<T>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -1296,12 +1626,13 @@ int64_t ntiles(const TileCfg& c, const GemmArgs& g) {
 }
 
 // Tile and split choice, from measurements of the layer's contraction
-// shapes on MI355X (every configuration x split 1/2/4): the 256x256
-// 32x32x16-MFMA tile when it alone gives (nearly) every CU a block; for
-// weight gradients (both operands outer-contiguous, long k) that tile split
-// four ways, or the asynchronous 128x64 tile split four ways for small
-// outputs; otherwise the asynchronous 128x64 tile.  Explicit choices
-// (cfg >= 0, splits > 0) are kept.
+// shapes on MI355X (every configuration x split 1/2/4): the 256x256 tile
+// (the lean 4-wave kernel when the contraction qualifies, else the 8-wave
+// one) when it alone gives (nearly) every CU a block; for weight gradients
+// (both operands outer-contiguous, long k) that tile split four ways, or the
+// asynchronous 128x64 tile split four ways for small outputs; otherwise the
+// asynchronous 128x64 tile.  Explicit choices (cfg >= 0, splits > 0) are
+// kept.
 void choose(GemmArgs& g) {
     constexpr int64_t CUS = 256;
     const bool split_ok = g.split_ws != nullptr && g.batch == 1;
@@ -1310,16 +1641,20 @@ void choose(GemmArgs& g) {
     if (g.cfg < 0 || g.cfg >= NCFG) {
         if (g.N <= 64) {
             g.cfg = 8;
-        } else if (ntiles(CFGS[9], g) * 4 >= CUS * 3) {
-            g.cfg = 9;
+        } else if (ntiles(CFGS[13], g) * 4 >= CUS * 3) {
+            g.cfg = 13;
         } else if (split_ok && both_outer && g.K >= 2048) {
             const bool small_out = (int64_t)g.M * g.N < ((int64_t)2 << 20);
-            g.cfg = small_out ? 8 : 9;
+            g.cfg = small_out ? 8 : 13;
             want_split = 4;
         } else {
             g.cfg = 8;
         }
     }
+    // the 32x32x16 kernels' epilogue takes no residual operand, no bias
+    // along m and only output maps affine over 32-wide blocks
+    if ((g.c.resid || (g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
+    // the lean 256x256 kernel's conditions are checked after the split is set
     const TileCfg& c = CFGS[g.cfg];
     g.tiles_m = (g.M + c.bm - 1) / c.bm;
     g.tiles_n = (g.N + c.bn - 1) / c.bn;
@@ -1333,12 +1668,14 @@ void choose(GemmArgs& g) {
         g.kper = (ksteps + g.splits - 1) / g.splits * BK;
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
+    if (g.cfg == 13 && !lean_ok(g)) g.cfg = 14;
 }
 
 // Classifies the output addressing for the fast store pass.
 void set_affine(GemmArgs& g) {
     const Epilogue& e = g.c;
     const bool cn = e.contig_n != 0;
+    g.blk32 = block32_linear(e.mmap) && block32_linear(e.nmap);
     g.affine = 0;
     g.bias_mode = 0;
     g.ldc = 0;
@@ -1369,9 +1706,11 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     } else {
         if (g.K % 8 || g.M % 8 || g.N % 8)
             return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
+        if (g.c.bias[0] && ((g.c.bias_on_m != 0) == (g.c.contig_n == 0)) && g.c.bias_map.r0 % 8 != 0)
+            return set_error(DM_ERR_UNSUPPORTED, "bias map radix along the output vector must be a multiple of 8");
         if (!g.split_ws) g.splits = 1;
-        choose(g);
         set_affine(g);
+        choose(g);
         if (g.splits > 1 && (int64_t)g.splits * g.batch * g.M * g.N > g.split_cap)
             return set_error(DM_ERR_WORKSPACE, "split-k scratch too small");
         if ((int64_t)g.batch * g.splits > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction grid too large");

@@ -84,6 +84,9 @@ struct GemmArgs {
     // contiguous output index (unit stride), 2 along the other index
     int affine, bias_mode;
     int64_t ldc;
+    // set by the launcher: output maps affine over aligned blocks of 32
+    // rows and columns (offsets then computed once per block)
+    int blk32;
 };
 
 // Scratch bytes for a split-K contraction.
