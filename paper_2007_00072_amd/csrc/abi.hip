@@ -386,7 +386,7 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
         return set_error(DM_ERR_UNSUPPORTED, "M, N, K must be multiples of 8");
     DM_TRY(check_ptr(A, "A")); DM_TRY(check_ptr(B, "B")); DM_TRY(check_ptr(C, "C"));
     if (bias) DM_TRY(check_ptr(bias, "bias"));
-    if (tile_cfg < -1 || tile_cfg > 14) return set_error(DM_ERR_ARG, "tile_cfg %d outside [-1, 14]", tile_cfg);
+    if (tile_cfg < -1 || tile_cfg > 15) return set_error(DM_ERR_ARG, "tile_cfg %d outside [-1, 15]", tile_cfg);
     if (splits < 0 || splits > 64) return set_error(DM_ERR_ARG, "splits %d outside [0, 64]", splits);
     if (splits > 1 && (!ws || ws_bytes < gemm_split_ws_bytes(M, N, batch, splits)))
         return set_error(DM_ERR_WORKSPACE, "split-k workspace too small");

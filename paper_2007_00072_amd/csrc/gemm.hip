@@ -22,6 +22,8 @@
 // (deterministic), for contractions with few output tiles and a long k.
 // The epilogue stages the fp32 tile through LDS in 64-column passes and
 // writes 16-byte vectors along whichever output index is contiguous.
+#include <algorithm>
+
 #include "gemm.hpp"
 #include "internal.hpp"
 
@@ -1197,96 +1199,134 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_big(GemmArgs g) {
     epilogue_direct<T, WM, WN>(g, acc, m0 + wm * WM, n0 + wn * WN, z, sidx, splits);
 }
 
-// ------------------------------------------ lean 256x256 kernel, 4 waves
-// The same tile, wave layout, LDS layouts and pipeline as gemm_big, for the
-// contractions whose operands are plain strided matrices (row map a single
-// stride), whose k is a multiple of 32 and whose output is affine: a single
-// base pointer per operand row and a single pointer increment per k-step
-// replace the per-copy index arithmetic and bounds selects, and the
-// epilogue writes straight from the accumulators with one address per 32x32
-// block.  Rows and columns past M / N read a clamped valid row and their
-// results are never stored, so no copy needs a bounds test.
+// ------------------------------------------------------ lean kernels
+// 32x32x16-MFMA contractions with BM x BN block tiles, WGM x WGN waves,
+// k-steps of BKS (32 or 64) and a ring of STAGES LDS stages filled by
+// asynchronous global -> LDS copies STAGES - 1 steps ahead.  Compared with
+// the general kernels above, operand addresses are set up so that the
+// k-loop does one pointer offset per copy and no bounds test: a
+// k-contiguous operand keeps one pointer per row (any row map, evaluated
+// once), an outer-contiguous operand's row map must be affine over each
+// k-step (one wave-uniform map evaluation per step plus fixed per-thread
+// offsets), k must be a multiple of BKS, and rows / columns past M / N
+// read a clamped valid row whose results are never stored.  The epilogue
+// writes straight from the accumulators with one address per 32x32 block,
+// which needs output maps affine over aligned 32-blocks (g.blk32).
+// Several waves per SIMD matter here: one wave alone cannot issue LDS
+// fragment reads fast enough to keep its MFMAs busy.
 
-// k-contiguous operand: slot q = i*NT + tid of a stage holds row q/4,
-// physical chunk q%4 = logical chunk ^ ((row >> 2) & 3).
-template <typename T, int NT>
+// LDS chunk (16 bytes) position of logical chunk c of k-contiguous row r,
+// rows of CPR chunks: 16 consecutive rows read at one chunk cover all 64
+// banks once.
+template <int CPR>
+__device__ __forceinline__ int lswz(int r, int c) {
+    if constexpr (CPR == 4) return c ^ ((r >> 2) & 3);
+    else return c ^ ((r >> 1) & 7);
+}
+
+// k-contiguous operand of R rows: slot q = i*NT + tid of a stage holds
+// row q / CPR, physical chunk q % CPR.
+template <typename T, int R, int BKS, int NT>
 struct LeanK {
-    static constexpr int NV = 256 * 4 / NT;
+    static constexpr int CPR = BKS / 8;
+    static constexpr int NV = R * CPR / NT;
+    static_assert(NV >= 1 && NV * NT == R * CPR, "tile / thread mismatch");
     const T* src[NV];
-    __device__ __forceinline__ void init(const T* base, int64_t ld, int o0, int omax) {
+    __device__ __forceinline__ void init(const Operand& op, int64_t boff, int kb, int o0, int omax) {
         const int tid = threadIdx.x;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            const int q = i * NT + tid, r = q >> 2, c = swz4(r, q & 3);
+            const int q = i * NT + tid, r = q / CPR, c = lswz<CPR>(r, q % CPR);
             const int o = o0 + r < omax ? o0 + r : omax - 1;
-            src[i] = base + (int64_t)o * ld + c * 8;
+            int seg = 0;
+            const int64_t off = map_off(op.row, (uint32_t)o, op.nseg, &seg);
+            src[i] = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off + kb + c * 8;
         }
     }
-    __device__ __forceinline__ void issue(int k0, uint32_t st) const {
+    __device__ __forceinline__ void issue(const Operand&, int64_t, int kb, int s, uint32_t st) const {
         const int w = threadIdx.x >> 6;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) lds_dma16(src[i] + k0, st + (uint32_t)(i * NT + w * 64) * 16u);
+        for (int i = 0; i < NV; ++i) lds_dma16(src[i] + s * BKS, st + (uint32_t)(i * NT + w * 64) * 16u);
+        (void)kb;
     }
+    // lane l: row ob + l % 32, k = kk + 8 (l / 32) .. +7
     __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
-        return Dma2<T, 256, NT, true>::frag(lds, ob, kk, lane);
+        const int r = ob + (lane & 31);
+        const int c = (kk >> 3) + (lane >> 5);
+        return *reinterpret_cast<const u32x4*>(lds + r * BKS + lswz<CPR>(r, c) * 8);
     }
 };
 
-// outer-contiguous operand ([k][outer] rows of 256 elements in LDS): slot q
-// holds k-row q/32, physical chunk q%32 = logical chunk ^ (4 (row & 3)).
-template <typename T, int NT>
+// outer-contiguous operand ([k][outer] rows of R elements in LDS): slot q
+// holds k-row q / CPR, physical chunk q % CPR = logical chunk ^ 4 (row & 3).
+template <typename T, int R, int BKS, int NT>
 struct LeanO {
-    static constexpr int NV = BK2 * 32 / NT;
-    const T* src[NV];
-    int64_t step;  // elements per k-step
-    __device__ __forceinline__ void init(const T* base, int64_t ld, int o0, int omax) {
+    static constexpr int CPR = R / 8;
+    static constexpr int NV = BKS * CPR / NT;
+    static_assert(NV >= 1 && NV * NT == BKS * CPR, "tile / thread mismatch");
+    int64_t poff[NV];  // k-row * stride + outer offset
+    __device__ __forceinline__ void init(const Operand& op, int64_t, int, int o0, int omax) {
         const int tid = threadIdx.x;
-        step = (int64_t)BK2 * ld;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            const int q = i * NT + tid, kr = q >> 5, c = (q & 31) ^ (4 * (kr & 3));
+            const int q = i * NT + tid, kr = q / CPR, c = (q % CPR) ^ (4 * (kr & 3));
             const int o = o0 + c * 8 < omax ? o0 + c * 8 : 0;
-            src[i] = base + (int64_t)kr * ld + o;
+            poff[i] = (int64_t)kr * op.row.s0 + o;
         }
     }
-    __device__ __forceinline__ void issue(int s, uint32_t st) const {
+    __device__ __forceinline__ void issue(const Operand& op, int64_t boff, int kb, int s, uint32_t st) const {
         const int w = threadIdx.x >> 6;
+        int seg = 0;
+        const int64_t off = map_off(op.row, (uint32_t)(kb + s * BKS), op.nseg, &seg);
+        const T* base = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) lds_dma16(src[i] + s * step, st + (uint32_t)(i * NT + w * 64) * 16u);
+        for (int i = 0; i < NV; ++i) lds_dma16(base + poff[i], st + (uint32_t)(i * NT + w * 64) * 16u);
     }
     __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
-        return Frag32<T, 256, false>::read(lds, ob, kk, lane);
+        return Frag32<T, R, false>::read(lds, ob, kk, lane);
     }
 };
 
-template <typename T, bool KC, int NT>
-struct Lean;
-template <typename T, int NT>
-struct Lean<T, true, NT> : LeanK<T, NT> {
-    __device__ __forceinline__ void go(int s, uint32_t st) const { this->issue(s * BK2, st); }
-};
-template <typename T, int NT>
-struct Lean<T, false, NT> : LeanO<T, NT> {
-    __device__ __forceinline__ void go(int s, uint32_t st) const { this->issue(s, st); }
+template <typename T, int R, int BKS, int NT, bool KC>
+struct LeanSel { typedef LeanK<T, R, BKS, NT> type; };
+template <typename T, int R, int BKS, int NT>
+struct LeanSel<T, R, BKS, NT, false> { typedef LeanO<T, R, BKS, NT> type; };
+
+// Output addressing of the lean epilogue (also used for split-k partials:
+// row-major floats, one pointer).
+struct LeanOut {
+    void* ptr[3];
+    int nseg, seg_on_m, affine, cn;
+    int64_t ldc, coff;
+    IdxMap mmap, nmap;
 };
 
-// Affine output straight from the accumulators (layout of a 32x32 result:
-// lane l holds column l % 32 at rows 8 (r / 4) + 4 (l / 32) + r % 4): along
-// n, the 32 lanes of a half-wave write 32 consecutive elements of a row;
-// along m, each lane writes the 4 consecutive rows of a group as one
-// vector.  Bias (along n) is loaded before the first store.
+// Stores of one wave's tile straight from the accumulators (a 32x32 result
+// holds column l % 32 in lane l at rows 8 (r / 4) + 4 (l / 32) + r % 4):
+// along n, the 32 lanes of a half-wave write 32 consecutive elements of a
+// row; along m, each lane writes the 4 consecutive rows of a group as one
+// vector.  One address per 32x32 block (row part wave-uniform).  M is a
+// multiple of 8, so a group of 4 rows is wholly inside or outside.
 template <typename OutT, bool CN, int FM, int FN>
-__device__ __forceinline__ void lean_store(const GemmArgs& g, const floatx16 (&acc)[FM][FN], OutT* C, int64_t ldc,
+__device__ __forceinline__ void lean_store(const GemmArgs& g, const LeanOut& o, const floatx16 (&acc)[FM][FN],
                                            int mw, int nw, const float (&bn)[FN], float alpha) {
     const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
+    const int64_t rs = o.affine ? (CN ? o.ldc : 1) : o.mmap.s0;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int mb = mw + i * 32;
+        if (mb >= g.M) break;
+        int mseg = 0;
+        const int64_t rbase = o.affine ? (int64_t)mb * rs : map_off(o.mmap, (uint32_t)mb, o.seg_on_m ? o.nseg : 1, &mseg);
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
             const int n = nw + j * 32 + c;
             if (n >= g.N) continue;
-            OutT* pb = CN ? C + (int64_t)(mb + 4 * h) * ldc + n : C + (int64_t)n * ldc + mb + 4 * h;
+            int nsg = 0;
+            const int64_t ncol = o.affine ? (CN ? (int64_t)n : (int64_t)n * o.ldc)
+                                          : map_off(o.nmap, (uint32_t)n, o.seg_on_m ? 1 : o.nseg, &nsg);
+            OutT* pb = reinterpret_cast<OutT*>(seg_ptr(o.ptr, o.seg_on_m ? mseg : nsg)) + o.coff + rbase + ncol +
+                       (CN ? (int64_t)(4 * h) * rs : (int64_t)(4 * h));
 #pragma unroll
             for (int rg = 0; rg < 4; ++rg) {
                 if (mb + 8 * rg + 4 * h >= g.M) continue;
@@ -1295,10 +1335,10 @@ __device__ __forceinline__ void lean_store(const GemmArgs& g, const floatx16 (&a
                 for (int k = 0; k < 4; ++k) v[k] = acc[i][j][4 * rg + k] * alpha + bn[j];
                 if constexpr (CN) {
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) pb[(int64_t)(8 * rg + k) * ldc] = from_f<OutT>(v[k]);
+                    for (int k = 0; k < 4; ++k) pb[(int64_t)(8 * rg + k) * rs] = from_f<OutT>(v[k]);
                 } else if constexpr (sizeof(OutT) == 4) {
-                    floatx4 o = {v[0], v[1], v[2], v[3]};
-                    *reinterpret_cast<floatx4*>(pb + 8 * rg) = o;
+                    floatx4 ov = {v[0], v[1], v[2], v[3]};
+                    *reinterpret_cast<floatx4*>(pb + 8 * rg) = ov;
                 } else {
                     OutT o4[4];
 #pragma unroll
@@ -1310,37 +1350,35 @@ __device__ __forceinline__ void lean_store(const GemmArgs& g, const floatx16 (&a
     }
 }
 
-template <typename T, bool AKC, bool BKC>
-__global__ __launch_bounds__(256) void gemm_lean(GemmArgs g) {
-    constexpr int NT = 256, WM = 128, WN = 128, FM = 4, FN = 4, STAGES = 4;
-    constexpr int AS = 256 * BK2, BS = 256 * BK2;
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean(GemmArgs g) {
+    constexpr int NT = 64 * WGM * WGN, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
+    constexpr int NQ = BKS / 16;  // 16-wide k slices per step
+    constexpr int AS = BM * BKS, BS = BN * BKS;
     constexpr int STAGE = (AS + BS) * (int)sizeof(T);
+    static_assert(STAGES >= 3 && FM >= 1 && FN >= 1 && STAGES * STAGE <= 160 * 1024, "configuration");
     __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
-    typedef Lean<T, AKC, NT> DA;
-    typedef Lean<T, BKC, NT> DB;
-    constexpr int NL = DA::NV + DB::NV;
+    typedef typename LeanSel<T, BM, BKS, NT, AKC>::type DA;
+    typedef typename LeanSel<T, BN, BKS, NT, BKC>::type DB;
+    constexpr int NL = DA::NV + DB::NV;  // copies per thread per step
     typedef typename Mfma32<T>::frag frag;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
     tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
-    const int m0 = tm * 256, n0 = tn * 256;
+    const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
     const uint32_t z = blockIdx.y / splits;
     const int sidx = blockIdx.y - (int)z * splits;
     const int kb = splits > 1 ? sidx * g.kper : 0;
     const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
     int dummy = 0;
-    // operand bases at k = kb (row map: a single stride s0)
-    const T* abase = reinterpret_cast<const T*>(g.a.ptr[0]) + map_off(g.a.batch, z, 1, &dummy) +
-                     (AKC ? (int64_t)kb : (int64_t)kb * g.a.row.s0);
-    const T* bbase = reinterpret_cast<const T*>(g.b.ptr[0]) + map_off(g.b.batch, z, 1, &dummy) +
-                     (BKC ? (int64_t)kb : (int64_t)kb * g.b.row.s0);
+    const int64_t aoff = map_off(g.a.batch, z, 1, &dummy), boff = map_off(g.b.batch, z, 1, &dummy);
     DA da;
     DB db;
-    da.init(abase, g.a.row.s0, m0, g.M);
-    db.init(bbase, g.b.row.s0, n0, g.N);
+    da.init(g.a, aoff, kb, m0, g.M);
+    db.init(g.b, boff, kb, n0, g.N);
     const uint32_t base = lds_addr(smem);
 
     floatx16 acc[FM][FN];
@@ -1351,20 +1389,20 @@ __global__ __launch_bounds__(256) void gemm_lean(GemmArgs g) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    const int nk = (ke - kb) / BK2;
+    const int nk = (ke - kb) / BKS;
     auto issue = [&](int s) {
-        const uint32_t st = base + (uint32_t)((s & 3) * STAGE);
-        da.go(s, st);
-        db.go(s, st + (uint32_t)(AS * sizeof(T)));
+        const uint32_t st = base + (uint32_t)((s % STAGES) * STAGE);
+        da.issue(g.a, aoff, kb, s, st);
+        db.issue(g.b, boff, kb, s, st + (uint32_t)(AS * sizeof(T)));
     };
     frag a[2][FM], b[2][FN];
-    auto read = [&](int buf, int s, int kk) {
-        const T* A = reinterpret_cast<const T*>(smem + (s & 3) * STAGE);
+    auto read = [&](int buf, int s, int q) {
+        const T* A = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
         const T* B = A + AS;
 #pragma unroll
-        for (int i = 0; i < FM; ++i) a[buf][i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, kk, lane));
+        for (int i = 0; i < FM; ++i) a[buf][i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, q * 16, lane));
 #pragma unroll
-        for (int j = 0; j < FN; ++j) b[buf][j] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + j * 32, kk, lane));
+        for (int j = 0; j < FN; ++j) b[buf][j] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + j * 32, q * 16, lane));
     };
     auto mma = [&](int buf) {
 #pragma unroll
@@ -1374,42 +1412,44 @@ __global__ __launch_bounds__(256) void gemm_lean(GemmArgs g) {
     };
 
     if (nk > 0) {
-        issue(0);
-        if (nk > 1) issue(1);
-        if (nk > 2) issue(2);
-        if (nk > 2) wait_vm<2 * NL>();
-        else if (nk > 1) wait_vm<NL>();
+#pragma unroll
+        for (int s = 0; s < STAGES - 1; ++s)
+            if (s < nk) issue(s);
+        if (nk >= STAGES - 1) wait_vm<(STAGES - 2) * NL>();
         else wait_vm<0>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         read(0, 0, 0);
     }
-    // per k-step: slice 0's MFMAs while slice 1's fragments are read; then
-    // (step s+1 landed, this wave done reading step s) barrier, refill the
-    // slot of step s-1 with step s+3, and slice 1's MFMAs while slice 0 of
-    // step s+1 is read (after the last step that read is of a stale slot,
-    // unused)
+    // Every 16-wide slice: the next slice's fragments are read while this
+    // slice's MFMAs run.  Before the last slice of step s, once step s+1 has
+    // landed and this wave's reads of step s are done, one barrier lets the
+    // slot of step s-1 be refilled with step s+STAGES-1 (after the last step
+    // the read is of a stale slot, unused).
     for (int s = 0; s < nk; ++s) {
-        read(1, s, 16);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_sched_barrier(0);
-        mma(0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (s + 2 < nk) wait_vm<NL>();
-        else wait_vm<0>();
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        if (s + 3 < nk) issue(s + 3);
-        read(0, s + 1, 0);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_sched_barrier(0);
-        mma(1);
-        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int cur = q & 1;
+            if (q + 1 < NQ) {
+                read(cur ^ 1, s, q + 1);
+            } else {
+                if (s + STAGES - 2 < nk) wait_vm<(STAGES - 3) * NL>();
+                else wait_vm<0>();
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                asm volatile("" ::: "memory");
+                if (s + STAGES - 1 < nk) issue(s + STAGES - 1);
+                read(cur ^ 1, s + 1, 0);
+            }
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_sched_barrier(0);
+            mma(cur);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 
-    // split k: float partial sums, row-major [M][N] per split, through the
-    // same store routine as float outputs (one code path keeps registers few)
+    // epilogue: split-k partials as row-major floats through the same
+    // store routine as float outputs (one code path keeps registers few)
     const int mw = m0 + wm * WM, nw = n0 + wn * WN, c = lane & 31;
     const Epilogue& e = g.c;
     const bool part = splits > 1;
@@ -1417,29 +1457,39 @@ __global__ __launch_bounds__(256) void gemm_lean(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int n = nw + j * 32 + c;
-        bn[j] = (!part && e.bias[0]) ? to_f(reinterpret_cast<const T*>(e.bias[0])[n < g.N ? n : 0]) : 0.f;
+        bn[j] = 0.f;
+        if (!part && e.bias[0]) {
+            int bseg = 0;
+            const int64_t bo = map_off(e.bias_map, (uint32_t)(n < g.N ? n : 0), e.bias_nseg, &bseg);
+            bn[j] = to_f(reinterpret_cast<const T*>(seg_ptr(e.bias, bseg))[bo]);
+        }
     }
-    const int64_t coff = map_off(e.batch, z, 1, &dummy);
-    if (part || (e.contig_n && e.out_f32)) {
-        float* C = part ? g.split_ws + ((int64_t)sidx * g.batch + z) * g.M * (int64_t)g.N
-                        : reinterpret_cast<float*>(e.ptr[0]) + coff;
-        lean_store<float, true, FM, FN>(g, acc, C, part ? (int64_t)g.N : g.ldc, mw, nw, bn, part ? 1.0f : e.alpha);
-    } else if (e.contig_n) {
-        lean_store<T, true, FM, FN>(g, acc, reinterpret_cast<T*>(e.ptr[0]) + coff, g.ldc, mw, nw, bn, e.alpha);
-    } else if (e.out_f32) {
-        lean_store<float, false, FM, FN>(g, acc, reinterpret_cast<float*>(e.ptr[0]) + coff, g.ldc, mw, nw, bn, e.alpha);
+    LeanOut o;
+    if (part) {
+        o.ptr[0] = o.ptr[1] = o.ptr[2] = g.split_ws + ((int64_t)sidx * g.batch + z) * g.M * (int64_t)g.N;
+        o.nseg = 1; o.seg_on_m = 0; o.affine = 1; o.cn = 1; o.ldc = g.N; o.coff = 0;
+        o.mmap = e.mmap; o.nmap = e.nmap;
     } else {
-        lean_store<T, false, FM, FN>(g, acc, reinterpret_cast<T*>(e.ptr[0]) + coff, g.ldc, mw, nw, bn, e.alpha);
+        o.ptr[0] = e.ptr[0]; o.ptr[1] = e.ptr[1]; o.ptr[2] = e.ptr[2];
+        o.nseg = e.nseg; o.seg_on_m = e.seg_on_m; o.affine = g.affine; o.cn = e.contig_n; o.ldc = g.ldc;
+        o.coff = map_off(e.batch, z, 1, &dummy);
+        o.mmap = e.mmap; o.nmap = e.nmap;
     }
+    const float alpha = part ? 1.0f : e.alpha;
+    if (part || (o.cn && e.out_f32)) lean_store<float, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
+    else if (o.cn) lean_store<T, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
+    else if (e.out_f32) lean_store<float, false, FM, FN>(g, o, acc, mw, nw, bn, alpha);
+    else lean_store<T, false, FM, FN>(g, o, acc, mw, nw, bn, alpha);
 }
 
-// True when the lean kernel takes this contraction (see gemm_lean).
-bool lean_ok(const GemmArgs& g) {
+// True when a lean kernel with k-steps of bks takes this contraction.
+bool lean_ok(const GemmArgs& g, int bks) {
     const Epilogue& e = g.c;
-    if (g.K % BK2 || (g.splits > 1 && g.kper % BK2)) return false;
-    if (g.a.nseg != 1 || g.a.row.r0 != 0 || g.b.nseg != 1 || g.b.row.r0 != 0) return false;
-    if (!g.affine || e.resid) return false;
-    if (e.bias[0] && (e.bias_on_m || e.bias_nseg != 1 || e.bias_map.r0 != 0 || e.bias_map.s0 != 1)) return false;
+    if (g.K % bks || (g.splits > 1 && g.kper % bks)) return false;
+    // outer-contiguous operands: row map affine over every k-step
+    if (!g.a.kcontig && g.a.row.r0 % bks) return false;
+    if (!g.b.kcontig && g.b.row.r0 % bks) return false;
+    if (!g.blk32 || e.resid || (e.bias[0] && e.bias_on_m)) return false;
     return true;
 }
 
@@ -1523,13 +1573,15 @@ struct TileCfg {
     int bm, bn, wgm, wgn;
 };
 // 0-4: register-staged kernel; 5-8: asynchronous (global -> LDS) kernel;
-// 9-12: asynchronous kernel on 32x32x16 MFMAs; 13, 14: 256x256 kernel with
-// a four-stage ring of 32-wide k-steps, 4 waves of 128x128 (the lean kernel;
-// contractions it does not take run as 14) or 8 of 128x64.
+// 9-12: asynchronous kernel on 32x32x16 MFMAs; 13: lean 256x256 kernel
+// (8 waves of 128x64, four stages of 32-wide k-steps); 14: the general
+// 256x256 kernel with the same waves; 15: lean 128x128 kernel (8 waves of
+// 64x32, four stages of 64-wide k-steps).  Contractions a lean kernel does
+// not take run on 14 (for 13) or 11 (for 15).
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
-                            {256, 256, 2, 2}, {256, 256, 2, 4}};
+                            {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}};
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
 template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH>
@@ -1574,13 +1626,18 @@ void launch_x32(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, false, false>), grid, block, 0, st, g);
 }
 
-template <typename T>
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean(const GemmArgs& g, hipStream_t st) {
     dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
-    if (g.a.kcontig && g.b.kcontig) hipLaunchKernelGGL((gemm_lean<T, true, true>), grid, dim3(256), 0, st, g);
-    else if (g.a.kcontig) hipLaunchKernelGGL((gemm_lean<T, true, false>), grid, dim3(256), 0, st, g);
-    else if (g.b.kcontig) hipLaunchKernelGGL((gemm_lean<T, false, true>), grid, dim3(256), 0, st, g);
-    else hipLaunchKernelGGL((gemm_lean<T, false, false>), grid, dim3(256), 0, st, g);
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig && g.b.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true>), grid, block, 0, st, g);
+    else if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, false>), grid, block, 0, st, g);
+    else if (g.b.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true>), grid, block, 0, st, g);
+    else
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false>), grid, block, 0, st, g);
 }
 
 template <typename T, int WGM, int WGN>
@@ -1596,7 +1653,8 @@ void launch_big(const GemmArgs& g, hipStream_t st) {
 template <typename T>
 void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
-        case 13: launch_lean<T>(g, st); break;
+        case 13: launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st); break;
+        case 15: launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -1626,35 +1684,31 @@ int64_t ntiles(const TileCfg& c, const GemmArgs& g) {
 }
 
 // Tile and split choice, from measurements of the layer's contraction
-// shapes on MI355X (every configuration x split 1/2/4): the 256x256 tile
-// (the lean 4-wave kernel when the contraction qualifies, else the 8-wave
-// one) when it alone gives (nearly) every CU a block; for weight gradients
-// (both operands outer-contiguous, long k) that tile split four ways, or the
-// asynchronous 128x64 tile split four ways for small outputs; otherwise the
-// asynchronous 128x64 tile.  Explicit choices (cfg >= 0, splits > 0) are
-// kept.
+// shapes on MI355X (every configuration x split 1/2/4): the lean 256x256
+// kernel when that tile alone gives (nearly) every CU a block; otherwise the
+// lean 128x128 kernel, split along k for long-k contractions with few
+// output tiles (up to four ways, towards one block per CU); narrow outputs
+// (n <= 64) on the asynchronous 128x64 tile.  A lean kernel hands
+// contractions it does not take to its general counterpart.  Explicit
+// choices (cfg >= 0, splits > 0) are kept.
 void choose(GemmArgs& g) {
     constexpr int64_t CUS = 256;
     const bool split_ok = g.split_ws != nullptr && g.batch == 1;
-    const bool both_outer = !g.a.kcontig && !g.b.kcontig;
     int want_split = 1;
     if (g.cfg < 0 || g.cfg >= NCFG) {
         if (g.N <= 64) {
             g.cfg = 8;
         } else if (ntiles(CFGS[13], g) * 4 >= CUS * 3) {
             g.cfg = 13;
-        } else if (split_ok && both_outer && g.K >= 2048) {
-            const bool small_out = (int64_t)g.M * g.N < ((int64_t)2 << 20);
-            g.cfg = small_out ? 8 : 13;
-            want_split = 4;
         } else {
-            g.cfg = 8;
+            g.cfg = 15;
+            const int64_t t = ntiles(CFGS[15], g);
+            if (split_ok && g.K >= 2048 && t < CUS * 3 / 4) want_split = (int)std::min<int64_t>(4, std::max<int64_t>(1, CUS / t));
         }
     }
     // the 32x32x16 kernels' epilogue takes no residual operand, no bias
     // along m and only output maps affine over 32-wide blocks
     if ((g.c.resid || (g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
-    // the lean 256x256 kernel's conditions are checked after the split is set
     const TileCfg& c = CFGS[g.cfg];
     g.tiles_m = (g.M + c.bm - 1) / c.bm;
     g.tiles_n = (g.N + c.bn - 1) / c.bn;
@@ -1668,7 +1722,8 @@ void choose(GemmArgs& g) {
         g.kper = (ksteps + g.splits - 1) / g.splits * BK;
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
-    if (g.cfg == 13 && !lean_ok(g)) g.cfg = 14;
+    if (g.cfg == 13 && !lean_ok(g, 32)) g.cfg = 14;
+    if (g.cfg == 15 && !lean_ok(g, 64)) g.cfg = 11;
 }
 
 // Classifies the output addressing for the fast store pass.
