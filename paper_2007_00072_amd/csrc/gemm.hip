@@ -1309,7 +1309,8 @@ struct LeanOut {
 // multiple of 8, so a group of 4 rows is wholly inside or outside.
 template <typename OutT, bool CN, int FM, int FN>
 __device__ __forceinline__ void lean_store(const GemmArgs& g, const LeanOut& o, const floatx16 (&acc)[FM][FN],
-                                           int mw, int nw, const float (&bn)[FN], float alpha) {
+                                           int mw, int nw, const float (&bn)[FN], float alpha,
+                                           const floatx16 (*res)[FN] = nullptr) {
     const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
     const int64_t rs = o.affine ? (CN ? o.ldc : 1) : o.mmap.s0;
 #pragma unroll
@@ -1332,7 +1333,7 @@ __device__ __forceinline__ void lean_store(const GemmArgs& g, const LeanOut& o, 
                 if (mb + 8 * rg + 4 * h >= g.M) continue;
                 float v[4];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) v[k] = acc[i][j][4 * rg + k] * alpha + bn[j];
+                for (int k = 0; k < 4; ++k) v[k] = acc[i][j][4 * rg + k] * alpha + bn[j] + (res ? res[i][j][4 * rg + k] : 0.f);
                 if constexpr (CN) {
 #pragma unroll
                     for (int k = 0; k < 4; ++k) pb[(int64_t)(8 * rg + k) * rs] = from_f<OutT>(v[k]);
@@ -1476,6 +1477,43 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean(GemmArgs g) {
         o.mmap = e.mmap; o.nmap = e.nmap;
     }
     const float alpha = part ? 1.0f : e.alpha;
+    if constexpr (FM * FN <= 2) {
+        // residual operand (same addressing as the output, along n, input
+        // dtype): every value of the wave's tile is loaded before the first
+        // store, since vector-memory waits count loads and stores together
+        if (!part && e.resid && o.cn && !e.out_f32) {
+            floatx16 res[FM][FN];
+            const int h = lane >> 5;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int mb = mw + i * 32;
+                int mseg = 0;
+                const int64_t rs = o.affine ? o.ldc : o.mmap.s0;
+                const int64_t rbase = o.affine ? (int64_t)(mb < g.M ? mb : 0) * rs
+                                               : map_off(o.mmap, (uint32_t)(mb < g.M ? mb : 0), 1, &mseg);
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    const int n = nw + j * 32 + c;
+                    int nsg = 0;
+                    const int64_t ncol = o.affine ? (int64_t)(n < g.N ? n : 0)
+                                                  : map_off(o.nmap, (uint32_t)(n < g.N ? n : 0), 1, &nsg);
+                    // unconditional loads (a clamped offset for elements
+                    // outside the output, whose values are never stored), so
+                    // all of them are in flight before the first wait
+                    const T* rp = reinterpret_cast<const T*>(e.resid) + o.coff;
+                    const int64_t boff = rbase + ncol;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int rr = 8 * (r >> 2) + 4 * h + (r & 3);
+                        const bool in = mb + rr < g.M && n < g.N;
+                        res[i][j][r] = to_f(rp[in ? boff + (int64_t)rr * rs : 0]);
+                    }
+                }
+            }
+            lean_store<T, true, FM, FN>(g, o, acc, mw, nw, bn, alpha, res);
+            return;
+        }
+    }
     if (part || (o.cn && e.out_f32)) lean_store<float, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
     else if (o.cn) lean_store<T, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
     else if (e.out_f32) lean_store<float, false, FM, FN>(g, o, acc, mw, nw, bn, alpha);
@@ -1489,7 +1527,10 @@ bool lean_ok(const GemmArgs& g, int bks) {
     // outer-contiguous operands: row map affine over every k-step
     if (!g.a.kcontig && g.a.row.r0 % bks) return false;
     if (!g.b.kcontig && g.b.row.r0 % bks) return false;
-    if (!g.blk32 || e.resid || (e.bias[0] && e.bias_on_m)) return false;
+    if (!g.blk32 || (e.bias[0] && e.bias_on_m)) return false;
+    // a residual operand: only on the 128x128 tile (small wave tiles), along
+    // n, in the input dtype, through a single pointer
+    if (e.resid && (bks != 64 || !e.contig_n || e.out_f32 || e.nseg != 1)) return false;
     return true;
 }
 
@@ -1706,9 +1747,11 @@ void choose(GemmArgs& g) {
             if (split_ok && g.K >= 2048 && t < CUS * 3 / 4) want_split = (int)std::min<int64_t>(4, std::max<int64_t>(1, CUS / t));
         }
     }
-    // the 32x32x16 kernels' epilogue takes no residual operand, no bias
-    // along m and only output maps affine over 32-wide blocks
-    if ((g.c.resid || (g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
+    // the 32x32x16 kernels' epilogues take no bias along m and only output
+    // maps affine over 32-wide blocks; of them only the lean 128x128 kernel
+    // takes a residual operand
+    if (((g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
+    if (g.c.resid && g.cfg >= 9 && g.cfg != 15) g.cfg = 8;
     const TileCfg& c = CFGS[g.cfg];
     g.tiles_m = (g.M + c.bm - 1) / c.bm;
     g.tiles_n = (g.N + c.bn - 1) / c.bn;
@@ -1723,7 +1766,7 @@ void choose(GemmArgs& g) {
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
     if (g.cfg == 13 && !lean_ok(g, 32)) g.cfg = 14;
-    if (g.cfg == 15 && !lean_ok(g, 64)) g.cfg = 11;
+    if (g.cfg == 15 && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
 }
 
 // Classifies the output addressing for the fast store pass.
