@@ -106,7 +106,20 @@ __device__ __forceinline__ float group_max(float v) {
 // Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11): the round
 // multiplies counter words 0 and 2 by two constants and mixes the high
 // product halves with words 1 and 3 and the round key; the key is bumped by
-// two Weyl constants between rounds.
+// two Weyl constants between rounds.  Each 32x32 -> 64-bit product is one
+// v_mad_u64_u32 (both halves at once) and each three-way mix one
+// v_bitop3_b32, about half the instructions of separate high / low
+// multiplies and two-input xors; the generator is ALU-bound in the fused
+// kernels that draw masks.
+// a ^ b ^ k with k wave-uniform (the round keys derive from kernel
+// arguments only), taken from a scalar register: gfx950's three-input
+// bitwise operation with truth table 0x96 (odd parity of the three bits)
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t k) {
+    uint32_t r;
+    asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(k));
+    return r;
+}
+
 struct Philox {
     static constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
     static constexpr uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
@@ -114,10 +127,9 @@ struct Philox {
                                                 uint32_t k0, uint32_t k1) {
 #pragma unroll
         for (int r = 0; r < 10; ++r) {
-            uint32_t lo0 = c0 * M0, hi0 = __umulhi(c0, M0);
-            uint32_t lo1 = c2 * M1, hi1 = __umulhi(c2, M1);
-            uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
-            c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+            const uint64_t p0 = (uint64_t)c0 * M0, p1 = (uint64_t)c2 * M1;
+            const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0), n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
+            c0 = n0; c1 = (uint32_t)p1; c2 = n2; c3 = (uint32_t)p0;
             k0 += W0; k1 += W1;
         }
         u32x4 o; o[0] = c0; o[1] = c1; o[2] = c2; o[3] = c3;
@@ -145,10 +157,12 @@ __device__ __forceinline__ void dropout8(const DropParams& d, uint64_t e0, float
     u32x4 a = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
     blk += 1;
     u32x4 b = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
+    // enabled means p > 0, so thr < 2^32 fits 32 bits
+    const uint32_t thr = (uint32_t)d.thr;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        v[i] = ((uint64_t)a[i] < d.thr) ? v[i] * d.scale : 0.0f;
-        v[4 + i] = ((uint64_t)b[i] < d.thr) ? v[4 + i] * d.scale : 0.0f;
+        v[i] = a[i] < thr ? v[i] * d.scale : 0.0f;
+        v[4 + i] = b[i] < thr ? v[4 + i] * d.scale : 0.0f;
     }
 }
 
@@ -166,24 +180,47 @@ __device__ __forceinline__ void keep8(const DropParams& d, uint64_t e0, uint8_t 
     u32x4 b = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), d.site, d.layer, k0, k1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        out[i] = (uint64_t)a[i] < d.thr;
-        out[4 + i] = (uint64_t)b[i] < d.thr;
+        out[i] = a[i] < (uint32_t)d.thr;
+        out[4 + i] = b[i] < (uint32_t)d.thr;
     }
 }
 
 // ----------------------------------------------------------- activations
 enum Act { ACT_GELU = 0, ACT_RELU = 1 };
 
+// erf(x) for x >= 0 and e = exp(-x^2), by the rational approximation of
+// Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) e, t = 1 / (1 + p x),
+// absolute error <= 1.5e-7.  The exponential is the one the GELU density
+// needs anyway (exp(-u^2 / 2) with x = u / sqrt 2), so GELU and its
+// derivative cost one exp and one reciprocal.
+__device__ __forceinline__ float erf_pos(float x, float e) {
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+    const float poly =
+        t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f),
+                 0.254829592f);
+    return fmaf(-poly, e, 1.0f);
+}
+
+// GELU (exact erf form): Phi(u) = (1 + erf(u / sqrt 2)) / 2
+__device__ __forceinline__ float gelu_cdf(float u, float& e) {
+    const float x = u * 0.70710678118654752f;
+    e = __expf(-x * x);
+    const float ea = erf_pos(fabsf(x), e);
+    return 0.5f + 0.5f * (x < 0.0f ? -ea : ea);
+}
+
 __device__ __forceinline__ float act_fwd(float u, int act) {
     if (act == ACT_RELU) return fmaxf(u, 0.0f);
-    return 0.5f * u * (1.0f + erff(u * 0.70710678118654752f));
+    float e;
+    return u * gelu_cdf(u, e);
 }
-// d/du of the activation: GELU' = Phi(u) + u * phi(u)
+// d/du of the activation: GELU' = Phi(u) + u * phi(u), phi(u) = exp(-u^2/2) / sqrt(2 pi)
 __device__ __forceinline__ float act_grad(float u, int act) {
     if (act == ACT_RELU) return u > 0.0f ? 1.0f : 0.0f;
-    float cdf = 0.5f * (1.0f + erff(u * 0.70710678118654752f));
-    float pdf = 0.39894228040143268f * __expf(-0.5f * u * u);
-    return cdf + u * pdf;
+    float e;
+    const float cdf = gelu_cdf(u, e);
+    return fmaf(u * 0.39894228040143268f, e, cdf);
 }
 
 }  // namespace dm

@@ -184,14 +184,18 @@ __global__ __launch_bounds__(NT) void softmax_bwd_k(int64_t rows, int B, int H, 
 }
 
 // ------------------------------------------------------ LayerNorm backward family
-// Each block takes a contiguous range of rows; one lane group per row.
-// Column partial sums are kept per lane (a lane always owns the same
-// columns), reduced over the wave's lane groups with shuffles and over the
-// block's 4 waves through LDS, and written as part[q][blockIdx.x][cols].
+// Each block (8 waves) takes a contiguous range of rows; one lane group per
+// row, so every wave has its own rows' loads in flight at once.  Column
+// partial sums are kept per lane (a lane always owns the same columns),
+// reduced over the wave's lane groups with shuffles and over the block's 8
+// waves through LDS in a fixed order, and written as
+// part[q][blockIdx.x][cols].
+constexpr int NTL = 512;  // threads per LayerNorm-backward block
+
 template <typename T, int LPR, int NV>
-__global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, int nblk) {
+__global__ __launch_bounds__(NTL) void ln_bwd_k(LnBwdArgs a, int rows_per_block, int nblk) {
     constexpr int RPW = 64 / LPR;
-    constexpr int GROUPS = 4 * RPW;  // row slots per block iteration
+    constexpr int GROUPS = (NTL / 64) * RPW;  // row slots per block iteration
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int gi = lane / LPR, gl = lane % LPR;
     const int cols = a.cols;
@@ -218,12 +222,15 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, 
     // before the first row's reductions.
     constexpr int UR = NV <= 2 ? 2 : 1;
     for (int64_t rb = r0; rb < r1; rb += GROUPS * UR) {
-        float dy[UR][NV][8], xh[UR][NV][8];
+        float dy[UR][NV][8], xh[UR][NV][8], rsv[UR];
 #pragma unroll
         for (int u = 0; u < UR; ++u) {
             const int64_t row = rb + u * GROUPS + wave * RPW + gi;
             const bool active = row < r1;
             const int64_t base = row * cols;
+            // the row's 1/std is loaded with its other inputs, not after the
+            // reductions (a load issued there costs a full memory latency)
+            rsv[u] = do_ds && active ? a.rstd[row] : 0.f;
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
                 const int c = (gl + i * LPR) * 8;
@@ -265,7 +272,7 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, 
                 const float m1 = group_sum<LPR>(s1) * inv;
                 const float m2 = group_sum<LPR>(s2) * inv;
                 if (active) {
-                    const float rs = a.rstd[row];
+                    const float rs = rsv[u];
 #pragma unroll
                     for (int i = 0; i < NV; ++i) {
                         const int c = (gl + i * LPR) * 8;
@@ -292,7 +299,7 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, 
     if (!do_part) return;
 
     // reduce partials over the RPW lane groups of the wave
-    __shared__ float red[4][2048];
+    __shared__ float red[NTL / 64][2048];
     const int nq = a.want_dsub_sum ? 3 : 2;
     for (int qn = 0; qn < nq; ++qn) {
         float(*pp)[8] = qn == 0 ? p_dyx : (qn == 1 ? p_dy : p_dsub);
@@ -318,8 +325,9 @@ __global__ __launch_bounds__(NT) void ln_bwd_k(LnBwdArgs a, int rows_per_block, 
         }
         __syncthreads();
         float* out = a.part + ((int64_t)qn * nblk + blockIdx.x) * cols;
-        for (int c = threadIdx.x; c < cols; c += NT)
-            out[c] = (red[0][c] + red[1][c]) + (red[2][c] + red[3][c]);
+        for (int c = threadIdx.x; c < cols; c += NTL)
+            out[c] = ((red[0][c] + red[1][c]) + (red[2][c] + red[3][c])) +
+                     ((red[4][c] + red[5][c]) + (red[6][c] + red[7][c]));
     }
 }
 
@@ -392,35 +400,39 @@ __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, c
 }
 
 // out[c] = sum over the nblk partial rows in a fixed order.  Block x covers
-// columns 64x .. 64x+63 as 16 four-column groups x 16 row phases; block y
-// selects one of up to three partial sets (part + y*nblk*cols -> outs[y]).
-// With qkv_H > 0 the columns are (s, h, p) of a fused projection and land
-// in outs[s][p * qkv_H + h] (single partial set).
+// columns 16x .. 16x+15 as 4 four-column groups x 64 row phases (each phase
+// sums rows ph, ph+64, ... with several loads in flight); block y selects
+// one of up to three partial sets (part + y*nblk*cols -> outs[y]).  With
+// qkv_H > 0 the columns are (s, h, p) of a fused projection and land in
+// outs[s][p * qkv_H + h] (single partial set).
 struct FinishOut {
     float* out[3];
 };
 
 __global__ __launch_bounds__(NT) void colsum_finish_k(int nblk, int cols, const float* __restrict__ part,
                                                       FinishOut fo, int qkv_H, int qkv_P) {
-    __shared__ floatx4 red[16][16];
-    const int cg = threadIdx.x & 15, ph = threadIdx.x >> 4;
-    const int c = blockIdx.x * 64 + cg * 4;
+    __shared__ floatx4 red[64][4];
+    const int cg = threadIdx.x & 3, ph = threadIdx.x >> 2;
+    const int c = blockIdx.x * 16 + cg * 4;
     const float* base = part + (int64_t)blockIdx.y * nblk * cols;
-    floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
+    floatx4 s[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s[u] = floatx4{0.f, 0.f, 0.f, 0.f};
     if (c < cols) {
         int b = ph;
-        for (; b + 16 < nblk; b += 32) {
-            s0 += *reinterpret_cast<const floatx4*>(base + (int64_t)b * cols + c);
-            s1 += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + 16) * cols + c);
+        for (; b + 192 < nblk; b += 256) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + 64 * u) * cols + c);
         }
-        if (b < nblk) s0 += *reinterpret_cast<const floatx4*>(base + (int64_t)b * cols + c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (b + 64 * u < nblk) s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + 64 * u) * cols + c);
     }
-    red[ph][cg] = s0 + s1;
+    red[ph][cg] = (s[0] + s[1]) + (s[2] + s[3]);
     __syncthreads();
     if (ph == 0 && c < cols) {
         floatx4 t = red[0][cg];
-#pragma unroll
-        for (int i = 1; i < 16; ++i) t += red[i][cg];
+        for (int i = 1; i < 64; ++i) t += red[i][cg];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int cc = c + q;
@@ -582,7 +594,7 @@ void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
     const int nblk = colsum_blocks(a.rows);
     const int rpb = (int)((a.rows + nblk - 1) / nblk);
 #define L(LPR, NV) \
-    { hipLaunchKernelGGL((ln_bwd_k<T, LPR, NV>), dim3(nblk), dim3(NT), 0, st, a, rpb, nblk); }
+    { hipLaunchKernelGGL((ln_bwd_k<T, LPR, NV>), dim3(nblk), dim3(NTL), 0, st, a, rpb, nblk); }
     DM_ROW_CASES(L)
 #undef L
 }
@@ -590,8 +602,8 @@ void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
 }  // namespace
 
 int colsum_blocks(int64_t rows) {
-    int64_t b = (rows + 15) / 16;
-    if (b > 256) b = 256;
+    int64_t b = (rows + 7) / 8;
+    if (b > 512) b = 512;
     return (int)(b < 1 ? 1 : b);
 }
 
@@ -654,14 +666,14 @@ void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float*
 
 void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st) {
     FinishOut fo{{out, nullptr, nullptr}};
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 15) / 16, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
                        fo, 0, 0);
 }
 
 void run_colsum_finish3(int64_t rows, int cols, const float* part, float* o0, float* o1, float* o2,
                         hipStream_t st) {
     FinishOut fo{{o0, o1, o2}};
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64, 3), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 15) / 16, 3), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
                        fo, 0, 0);
 }
 
@@ -669,7 +681,7 @@ void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* pa
                            float* dbv, hipStream_t st) {
     const int cols = nseg * H * P;
     FinishOut fo{{dbq, dbk, dbv}};
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 63) / 64, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
+    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 15) / 16, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
                        fo, H, P);
 }
 
