@@ -19,7 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdmtx.so")
-SOURCES = ["gemm.hip", "fused.hip", "abi.hip", "layer.hip"]
+SOURCES = ["gemm.hip", "fused.hip", "attn.hip", "abi.hip", "layer.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

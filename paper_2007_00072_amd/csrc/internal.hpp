@@ -48,6 +48,22 @@ void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void*
                    const void* resid, const void* gamma, const void* beta, float eps,
                    const DropParams& dp, void* y, void* xhat, float* rstd, hipStream_t st);
 
+// Attention scores without the score tensor in HBM (attn.hip).  Operand
+// element (z = b*H + h, row r, contraction index d) sits at
+// ptr + b*outer + h*inner + r*ld + d; P, alpha and d(beta) are [B][H][J][K].
+// attn_fused_ok: dtype fp16 / bf16, K a multiple of 32 up to 960, D (the
+// contraction length) in {16, 32, 48, 64, 96, 128}.
+bool attn_fused_ok(int dtype, int K, int D);
+// P = softmax_k(round(scaler * Q K^T)), alpha = dropout(P)
+void run_attn_scores_fwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* q, int64_t q_outer,
+                         int64_t q_inner, int64_t q_ld, const void* k, int64_t k_outer, int64_t k_inner, int64_t k_ld,
+                         const DropParams& dp, void* prob, void* alpha, hipStream_t st);
+// d(beta) = scaler * P * (dP - sum_k dP P), dP = dropout(round(d(gamma) V^T))
+void run_attn_scores_bwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* dgamma,
+                         int64_t dg_outer, int64_t dg_inner, int64_t dg_ld, const void* v, int64_t v_outer,
+                         int64_t v_inner, int64_t v_ld, const void* prob, const DropParams& dp, void* dbeta,
+                         hipStream_t st);
+
 void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta,
                      const DropParams& dp, void* prob, void* alpha, hipStream_t st);
 

@@ -306,6 +306,13 @@ int project_fused(const Dims& x, int layout, const void* in, const dm_layer_para
 int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const void* q, const void* k,
                        const void* v, void* beta, void* prob, void* alpha, void* gamma, hipStream_t st) {
     const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, HW = x.H * x.W;
+    if (attn_fused_ok(x.dtype, (int)K, (int)P)) {
+        // QK^T and the softmax + dropout in one launch (beta stays on chip)
+        TraceScope t_("F2-3 qkt_softmax", st);
+        run_attn_scores_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, (int)P, scaler, q, x.H * J * P, J * P, P, k,
+                            x.H * K * P, K * P, P, dp, prob, alpha, st);
+        DM_TRY(check_launch("attention scores"));
+    } else {
     // beta[z][j][k] = scaler * sum_p Q[z][j][p] K[z][k][p]
     Epilogue cb = epi(beta, linear_map(K), linear_map(1), true, false, linear_map(J * K));
     cb.alpha = scaler;
@@ -321,6 +328,7 @@ int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const 
         run_softmax_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, 1.0f, beta, dp, prob, alpha, st);
     }
     DM_TRY(check_launch("softmax"));
+    }
     // gamma[(b,j)][(h,w)] = sum_k alpha[z][j][k] V[z][k][w]
     Epilogue cg = epi(gamma, linear_map(HW), linear_map(1), true, false, make_map((uint32_t)x.H, 0, W, J * HW, 0));
     TraceScope t_("F4 gamma", st);
@@ -366,6 +374,15 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
                        st));
     const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
     t12.stop();
+    const bool fused = attn_fused_ok(x.dtype, (int)K, (int)W);
+    if (fused) {
+        // Gamma dX1 and the scaled softmax + dropout backward in one launch
+        // (dalpha stays on chip): dbeta[z][j][k]
+        TraceScope t_("B13-15 gamma_dx1_softmax_bwd", st);
+        run_attn_scores_bwd(x.dtype, (int)x.B, (int)H, (int)J, (int)K, (int)W, scaler, dgamma, J * HW, W, HW, v,
+                            H * K * W, K * W, W, prob, dp, dbeta, st);
+        DM_TRY(check_launch("attention score backward"));
+    } else {
     // Gamma dX1: dalpha[z][j][k] = sum_w dgamma[(b,j)][(h,w)] V[z][k][w]
     TraceScope t13("B13 gamma_dx1", st);
     DM_TRY(launch_gemm(x.dtype,
@@ -374,6 +391,7 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
                             epi(dalpha, linear_map(K), linear_map(1), true, false, linear_map(J * K))),
                        st));
     t13.stop();
+    }
     // Gamma dX2: dV[z][k][w] = sum_j alpha[z][j][k] dgamma[(b,j)][(h,w)]
     TraceScope t14("B14 gamma_dx2", st);
     DM_TRY(launch_gemm(x.dtype,
@@ -383,11 +401,12 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
                                 make_map((uint32_t)H, 0, W, K * ldv, 0))),
                        st));
     t14.stop();
-    // Scaled softmax dX
-    TraceScope t15("B15 softmax_bwd", st);
-    run_softmax_bwd(x.dtype, (int)x.B, (int)H, (int)J, (int)K, scaler, dalpha, prob, dp, dbeta, st);
-    DM_TRY(check_launch("softmax backward"));
-    t15.stop();
+    if (!fused) {
+        // Scaled softmax dX
+        TraceScope t15("B15 softmax_bwd", st);
+        run_softmax_bwd(x.dtype, (int)x.B, (int)H, (int)J, (int)K, scaler, dalpha, prob, dp, dbeta, st);
+        DM_TRY(check_launch("softmax backward"));
+    }
     // QK^T dX1: dQ[z][j][p] = sum_k dbeta[z][j][k] K[z][k][p]
     TraceScope t16("B16 qkt_dx1", st);
     DM_TRY(launch_gemm(x.dtype,

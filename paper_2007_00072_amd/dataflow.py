@@ -52,6 +52,8 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["F1 qkv"] = g(T, 3 * I, I, N, 3 * I * I, 3 * N, extra=3 * I * es)
     w["F2 qkt"] = _att(Z, J, K, P, es, dtype, S, N)
     w["F3 softmax"] = m(3 * S * es)
+    # QK^T and softmax + dropout in one launch: Q, K read; P and alpha written
+    w["F2-3 qkt_softmax"] = Work(2.0 * Z * J * K * P, float((2 * N + 2 * S) * es), "hbm")
     w["F4 gamma"] = _att(Z, J, W, K, es, dtype, S, N)
     w["F5 out"] = g(T, I, I, N, I * I, N)
     w["F6 bdrln1"] = m(4 * N * es + 4 * T + 3 * I * es)
@@ -75,6 +77,9 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["B13 gamma_dx1"] = _att(Z, J, K, W, es, dtype, S, N)
     w["B14 gamma_dx2"] = _att(Z, K, W, J, es, dtype, S, N)
     w["B15 softmax_bwd"] = m(3 * S * es)
+    # Gamma dX1 and the softmax + dropout backward in one launch: dGamma, V
+    # and P read, dbeta written
+    w["B13-15 gamma_dx1_softmax_bwd"] = Work(2.0 * Z * J * K * W, float((2 * N + 2 * S) * es), "hbm")
     w["B16 qkt_dx1"] = _att(Z, J, P, K, es, dtype, S, N)
     w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read

@@ -193,6 +193,23 @@ def test_mha_reduced(layout, self_attention):
     check_mha(wl, self_attention)
 
 
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_mha_fused_scores_ragged_rows(dtype):
+    # attention scores kept on chip (key length a multiple of 32): query
+    # rows not a multiple of the kernels' 32-row blocks, contraction lengths
+    # 48 (Q K^T) and 64 (dGamma V^T)
+    wl = WORKLOADS["mha_large_f16"].with_(shape=Shape(B=2, J=72, K=96, H=3, P=48, W=64, I=144), dtype=dtype,
+                                          layout="bji", p_attn=0.2)
+    check_mha(wl, self_attention=False)
+
+
+@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
+def test_encoder_fused_scores(name):
+    # several 32-row blocks per head through the on-chip score kernels
+    wl = small(name, B=2, J=96, K=96, H=4, P=64, W=64, I=256, F=512)
+    check_encoder(wl, layer=2)
+
+
 def test_mha_tiny_f32_general():
     wl = WORKLOADS["mha_large_f16"].with_(shape=Shape(B=2, J=16, K=24, H=2, P=8, W=16, I=24), dtype="f32")
     check_mha(wl, self_attention=False)
