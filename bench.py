@@ -180,8 +180,8 @@ def main() -> int:
             "per_launch_us": dom["us"],
             "algorithmic_per_launch": dw.flop if dw.bound == "mfma" else dw.bytes}
     # operator classes; second launches (reduce / finish) count with their operator
-    is_fused = lambda r: work.get(r["op"]) is not None and work[r["op"]].flop == 0.0
-    is_contr = lambda r: work.get(r["op"]) is not None and work[r["op"]].flop > 0.0
+    is_fused = lambda r: work.get(r["op"]) is not None and work[r["op"]].cls == "fused"
+    is_contr = lambda r: work.get(r["op"]) is not None and work[r["op"]].cls == "contraction"
     fused = [r for r in table if is_fused(r)]
     fb = sum(work[r["op"]].bytes * r["launches_per_step"] for r in fused if r["op"] == r["kernel"])
     ft = step_us(fused) * 1e-6

@@ -26,6 +26,11 @@ class Work:
     flop: float
     bytes: float
     bound: str     # "mfma" or "hbm"
+    cls: str = ""  # "fused" (memory-bound fused operator) or "contraction"; default from flop
+
+    def __post_init__(self):
+        if not self.cls:
+            self.cls = "fused" if self.flop == 0.0 else "contraction"
 
 
 def ridge(dtype: str) -> float:
@@ -39,8 +44,18 @@ def _gemm(M, N, K, a_el, b_el, c_el, es, c_es=None, dtype="f16", extra=0.0) -> W
     return Work(flop, byt, "mfma" if flop / byt > ridge(dtype) else "hbm")
 
 
+# Launch groups that stand in for several others when attention scores stay
+# on chip; a layer runs either the group or all of the groups it replaces.
+REPLACES = {
+    "F2-3 qkt_softmax": ("F2 qkt", "F3 softmax"),
+    "B13-15 gamma_dx1_softmax_bwd": ("B13 gamma_dx1", "B15 softmax_bwd"),
+}
+
+
 def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
-    """Work of each labelled launch group of one encoder-layer forward + backward."""
+    """Work of each labelled launch group of one encoder-layer forward + backward.
+
+    Holds both forms of the attention-score steps (see REPLACES)."""
     es = 4 if dtype == "f32" else 2
     T, I, F, H, P, W = s.B * s.J, s.I, s.F, s.H, s.P, s.W
     Z, J, K = s.B * s.H, s.J, s.K
@@ -53,7 +68,7 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["F2 qkt"] = _att(Z, J, K, P, es, dtype, S, N)
     w["F3 softmax"] = m(3 * S * es)
     # QK^T and softmax + dropout in one launch: Q, K read; P and alpha written
-    w["F2-3 qkt_softmax"] = Work(2.0 * Z * J * K * P, float((2 * N + 2 * S) * es), "hbm")
+    w["F2-3 qkt_softmax"] = Work(2.0 * Z * J * K * P, float((2 * N + 2 * S) * es), "hbm", "fused")
     w["F4 gamma"] = _att(Z, J, W, K, es, dtype, S, N)
     w["F5 out"] = g(T, I, I, N, I * I, N)
     w["F6 bdrln1"] = m(4 * N * es + 4 * T + 3 * I * es)
@@ -79,7 +94,7 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["B15 softmax_bwd"] = m(3 * S * es)
     # Gamma dX1 and the softmax + dropout backward in one launch: dGamma, V
     # and P read, dbeta written
-    w["B13-15 gamma_dx1_softmax_bwd"] = Work(2.0 * Z * J * K * W, float((2 * N + 2 * S) * es), "hbm")
+    w["B13-15 gamma_dx1_softmax_bwd"] = Work(2.0 * Z * J * K * W, float((2 * N + 2 * S) * es), "hbm", "fused")
     w["B16 qkt_dx1"] = _att(Z, J, P, K, es, dtype, S, N)
     w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read

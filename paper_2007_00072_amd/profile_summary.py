@@ -29,6 +29,19 @@ def short_name(sym: str) -> str:
         dt = "f16" if m.group(1) == "DF16_" else "bf16"
         mode = lambda b: "k" if b == "1" else "o"
         return f"gemm_dma<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},A:{mode(m.group(6))},B:{mode(m.group(7))}>"
+    m = re.search(r"gemm_leanI(DF16_|DF16b)Li(\d+)ELi(\d+)ELi(\d)ELi(\d)ELi(\d+)ELi(\d)ELb(\d)ELb(\d)", sym)
+    if m:
+        dt = "f16" if m.group(1) == "DF16_" else "bf16"
+        mode = lambda b: "k" if b == "1" else "o"
+        return (f"gemm_lean<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},bk {m.group(6)},"
+                f"A:{mode(m.group(8))},B:{mode(m.group(9))}>")
+    m = re.search(r"gemm_(x32|big)I(DF16_|DF16b)", sym)
+    if m:
+        return f"gemm_{m.group(1)}<{'f16' if m.group(2) == 'DF16_' else 'bf16'}>"
+    m = re.search(r"attn_fused_kI(DF16_|DF16b)Li(\d+)ELi(\d)ELi(\d)ELb(\d)", sym)
+    if m:
+        dt = "f16" if m.group(1) == "DF16_" else "bf16"
+        return f"attn_fused_k<{dt},{'bwd' if m.group(5) == '1' else 'fwd'},D {16 * int(m.group(4))}>"
     m = re.search(r"_ZN2dm12_GLOBAL__N_1\d+(\w+?)I", sym)
     if m:
         return m.group(1)

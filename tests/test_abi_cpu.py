@@ -133,4 +133,7 @@ def test_fused_op_validation(lib):
     with pytest.raises(lib.DmError) as e:
         lib.contract(2, 1, 12, 16, 16, 1.0, 0x10000, 0, 0, 0x10000, 0, 0, None, 0x10000, 0, 0, stream=None)
     assert e.value.code == lib.DM_ERR_UNSUPPORTED
-    assert lib.colsum_ws_bytes(4096, 1024) == 3 * 256 * 1024 * 4
+    # three float partial rows per row block; row blocks = clamp(ceil(rows / 8), 1, 512)
+    assert lib.colsum_ws_bytes(4096, 1024) == 3 * 512 * 1024 * 4
+    assert lib.colsum_ws_bytes(100, 64) == 3 * 13 * 64 * 4
+    assert lib.colsum_ws_bytes(1 << 20, 16) == 3 * 512 * 16 * 4
