@@ -42,11 +42,14 @@ template <> struct V8<half_t> {
     __device__ __forceinline__ static void load(const half_t* p, float v[8]) {
         unpack(*reinterpret_cast<const u32x4*>(p), v);
     }
-    __device__ __forceinline__ static void store(half_t* p, const float v[8]) {
+    __device__ __forceinline__ static u32x4 pack(const float v[8]) {
         half8 h;
 #pragma unroll
         for (int i = 0; i < 8; ++i) h[i] = (half_t)v[i];
-        *reinterpret_cast<u32x4*>(p) = __builtin_bit_cast(u32x4, h);
+        return __builtin_bit_cast(u32x4, h);
+    }
+    __device__ __forceinline__ static void store(half_t* p, const float v[8]) {
+        *reinterpret_cast<u32x4*>(p) = pack(v);
     }
 };
 
@@ -63,11 +66,14 @@ template <> struct V8<bf16_t> {
     __device__ __forceinline__ static void load(const bf16_t* p, float v[8]) {
         unpack(*reinterpret_cast<const u32x4*>(p), v);
     }
-    __device__ __forceinline__ static void store(bf16_t* p, const float v[8]) {
+    __device__ __forceinline__ static u32x4 pack(const float v[8]) {
         bf16x8 h;
 #pragma unroll
         for (int i = 0; i < 8; ++i) h[i] = (bf16_t)v[i];
-        *reinterpret_cast<u32x4*>(p) = __builtin_bit_cast(u32x4, h);
+        return __builtin_bit_cast(u32x4, h);
+    }
+    __device__ __forceinline__ static void store(bf16_t* p, const float v[8]) {
+        *reinterpret_cast<u32x4*>(p) = pack(v);
     }
 };
 

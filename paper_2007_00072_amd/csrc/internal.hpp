@@ -54,15 +54,32 @@ void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void*
 // attn_fused_ok: dtype fp16 / bf16, K a multiple of 32 up to 960, D (the
 // contraction length) in {16, 32, 48, 64, 96, 128}.
 bool attn_fused_ok(int dtype, int K, int D);
-// P = softmax_k(round(scaler * Q K^T)), alpha = dropout(P)
+// The contraction that follows in the same launch: out[z][j][n] =
+// sum_k tile[z][j][k] x[z][k][n] with x element (z, k, n) at
+// x + b*x_outer + h*x_inner + k*x_ld + n and out element (z, j, n) at
+// out + b*o_outer + h*o_inner + j*o_ld + n; n < N.  attn_next_ok: the
+// scores' own conditions, D (the first contraction's length) and N in
+// {32, 64, 128}, x 16-byte aligned with strides that are multiples of 8
+// elements, and the block's LDS within 64 KB.
+struct AttnNext {
+    const void* x = nullptr;
+    int64_t x_outer = 0, x_inner = 0, x_ld = 0;
+    void* out = nullptr;
+    int64_t o_outer = 0, o_inner = 0, o_ld = 0;
+    int N = 0;
+};
+bool attn_next_ok(int dtype, int K, int D, const AttnNext& n);
+// P = softmax_k(round(scaler * Q K^T)), alpha = dropout(P); with `next`,
+// also gamma = alpha V
 void run_attn_scores_fwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* q, int64_t q_outer,
                          int64_t q_inner, int64_t q_ld, const void* k, int64_t k_outer, int64_t k_inner, int64_t k_ld,
-                         const DropParams& dp, void* prob, void* alpha, hipStream_t st);
-// d(beta) = scaler * P * (dP - sum_k dP P), dP = dropout(round(d(gamma) V^T))
+                         const DropParams& dp, void* prob, void* alpha, const AttnNext* next, hipStream_t st);
+// d(beta) = scaler * P * (dP - sum_k dP P), dP = dropout(round(d(gamma) V^T));
+// with `next`, also dQ = d(beta) K
 void run_attn_scores_bwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* dgamma,
                          int64_t dg_outer, int64_t dg_inner, int64_t dg_ld, const void* v, int64_t v_outer,
                          int64_t v_inner, int64_t v_ld, const void* prob, const DropParams& dp, void* dbeta,
-                         hipStream_t st);
+                         const AttnNext* next, hipStream_t st);
 
 void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta,
                      const DropParams& dp, void* prob, void* alpha, hipStream_t st);

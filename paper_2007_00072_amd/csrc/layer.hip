@@ -307,11 +307,17 @@ int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const 
                        const void* v, void* beta, void* prob, void* alpha, void* gamma, hipStream_t st) {
     const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, HW = x.H * x.W;
     if (attn_fused_ok(x.dtype, (int)K, (int)P)) {
-        // QK^T and the softmax + dropout in one launch (beta stays on chip)
-        TraceScope t_("F2-3 qkt_softmax", st);
+        // QK^T and the softmax + dropout in one launch (beta stays on chip),
+        // and Gamma in the same launch when its shape allows
+        AttnNext nx;
+        nx.x = v; nx.x_outer = x.H * K * W; nx.x_inner = K * W; nx.x_ld = W;
+        nx.out = gamma; nx.o_outer = J * HW; nx.o_inner = W; nx.o_ld = HW; nx.N = (int)W;
+        const bool with_gamma = attn_next_ok(x.dtype, (int)K, (int)P, nx);
+        TraceScope t_(with_gamma ? "F2-4 qkt_softmax_gamma" : "F2-3 qkt_softmax", st);
         run_attn_scores_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, (int)P, scaler, q, x.H * J * P, J * P, P, k,
-                            x.H * K * P, K * P, P, dp, prob, alpha, st);
+                            x.H * K * P, K * P, P, dp, prob, alpha, with_gamma ? &nx : nullptr, st);
         DM_TRY(check_launch("attention scores"));
+        if (with_gamma) return DM_OK;
     } else {
     // beta[z][j][k] = scaler * sum_p Q[z][j][p] K[z][k][p]
     Epilogue cb = epi(beta, linear_map(K), linear_map(1), true, false, linear_map(J * K));
@@ -375,12 +381,17 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
     const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
     t12.stop();
     const bool fused = attn_fused_ok(x.dtype, (int)K, (int)W);
+    AttnNext nq;
+    nq.x = k; nq.x_outer = H * K * P; nq.x_inner = K * P; nq.x_ld = P;
+    nq.out = dq; nq.o_outer = J * ldq; nq.o_inner = P; nq.o_ld = ldq; nq.N = (int)P;
+    const bool with_dq = fused && attn_next_ok(x.dtype, (int)K, (int)W, nq);
     if (fused) {
         // Gamma dX1 and the scaled softmax + dropout backward in one launch
-        // (dalpha stays on chip): dbeta[z][j][k]
-        TraceScope t_("B13-15 gamma_dx1_softmax_bwd", st);
+        // (dalpha stays on chip): dbeta[z][j][k]; QK^T dX1 in the same
+        // launch when its shape allows
+        TraceScope t_(with_dq ? "B13+15+16 score_bwd_dq" : "B13-15 gamma_dx1_softmax_bwd", st);
         run_attn_scores_bwd(x.dtype, (int)x.B, (int)H, (int)J, (int)K, (int)W, scaler, dgamma, J * HW, W, HW, v,
-                            H * K * W, K * W, W, prob, dp, dbeta, st);
+                            H * K * W, K * W, W, prob, dp, dbeta, with_dq ? &nq : nullptr, st);
         DM_TRY(check_launch("attention score backward"));
     } else {
     // Gamma dX1: dalpha[z][j][k] = sum_w dgamma[(b,j)][(h,w)] V[z][k][w]
@@ -407,15 +418,16 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
         run_softmax_bwd(x.dtype, (int)x.B, (int)H, (int)J, (int)K, scaler, dalpha, prob, dp, dbeta, st);
         DM_TRY(check_launch("softmax backward"));
     }
-    // QK^T dX1: dQ[z][j][p] = sum_k dbeta[z][j][k] K[z][k][p]
-    TraceScope t16("B16 qkt_dx1", st);
-    DM_TRY(launch_gemm(x.dtype,
-                       gemm(J, P, K, Z, opnd(dbeta, true, linear_map(K), linear_map(J * K)),
-                            opnd(k, false, linear_map(P), linear_map(K * P)),
-                            epi(dq, linear_map(ldq), linear_map(1), true, false,
-                                make_map((uint32_t)H, 0, P, J * ldq, 0))),
-                       st));
-    t16.stop();
+    if (!with_dq) {
+        // QK^T dX1: dQ[z][j][p] = sum_k dbeta[z][j][k] K[z][k][p]
+        TraceScope t16("B16 qkt_dx1", st);
+        DM_TRY(launch_gemm(x.dtype,
+                           gemm(J, P, K, Z, opnd(dbeta, true, linear_map(K), linear_map(J * K)),
+                                opnd(k, false, linear_map(P), linear_map(K * P)),
+                                epi(dq, linear_map(ldq), linear_map(1), true, false,
+                                    make_map((uint32_t)H, 0, P, J * ldq, 0))),
+                           st));
+    }
     // QK^T dX2: dK[z][k][p] = sum_j dbeta[z][j][k] Q[z][j][p]
     TraceScope t17("B17 qkt_dx2", st);
     DM_TRY(launch_gemm(x.dtype,

@@ -48,8 +48,24 @@ def _gemm(M, N, K, a_el, b_el, c_el, es, c_es=None, dtype="f16", extra=0.0) -> W
 # on chip; a layer runs either the group or all of the groups it replaces.
 REPLACES = {
     "F2-3 qkt_softmax": ("F2 qkt", "F3 softmax"),
+    "F2-4 qkt_softmax_gamma": ("F2 qkt", "F3 softmax", "F4 gamma"),
     "B13-15 gamma_dx1_softmax_bwd": ("B13 gamma_dx1", "B15 softmax_bwd"),
+    "B13+15+16 score_bwd_dq": ("B13 gamma_dx1", "B15 softmax_bwd", "B16 qkt_dx1"),
 }
+# The launch sets one layer can run: every score step separate, scores on
+# chip, and scores on chip with the next contraction in the same launch.
+PATHS = {
+    "separate": (),
+    "scores": ("F2-3 qkt_softmax", "B13-15 gamma_dx1_softmax_bwd"),
+    "scores_next": ("F2-4 qkt_softmax_gamma", "B13+15+16 score_bwd_dq"),
+}
+
+
+def path_groups(w: Dict[str, "Work"], path: str) -> Dict[str, "Work"]:
+    """The launch groups of `w` that path `path` runs."""
+    fused = PATHS[path]
+    gone = {p for f in fused for p in REPLACES[f]}
+    return {k: v for k, v in w.items() if (k not in REPLACES or k in fused) and k not in gone}
 
 
 def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
@@ -69,6 +85,8 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["F3 softmax"] = m(3 * S * es)
     # QK^T and softmax + dropout in one launch: Q, K read; P and alpha written
     w["F2-3 qkt_softmax"] = Work(2.0 * Z * J * K * P, float((2 * N + 2 * S) * es), "hbm", "fused")
+    # ... and Gamma = alpha V in the same launch: V read and Gamma written too
+    w["F2-4 qkt_softmax_gamma"] = Work(2.0 * Z * J * K * (P + W), float((4 * N + 2 * S) * es), "hbm", "fused")
     w["F4 gamma"] = _att(Z, J, W, K, es, dtype, S, N)
     w["F5 out"] = g(T, I, I, N, I * I, N)
     w["F6 bdrln1"] = m(4 * N * es + 4 * T + 3 * I * es)
@@ -95,6 +113,8 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     # Gamma dX1 and the softmax + dropout backward in one launch: dGamma, V
     # and P read, dbeta written
     w["B13-15 gamma_dx1_softmax_bwd"] = Work(2.0 * Z * J * K * W, float((2 * N + 2 * S) * es), "hbm", "fused")
+    # ... and dQ = dbeta K in the same launch: K read and dQ written too
+    w["B13+15+16 score_bwd_dq"] = Work(2.0 * Z * J * K * (W + P), float((4 * N + 2 * S) * es), "hbm", "fused")
     w["B16 qkt_dx1"] = _att(Z, J, P, K, es, dtype, S, N)
     w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read

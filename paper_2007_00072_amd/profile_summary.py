@@ -38,10 +38,11 @@ def short_name(sym: str) -> str:
     m = re.search(r"gemm_(x32|big)I(DF16_|DF16b)", sym)
     if m:
         return f"gemm_{m.group(1)}<{'f16' if m.group(2) == 'DF16_' else 'bf16'}>"
-    m = re.search(r"attn_fused_kI(DF16_|DF16b)Li(\d+)ELi(\d)ELi(\d)ELb(\d)", sym)
+    m = re.search(r"attn_fused_kI(DF16_|DF16b)Li(\d+)ELi(\d)ELi(\d)ELb(\d)(?:ELi(\d))?", sym)
     if m:
         dt = "f16" if m.group(1) == "DF16_" else "bf16"
-        return f"attn_fused_k<{dt},{'bwd' if m.group(5) == '1' else 'fwd'},D {16 * int(m.group(4))}>"
+        nxt = f",next {32 * int(m.group(6))}" if m.group(6) and m.group(6) != "0" else ""
+        return f"attn_fused_k<{dt},{'bwd' if m.group(5) == '1' else 'fwd'},D {16 * int(m.group(4))}{nxt}>"
     m = re.search(r"_ZN2dm12_GLOBAL__N_1\d+(\w+?)I", sym)
     if m:
         return m.group(1)

@@ -23,15 +23,16 @@ def test_layer_model_flops_consistent():
     s = WORKLOADS["bert_large_f16"].shape
     w = dataflow.encoder_layer(s, "f16")
     table3 = sum(dataflow.contraction_gflop(s).values())
-    fused = set(dataflow.REPLACES)
-    parts = {p for v in dataflow.REPLACES.values() for p in v}
-    unfused_total = sum(x.flop for k, x in w.items() if k not in fused) / 1e9
-    fused_total = sum(x.flop for k, x in w.items() if k not in parts) / 1e9
-    assert unfused_total == pytest.approx(table3, rel=1e-12)
-    assert fused_total == pytest.approx(table3, rel=1e-12)
+    for path in dataflow.PATHS:
+        groups = dataflow.path_groups(w, path)
+        assert sum(x.flop for x in groups.values()) / 1e9 == pytest.approx(table3, rel=1e-12), path
+    assert "F4 gamma" in dataflow.path_groups(w, "scores")
+    assert "F4 gamma" not in dataflow.path_groups(w, "scores_next")
     for k, v in dataflow.REPLACES.items():
         assert w[k].flop == sum(w[p].flop for p in v)
         assert w[k].cls == "fused"
+        # a fused group moves less than the groups it stands in for
+        assert w[k].bytes < sum(w[p].bytes for p in v)
     # the projection / feed-forward contractions are MFMA-bound, attention and fused ops HBM-bound
     assert w["F7 linear1"].bound == "mfma" and w["F1 qkv"].bound == "mfma"
     assert w["F2 qkt"].bound == "hbm" and w["F3 softmax"].bound == "hbm"

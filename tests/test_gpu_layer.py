@@ -203,6 +203,24 @@ def test_mha_fused_scores_ragged_rows(dtype):
     check_mha(wl, self_attention=False)
 
 
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("shape", [
+    # Gamma and dQ 64 wide: 34 k16 steps over 4 waves per column block, so
+    # the key-side rows arrive in two register groups; ragged query rows
+    dict(B=1, J=72, K=544, H=2, P=64, W=64, I=96),
+    # Gamma 128 wide (4 column blocks, 2 waves each, two register groups),
+    # dQ 64 wide after a 128-long Gamma dX1 contraction
+    dict(B=2, J=40, K=320, H=2, P=64, W=128, I=160),
+    # a single pair of k16 steps: most waves idle; one partial query block
+    dict(B=1, J=24, K=32, H=3, P=128, W=32, I=96),
+])
+def test_mha_fused_next_contraction(dtype, shape):
+    # Gamma = alpha V in the attention-score launch and dQ = dbeta K in the
+    # score-backward launch, from the rounded row tile in LDS
+    wl = WORKLOADS["mha_large_f16"].with_(shape=Shape(**shape), dtype=dtype, layout="bji", p_attn=0.1)
+    check_mha(wl, self_attention=False)
+
+
 @pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
 def test_encoder_fused_scores(name):
     # several 32-row blocks per head through the on-chip score kernels
