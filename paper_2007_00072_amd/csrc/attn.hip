@@ -54,6 +54,11 @@ template <> struct AMfma<bf16_t> {
     }
 };
 
+template <typename T>
+__device__ __forceinline__ uint32_t bits16(T v) {
+    return (uint32_t)__builtin_bit_cast(uint16_t, v);
+}
+
 // Operand rows: element (z = b*H + h, row r, contraction index d) at
 // ptr + b*outer + h*inner + r*ld + d.
 struct AttnOp {
@@ -101,7 +106,7 @@ constexpr int STG_BYTES = 2048;  // per-wave staging slot: two 16 x 32 pieces
 constexpr int PF2 = 8;           // k16 steps of the second contraction loaded ahead into registers
 
 inline size_t attn_lds_bytes(int K, int es, int nb2) {
-    const size_t s = ((size_t)32 * (K + 16) * es + 15) / 16 * 16;
+    const size_t s = ((size_t)32 * (K + 8) * es + 15) / 16 * 16;
     if (nb2 == 0) return s;
     const size_t ks = 8 / nb2;
     return std::max(s + (size_t)(NTA / 64) * STG_BYTES, (ks - 1) * nb2 * 4096);
@@ -111,11 +116,36 @@ template <typename T, int LPR, int NV, int DK, bool BWD, int NB2>
 __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     T* S = reinterpret_cast<T*>(smem_raw);
-    const int K = g.K, J = g.J, pitch = K + 16;  // 4 rows apart = 32 banks mod 64: the half-waves' writes do not collide
+    // rows 16 bytes apart in bank space: the 8-byte tile writes, the 16-byte
+    // fragment reads and the row operator's 16-byte accesses all spread over
+    // the 64 banks
+    const int K = g.K, J = g.J, pitch = K + 8;
     const int z = blockIdx.y, j0 = blockIdx.x * 32;
     const int b = z / g.H, h = z - b * g.H;
     const int tid = threadIdx.x, lane = tid & 63, c = lane & 31, hh = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // row phase geometry: one lane group of LPR lanes per row, NV 8-element
+    // vectors per lane, NIT rows per lane group
+    constexpr int RPW = 64 / LPR;
+    constexpr int NIT = (32 + (NTA / 64) * RPW - 1) / ((NTA / 64) * RPW);  // lane groups past row 31 stay idle
+    const int gi = lane / LPR, gl = lane % LPR;
+    const int nr = min(32, J - j0);
+
+    // backward: the rows of P this lane reads start loading now and arrive
+    // while the first contraction runs (clamped to valid rows and columns;
+    // what lies outside is never used)
+    [[maybe_unused]] u32x4 pre[BWD ? NIT : 1][NV];
+    if constexpr (BWD) {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const int jj = min(j0 + it * (NTA / 64) * RPW + wave * RPW + gi, J - 1);
+#pragma unroll
+            for (int i = 0; i < NV; ++i)
+                pre[it][i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(g.prob) +
+                                                             ((int64_t)z * J + jj) * K + min((gl + i * LPR) * 8, K - 8));
+        }
+    }
 
     // ---- contraction: S[32][K] = out_scale * A_rows . B_rows^T
     {
@@ -134,39 +164,50 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
             floatx16 acc;
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+            // key rows as the MFMA's first operand: the result is the tile's
+            // transpose, so lane l holds query row l % 32 at 4 consecutive
+            // keys per accumulator quad and writes them as one 8-byte piece
 #pragma unroll
-            for (int s = 0; s < DK; ++s) acc = AMfma<T>::run(af[s], bf[s], acc);
+            for (int s = 0; s < DK; ++s) acc = AMfma<T>::run(bf[s], af[s], acc);
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                S[(8 * (r >> 2) + 4 * hh + (r & 3)) * pitch + cb * 32 + c] = from_f<T>(acc[r] * g.out_scale);
+            for (int q = 0; q < 4; ++q) {
+                uint2 pk;
+                pk.x = bits16(from_f<T>(acc[4 * q] * g.out_scale)) | (bits16(from_f<T>(acc[4 * q + 1] * g.out_scale)) << 16);
+                pk.y = bits16(from_f<T>(acc[4 * q + 2] * g.out_scale)) |
+                       (bits16(from_f<T>(acc[4 * q + 3] * g.out_scale)) << 16);
+                *reinterpret_cast<uint2*>(S + c * pitch + cb * 32 + 8 * q + 4 * hh) = pk;
+            }
         }
     }
     __syncthreads();
 
-    // ---- second contraction, part 1: its key-side rows start loading now
-    // and arrive while the row phase runs.  Wave w takes output columns
-    // 32 (w % NB2) .. +31 and the k16 steps s = w / NB2 + KS i.
+    // ---- second contraction, part 1: its key-side rows start loading
+    // before the row phase forward (arriving while it runs) and right after
+    // it backward (where P's preloaded rows hold the registers until then).
+    // Wave w takes output columns 32 (w % NB2) .. +31 and the k16 steps
+    // s = w / NB2 + KS i.
     constexpr int KS = NB2 > 0 ? 8 / NB2 : 1;
     const int cbn = NB2 > 0 ? wave % NB2 : 0, ks = NB2 > 0 ? wave / NB2 : 0;
     const int nst = K / 16;
     const int cnt = (NB2 > 0 && ks < KS) ? (nst - ks + KS - 1) / KS : 0;
     [[maybe_unused]] u32x4 xr[NB2 > 0 ? PF2 : 1];
     [[maybe_unused]] const T* xbase = nullptr;
-    if constexpr (NB2 > 0) {
-        xbase = reinterpret_cast<const T*>(g.x.ptr) + b * g.x.outer + h * g.x.inner + cbn * 32 + 8 * (lane & 3);
-        // every wave loads (idle ones and steps past the end re-read the last step)
+    // every wave loads (idle ones and steps past the end re-read the last step)
+    auto load_next = [&](int g0) {
 #pragma unroll
         for (int i = 0; i < PF2; ++i)
-            xr[i] = *reinterpret_cast<const u32x4*>(xbase + (int64_t)(16 * min(ks + KS * i, nst - 1) + (lane >> 2)) *
-                                                                g.x.ld);
+            xr[i] = *reinterpret_cast<const u32x4*>(xbase + (int64_t)(16 * min(ks + KS * (g0 + i), nst - 1) +
+                                                                       (lane >> 2)) * g.x.ld);
+    };
+    if constexpr (NB2 > 0) {
+        xbase = reinterpret_cast<const T*>(g.x.ptr) + b * g.x.outer + h * g.x.inner + cbn * 32 + 8 * (lane & 3);
+        if constexpr (!BWD) load_next(0);
     }
 
-    // ---- row phase: one lane group of LPR lanes per row, NV 8-element vectors per lane
-    constexpr int RPW = 64 / LPR;
-    const int gi = lane / LPR, gl = lane % LPR;
-    const int nr = min(32, J - j0);
-    for (int rb = 0; rb < 32; rb += (NTA / 64) * RPW) {
-        const int lr = rb + wave * RPW + gi;
+    // ---- row phase
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int lr = it * (NTA / 64) * RPW + wave * RPW + gi;
         const bool active = lr < nr;
         const int j = j0 + lr;
         const int64_t base = ((int64_t)z * J + j) * K;              // row of P / alpha / d(beta)
@@ -188,13 +229,14 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
             }
             mx = group_max<LPR>(mx);
             float sum = 0.f;
+            const ExpShift ex(mx);
 #pragma unroll
             for (int i = 0; i < NV; ++i)
 #pragma unroll
-                for (int q = 0; q < 8; ++q) { v[i][q] = __expf(v[i][q] - mx); sum += v[i][q]; }
+                for (int q = 0; q < 8; ++q) { v[i][q] = ex(v[i][q]); sum += v[i][q]; }
             sum = group_sum<LPR>(sum);
             if (!active) continue;
-            const float rinv = 1.0f / sum;
+            const float rinv = __builtin_amdgcn_rcpf(sum);
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
                 const int col = (gl + i * LPR) * 8;
@@ -215,7 +257,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
             for (int i = 0; i < NV; ++i) {
                 const int col = (gl + i * LPR) * 8;
                 if (active && col < K) {
-                    V8<T>::load(reinterpret_cast<const T*>(g.prob) + base + col, p[i]);
+                    V8<T>::unpack(pre[it][i], p[i]);
                     V8<T>::unpack(*reinterpret_cast<const u32x4*>(S + lr * pitch + col), v[i]);
                     dropout8(g.dp, (uint64_t)(ebase + col), v[i]);
 #pragma unroll
@@ -245,6 +287,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
     // ---- second contraction, part 2: out2[j][n] = sum_k S[j][k] X[k][n] over
     // the rounded row tile now in LDS (alpha forward, d(beta) backward)
     if constexpr (NB2 > 0) {
+        if constexpr (BWD) load_next(0);
         __syncthreads();
         const size_t s_bytes = ((size_t)32 * pitch * sizeof(T) + 15) / 16 * 16;
         T* stg = reinterpret_cast<T*>(smem_raw + s_bytes + wave * STG_BYTES);
@@ -253,12 +296,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
         for (int r = 0; r < 16; ++r) acc[r] = 0.f;
         const T* arow = S + c * pitch + 8 * hh;
         for (int g0 = 0; g0 < cnt; g0 += PF2) {
-            if (g0 > 0) {
-#pragma unroll
-                for (int i = 0; i < PF2; ++i)
-                    xr[i] = *reinterpret_cast<const u32x4*>(
-                        xbase + (int64_t)(16 * min(ks + KS * (g0 + i), nst - 1) + (lane >> 2)) * g.x.ld);
-            }
+            if (g0 > 0) load_next(g0);
 #pragma unroll
             for (int i = 0; i < PF2; i += 2) {
                 if (g0 + i < cnt) {

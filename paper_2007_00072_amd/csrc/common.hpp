@@ -94,18 +94,59 @@ template <> struct V8<float> {
 };
 
 // ------------------------------------------------------ wave64 reductions
-// Butterfly over `width` consecutive lanes (a power of two <= 64).
+// Reduction over `width` consecutive lanes (a power of two <= 64); every
+// lane of the group receives the result.  Within a row of 16 lanes the
+// partners come from DPP operand permutations, which cost one VALU
+// instruction per step (a lane shuffle through the LDS unit costs about
+// seven, with an LDS round trip): quad_perm [1,0,3,2] and [2,3,0,1] pair
+// lanes 1 and 2 apart, then row_half_mirror (lane i <-> 7 - i within 8) and
+// row_mirror (i <-> 15 - i within 16) join the halves that already hold
+// their partial results.  Across rows: one shuffle for 32 lanes; for the
+// whole wave the four row results are read into scalar registers, so the
+// result is wave-uniform.
+namespace dpp {
+constexpr int QUAD_XOR1 = 0xB1, QUAD_XOR2 = 0x4E, ROW_HALF_MIRROR = 0x141, ROW_MIRROR = 0x140;
+template <int CTRL>
+__device__ __forceinline__ float perm(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+}  // namespace dpp
+
+template <int WIDTH, typename Op>
+__device__ __forceinline__ float group_reduce(float v, Op op) {
+    static_assert(WIDTH >= 1 && WIDTH <= 64 && (WIDTH & (WIDTH - 1)) == 0, "group width");
+    if constexpr (WIDTH >= 2) v = op(v, dpp::perm<dpp::QUAD_XOR1>(v));
+    if constexpr (WIDTH >= 4) v = op(v, dpp::perm<dpp::QUAD_XOR2>(v));
+    if constexpr (WIDTH >= 8) v = op(v, dpp::perm<dpp::ROW_HALF_MIRROR>(v));
+    if constexpr (WIDTH >= 16) v = op(v, dpp::perm<dpp::ROW_MIRROR>(v));
+    if constexpr (WIDTH == 32) v = op(v, __shfl_xor(v, 16, 64));
+    if constexpr (WIDTH == 64) {
+        const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+        const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+        const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+        const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+        v = op(op(r0, r1), op(r2, r3));
+    }
+    return v;
+}
+// e^(x - m) for the softmax rows, as 2^(x log2(e) - m log2(e)): one fma and
+// one v_exp_f32 per element (the subtraction folds into the fma; results
+// below 2^-126 flush to zero, far under the storage types' resolution).
+struct ExpShift {
+    float ml;
+    __device__ __forceinline__ explicit ExpShift(float m) : ml(m * 1.4426950408889634f) {}
+    __device__ __forceinline__ float operator()(float x) const {
+        return __builtin_amdgcn_exp2f(fmaf(x, 1.4426950408889634f, -ml));
+    }
+};
+
 template <int WIDTH>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-    for (int o = WIDTH / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+    return group_reduce<WIDTH>(v, [](float a, float b) { return a + b; });
 }
 template <int WIDTH>
 __device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-    for (int o = WIDTH / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+    return group_reduce<WIDTH>(v, [](float a, float b) { return fmaxf(a, b); });
 }
 
 // ------------------------------------------------- counter-based dropout

@@ -111,13 +111,14 @@ __global__ __launch_bounds__(NT) void softmax_fwd_k(int64_t rows, int B, int H, 
     }
     mx = group_max<LPR>(mx);
     float sum = 0.f;
+    const ExpShift ex(mx);
 #pragma unroll
     for (int i = 0; i < NV; ++i)
 #pragma unroll
-        for (int q = 0; q < 8; ++q) { v[i][q] = __expf(v[i][q] - mx); sum += v[i][q]; }
+        for (int q = 0; q < 8; ++q) { v[i][q] = ex(v[i][q]); sum += v[i][q]; }
     sum = group_sum<LPR>(sum);
     if (!active) return;
-    const float rinv = 1.0f / sum;
+    const float rinv = __builtin_amdgcn_rcpf(sum);
     const int j = (int)(row % J);
     const int64_t bh = row / J;
     const int h = (int)(bh % H), b = (int)(bh / H);
