@@ -252,9 +252,9 @@ int ln_param_bwd(int32_t dtype, int64_t rows, int32_t cols, const void* dy, cons
     a.dtype = dtype; a.rows = rows; a.cols = cols; a.dya = dy; a.xhat = xhat;
     a.dp = make_drop(0.f, 0, 0, 0); a.part = (float*)ws;
     run_ln_bwd(a, S(stream));
-    const int nb = colsum_blocks(rows);
-    run_colsum_finish(rows, cols, (float*)ws, dgamma, S(stream));
-    run_colsum_finish(rows, cols, (float*)ws + (size_t)nb * cols, dbeta, S(stream));
+    const int nb = ln_bwd_blocks(rows, cols, dtype);
+    run_colsum_finish(nb, cols, (float*)ws, dgamma, S(stream));
+    run_colsum_finish(nb, cols, (float*)ws + (size_t)nb * cols, dbeta, S(stream));
     return check_launch("ln_param_bwd");
 }
 
@@ -288,9 +288,9 @@ int residual_ln_param_bwd(int32_t dtype, int64_t rows, int32_t cols, const void*
     a.dtype = dtype; a.rows = rows; a.cols = cols; a.dya = da; a.dyb = db; a.xhat = xhat;
     a.dp = make_drop(0.f, 0, 0, 0); a.dysum = dsum; a.part = (float*)ws;
     run_ln_bwd(a, S(stream));
-    const int nb = colsum_blocks(rows);
-    run_colsum_finish(rows, cols, (float*)ws, dgamma, S(stream));
-    run_colsum_finish(rows, cols, (float*)ws + (size_t)nb * cols, dbeta, S(stream));
+    const int nb = ln_bwd_blocks(rows, cols, dtype);
+    run_colsum_finish(nb, cols, (float*)ws, dgamma, S(stream));
+    run_colsum_finish(nb, cols, (float*)ws + (size_t)nb * cols, dbeta, S(stream));
     return check_launch("residual_ln_param_bwd");
 }
 
@@ -310,9 +310,9 @@ int act_bias_bwd(int32_t dtype, int64_t rows, int32_t F, int32_t I, const void* 
     if (ws_bytes < colsum_ws_bytes(rows, mx)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
     float* part = (float*)ws;
     run_act_bwd(dtype, rows, F, da, h, b1, act, make_drop(drop), dh, part, S(stream));
-    run_colsum_finish(rows, F, part, db1, S(stream));
+    run_colsum_finish(colsum_blocks(rows), F, part, db1, S(stream));
     run_colsum_partial(dtype, rows, I, dout, part, S(stream));
-    run_colsum_finish(rows, I, part, db2, S(stream));
+    run_colsum_finish(colsum_blocks(rows), I, part, db2, S(stream));
     return check_launch("act_bias_bwd");
 }
 
@@ -337,7 +337,7 @@ int bias_grad(int32_t dtype, int64_t rows, int32_t cols, const void* x, float* d
     if (ws_bytes < colsum_ws_bytes(rows, cols)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
     run_colsum_partial(dtype, rows, cols, x, (float*)ws, S(stream));
     trace_next("finish");
-    run_colsum_finish(rows, cols, (float*)ws, db, S(stream));
+    run_colsum_finish(colsum_blocks(rows), cols, (float*)ws, db, S(stream));
     return check_launch("bias_grad");
 }
 
@@ -351,7 +351,7 @@ int attn_input_bias_grad(int32_t dtype, int64_t rows, int32_t H, int32_t P, cons
     if (!dbq || !dbk || !dbv) return set_error(DM_ERR_ARG, "bias gradient pointer is NULL");
     if (ws_bytes < colsum_ws_bytes(rows, 3 * H * P)) return set_error(DM_ERR_WORKSPACE, "workspace too small");
     run_colsum_partial(dtype, rows, 3 * H * P, x, (float*)ws, S(stream));
-    run_colsum_finish_qkv(rows, H, P, 3, (float*)ws, dbq, dbk, dbv, S(stream));
+    run_colsum_finish_qkv(colsum_blocks(rows), H, P, 3, (float*)ws, dbq, dbk, dbv, S(stream));
     return check_launch("attn_input_bias_grad");
 }
 

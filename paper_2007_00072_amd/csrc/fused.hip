@@ -400,22 +400,28 @@ __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, c
     V8<float>::store(part + (int64_t)blockIdx.x * cols + v * 8, acc);
 }
 
-// out[c] = sum over the nblk partial rows in a fixed order.  Block x covers
-// columns 16x .. 16x+15 as 4 four-column groups x 64 row phases (each phase
-// sums rows ph, ph+64, ... with several loads in flight); block y selects
-// one of up to three partial sets (part + y*nblk*cols -> outs[y]).  With
+// out[c] = sum over the nblk partial rows in a fixed order.  A launch runs
+// a list of jobs (partial sets of several operators, finished together);
+// each block finds its job from the jobs' first-block table, then covers
+// columns 16x .. 16x+15 of one partial set as 4 four-column groups x 64 row
+// phases (each phase sums rows ph, ph+64, ... with several loads in
+// flight).  Set y of a job is part + y*nblk*cols -> out[y].  With
 // qkv_H > 0 the columns are (s, h, p) of a fused projection and land in
-// outs[s][p * qkv_H + h] (single partial set).
-struct FinishOut {
-    float* out[3];
-};
-
-__global__ __launch_bounds__(NT) void colsum_finish_k(int nblk, int cols, const float* __restrict__ part,
-                                                      FinishOut fo, int qkv_H, int qkv_P) {
+// out[s][p * qkv_H + h] (single partial set).
+__global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
     __shared__ floatx4 red[64][4];
+    int jb = 0;
+#pragma unroll
+    for (int i = 1; i < MAX_FINISH_JOBS; ++i)
+        if (i < fj.n && (int)blockIdx.x >= fj.first[i]) jb = i;
+    const FinishJob& job = fj.job[jb];
+    const int cols = job.cols, nblk = job.nblk;
+    const int local = (int)blockIdx.x - fj.first[jb];
+    const int ncb = (cols + 15) / 16;
+    const int set = local / ncb, cbk = local - set * ncb;
     const int cg = threadIdx.x & 3, ph = threadIdx.x >> 2;
-    const int c = blockIdx.x * 16 + cg * 4;
-    const float* base = part + (int64_t)blockIdx.y * nblk * cols;
+    const int c = cbk * 16 + cg * 4;
+    const float* base = job.part + (int64_t)set * nblk * cols;
     floatx4 s[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) s[u] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -437,13 +443,13 @@ __global__ __launch_bounds__(NT) void colsum_finish_k(int nblk, int cols, const 
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int cc = c + q;
-            if (qkv_H > 0) {
+            if (job.qkv_H > 0) {
                 // column (s, h, p) of a fused projection -> bias gradient b_s[p][h]
-                const int I = qkv_H * qkv_P;
-                const int sg = cc / I, hp = cc - sg * I, hh = hp / qkv_P, pp = hp - hh * qkv_P;
-                fo.out[sg][pp * qkv_H + hh] = t[q];
+                const int I = job.qkv_H * job.qkv_P;
+                const int sg = cc / I, hp = cc - sg * I, hh = hp / job.qkv_P, pp = hp - hh * job.qkv_P;
+                job.out[sg][pp * job.qkv_H + hh] = t[q];
             } else {
-                fo.out[blockIdx.y][cc] = t[q];
+                job.out[set][cc] = t[q];
             }
         }
     }
@@ -589,10 +595,150 @@ void softmax_bwd_t(int B, int H, int J, int len, float scale, const void* dalpha
 #undef L
 }
 
+// Column-split form for rows of 320 .. 1024 elements (multiples of 64):
+// the block's 8 waves own 8 column slices of 16-row tiles, a lane group of
+// LG lanes (a power of two covering the slice's cols/64 vectors) takes one
+// row of its slice, and a wave covers 64/LG rows per pass.  The row
+// statistics need the whole row: each lane group reduces its slice with
+// DPP steps and the 8 slice sums meet in LDS, added in slice order (the
+// tiles alternate between two LDS halves, so one barrier per tile
+// suffices).  Column partial sums never leave their wave: a lane keeps
+// its 8 columns' sums over all the rows it sees, the wave's lane groups
+// are added with shuffles at the end, and lane group 0 writes
+// part[q][blockIdx.x][columns].  Blocks stride over the tiles, so the
+// partial count is ln_bwd_blocks(rows, cols).
+constexpr int LN_TILE = 16;
+
+template <typename T, int LG>
+__global__ __launch_bounds__(NTL) void ln_bwd_cs_k(LnBwdArgs a, int nblk) {
+    constexpr int NW = NTL / 64;       // column slices
+    constexpr int RPP = 64 / LG;       // rows per pass of one wave
+    constexpr int NP = LN_TILE / RPP;  // passes per tile
+    __shared__ float rowred[2][LN_TILE][NW][2];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int gi = lane / LG, v = lane % LG;
+    const int cols = a.cols, vpr = cols / (8 * NW);
+    const bool vact = v < vpr;
+    const int c = (wave * vpr + (vact ? v : 0)) * 8;  // this lane's 8 columns (idle lanes alias the slice's first)
+    const T* dya = reinterpret_cast<const T*>(a.dya);
+    const T* dyb = reinterpret_cast<const T*>(a.dyb);
+    const T* xhat = reinterpret_cast<const T*>(a.xhat);
+    const bool do_ds = a.ds || a.dsub;
+    const bool do_part = a.part != nullptr;
+    const float inv = 1.0f / (float)cols;
+
+    float g[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) g[q] = 0.f;
+    if (do_ds) V8<T>::load(reinterpret_cast<const T*>(a.gamma) + c, g);
+    float p_dyx[8], p_dy[8], p_dsub[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) { p_dyx[q] = 0.f; p_dy[q] = 0.f; p_dsub[q] = 0.f; }
+
+    int buf = 0;
+    for (int64_t t0 = (int64_t)blockIdx.x * LN_TILE; t0 < a.rows; t0 += (int64_t)nblk * LN_TILE, buf ^= 1) {
+        // every load of the tile is issued before any arithmetic (rows past
+        // the end re-read the tile's first row; their results are dropped)
+        u32x4 ldy[NP], lxh[NP], ldb[NP];
+        float rs[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const int64_t row = t0 + p * RPP + gi;
+            const int64_t rr = row < a.rows ? row : t0;
+            ldy[p] = *reinterpret_cast<const u32x4*>(dya + rr * cols + c);
+            lxh[p] = *reinterpret_cast<const u32x4*>(xhat + rr * cols + c);
+            if (dyb) ldb[p] = *reinterpret_cast<const u32x4*>(dyb + rr * cols + c);
+            rs[p] = do_ds ? a.rstd[rr] : 0.f;
+        }
+        float dy[NP][8], xh[NP][8];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            V8<T>::unpack(ldy[p], dy[p]);
+            V8<T>::unpack(lxh[p], xh[p]);
+            if (dyb) {
+                float t[8];
+                V8<T>::unpack(ldb[p], t);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) dy[p][q] += t[q];
+            }
+        }
+        if (do_ds) {
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                float s1 = 0.f, s2 = 0.f;
+                if (vact) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) { const float gy = dy[p][q] * g[q]; s1 += gy; s2 += gy * xh[p][q]; }
+                }
+                s1 = group_sum<LG>(s1);
+                s2 = group_sum<LG>(s2);
+                if (v == 0) {
+                    rowred[buf][p * RPP + gi][wave][0] = s1;
+                    rowred[buf][p * RPP + gi][wave][1] = s2;
+                }
+            }
+            __syncthreads();
+        }
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const int64_t row = t0 + p * RPP + gi;
+            const bool act = row < a.rows && vact;
+            const int64_t off = row * cols + c;
+            if (act && a.dysum) V8<T>::store(reinterpret_cast<T*>(a.dysum) + off, dy[p]);
+            if (act && do_part) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) { p_dyx[q] += dy[p][q] * xh[p][q]; p_dy[q] += dy[p][q]; }
+            }
+            if (!do_ds) continue;
+            float m1 = 0.f, m2 = 0.f;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) { m1 += rowred[buf][p * RPP + gi][w][0]; m2 += rowred[buf][p * RPP + gi][w][1]; }
+            m1 *= inv;
+            m2 *= inv;
+            if (!act) continue;
+            float o[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) o[q] = rs[p] * (dy[p][q] * g[q] - m1 - xh[p][q] * m2);
+            if (a.ds) V8<T>::store(reinterpret_cast<T*>(a.ds) + off, o);
+            if (a.dsub) {
+                dropout8(a.dp, (uint64_t)off, o);
+                V8<T>::store(reinterpret_cast<T*>(a.dsub) + off, o);
+                if (do_part && a.want_dsub_sum) {
+                    // sum the stored (rounded) values that later consumers see
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) p_dsub[q] += to_f(from_f<T>(o[q]));
+                }
+            }
+        }
+    }
+    if (!do_part) return;
+    const int nq = a.want_dsub_sum ? 3 : 2;
+    for (int qn = 0; qn < nq; ++qn) {
+        float* pp = qn == 0 ? p_dyx : (qn == 1 ? p_dy : p_dsub);
+        float o[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            float t = pp[q];
+#pragma unroll
+            for (int d = LG; d < 64; d <<= 1) t += __shfl_xor(t, d, 64);
+            o[q] = t;
+        }
+        if (gi == 0 && vact) V8<float>::store(a.part + ((int64_t)qn * nblk + blockIdx.x) * cols + c, o);
+    }
+}
+
 template <typename T>
 void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
+    const int nblk = ln_bwd_blocks(a.rows, a.cols, a.dtype);
+    if constexpr (sizeof(T) == 2) {
+        if (ln_bwd_split_ok(a.cols, a.dtype)) {
+            if (a.cols / 64 <= 8) hipLaunchKernelGGL((ln_bwd_cs_k<T, 8>), dim3(nblk), dim3(NTL), 0, st, a, nblk);
+            else hipLaunchKernelGGL((ln_bwd_cs_k<T, 16>), dim3(nblk), dim3(NTL), 0, st, a, nblk);
+            return;
+        }
+    }
     const int len = a.cols;
-    const int nblk = colsum_blocks(a.rows);
     const int rpb = (int)((a.rows + nblk - 1) / nblk);
 #define L(LPR, NV) \
     { hipLaunchKernelGGL((ln_bwd_k<T, LPR, NV>), dim3(nblk), dim3(NTL), 0, st, a, rpb, nblk); }
@@ -604,6 +750,13 @@ void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
 
 int colsum_blocks(int64_t rows) {
     int64_t b = (rows + 7) / 8;
+    if (b > 512) b = 512;
+    return (int)(b < 1 ? 1 : b);
+}
+
+int ln_bwd_blocks(int64_t rows, int cols, int dtype) {
+    if (!ln_bwd_split_ok(cols, dtype)) return colsum_blocks(rows);
+    int64_t b = (rows + LN_TILE - 1) / LN_TILE;
     if (b > 512) b = 512;
     return (int)(b < 1 ? 1 : b);
 }
@@ -665,25 +818,27 @@ void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float*
                                               (const T*)x, part, rpb));
 }
 
-void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st) {
-    FinishOut fo{{out, nullptr, nullptr}};
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 15) / 16, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
-                       fo, 0, 0);
+void run_colsum_finish_jobs(const FinishJob* jobs, int n, hipStream_t st) {
+    FinishJobs fj{};
+    fj.n = n;
+    int blocks = 0;
+    for (int i = 0; i < n; ++i) {
+        fj.job[i] = jobs[i];
+        fj.first[i] = blocks;
+        blocks += (jobs[i].cols + 15) / 16 * jobs[i].nsets;
+    }
+    hipLaunchKernelGGL(colsum_finish_k, dim3(blocks), dim3(NT), 0, st, fj);
 }
 
-void run_colsum_finish3(int64_t rows, int cols, const float* part, float* o0, float* o1, float* o2,
-                        hipStream_t st) {
-    FinishOut fo{{o0, o1, o2}};
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 15) / 16, 3), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
-                       fo, 0, 0);
+void run_colsum_finish(int nblk, int cols, const float* part, float* out, hipStream_t st) {
+    const FinishJob j = finish_job(part, nblk, cols, out);
+    run_colsum_finish_jobs(&j, 1, st);
 }
 
-void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* part, float* dbq, float* dbk,
+void run_colsum_finish_qkv(int nblk, int H, int P, int nseg, const float* part, float* dbq, float* dbk,
                            float* dbv, hipStream_t st) {
-    const int cols = nseg * H * P;
-    FinishOut fo{{dbq, dbk, dbv}};
-    hipLaunchKernelGGL(colsum_finish_k, dim3((cols + 15) / 16, 1), dim3(NT), 0, st, colsum_blocks(rows), cols, part,
-                       fo, H, P);
+    const FinishJob j = finish_job_qkv(part, nblk, H, P, nseg, dbq, dbk, dbv);
+    run_colsum_finish_jobs(&j, 1, st);
 }
 
 void run_rowsum(int dtype, int64_t rows, int len, const void* x, float* out, hipStream_t st) {

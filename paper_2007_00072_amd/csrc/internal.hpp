@@ -38,8 +38,16 @@ inline DropParams make_drop(const dm_dropout* d) {
     return make_drop(d->p, d->seed, d->site, d->layer);
 }
 
-// Column-sum scratch: partial sums of `nblk` row blocks.
+// Column-sum scratch: partial sums of `nblk` row blocks (colsum_blocks for
+// the column-sum and activation-backward kernels, ln_bwd_blocks for the
+// LayerNorm backward; never more than colsum_blocks(rows)).
 int colsum_blocks(int64_t rows);
+int ln_bwd_blocks(int64_t rows, int cols, int dtype);
+// LayerNorm backward takes its column-split form for these row lengths
+// (16-bit storage types)
+inline bool ln_bwd_split_ok(int cols, int dtype) {
+    return dtype != DM_F32 && cols % 64 == 0 && cols >= 320 && cols <= 1024;
+}
 
 // ------------------------------------------------------- kernel launchers
 // All take element counts, device pointers and a stream, and assume the
@@ -126,11 +134,37 @@ void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float*
 
 // out[map(c)] = sum_b part[b][c] for c < cols.  With H, P > 0 the columns
 // are (s, h, p) of a fused projection and go to outs[s][p*H + h].
-void run_colsum_finish(int64_t rows, int cols, const float* part, float* out, hipStream_t st);
-// three partial sets part[q][nblk][cols] -> o0, o1, o2 in one launch
-void run_colsum_finish3(int64_t rows, int cols, const float* part, float* o0, float* o1, float* o2,
-                        hipStream_t st);
-void run_colsum_finish_qkv(int64_t rows, int H, int P, int nseg, const float* part, float* dbq,
+// A job is one operator's partial sets (part[nsets][nblk][cols], all from
+// `rows` rows); run_colsum_finish_jobs finishes several in one launch.
+struct FinishJob {
+    const float* part;
+    float* out[3];
+    int nblk, cols, nsets, qkv_H, qkv_P;
+};
+constexpr int MAX_FINISH_JOBS = 4;
+struct FinishJobs {
+    FinishJob job[MAX_FINISH_JOBS];
+    int first[MAX_FINISH_JOBS];  // first block of each job
+    int n;
+};
+inline FinishJob finish_job(const float* part, int nblk, int cols, float* out) {
+    return FinishJob{part, {out, nullptr, nullptr}, nblk, cols, 1, 0, 0};
+}
+inline FinishJob finish_job3(const float* part, int nblk, int cols, float* o0, float* o1, float* o2) {
+    return FinishJob{part, {o0, o1, o2}, nblk, cols, 3, 0, 0};
+}
+inline FinishJob finish_job_qkv(const float* part, int nblk, int H, int P, int nseg, float* dbq, float* dbk,
+                                float* dbv) {
+    return FinishJob{part, {dbq, dbk, dbv}, nblk, nseg * H * P, 1, H, P};
+}
+// bytes of `nsets` partial sets of `nblk` row blocks of `cols` columns
+inline size_t colsum_part_bytes(int nblk, int64_t cols, int nsets) {
+    return (size_t)nsets * (size_t)nblk * (size_t)cols * sizeof(float);
+}
+void run_colsum_finish_jobs(const FinishJob* jobs, int n, hipStream_t st);
+// single jobs; nblk is the partial row count the producing kernel used
+void run_colsum_finish(int nblk, int cols, const float* part, float* out, hipStream_t st);
+void run_colsum_finish_qkv(int nblk, int H, int P, int nseg, const float* part, float* dbq,
                            float* dbk, float* dbv, hipStream_t st);
 
 // out[r] = sum_c x[r][c] (float) for rows of length len (multiple of 8).

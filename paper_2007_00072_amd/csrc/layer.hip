@@ -62,6 +62,7 @@ struct EncPlan {
     size_t xhat1, rstd1, y1, h, a, xhat2, rstd2, saved_total;
     size_t ao, o, fwd_split, fwd_total;
     size_t dS2, dO, dA, dH, dY1f, dS1, dAO, bwd_split, bwd_total;
+    size_t part_ln2, part_act, part_ln1;  // column partials finished together at the end of the backward
     int64_t split_floats;
 };
 
@@ -130,7 +131,10 @@ EncPlan plan_encoder(const Dims& x) {
     e.dY1f = bw.take(es * x.N);
     e.dS1 = bw.take(es * x.N);
     e.dAO = bw.take(es * x.N);
-    e.m.part = bw.take(colsum_ws_bytes(T, (int32_t)max3(3 * x.I, x.F, x.I)));
+    e.part_ln2 = bw.take(colsum_part_bytes(ln_bwd_blocks(T, (int)x.I, x.dtype), x.I, 3));
+    e.part_act = bw.take(colsum_part_bytes(colsum_blocks(T), x.F, 1));
+    e.part_ln1 = bw.take(colsum_part_bytes(ln_bwd_blocks(T, (int)x.I, x.dtype), x.I, 3));
+    e.m.part = bw.take(colsum_part_bytes(colsum_blocks(T), 3 * x.I, 1));
     e.bwd_split = bw.take(4 * e.split_floats);
     e.bwd_total = bw.total;
     return e;
@@ -608,20 +612,22 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     void *dY1f = B8(ws, e.dY1f), *dS1 = B8(ws, e.dS1), *dAO = B8(ws, e.dAO);
     void *dgamma = B8(ws, e.m.dgamma), *dalpha = B8(ws, e.m.dalpha), *dbeta = B8(ws, e.m.dbeta);
     void* dqkv = B8(ws, e.m.dq);
+    // Every column-sum partial set of the layer has its own region; one
+    // launch at the end adds them all up (the parameter gradients they give
+    // are read by no later step of the backward).
     float* part = (float*)B8(ws, e.m.part);
+    float* part_ln2 = (float*)B8(ws, e.part_ln2);
+    float* part_act = (float*)B8(ws, e.part_act);
+    float* part_ln1 = (float*)B8(ws, e.part_ln1);
 
     // LayerNorm-2 scale/shift grads, LayerNorm-2 dX, dropout dX, Linear-2 bias grad
     LnBwdArgs l2{};
     l2.dtype = dt; l2.rows = T; l2.cols = (int)I; l2.dya = dy; l2.xhat = xhat2; l2.gamma = prm->g2; l2.rstd = rstd2;
-    l2.dp = make_drop(d->p_ffn_out, d->seed, 2, d->layer_id); l2.ds = dS2; l2.dsub = dO; l2.part = part;
+    l2.dp = make_drop(d->p_ffn_out, d->seed, 2, d->layer_id); l2.ds = dS2; l2.dsub = dO; l2.part = part_ln2;
     l2.want_dsub_sum = 1;
     {
         TraceScope t_("B1-2 ln2_bwd", st);
         run_ln_bwd(l2, st);
-    }
-    {
-        TraceScope t_("B1-2 colsum", st);
-        run_colsum_finish3(T, (int)I, part, g->dg2, g->dbe2, g->db2, st);
     }
     DM_TRY(check_launch("LayerNorm-2 backward"));
     // Linear 2 dX and dW
@@ -643,11 +649,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     {
         TraceScope t_("B5 act_bwd", st);
         run_act_bwd(dt, T, (int)F, dA, hbuf, prm->b1, d->act, make_drop(d->p_ffn_act, d->seed, 3, d->layer_id), dH,
-                    part, st);
-    }
-    {
-        TraceScope t_("B5 colsum", st);
-        run_colsum_finish(T, (int)F, part, g->db1, st);
+                    part_act, st);
     }
     DM_TRY(check_launch("activation backward"));
     // Linear 1 dX and dW
@@ -669,14 +671,10 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     LnBwdArgs l1{};
     l1.dtype = dt; l1.rows = T; l1.cols = (int)I; l1.dya = dY1f; l1.dyb = dS2; l1.xhat = xhat1; l1.gamma = prm->g1;
     l1.rstd = rstd1; l1.dp = make_drop(d->p_attn_out, d->seed, 1, d->layer_id); l1.ds = dS1; l1.dsub = dAO;
-    l1.part = part; l1.want_dsub_sum = 1;
+    l1.part = part_ln1; l1.want_dsub_sum = 1;
     {
         TraceScope t_("B8-10 ln1_bwd", st);
         run_ln_bwd(l1, st);
-    }
-    {
-        TraceScope t_("B8-10 colsum", st);
-        run_colsum_finish3(T, (int)I, part, g->dg1, g->dbe1, g->dbo, st);
     }
     DM_TRY(check_launch("LayerNorm-1 backward"));
     // attention backward into the token-major [T][3][H][P] gradient
@@ -687,10 +685,19 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     // Q, K, V dX (fused) + encoder-input residual; Q, K, V dW (fused)
     DM_TRY(project_fused_bwd(x, DM_BJI, x_in, dqkv, prm, dx, g, dS1, st));
     // input-bias grads
-    TraceScope t20("B20 qkv_bias_grad", st);
-    run_colsum_partial(dt, T, (int)(3 * I), dqkv, part, st);
-    trace_next("finish");
-    run_colsum_finish_qkv(T, (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
+    {
+        TraceScope t20("B20 qkv_bias_grad", st);
+        run_colsum_partial(dt, T, (int)(3 * I), dqkv, part, st);
+    }
+    // LayerNorm-2 (dgamma2, dbeta2, db2), activation (db1), LayerNorm-1
+    // (dgamma1, dbeta1, dbo) and input-bias (dbq, dbk, dbv) column sums
+    const int nln = ln_bwd_blocks(T, (int)I, dt), ncs = colsum_blocks(T);
+    const FinishJob jobs[4] = {finish_job3(part_ln2, nln, (int)I, g->dg2, g->dbe2, g->db2),
+                               finish_job(part_act, ncs, (int)F, g->db1),
+                               finish_job3(part_ln1, nln, (int)I, g->dg1, g->dbe1, g->dbo),
+                               finish_job_qkv(part, ncs, (int)x.H, (int)x.P, 3, g->dbq, g->dbk, g->dbv)};
+    TraceScope tf("B colsum finish", st);
+    run_colsum_finish_jobs(jobs, 4, st);
     return check_launch("input-bias backward");
 }
 
@@ -771,7 +778,7 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     if (x.layout == DM_BJI) {
         run_colsum_partial(dt, x.Tq, (int)x.I, dout, part, st);
         trace_next("finish");
-        run_colsum_finish(x.Tq, (int)x.I, part, g->dbo, st);
+        run_colsum_finish(colsum_blocks(x.Tq), (int)x.I, part, g->dbo, st);
     } else {
         run_rowsum(dt, x.I, (int)x.Tq, dout, g->dbo, st);
     }
@@ -786,18 +793,18 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
         TraceScope t_("B20 qkv_bias_grad", st);
         run_colsum_partial(dt, x.Tq, (int)(3 * x.H * x.P), bq, part, st);
         trace_next("finish");
-        run_colsum_finish_qkv(x.Tq, (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
+        run_colsum_finish_qkv(colsum_blocks(x.Tq), (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
     } else {
         TraceScope t_("B18-20 q,k,v_bwd", st);
         DM_TRY(project_bwd(x, x.layout, qin, x.Tq, x.P, bq, s.p.ldq, prm->wq, dq, g->dwq, nullptr, st));
         DM_TRY(project_bwd(x, x.layout, kin, x.Tk, x.P, bk, s.p.ldk, prm->wk, dk, g->dwk, nullptr, st));
         DM_TRY(project_bwd(x, x.layout, vin, x.Tk, x.W, bv, s.p.ldv, prm->wv, dv, g->dwv, nullptr, st));
         run_colsum_partial(dt, x.Tq, (int)(x.H * x.P), bq, part, st);
-        run_colsum_finish_qkv(x.Tq, (int)x.H, (int)x.P, 1, part, g->dbq, nullptr, nullptr, st);
+        run_colsum_finish_qkv(colsum_blocks(x.Tq), (int)x.H, (int)x.P, 1, part, g->dbq, nullptr, nullptr, st);
         run_colsum_partial(dt, x.Tk, (int)(x.H * x.P), bk, part, st);
-        run_colsum_finish_qkv(x.Tk, (int)x.H, (int)x.P, 1, part, g->dbk, nullptr, nullptr, st);
+        run_colsum_finish_qkv(colsum_blocks(x.Tk), (int)x.H, (int)x.P, 1, part, g->dbk, nullptr, nullptr, st);
         run_colsum_partial(dt, x.Tk, (int)(x.H * x.W), bv, part, st);
-        run_colsum_finish_qkv(x.Tk, (int)x.H, (int)x.W, 1, part, g->dbv, nullptr, nullptr, st);
+        run_colsum_finish_qkv(colsum_blocks(x.Tk), (int)x.H, (int)x.W, 1, part, g->dbv, nullptr, nullptr, st);
     }
     return check_launch("input-bias backward");
 }

@@ -96,15 +96,12 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["F10 bdrln2"] = m(4 * N * es + 4 * T + 3 * I * es)
     # backward
     w["B1-2 ln2_bwd"] = m(4 * N * es + 4 * T + I * es + 3 * I * 4)
-    w["B1-2 colsum"] = m(0)
     w["B3 linear2_dx"] = g(T, F, I, N, I * F, Fh)
     w["B4 linear2_dw"] = g(I, F, T, N, Fh, I * F, c_es=4)
     w["B5 act_bwd"] = m(3 * Fh * es + F * es + F * 4)
-    w["B5 colsum"] = m(0)
     w["B6 linear1_dx"] = g(T, I, F, Fh, F * I, N)
     w["B7 linear1_dw"] = g(F, I, T, Fh, N, F * I, c_es=4)
     w["B8-10 ln1_bwd"] = m(5 * N * es + 4 * T + I * es + 3 * I * 4)
-    w["B8-10 colsum"] = m(0)
     w["B11 out_dx"] = g(T, I, I, N, I * I, N)
     w["B12 out_dw"] = g(I, I, T, N, N, I * I, c_es=4)
     w["B13 gamma_dx1"] = _att(Z, J, K, W, es, dtype, S, N)
@@ -120,6 +117,8 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read
     w["B19 qkv_dw"] = g(3 * I, I, T, 3 * N, N, 3 * I * I, c_es=4)
     w["B20 qkv_bias_grad"] = m(3 * N * es + 3 * I * 4)
+    # column-sum partials of B1-2, B5, B8-10 and B20 finished in one launch
+    w["B colsum finish"] = m(0)
     return w
 
 

@@ -132,7 +132,7 @@ def _ln_inputs(dt, rows, cols, seed=41):
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
-@pytest.mark.parametrize("rows,cols", [(37, 32), (300, 768), (129, 1024)])
+@pytest.mark.parametrize("rows,cols", [(37, 32), (300, 768), (129, 1024), (8211, 384)])
 def test_ln_dropout_bwd(lib, dt, rows, cols):
     dy, xh, rs, g = _ln_inputs(dt, rows, cols)
     ds = torch.empty((rows, cols), dtype=dy.dtype, device=DEV)
@@ -159,9 +159,17 @@ def test_ln_param_bwd(lib, dt, rows, cols):
     assert_close("dbeta", db, f64(dy).sum(0), dt, param_grad=True)
 
 
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_residual_ln_param_bwd(lib, dt):
-    rows, cols = 333, 256
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("rows,cols", [
+    (333, 256),
+    # column-split kernel: 8-lane groups, more 16-row tiles than blocks
+    (9000, 512),
+    # 6 vectors per 8-lane group (2 idle lanes), a single partial tile
+    (20, 384),
+    # 10 vectors per 16-lane group, tiles striding over 512 blocks
+    (8250, 640),
+])
+def test_residual_ln_param_bwd(lib, dt, rows, cols):
     da = make_tensor((rows, cols), dt, 61)
     dbb = make_tensor((rows, cols), dt, 62)
     _, xh, _, _ = _ln_inputs(dt, rows, cols, seed=63)
