@@ -403,13 +403,17 @@ __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, c
 // out[c] = sum over the nblk partial rows in a fixed order.  A launch runs
 // a list of jobs (partial sets of several operators, finished together);
 // each block finds its job from the jobs' first-block table, then covers
-// columns 16x .. 16x+15 of one partial set as 4 four-column groups x 64 row
-// phases (each phase sums rows ph, ph+64, ... with several loads in
-// flight).  Set y of a job is part + y*nblk*cols -> out[y].  With
-// qkv_H > 0 the columns are (s, h, p) of a fused projection and land in
-// out[s][p * qkv_H + h] (single partial set).
+// columns 32x .. 32x+31 of one partial set (a whole 128-byte line of every
+// partial row) as 8 four-column groups x 32 row phases; each phase sums
+// rows ph, ph+32, ... with four loads in flight, and the 32 phase sums are
+// added in phase order.  Set y of a job is part + y*nblk*cols -> out[y].
+// With qkv_H > 0 the columns are (s, h, p) of a fused projection and land
+// in out[s][p * qkv_H + h] (single partial set).
+constexpr int FIN_COLS = 32;
+
 __global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
-    __shared__ floatx4 red[64][4];
+    constexpr int NPH = NT / (FIN_COLS / 4);  // row phases
+    __shared__ floatx4 red[NPH][FIN_COLS / 4];
     int jb = 0;
 #pragma unroll
     for (int i = 1; i < MAX_FINISH_JOBS; ++i)
@@ -417,29 +421,30 @@ __global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
     const FinishJob& job = fj.job[jb];
     const int cols = job.cols, nblk = job.nblk;
     const int local = (int)blockIdx.x - fj.first[jb];
-    const int ncb = (cols + 15) / 16;
+    const int ncb = (cols + FIN_COLS - 1) / FIN_COLS;
     const int set = local / ncb, cbk = local - set * ncb;
-    const int cg = threadIdx.x & 3, ph = threadIdx.x >> 2;
-    const int c = cbk * 16 + cg * 4;
+    const int cg = threadIdx.x % (FIN_COLS / 4), ph = threadIdx.x / (FIN_COLS / 4);
+    const int c = cbk * FIN_COLS + cg * 4;
     const float* base = job.part + (int64_t)set * nblk * cols;
     floatx4 s[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) s[u] = floatx4{0.f, 0.f, 0.f, 0.f};
     if (c < cols) {
         int b = ph;
-        for (; b + 192 < nblk; b += 256) {
+        for (; b + 3 * NPH < nblk; b += 4 * NPH) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + 64 * u) * cols + c);
+            for (int u = 0; u < 4; ++u)
+                s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + NPH * u) * cols + c);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-            if (b + 64 * u < nblk) s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + 64 * u) * cols + c);
+            if (b + NPH * u < nblk) s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + NPH * u) * cols + c);
     }
     red[ph][cg] = (s[0] + s[1]) + (s[2] + s[3]);
     __syncthreads();
     if (ph == 0 && c < cols) {
         floatx4 t = red[0][cg];
-        for (int i = 1; i < 64; ++i) t += red[i][cg];
+        for (int i = 1; i < NPH; ++i) t += red[i][cg];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int cc = c + q;
@@ -825,7 +830,7 @@ void run_colsum_finish_jobs(const FinishJob* jobs, int n, hipStream_t st) {
     for (int i = 0; i < n; ++i) {
         fj.job[i] = jobs[i];
         fj.first[i] = blocks;
-        blocks += (jobs[i].cols + 15) / 16 * jobs[i].nsets;
+        blocks += (jobs[i].cols + FIN_COLS - 1) / FIN_COLS * jobs[i].nsets;
     }
     hipLaunchKernelGGL(colsum_finish_k, dim3(blocks), dim3(NT), 0, st, fj);
 }
