@@ -120,7 +120,14 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
     // fragment reads and the row operator's 16-byte accesses all spread over
     // the 64 banks
     const int K = g.K, J = g.J, pitch = K + 8;
-    const int z = blockIdx.y, j0 = blockIdx.x * 32;
+    // Workgroups reach the 8 XCDs round-robin by linear id; the row blocks
+    // of one (b, h) are given consecutive ids within one XCD's share, so
+    // that XCD's L2 serves the head's key-side rows to all of them
+    // instead of each XCD fetching every head's rows.
+    const int nrb = (int)gridDim.x, nblocks = nrb * (int)gridDim.y;
+    int lid = (int)blockIdx.y * nrb + (int)blockIdx.x;
+    if ((nblocks & 7) == 0) lid = (lid & 7) * (nblocks >> 3) + (lid >> 3);
+    const int z = lid / nrb, j0 = (lid - z * nrb) * 32;
     const int b = z / g.H, h = z - b * g.H;
     const int tid = threadIdx.x, lane = tid & 63, c = lane & 31, hh = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);

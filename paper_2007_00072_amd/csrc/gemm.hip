@@ -395,13 +395,20 @@ __device__ __forceinline__ void epilogue(const GemmArgs& g, const floatx4 (&acc)
     }
 }
 
-// Tile index of block `bid` among nt tiles: each XCD (blocks are dealt to
-// the 8 XCDs round-robin) gets a contiguous run of tile indices, and runs
-// are walked GM tile-rows at a time so neighbouring blocks share operands.
-__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+// Block -> (tile, batch index).  Workgroups reach the 8 XCDs round-robin
+// by linear id (x fastest); linear ids are renumbered so that each XCD's
+// share is one contiguous run of (batch, tile) indices: the tiles of one
+// batch entry, and neighbouring tiles of a large contraction, then share
+// that XCD's L2.  Within a batch entry tiles go in groups of GM tile rows
+// (column-major inside a group) so concurrently running tiles reuse both
+// operand panels.
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn, int& by) {
     const int nt = tiles_m * tiles_n;
-    int t = bid;
-    if ((nt & 7) == 0) t = (bid & 7) * (nt >> 3) + (bid >> 3);
+    const int total = nt * (int)gridDim.y;
+    int lid = (int)blockIdx.y * nt + (int)blockIdx.x;
+    if ((total & 7) == 0) lid = (lid & 7) * (total >> 3) + (lid >> 3);
+    by = lid / nt;
+    const int t = lid - by * nt;
     constexpr int GM = 4;
     const int per_group = GM * tiles_n;
     const int grp = t / per_group;
@@ -429,11 +436,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
-    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    int by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
     const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
-    const uint32_t z = blockIdx.y / splits;
-    const int sidx = blockIdx.y - (int)z * splits;
+    const uint32_t z = (uint32_t)by / splits;
+    const int sidx = by - (int)z * splits;
     const int kb = splits > 1 ? sidx * g.kper : 0;
     const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
 
@@ -661,11 +669,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
-    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    int by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
     const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
-    const uint32_t z = blockIdx.y / splits;
-    const int sidx = blockIdx.y - (int)z * splits;
+    const uint32_t z = (uint32_t)by / splits;
+    const int sidx = by - (int)z * splits;
     const int kb = splits > 1 ? sidx * g.kper : 0;
     const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
     int dummy = 0;
@@ -935,11 +944,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x32(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
-    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    int by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
     const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
-    const uint32_t z = blockIdx.y / splits;
-    const int sidx = blockIdx.y - (int)z * splits;
+    const uint32_t z = (uint32_t)by / splits;
+    const int sidx = by - (int)z * splits;
     const int kb = splits > 1 ? sidx * g.kper : 0;
     const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
     int dummy = 0;
@@ -1115,11 +1125,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_big(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
-    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    int by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
     const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
-    const uint32_t z = blockIdx.y / splits;
-    const int sidx = blockIdx.y - (int)z * splits;
+    const uint32_t z = (uint32_t)by / splits;
+    const int sidx = by - (int)z * splits;
     const int kb = splits > 1 ? sidx * g.kper : 0;
     const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
     int dummy = 0;
@@ -1367,11 +1378,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
-    tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+    int by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
     const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
-    const uint32_t z = blockIdx.y / splits;
-    const int sidx = blockIdx.y - (int)z * splits;
+    const uint32_t z = (uint32_t)by / splits;
+    const int sidx = by - (int)z * splits;
     const int kb = splits > 1 ? sidx * g.kper : 0;
     const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
     int dummy = 0;
