@@ -64,7 +64,11 @@ def main() -> None:
     ev = {r["kernel"]: r["us"] for r in seq_info["kernels"]}
     rows = list(csv.DictReader(open(a.trace)))
     lib = [r for r in rows if "dm::" in r["Kernel_Name"] or "_ZN2dm" in r["Kernel_Name"]]
-    lib.sort(key=lambda r: int(r["Start_Timestamp"]))
+    # host submission order: the backward issues some launches on a second
+    # stream, so start times may interleave differently from step to step
+    key = "Correlation_Id" if lib and "Correlation_Id" in lib[0] else "Dispatch_Id"
+    lib.sort(key=lambda r: int(r[key]))
+    streams = {(r.get("Queue_Id"), r.get("Stream_Id")) for r in lib}
     n = len(seq)
     if len(lib) % n:
         raise SystemExit(f"{len(lib)} library dispatches are not a whole number of {n}-launch steps")
@@ -86,7 +90,10 @@ def main() -> None:
         total += avg
         lines.append(f"| {p} | {seq[p]} | `{short_name(names.pop())}` | {avg:.1f} | {ev[seq[p]]:.1f} |")
     lines += ["", f"Sum of per-launch averages: {total / 1e3:.3f} ms per step "
-                  f"(bench event timing of the whole step: {seq_info['ms_per_step']:.3f} ms).", ""]
+                  f"(bench event timing of the whole step: {seq_info['ms_per_step']:.3f} ms)."]
+    if len(streams) > 1:
+        lines += ["Launches ran on more than one stream and overlap, so their sum exceeds the step time."]
+    lines += [""]
     if a.stats and os.path.exists(a.stats):
         st = list(csv.DictReader(open(a.stats)))
         st.sort(key=lambda r: -float(r["TotalDurationNs"]))
