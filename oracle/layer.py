@@ -101,8 +101,15 @@ def contract(spec: str, a: np.ndarray, b: np.ndarray) -> np.ndarray:
 
 
 # ----------------------------------------------------------- element-wise ops
-def softmax_k(beta: np.ndarray) -> np.ndarray:
-    """Softmax over the last index (k)."""
+def softmax_k(beta: np.ndarray, causal: bool = False) -> np.ndarray:
+    """Softmax over the last index (k).  causal: query j (second-to-last
+    index) sees keys k <= j only, as in decoder self-attention; the other
+    probabilities are exactly zero."""
+    if causal:
+        J, K = beta.shape[-2], beta.shape[-1]
+        if J != K:
+            raise ValueError("a causal mask needs as many keys as queries")
+        beta = np.where(np.arange(K)[None, :] <= np.arange(J)[:, None], beta, -np.inf)
     z = np.exp(beta - beta.max(axis=-1, keepdims=True))
     return z / z.sum(axis=-1, keepdims=True)
 
@@ -160,6 +167,7 @@ class Config:
     eps: float = 1e-12
     act: str = "gelu"
     store_dtype: str = "f64"
+    causal: bool = False     # decoder self-attention: query j attends to keys k <= j
 
     @property
     def s(self) -> float:
@@ -201,8 +209,9 @@ def mha_forward(q, k, v, prm: Dict[str, np.ndarray], cfg: Config, out_bias: bool
     vv = r(contract("whi,ibk->whbk", wv, v) + prm["bv"][:, :, None, None])
     # QK^T, scaled.
     beta = r(cfg.s * contract("phbk,phbj->hbjk", kk, qq))
-    # Softmax over k, then dropout on the probabilities.
-    prob_x = softmax_k(beta)
+    # Softmax over k (keys after the query masked out when causal), then
+    # dropout on the probabilities.
+    prob_x = softmax_k(beta, cfg.causal)
     prob = r(prob_x)
     m_attn = attn_dropout(cfg)
     alpha = r(prob_x * m_attn)
