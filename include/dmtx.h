@@ -74,6 +74,8 @@ typedef struct {
     uint64_t seed;           /* dropout key                                                */
     uint32_t layer_id;       /* fourth counter word                                        */
     int32_t self_attention;  /* attention only: 1 = q, k, v are one tensor (fused QKV)     */
+    int32_t causal;          /* 1 = query j attends to keys k <= j only (decoder self-     */
+                             /* attention, as in GPT-style layers); needs J == K; 0 = all  */
 } dm_layer_desc;
 
 /* Parameters in the paper's index order (Fig. 1a), row-major, dtype of the

@@ -79,6 +79,7 @@ struct AttnArgs {
     AttnOp x;            // second contraction: key-side rows [k][n] (V forward, K backward)
     AttnOp o2;           // its output: element (z, j, n) at ptr + b*outer + h*inner + j*ld + n
     int N2;              // its width (a multiple of 32), 0 when there is none
+    int causal;          // forward: query j sees keys k <= j only
 };
 
 // One k16 step of the second contraction stages a 16 x 32 piece of the
@@ -227,6 +228,11 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
                 const int col = (gl + i * LPR) * 8;
                 if (active && col < K) {
                     V8<T>::unpack(*reinterpret_cast<const u32x4*>(S + lr * pitch + col), v[i]);
+                    if (g.causal) {
+#pragma unroll
+                        for (int q = 0; q < 8; ++q)
+                            if (col + q > j) v[i][q] = -INFINITY;  // keys after the query (probability 0)
+                    }
 #pragma unroll
                     for (int q = 0; q < 8; ++q) mx = fmaxf(mx, v[i][q]);
                 } else {
@@ -417,9 +423,11 @@ void set_next(AttnArgs& g, const AttnNext* n) {
 
 void run_attn_scores_fwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* q, int64_t q_outer,
                          int64_t q_inner, int64_t q_ld, const void* k, int64_t k_outer, int64_t k_inner, int64_t k_ld,
-                         const DropParams& dp, void* prob, void* alpha, const AttnNext* next, hipStream_t st) {
+                         const DropParams& dp, void* prob, void* alpha, const AttnNext* next, hipStream_t st,
+                         int causal) {
     AttnArgs g{};
     set_next(g, next);
+    g.causal = causal;
     g.a = attn_op(q, q_outer, q_inner, q_ld);
     g.b = attn_op(k, k_outer, k_inner, k_ld);
     g.B = B; g.H = H; g.J = J; g.K = K; g.D = D;

@@ -85,16 +85,18 @@ __global__ __launch_bounds__(NT) void bdrln_fwd_k(int64_t rows, int cols, const 
 
 // ------------------------------------------------------ scaled softmax + dropout
 // Physical rows are [B][H][J]; the dropout logical index is (h, b, j, k).
+// causal: keys k > j are masked (probability exactly zero).
 template <typename T, int LPR, int NV>
 __global__ __launch_bounds__(NT) void softmax_fwd_k(int64_t rows, int B, int H, int J, int K, float scale,
                                                     const T* __restrict__ beta, DropParams dp,
-                                                    T* __restrict__ prob, T* __restrict__ alpha) {
+                                                    T* __restrict__ prob, T* __restrict__ alpha, int causal) {
     constexpr int RPW = 64 / LPR;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int gi = lane / LPR, gl = lane % LPR;
     const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * RPW + gi;
     const bool active = row < rows;
     const int64_t base = row * K;
+    const int kmax = causal ? (int)(row % J) : K - 1;  // last key the row sees
     float v[NV][8];
     float mx = -INFINITY;
 #pragma unroll
@@ -103,7 +105,10 @@ __global__ __launch_bounds__(NT) void softmax_fwd_k(int64_t rows, int B, int H, 
         if (active && c < K) {
             V8<T>::load(beta + base + c, v[i]);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) { v[i][q] *= scale; mx = fmaxf(mx, v[i][q]); }
+            for (int q = 0; q < 8; ++q) {
+                v[i][q] = c + q <= kmax ? v[i][q] * scale : -INFINITY;
+                mx = fmaxf(mx, v[i][q]);
+            }
         } else {
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[i][q] = -INFINITY;
@@ -573,13 +578,13 @@ void bdrln_t(int64_t rows, int len, const void* x, const void* bias, const void*
 
 template <typename T>
 void softmax_t(int B, int H, int J, int len, float scale, const void* beta, const DropParams& dp,
-               void* prob, void* alpha, hipStream_t st) {
+               void* prob, void* alpha, int causal, hipStream_t st) {
     int64_t rows = (int64_t)B * H * J;
 #define L(LPR, NV)                                                                                \
     {                                                                                             \
         int64_t rpb = 4 * (64 / LPR);                                                             \
         hipLaunchKernelGGL((softmax_fwd_k<T, LPR, NV>), dim3((rows + rpb - 1) / rpb), dim3(NT), 0, \
-                           st, rows, B, H, J, len, scale, (const T*)beta, dp, (T*)prob, (T*)alpha); \
+                           st, rows, B, H, J, len, scale, (const T*)beta, dp, (T*)prob, (T*)alpha, causal); \
     }
     DM_ROW_CASES(L)
 #undef L
@@ -780,8 +785,8 @@ void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void*
 }
 
 void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta, const DropParams& dp,
-                     void* prob, void* alpha, hipStream_t st) {
-    DM_DTYPE_SWITCH(dtype, softmax_t<T>(B, H, J, K, scale, beta, dp, prob, alpha, st));
+                     void* prob, void* alpha, hipStream_t st, int causal) {
+    DM_DTYPE_SWITCH(dtype, softmax_t<T>(B, H, J, K, scale, beta, dp, prob, alpha, causal, st));
 }
 
 void run_softmax_bwd(int dtype, int B, int H, int J, int K, float scale, const void* dalpha, const void* prob,

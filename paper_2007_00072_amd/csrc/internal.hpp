@@ -78,10 +78,11 @@ struct AttnNext {
 };
 bool attn_next_ok(int dtype, int K, int D, const AttnNext& n);
 // P = softmax_k(round(scaler * Q K^T)), alpha = dropout(P); with `next`,
-// also gamma = alpha V
+// also gamma = alpha V.  causal: query j sees keys k <= j only.
 void run_attn_scores_fwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* q, int64_t q_outer,
                          int64_t q_inner, int64_t q_ld, const void* k, int64_t k_outer, int64_t k_inner, int64_t k_ld,
-                         const DropParams& dp, void* prob, void* alpha, const AttnNext* next, hipStream_t st);
+                         const DropParams& dp, void* prob, void* alpha, const AttnNext* next, hipStream_t st,
+                         int causal = 0);
 // d(beta) = scaler * P * (dP - sum_k dP P), dP = dropout(round(d(gamma) V^T));
 // with `next`, also dQ = d(beta) K
 void run_attn_scores_bwd(int dtype, int B, int H, int J, int K, int D, float scaler, const void* dgamma,
@@ -89,8 +90,9 @@ void run_attn_scores_bwd(int dtype, int B, int H, int J, int K, int D, float sca
                          int64_t v_inner, int64_t v_ld, const void* prob, const DropParams& dp, void* dbeta,
                          const AttnNext* next, hipStream_t st);
 
+// causal: query row j sees keys k <= j only (probabilities after it exactly 0)
 void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta,
-                     const DropParams& dp, void* prob, void* alpha, hipStream_t st);
+                     const DropParams& dp, void* prob, void* alpha, hipStream_t st, int causal = 0);
 
 void run_bias_act_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias, int act,
                       const DropParams& dp, void* y, hipStream_t st);

@@ -28,6 +28,7 @@ struct Dims {
     int es;  // element size
     int dtype;
     int layout;
+    int causal;  // query j sees keys k <= j only
 };
 
 Dims dims_of(const dm_layer_desc* d) {
@@ -37,6 +38,7 @@ Dims dims_of(const dm_layer_desc* d) {
     x.dtype = d->dtype;
     x.layout = d->layout;
     x.es = d->dtype == DM_F32 ? 4 : 2;
+    x.causal = d->causal;
     return x;
 }
 
@@ -181,6 +183,8 @@ int check_desc(const dm_layer_desc* d, bool encoder) {
     if ((int64_t)d->B * d->H * d->J * d->K > ((int64_t)1 << 40)) return set_error(DM_ERR_UNSUPPORTED, "too large");
     if ((int64_t)d->B * (d->J > d->K ? d->J : d->K) * 3 * d->I >= ((int64_t)1 << 31))
         return set_error(DM_ERR_UNSUPPORTED, "token count too large");
+    if (d->causal != 0 && d->causal != 1) return set_error(DM_ERR_ARG, "causal must be 0 or 1");
+    if (d->causal && d->J != d->K) return set_error(DM_ERR_UNSUPPORTED, "a causal mask needs J == K");
     const float ps[4] = {d->p_attn, d->p_attn_out, d->p_ffn_out, d->p_ffn_act};
     for (float p : ps)
         if (!(p >= 0.f && p < 1.f)) return set_error(DM_ERR_ARG, "dropout probability %g outside [0,1)", p);
@@ -319,7 +323,7 @@ int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const 
         const bool with_gamma = attn_next_ok(x.dtype, (int)K, (int)P, nx);
         TraceScope t_(with_gamma ? "F2-4 qkt_softmax_gamma" : "F2-3 qkt_softmax", st);
         run_attn_scores_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, (int)P, scaler, q, x.H * J * P, J * P, P, k,
-                            x.H * K * P, K * P, P, dp, prob, alpha, with_gamma ? &nx : nullptr, st);
+                            x.H * K * P, K * P, P, dp, prob, alpha, with_gamma ? &nx : nullptr, st, x.causal);
         DM_TRY(check_launch("attention scores"));
         if (with_gamma) return DM_OK;
     } else {
@@ -335,7 +339,7 @@ int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const 
     }
     {
         TraceScope t_("F3 softmax", st);
-        run_softmax_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, 1.0f, beta, dp, prob, alpha, st);
+        run_softmax_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, 1.0f, beta, dp, prob, alpha, st, x.causal);
     }
     DM_TRY(check_launch("softmax"));
     }

@@ -62,7 +62,7 @@ def test_sizes_valid(lib):
 @pytest.mark.parametrize("field,value,code", [
     ("I", 1004, 2), ("I", 1000, 1), ("W", 32, 1), ("K", 256, 1), ("dtype", 7, 2), ("layout", 1, 2),
     ("p_attn", 1.0, 1), ("p_ffn_out", -0.1, 1), ("ln_eps", 0.0, 1), ("F", 100, 2), ("B", 0, 1),
-    ("act", 9, 2), ("I", 4096, 2)])
+    ("act", 9, 2), ("I", 4096, 2), ("causal", 2, 1)])
 def test_sizes_reject_bad_descriptors(lib, field, value, code):
     d = _desc(lib, **{field: value})
     if field == "I" and value == 4096:
@@ -109,6 +109,11 @@ def test_mha_validation(lib):
         lib.mha_sizes(d)          # self-attention needs J == K
     d.self_attention = 0
     lib.mha_sizes(d)
+    d.causal = 1
+    with pytest.raises(lib.DmError) as e:
+        lib.mha_sizes(d)          # a causal mask needs J == K
+    assert e.value.code == lib.DM_ERR_UNSUPPORTED
+    d.causal = 0
     prm = lib.make_params({n: 0x10000 for n in lib._PNAMES[:8]})
     s, f, b = lib.mha_sizes(d)
     with pytest.raises(lib.DmError) as e:

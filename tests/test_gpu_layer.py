@@ -30,9 +30,9 @@ def run_encoder(wl, layer=0, x=None, dy=None, **desc_over):
     return L, params, x, dy, y, dx
 
 
-def check_encoder(wl, layer=0, x=None, dy=None, act="gelu", p_ffn_act=0.0):
-    L, params, x, dy, y, dx = run_encoder(wl, layer, x, dy, act=act, p_ffn_act=p_ffn_act)
-    cfg = oracle_config(wl, layer, act=act, p_ffn_act=p_ffn_act)
+def check_encoder(wl, layer=0, x=None, dy=None, act="gelu", p_ffn_act=0.0, causal=False):
+    L, params, x, dy, y, dx = run_encoder(wl, layer, x, dy, act=act, p_ffn_act=p_ffn_act, causal=causal)
+    cfg = oracle_config(wl, layer, act=act, p_ffn_act=p_ffn_act, causal=causal)
     prm = params64(params)
     ry, cache = OL.encoder_forward(f64(x), prm, cfg)
     rdx, rg, _ = OL.encoder_backward(f64(dy), cache, prm, cfg)
@@ -140,7 +140,7 @@ def test_encoder_stack_sampled_layers():
 
 
 # ----------------------------------------------------------- attention only
-def check_mha(wl, self_attention=True):
+def check_mha(wl, self_attention=True, causal=False):
     from paper_2007_00072_amd.runner import MultiHeadAttention, desc_for
     s = wl.shape
     params = make_params(wl)
@@ -153,12 +153,12 @@ def check_mha(wl, self_attention=True):
         kh = make_activation(wl, 2, length=s.K)
         vh = make_activation(wl, 3, length=s.K)
         k, v = kh.to(DEV), vh.to(DEV)
-    M = MultiHeadAttention(desc_for(wl, self_attention=self_attention), params, DEV)
+    M = MultiHeadAttention(desc_for(wl, self_attention=self_attention, causal=causal), params, DEV)
     qd = q.to(DEV)
     out = M.forward(qd, k, v)
     dq, dk, dv = M.backward(qd, dout.to(DEV), k, v)
     torch.cuda.synchronize()
-    cfg = oracle_config(wl)
+    cfg = oracle_config(wl, causal=causal)
     prm = params64(params)
     to_ibj = (lambda a: a) if wl.layout == "ibj" else (lambda a: a.transpose(2, 0, 1))
     from_ibj = (lambda a: a) if wl.layout == "ibj" else (lambda a: a.transpose(1, 2, 0))
@@ -219,6 +219,25 @@ def test_mha_fused_next_contraction(dtype, shape):
     # score-backward launch, from the rounded row tile in LDS
     wl = WORKLOADS["mha_large_f16"].with_(shape=Shape(**shape), dtype=dtype, layout="bji", p_attn=0.1)
     check_mha(wl, self_attention=False)
+
+
+@pytest.mark.parametrize("name,J", [("bert_large_f16", 96), ("bert_base_bf16", 96), ("bert_large_f16", 72)])
+def test_encoder_causal(name, J):
+    # decoder-style self-attention: J = 96 through the on-chip score kernels
+    # (a partial last row block), J = 72 through the two-launch softmax
+    wl = small(name, B=2, J=J, K=J, H=4, P=64, W=64, I=256, F=512).with_(p_attn=0.1)
+    check_encoder(wl, layer=1, causal=True)
+
+
+def test_encoder_causal_tiny_f32():
+    check_encoder(WORKLOADS["tiny_f32"].with_(p_attn=0.2), causal=True)
+
+
+@pytest.mark.parametrize("layout", ["ibj", "bji"])
+def test_mha_causal(layout):
+    wl = WORKLOADS["mha_large_f16"].with_(shape=Shape(B=2, J=128, K=128, H=2, P=64, W=64, I=128), layout=layout,
+                                          p_attn=0.1)
+    check_mha(wl, self_attention=True, causal=True)
 
 
 @pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
