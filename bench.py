@@ -92,6 +92,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="sequences in the CPU-oracle sample (0: the whole batch)")
     ap.add_argument("--kernels-json", default=None, help="write the per-kernel table here")
+    ap.add_argument("--plan", default=None,
+                    help="configuration plan written by paper_2007_00072_amd.tune (default: the built-in choices)")
     a = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if a.gpus != 1 or world != 1:
@@ -108,6 +110,14 @@ def main() -> int:
     s = wl.shape
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    plan_name = "built-in"
+    if a.plan:
+        from paper_2007_00072_amd.tune import load_plan
+        plan = load_plan(a.plan)
+        if plan.get("workload") != wl.name:
+            print(json.dumps({"error": f"plan {a.plan} was tuned for {plan.get('workload')}, not {wl.name}"}))
+            return 2
+        plan_name = os.path.basename(a.plan)
     layer = EncoderLayer(desc_for(wl), make_params(wl), dev)
     x = make_activation(wl, 0).to(dev)
     dy = make_activation(wl, 1).to(dev)
@@ -200,7 +210,8 @@ def main() -> int:
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic (seeded N(0,1) inputs, N(0,0.02) weights)",
         "config": {"workload": f"{wl.name}: BERT-large encoder layer fwd+bwd, B={s.B}, L={s.J}, I={s.I}, "
                                f"H={s.H}, P={s.P}, FFN={s.F}, GELU, post-LN, dropout p={wl.p_attn} x3",
-                   "global_batch": s.B, "seq_len": s.J, "parallelism": "single GPU"},
+                   "global_batch": s.B, "seq_len": s.J, "parallelism": "single GPU",
+                   "plan": plan_name},
         "roofline": roof,
         "fused_hbm": fused_summary,
         "contractions": {"tflops_all": round(cf / ct / 1e12, 1), "us_per_step": round(ct * 1e6, 1),

@@ -260,10 +260,11 @@ int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t
  * 2: 128x128, 3: 256x64, 4: 128x64; asynchronous-copy 16x16x32 kernel:
  * 5: 256x128, 6: 128x128, 7: 256x64, 8: 128x64; asynchronous-copy
  * 32x32x16 kernel: 9: 256x256, 10: 256x128 (4 waves), 11: 128x128,
- * 12: 256x128 (8 waves), 13: 256x256 with 4 waves of 128x128 (plain
- * strided operands, K a multiple of 32; otherwise run as 14), 14: 256x256
- * with 8 waves of 128x64; -1:
- * chosen from the shape; other values are
+ * 12: 256x128 (8 waves), 13: lean 256x256 kernel with 8 waves of 128x64
+ * and 32-wide k-steps (K a multiple of 32, operand maps block-aligned;
+ * otherwise run as 14), 14: 256x256 with 8 waves of 128x64, 15: lean
+ * 128x128 kernel with 8 waves of 64x32 and 64-wide k-steps (K a multiple
+ * of 64; otherwise run as 11); -1: chosen from the shape; other values are
  * DM_ERR_ARG); splits > 1 splits k, using `ws` (ws_bytes >=
  * splits*batch*M*N*4) for partial sums; splits = 0 chooses (no split
  * without ws). */
@@ -271,6 +272,42 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
              const void* A, int32_t a_trans, int64_t sa, const void* B, int32_t b_trans,
              int64_t sb, const void* bias, void* C, int32_t out_f32, int64_t sc,
              int32_t tile_cfg, int32_t splits, void* ws, size_t ws_bytes, void* stream);
+
+/* ----------------------------------------------------- configuration plans
+ * The configuration-selection step (Sec. "Configuration Selection"): the
+ * layer and attention entry points choose each contraction's kernel, tile
+ * and split factor from its shape, and the attention-score steps' launch
+ * grouping by itself; a plan replaces those choices.  A contraction is
+ * identified by its sizes, dtype and which operands are contiguous along
+ * the contraction index (dm_contract_choice without the label); a plan
+ * entry sets its tile_cfg (0..15, as for contract) and split factor (1 =
+ * none; larger values are cut to what the call's split-k scratch holds).
+ * Entries that a contraction's operands or epilogue do not allow fall back
+ * the way contract's tile_cfg does, so a plan never changes results beyond
+ * the order of the fp32 accumulation.  attn_path: 0 = automatic, 1 = QK^T,
+ * softmax + dropout and Gamma (and their backward steps) as separate
+ * launches, 2 = scores kept on chip (QK^T with softmax + dropout, Gamma dX1
+ * with its backward), 3 = as 2 with Gamma and QK^T dX1 in the same
+ * launches; a grouping a shape does not allow falls back to the next
+ * smaller one.  plan_set(NULL, 0, 0) restores the built-in choices.  The
+ * plan is process-wide: set it while no layer call is being enqueued.
+ *
+ * plan_log(1) clears and starts a record of the contractions the entry
+ * points launch (sizes, dtype, operand contiguity, the tile_cfg and splits
+ * that ran, and the kernel-timing label when timing is on); plan_log(0)
+ * stops it; plan_log_read copies up to `cap` records and sets *count to
+ * the number recorded. */
+typedef struct {
+    int64_t M, N, K, batch;        /* contraction sizes; batch: contractions in one launch */
+    int32_t dtype;                 /* dm_dtype                                             */
+    int32_t a_kcontig, b_kcontig;  /* 1: operand contiguous along the contraction index   */
+    int32_t tile_cfg;              /* 0..15 (contract's list)                              */
+    int32_t splits;                /* split-k factor, 1 = none                             */
+    char label[48];                /* log only: kernel-timing label, "" when timing is off */
+} dm_contract_choice;
+int plan_set(const dm_contract_choice* entries, int32_t n, int32_t attn_path);
+int plan_log(int32_t on);
+int plan_log_read(dm_contract_choice* out, int32_t cap, int32_t* count);
 
 /* ----------------------------------------------------- kernel timing
  * Optional per-launch timing for measurement: while enabled, every kernel

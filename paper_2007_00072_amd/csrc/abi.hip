@@ -63,6 +63,8 @@ static int trace_open(const char* label, const char* sub, hipStream_t st) {
     return (int)g_trace.size() - 1;
 }
 
+const char* trace_current_label() { return g_active ? g_active->label : ""; }
+
 TraceScope::TraceScope(const char* lab, hipStream_t s) : idx(-1), st(s), label(lab), outer(nullptr) {
     if (!g_trace_on.load(std::memory_order_relaxed)) return;
     idx = trace_open(label, "", st);
@@ -155,6 +157,31 @@ hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
 extern "C" {
 
 const char* dm_last_error(void) { return g_err; }
+
+int plan_set(const dm_contract_choice* entries, int32_t n, int32_t attn_path) {
+    if (n < 0 || (n > 0 && !entries)) return set_error(DM_ERR_ARG, "plan entries missing");
+    if (attn_path < 0 || attn_path > 3) return set_error(DM_ERR_ARG, "attn_path %d outside [0, 3]", attn_path);
+    for (int i = 0; i < n; ++i) {
+        const dm_contract_choice& e = entries[i];
+        if (e.tile_cfg < 0 || e.tile_cfg > 15) return set_error(DM_ERR_ARG, "plan entry %d: tile_cfg %d", i, e.tile_cfg);
+        if (e.splits < 1 || e.splits > 64) return set_error(DM_ERR_ARG, "plan entry %d: splits %d", i, e.splits);
+        if (e.M <= 0 || e.N <= 0 || e.K <= 0 || e.batch <= 0) return set_error(DM_ERR_ARG, "plan entry %d: sizes", i);
+    }
+    plan_contracts(entries, n);
+    set_attn_path(attn_path);
+    return DM_OK;
+}
+
+int plan_log(int32_t on) {
+    plan_log_set(on != 0);
+    return DM_OK;
+}
+
+int plan_log_read(dm_contract_choice* out, int32_t cap, int32_t* count) {
+    if (cap < 0 || (cap > 0 && !out) || !count) return set_error(DM_ERR_ARG, "plan_log_read arguments");
+    *count = plan_log_copy(out, cap);
+    return DM_OK;
+}
 
 int dm_trace_enable(int32_t on) {
     std::lock_guard<std::mutex> lk(g_trace_mu);

@@ -23,6 +23,9 @@
 // The epilogue stages the fp32 tile through LDS in 64-column passes and
 // writes 16-byte vectors along whichever output index is contiguous.
 #include <algorithm>
+#include <mutex>
+#include <string.h>
+#include <vector>
 
 #include "gemm.hpp"
 #include "internal.hpp"
@@ -1799,7 +1802,62 @@ void set_affine(GemmArgs& g) {
     g.affine = 1;
 }
 
+// Configuration plan (entries keyed by sizes, dtype and operand
+// contiguity) and the launch record.
+std::mutex g_plan_mu;
+std::vector<dm_contract_choice> g_plan;
+bool g_log_on = false;
+std::vector<dm_contract_choice> g_log;
+
+bool same_contraction(const dm_contract_choice& e, const GemmArgs& g, int dtype) {
+    return e.M == g.M && e.N == g.N && e.K == g.K && e.batch == g.batch && e.dtype == dtype &&
+           e.a_kcontig == (g.a.kcontig ? 1 : 0) && e.b_kcontig == (g.b.kcontig ? 1 : 0);
+}
+
+// A plan entry's tile and split factor for an automatically configured
+// contraction; the split factor is cut to what the scratch holds.
+void apply_plan(GemmArgs& g, int dtype) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    for (const dm_contract_choice& e : g_plan) {
+        if (!same_contraction(e, g, dtype)) continue;
+        g.cfg = e.tile_cfg;
+        int s = e.splits > 1 ? e.splits : 1;
+        if (!g.split_ws || g.batch != 1) s = 1;
+        while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
+        g.splits = s;
+        return;
+    }
+}
+
+void log_launch(const GemmArgs& g, int dtype) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    if (!g_log_on) return;
+    dm_contract_choice r{};
+    r.M = g.M; r.N = g.N; r.K = g.K; r.batch = g.batch; r.dtype = dtype;
+    r.a_kcontig = g.a.kcontig ? 1 : 0; r.b_kcontig = g.b.kcontig ? 1 : 0;
+    r.tile_cfg = g.cfg; r.splits = g.splits > 1 ? g.splits : 1;
+    strncpy(r.label, trace_current_label(), sizeof(r.label) - 1);
+    g_log.push_back(r);
+}
+
 }  // namespace
+
+void plan_contracts(const dm_contract_choice* e, int n) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    g_plan.assign(e, e + n);
+}
+
+void plan_log_set(bool on) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    g_log_on = on;
+    if (on) g_log.clear();
+}
+
+int plan_log_copy(dm_contract_choice* out, int cap) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    for (int i = 0; i < cap && i < (int)g_log.size(); ++i) out[i] = g_log[i];
+    return (int)g_log.size();
+}
 
 int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     GemmArgs g = args;
@@ -1813,6 +1871,8 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
             return set_error(DM_ERR_UNSUPPORTED, "fp32 contraction grid too large");
         dim3 grid(g.tiles_n, g.tiles_m * g.batch);
         hipLaunchKernelGGL(gemm_f32, grid, dim3(256), 0, st, g);
+        g.cfg = -1;
+        log_launch(g, dtype);
     } else {
         if (g.K % 8 || g.M % 8 || g.N % 8)
             return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
@@ -1820,12 +1880,14 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
             return set_error(DM_ERR_UNSUPPORTED, "bias map radix along the output vector must be a multiple of 8");
         if (!g.split_ws) g.splits = 1;
         set_affine(g);
+        if (g.cfg < 0) apply_plan(g, dtype);
         choose(g);
         if (g.splits > 1 && (int64_t)g.splits * g.batch * g.M * g.N > g.split_cap)
             return set_error(DM_ERR_WORKSPACE, "split-k scratch too small");
         if ((int64_t)g.batch * g.splits > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction grid too large");
         if (dtype == G_F16) launch_t<half_t>(g, st);
         else launch_t<bf16_t>(g, st);
+        log_launch(g, dtype);
     }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return set_error(DM_ERR_DEVICE, "contraction launch: %s", hipGetErrorString(err));

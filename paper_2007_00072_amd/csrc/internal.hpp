@@ -30,6 +30,15 @@ struct TraceScope {
 // Marks the start of a further launch of the innermost active scope (no-op
 // when tracing is off), so every launch has a record of its own.
 void trace_next(const char* sub);
+// label of the innermost active scope ("" when timing is off)
+const char* trace_current_label();
+// attention-score launch grouping: 0 automatic, 1 separate, 2 scores on
+// chip, 3 scores and the next contraction together (plan_set's attn_path)
+void set_attn_path(int path);
+// contraction configuration plan and launch record (plan_set / plan_log)
+void plan_contracts(const dm_contract_choice* entries, int n);
+void plan_log_set(bool on);
+int plan_log_copy(dm_contract_choice* out, int cap);
 
 // p in [0,1); seed/site/layer -> kernel parameters (thr, scale computed in double).
 DropParams make_drop(float p, uint64_t seed, uint32_t site, uint32_t layer);

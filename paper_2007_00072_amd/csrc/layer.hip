@@ -12,6 +12,8 @@
 // index maps inside the contraction kernel, never by a transpose pass.
 #include <math.h>
 
+#include <atomic>
+
 #include "gemm.hpp"
 #include "internal.hpp"
 
@@ -82,6 +84,8 @@ struct SplitScope {
 };
 
 int64_t max3(int64_t a, int64_t b, int64_t c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
+
+std::atomic<int> g_attn_path{0};  // plan_set's attn_path
 
 void plan_attention(const Dims& x, bool fused, Carver& sv, Carver& fw, Carver& bw, MhaPlan& p) {
     const size_t es = x.es;
@@ -314,13 +318,14 @@ int project_fused(const Dims& x, int layout, const void* in, const dm_layer_para
 int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const void* q, const void* k,
                        const void* v, void* beta, void* prob, void* alpha, void* gamma, hipStream_t st) {
     const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, HW = x.H * x.W;
-    if (attn_fused_ok(x.dtype, (int)K, (int)P)) {
+    const int path = g_attn_path.load(std::memory_order_relaxed);
+    if (path != 1 && attn_fused_ok(x.dtype, (int)K, (int)P)) {
         // QK^T and the softmax + dropout in one launch (beta stays on chip),
         // and Gamma in the same launch when its shape allows
         AttnNext nx;
         nx.x = v; nx.x_outer = x.H * K * W; nx.x_inner = K * W; nx.x_ld = W;
         nx.out = gamma; nx.o_outer = J * HW; nx.o_inner = W; nx.o_ld = HW; nx.N = (int)W;
-        const bool with_gamma = attn_next_ok(x.dtype, (int)K, (int)P, nx);
+        const bool with_gamma = path != 2 && attn_next_ok(x.dtype, (int)K, (int)P, nx);
         TraceScope t_(with_gamma ? "F2-4 qkt_softmax_gamma" : "F2-3 qkt_softmax", st);
         run_attn_scores_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, (int)P, scaler, q, x.H * J * P, J * P, P, k,
                             x.H * K * P, K * P, P, dp, prob, alpha, with_gamma ? &nx : nullptr, st, x.causal);
@@ -388,11 +393,12 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
                        st));
     const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
     t12.stop();
-    const bool fused = attn_fused_ok(x.dtype, (int)K, (int)W);
+    const int path = g_attn_path.load(std::memory_order_relaxed);
+    const bool fused = path != 1 && attn_fused_ok(x.dtype, (int)K, (int)W);
     AttnNext nq;
     nq.x = k; nq.x_outer = H * K * P; nq.x_inner = K * P; nq.x_ld = P;
     nq.out = dq; nq.o_outer = J * ldq; nq.o_inner = P; nq.o_ld = ldq; nq.N = (int)P;
-    const bool with_dq = fused && attn_next_ok(x.dtype, (int)K, (int)W, nq);
+    const bool with_dq = fused && path != 2 && attn_next_ok(x.dtype, (int)K, (int)W, nq);
     if (fused) {
         // Gamma dX1 and the scaled softmax + dropout backward in one launch
         // (dalpha stays on chip): dbeta[z][j][k]; QK^T dX1 in the same
@@ -486,6 +492,8 @@ int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqk
 }
 
 }  // namespace
+
+void dm::set_attn_path(int path) { g_attn_path.store(path, std::memory_order_relaxed); }
 
 extern "C" {
 

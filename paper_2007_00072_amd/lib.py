@@ -21,6 +21,10 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2007_00072_amd.build` "
                       "(or __graft_entry__.build())")
 
+# torch's HIP runtime is loaded first, so the library binds to the same one
+# (loading the library first would bring a second runtime into the process)
+import torch  # noqa: E402,F401
+
 _lib = C.CDLL(LIB_PATH)
 
 DM_OK, DM_ERR_ARG, DM_ERR_UNSUPPORTED, DM_ERR_WORKSPACE, DM_ERR_DEVICE = range(5)
@@ -40,7 +44,17 @@ EXPORTED = [
     "softmax_dropout_bwd", "bias_grad", "attn_input_bias_grad", "residual_add",
     "dropout_mask", "saved_tensor_view", "contract", "dm_last_error",
     "dm_trace_enable", "dm_trace_count", "dm_trace_get",
+    "plan_set", "plan_log", "plan_log_read",
 ]
+
+
+class ContractChoice(C.Structure):
+    _fields_ = [("M", C.c_int64), ("N", C.c_int64), ("K", C.c_int64), ("batch", C.c_int64),
+                ("dtype", C.c_int32), ("a_kcontig", C.c_int32), ("b_kcontig", C.c_int32),
+                ("tile_cfg", C.c_int32), ("splits", C.c_int32), ("label", C.c_char * 48)]
+
+    def key(self):
+        return (self.M, self.N, self.K, self.batch, self.dtype, self.a_kcontig, self.b_kcontig)
 
 
 class DmError(RuntimeError):
@@ -117,6 +131,9 @@ _f["dm_trace_enable"] = _sig("dm_trace_enable", I32, I32)
 _f["dm_trace_count"] = _sig("dm_trace_count", I32)
 _f["dm_trace_get"] = _sig("dm_trace_get", I32, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_char_p),
                           C.POINTER(C.c_float))
+_f["plan_set"] = _sig("plan_set", I32, C.POINTER(ContractChoice), I32, I32)
+_f["plan_log"] = _sig("plan_log", I32, I32)
+_f["plan_log_read"] = _sig("plan_log_read", I32, C.POINTER(ContractChoice), I32, C.POINTER(I32))
 
 
 def ptr(t) -> Optional[int]:
@@ -302,6 +319,28 @@ def trace_records():
     """All (label, sub-label, ms) records of the current timing session; an
     operator's second launch carries a sub-label (e.g. "reduce")."""
     return [dm_trace_get(i) for i in range(dm_trace_count())]
+
+
+def plan_set(entries, attn_path: int = 0) -> None:
+    """Install a configuration plan: entries are ContractChoice records
+    (or (M, N, K, batch, dtype, a_kcontig, b_kcontig, tile_cfg, splits)
+    tuples); plan_set([]) restores the built-in choices."""
+    recs = [e if isinstance(e, ContractChoice) else ContractChoice(*e) for e in entries]
+    arr = (ContractChoice * max(1, len(recs)))(*recs)
+    _call("plan_set", arr if recs else None, len(recs), attn_path)
+
+
+def plan_log(on: bool) -> None:
+    _call("plan_log", 1 if on else 0)
+
+
+def plan_log_read():
+    """The contractions launched since plan_log(True), as ContractChoice records."""
+    n = I32()
+    _call("plan_log_read", None, 0, C.byref(n))
+    arr = (ContractChoice * max(1, n.value))()
+    _call("plan_log_read", arr, n.value, C.byref(n))
+    return list(arr[: n.value])
 
 
 def dm_last_error() -> str:

@@ -1,0 +1,86 @@
+"""Configuration plans on the GPU: an installed plan changes the kernels and
+launch grouping that run, results still match the oracle, and the tuner
+(configuration selection) runs end to end."""
+import json
+
+import pytest
+import torch
+
+from paper_2007_00072_amd import lib, tune
+from paper_2007_00072_amd.inputs import WORKLOADS, Shape
+from test_gpu_layer import check_encoder, run_encoder, small
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _builtin_plan_after():
+    yield
+    lib.plan_set([], 0)
+
+
+def _launches(wl):
+    lib.dm_trace_enable(True)
+    lib.plan_log(True)
+    run_encoder(wl)
+    recs = lib.plan_log_read()
+    lib.plan_log(False)
+    labels = [lab for lab, _, _ in lib.trace_records()]
+    lib.dm_trace_enable(False)
+    return recs, labels
+
+
+def test_plan_entry_changes_the_kernel_and_keeps_parity():
+    wl = small("bert_large_f16", B=2, J=96, K=96, H=4, P=64, W=64, I=256, F=512)
+    recs, _ = _launches(wl)
+    lin1 = next(r for r in recs if r.label.decode() == "F7 linear1")
+    builtin = (lin1.tile_cfg, lin1.splits)
+    want = 6 if builtin[0] != 6 else 2
+    lib.plan_set([lib.ContractChoice(*lin1.key(), want, 1)], 0)
+    recs2, _ = _launches(wl)
+    got = next(r for r in recs2 if r.label.decode() == "F7 linear1")
+    assert (got.tile_cfg, got.splits) == (want, 1)
+    # every other contraction kept its built-in choice
+    for a, b in zip(recs, recs2):
+        if a.label.decode() != "F7 linear1":
+            assert (a.tile_cfg, a.splits) == (b.tile_cfg, b.splits)
+    check_encoder(wl, layer=1)
+
+
+@pytest.mark.parametrize("path,fwd,bwd", [
+    (1, ["F2 qkt", "F3 softmax", "F4 gamma"], ["B13 gamma_dx1", "B15 softmax_bwd", "B16 qkt_dx1"]),
+    (2, ["F2-3 qkt_softmax", "F4 gamma"], ["B13-15 gamma_dx1_softmax_bwd", "B16 qkt_dx1"]),
+    (3, ["F2-4 qkt_softmax_gamma"], ["B13+15+16 score_bwd_dq"]),
+])
+def test_attention_groupings(path, fwd, bwd):
+    wl = small("bert_base_bf16", B=2, J=64, K=64, H=4, P=64, W=64, I=256, F=512).with_(p_attn=0.1)
+    lib.plan_set([], path)
+    _, labels = _launches(wl)
+    for lab in fwd + bwd:
+        assert lab in labels, (lab, labels)
+    check_encoder(wl, layer=2)
+
+
+def test_plan_set_validation():
+    with pytest.raises(lib.DmError):
+        lib.plan_set([], 4)
+    with pytest.raises(lib.DmError):
+        lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 16, 1)], 0)
+    with pytest.raises(lib.DmError):
+        lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 5, 0)], 0)
+
+
+def test_tuner_end_to_end(tmp_path):
+    res = tune.tune("bert_large_f16", reps=1, log=lambda s: None,
+                    shape=Shape(B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024),
+                    tile_cfgs=(8, 13, 15), splits=(1, 2))
+    assert res["attn_path"] in (1, 2, 3)
+    assert res["entries"] and all(0 <= e["tile_cfg"] <= 15 for e in res["entries"])
+    for name in ("forward", "backward"):
+        assert res["passes"][name]["predicted_ms"] > 0
+    path = tmp_path / "plan.json"
+    path.write_text(json.dumps(res))
+    plan = tune.load_plan(str(path))
+    assert plan["attn_path"] == res["attn_path"]
+    wl = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
+    check_encoder(wl, layer=0)

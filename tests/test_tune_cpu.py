@@ -1,0 +1,63 @@
+"""Configuration selection (paper_2007_00072_amd/tune.py) on the CPU: the
+graph construction plus shortest path equal brute-force enumeration of
+every attention grouping and every configuration of every stage."""
+import itertools
+import math
+import random
+
+import pytest
+
+from paper_2007_00072_amd import tune
+
+
+def brute_force(chains, costs):
+    best = (math.inf, None, None)
+    for p, stages in chains.items():
+        options = [list(costs[st].items()) for st in stages]
+        for combo in itertools.product(*options):
+            t = sum(c[1] for c in combo)
+            if t < best[0]:
+                best = (t, p, {st: c[0] for st, c in zip(stages, combo)})
+    return best
+
+
+def random_case(rng):
+    pre = [f"F{i}" for i in range(rng.randint(0, 3))]
+    post = [f"G{i}" for i in range(rng.randint(0, 3))]
+    mids = {1: ["a1", "a2", "a3"], 2: ["b1", "a3"], 3: ["c1"]}
+    chains = {p: pre + m + post for p, m in mids.items()}
+    costs = {}
+    for stages in chains.values():
+        for st in stages:
+            if st not in costs:
+                costs[st] = {(k,): rng.uniform(0.1, 10.0) for k in range(rng.randint(1, 4))}
+    return chains, costs
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_selection_equals_brute_force(seed):
+    rng = random.Random(seed)
+    chains, costs = random_case(rng)
+    t, p, cfgs = tune.select(chains, costs)
+    bt, bp, bcfgs = brute_force(chains, costs)
+    assert t == pytest.approx(bt, rel=1e-12)
+    # the chosen stages are exactly one chain's, each at one of its configurations
+    assert set(cfgs) == set(chains[p])
+    assert sum(costs[st][c] for st, c in cfgs.items()) == pytest.approx(t, rel=1e-12)
+
+
+def test_shared_points_are_merged():
+    chains = {1: ["x", "a", "y"], 2: ["x", "b", "c", "y"]}
+    costs = {s: {(0,): 1.0} for s in "xabcy"}
+    n, edges, src, dst = tune.build_graph(chains, costs)
+    # points: start, after x (shared), after a / after b / after c, before y (shared suffix), ends, sink
+    starts = {u for u, v, w, pay in edges if pay[1] == "x"}
+    assert starts == {src}
+    y_from = {u for u, v, w, pay in edges if pay[1] == "y"}
+    assert len(y_from) == 1
+
+
+def test_shortest_path_rejects_negative_weights():
+    with pytest.raises(ValueError):
+        tune.shortest_path(2, [(0, 1, -1.0, None)], 0, 1)
+    assert tune.shortest_path(3, [(0, 1, 1.0, "e")], 0, 2) == (math.inf, [])
