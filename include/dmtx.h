@@ -76,6 +76,9 @@ typedef struct {
     int32_t self_attention;  /* attention only: 1 = q, k, v are one tensor (fused QKV)     */
     int32_t causal;          /* 1 = query j attends to keys k <= j only (decoder self-     */
                              /* attention, as in GPT-style layers); needs J == K; 0 = all  */
+    int32_t qkv_fusion;      /* self-attention input projections (Sec. "Algebraic Fusion")*/
+                             /* 0: [Wq Wk Wv] X as one contraction each way; 1: [Wq Wk] X */
+                             /* and Wv X; 2: three separate contractions                   */
 } dm_layer_desc;
 
 /* Parameters in the paper's index order (Fig. 1a), row-major, dtype of the

@@ -1767,9 +1767,6 @@ void choose(GemmArgs& g) {
     // takes a residual operand
     if (((g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
     if (g.c.resid && g.cfg >= 9 && g.cfg != 15) g.cfg = 8;
-    const TileCfg& c = CFGS[g.cfg];
-    g.tiles_m = (g.M + c.bm - 1) / c.bm;
-    g.tiles_n = (g.N + c.bn - 1) / c.bn;
     if (g.splits <= 0) {
         int s = split_ok ? want_split : 1;
         while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
@@ -1782,6 +1779,11 @@ void choose(GemmArgs& g) {
     }
     if (g.cfg == 13 && !lean_ok(g, 32)) g.cfg = 14;
     if (g.cfg == 15 && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
+    // tile counts of the configuration that runs (the fallback from 15 to 8
+    // changes the tile width)
+    const TileCfg& c = CFGS[g.cfg];
+    g.tiles_m = (g.M + c.bm - 1) / c.bm;
+    g.tiles_n = (g.N + c.bn - 1) / c.bn;
 }
 
 // Classifies the output addressing for the fast store pass.

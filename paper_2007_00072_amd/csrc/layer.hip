@@ -30,7 +30,8 @@ struct Dims {
     int es;  // element size
     int dtype;
     int layout;
-    int causal;  // query j sees keys k <= j only
+    int causal;      // query j sees keys k <= j only
+    int qkv_fusion;  // self-attention projections: 0 one stacked contraction, 1 QK + V, 2 separate
 };
 
 Dims dims_of(const dm_layer_desc* d) {
@@ -41,6 +42,7 @@ Dims dims_of(const dm_layer_desc* d) {
     x.layout = d->layout;
     x.es = d->dtype == DM_F32 ? 4 : 2;
     x.causal = d->causal;
+    x.qkv_fusion = d->qkv_fusion;
     return x;
 }
 
@@ -188,6 +190,7 @@ int check_desc(const dm_layer_desc* d, bool encoder) {
     if ((int64_t)d->B * (d->J > d->K ? d->J : d->K) * 3 * d->I >= ((int64_t)1 << 31))
         return set_error(DM_ERR_UNSUPPORTED, "token count too large");
     if (d->causal != 0 && d->causal != 1) return set_error(DM_ERR_ARG, "causal must be 0 or 1");
+    if (d->qkv_fusion < 0 || d->qkv_fusion > 2) return set_error(DM_ERR_ARG, "qkv_fusion must be 0, 1 or 2");
     if (d->causal && d->J != d->K) return set_error(DM_ERR_UNSUPPORTED, "a causal mask needs J == K");
     const float ps[4] = {d->p_attn, d->p_attn_out, d->p_ffn_out, d->p_ffn_act};
     for (float p : ps)
@@ -301,17 +304,50 @@ int project(const Dims& x, int layout, const void* in, int64_t L, int64_t n, con
 
 // Fused [Wq Wk Wv] projection of one input (self-attention, W == P): the
 // output columns (s, h, p) go to qkv + s*Nh with Nh = B*H*J*P.
+// Self-attention input projections (Sec. "Algebraic Fusion"): the stacked
+// weights [Wq Wk Wv] of segments [s0, s1) times X as one contraction, each
+// segment's output going to its own [B][H][J][P] tensor with its bias.
+// qkv_fusion picks the grouping: one stack, Q and K stacked plus V, or
+// three separate contractions.
+struct ProjGroup { int s0, s1; const char* sub; };
+int proj_groups(int fusion, ProjGroup* g) {
+    if (fusion == 1) { g[0] = {0, 2, ""}; g[1] = {2, 3, "v"}; return 2; }
+    if (fusion == 2) { g[0] = {0, 1, ""}; g[1] = {1, 2, "k"}; g[2] = {2, 3, "v"}; return 3; }
+    g[0] = {0, 3, ""};
+    return 1;
+}
+
+int project_segments(const Dims& x, int layout, const void* in, const dm_layer_params* prm, void* const* outs,
+                     int s0, int s1, hipStream_t st) {
+    const int64_t T = x.Tq, P = x.P, H = x.H;
+    const void* w[3] = {prm->wq, prm->wk, prm->wv};
+    const void* b[3] = {prm->bq, prm->bk, prm->bv};
+    const int ns = s1 - s0;
+    Operand A = act_mk(in, layout, T, x.I);
+    Operand Bw = opnd(w[s0], true, make_map((uint32_t)P, (uint32_t)H, H * x.I, x.I, 0));
+    Epilogue c = epi(outs[s0], make_map((uint32_t)x.J, 0, P, H * x.J * P, 0),
+                     make_map((uint32_t)P, (uint32_t)H, 1, x.J * P, 0), true, false);
+    for (int i = 0; i < ns; ++i) {
+        Bw.ptr[i] = w[s0 + i];
+        c.ptr[i] = outs[s0 + i];
+        c.bias[i] = b[s0 + i];
+    }
+    Bw.nseg = ns; c.nseg = ns; c.seg_on_m = 0; c.bias_nseg = ns;
+    c.bias_map = make_map((uint32_t)P, (uint32_t)H, H, 1, 0);
+    return launch_gemm(x.dtype, gemm(T, ns * H * P, x.I, 1, A, Bw, c), st);
+}
+
+// Q, K, V = projections of one input (self-attention), grouped by qkv_fusion.
 int project_fused(const Dims& x, int layout, const void* in, const dm_layer_params* prm, void* q, void* k,
                   void* v, hipStream_t st) {
-    const int64_t T = x.Tq, P = x.P, H = x.H;
-    Operand A = act_mk(in, layout, T, x.I);
-    Operand Bw = opnd3(prm->wq, prm->wk, prm->wv, true, make_map((uint32_t)P, (uint32_t)H, H * x.I, x.I, 0));
-    Epilogue c = epi(q, make_map((uint32_t)x.J, 0, P, H * x.J * P, 0),
-                     make_map((uint32_t)P, (uint32_t)H, 1, x.J * P, 0), true, false);
-    c.ptr[1] = k; c.ptr[2] = v; c.nseg = 3; c.seg_on_m = 0;
-    c.bias[0] = prm->bq; c.bias[1] = prm->bk; c.bias[2] = prm->bv; c.bias_nseg = 3;
-    c.bias_map = make_map((uint32_t)P, (uint32_t)H, H, 1, 0);
-    return launch_gemm(x.dtype, gemm(T, 3 * H * P, x.I, 1, A, Bw, c), st);
+    void* outs[3] = {q, k, v};
+    ProjGroup grp[3];
+    const int n = proj_groups(x.qkv_fusion, grp);
+    for (int i = 0; i < n; ++i) {
+        if (i > 0) trace_next(grp[i].sub);
+        DM_TRY(project_segments(x, layout, in, prm, outs, grp[i].s0, grp[i].s1, st));
+    }
+    return DM_OK;
 }
 
 // QK^T -> softmax + dropout -> alpha.V ; gamma token-major [Tq][H][W].
@@ -471,24 +507,46 @@ int project_bwd(const Dims& x, int layout, const void* in, int64_t T, int64_t n,
                        st);
 }
 
+// Backward of project_fused on the token-major [T][3][H][P] gradient: per
+// group, dX += dqkv[:, segments] [Wq Wk Wv][segments] (the first group adds
+// `resid`, later ones add the dX written so far, each output element read
+// and written by the same thread) and d[Wq Wk Wv][segments] = dqkv[:,
+// segments]^T X.
 int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqkv, const dm_layer_params* prm,
                       void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st) {
-    const int64_t H = x.H, I = x.I, P = x.P, T = x.Tq;
+    const int64_t H = x.H, I = x.I, P = x.P, T = x.Tq, HP = H * P;
     const IdxMap wmap = make_map((uint32_t)P, (uint32_t)H, H * I, I, 0);
-    Epilogue c = act_out(dx, layout, T, I);
-    c.resid = resid;
-    Operand Bw = opnd3(prm->wq, prm->wk, prm->wv, false, wmap);
+    const void* w[3] = {prm->wq, prm->wk, prm->wv};
+    float* dw[3] = {g->dwq, g->dwk, g->dwv};
+    ProjGroup grp[3];
+    const int n = proj_groups(x.qkv_fusion, grp);
     {
         TraceScope t_("B18 qkv_dx", st);
-        DM_TRY(launch_gemm(x.dtype, gemm(T, I, 3 * H * P, 1, opnd(dqkv, true, linear_map(3 * H * P)), Bw, c), st));
+        for (int i = 0; i < n; ++i) {
+            const int s0 = grp[i].s0, ns = grp[i].s1 - grp[i].s0;
+            if (i > 0) trace_next(grp[i].sub);
+            Epilogue c = act_out(dx, layout, T, I);
+            c.resid = i == 0 ? resid : dx;
+            Operand Bw = opnd(w[s0], false, wmap);
+            for (int j = 0; j < ns; ++j) Bw.ptr[j] = w[s0 + j];
+            Bw.nseg = ns;
+            const void* a = B8(dqkv, (size_t)x.es * s0 * HP);
+            DM_TRY(launch_gemm(x.dtype, gemm(T, I, ns * HP, 1, opnd(a, true, linear_map(3 * HP)), Bw, c), st));
+        }
     }
-    Epilogue cw = epi(g->dwq, wmap, linear_map(1), true, true);
-    cw.ptr[1] = g->dwk; cw.ptr[2] = g->dwv; cw.nseg = 3; cw.seg_on_m = 1;
     TraceScope t_("B19 qkv_dw", st);
-    return launch_gemm(x.dtype,
-                       gemm(3 * H * P, I, T, 1, opnd(dqkv, false, linear_map(3 * H * P)), act_kn(in, layout, T, I),
-                            cw),
-                       st);
+    for (int i = 0; i < n; ++i) {
+        const int s0 = grp[i].s0, ns = grp[i].s1 - grp[i].s0;
+        if (i > 0) trace_next(grp[i].sub);
+        Epilogue cw = epi(dw[s0], wmap, linear_map(1), true, true);
+        for (int j = 0; j < ns; ++j) cw.ptr[j] = dw[s0 + j];
+        cw.nseg = ns; cw.seg_on_m = 1;
+        const void* a = B8(dqkv, (size_t)x.es * s0 * HP);
+        DM_TRY(launch_gemm(x.dtype,
+                           gemm(ns * HP, I, T, 1, opnd(a, false, linear_map(3 * HP)), act_kn(in, layout, T, I), cw),
+                           st));
+    }
+    return DM_OK;
 }
 
 }  // namespace

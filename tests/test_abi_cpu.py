@@ -62,7 +62,7 @@ def test_sizes_valid(lib):
 @pytest.mark.parametrize("field,value,code", [
     ("I", 1004, 2), ("I", 1000, 1), ("W", 32, 1), ("K", 256, 1), ("dtype", 7, 2), ("layout", 1, 2),
     ("p_attn", 1.0, 1), ("p_ffn_out", -0.1, 1), ("ln_eps", 0.0, 1), ("F", 100, 2), ("B", 0, 1),
-    ("act", 9, 2), ("I", 4096, 2), ("causal", 2, 1)])
+    ("act", 9, 2), ("I", 4096, 2), ("causal", 2, 1), ("qkv_fusion", 3, 1)])
 def test_sizes_reject_bad_descriptors(lib, field, value, code):
     d = _desc(lib, **{field: value})
     if field == "I" and value == 4096:

@@ -30,8 +30,9 @@ def run_encoder(wl, layer=0, x=None, dy=None, **desc_over):
     return L, params, x, dy, y, dx
 
 
-def check_encoder(wl, layer=0, x=None, dy=None, act="gelu", p_ffn_act=0.0, causal=False):
-    L, params, x, dy, y, dx = run_encoder(wl, layer, x, dy, act=act, p_ffn_act=p_ffn_act, causal=causal)
+def check_encoder(wl, layer=0, x=None, dy=None, act="gelu", p_ffn_act=0.0, causal=False, **desc_over):
+    L, params, x, dy, y, dx = run_encoder(wl, layer, x, dy, act=act, p_ffn_act=p_ffn_act, causal=causal,
+                                          **desc_over)
     cfg = oracle_config(wl, layer, act=act, p_ffn_act=p_ffn_act, causal=causal)
     prm = params64(params)
     ry, cache = OL.encoder_forward(f64(x), prm, cfg)
@@ -140,7 +141,7 @@ def test_encoder_stack_sampled_layers():
 
 
 # ----------------------------------------------------------- attention only
-def check_mha(wl, self_attention=True, causal=False):
+def check_mha(wl, self_attention=True, causal=False, **desc_over):
     from paper_2007_00072_amd.runner import MultiHeadAttention, desc_for
     s = wl.shape
     params = make_params(wl)
@@ -153,7 +154,7 @@ def check_mha(wl, self_attention=True, causal=False):
         kh = make_activation(wl, 2, length=s.K)
         vh = make_activation(wl, 3, length=s.K)
         k, v = kh.to(DEV), vh.to(DEV)
-    M = MultiHeadAttention(desc_for(wl, self_attention=self_attention, causal=causal), params, DEV)
+    M = MultiHeadAttention(desc_for(wl, self_attention=self_attention, causal=causal, **desc_over), params, DEV)
     qd = q.to(DEV)
     out = M.forward(qd, k, v)
     dq, dk, dv = M.backward(qd, dout.to(DEV), k, v)
@@ -227,6 +228,32 @@ def test_encoder_causal(name, J):
     # (a partial last row block), J = 72 through the two-launch softmax
     wl = small(name, B=2, J=J, K=J, H=4, P=64, W=64, I=256, F=512).with_(p_attn=0.1)
     check_encoder(wl, layer=1, causal=True)
+
+
+@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
+def test_encoder_head_size_32(name):
+    # P = 32: the Q/K/V dX contraction with the encoder-input residual cannot
+    # take the lean 128x128 kernel (its k-steps cross the weight map's lowest
+    # radix) and falls back to the 128x64 tile, which must cover all of N
+    wl = small(name, B=2, J=64, K=64, H=6, P=32, W=32, I=192, F=384)
+    check_encoder(wl, layer=1)
+
+
+@pytest.mark.parametrize("fusion", [1, 2])
+@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
+def test_encoder_qkv_fusion_variants(name, fusion):
+    # Q and K stacked + V, or three separate projections (Sec. "Algebraic
+    # Fusion"); the backward accumulates dX over the groups in place
+    wl = small(name, B=2, J=72, K=72, H=4, P=64, W=64, I=256, F=512).with_(p_attn=0.1)
+    check_encoder(wl, layer=3, qkv_fusion=fusion)
+
+
+@pytest.mark.parametrize("fusion", [1, 2])
+@pytest.mark.parametrize("layout", ["ibj", "bji"])
+def test_mha_qkv_fusion_variants(layout, fusion):
+    wl = WORKLOADS["mha_large_f16"].with_(shape=Shape(B=2, J=64, K=64, H=4, P=32, W=32, I=192), layout=layout,
+                                          p_attn=0.15)
+    check_mha(wl, self_attention=True, qkv_fusion=fusion)
 
 
 def test_encoder_causal_tiny_f32():
