@@ -118,7 +118,8 @@ def main() -> int:
             print(json.dumps({"error": f"plan {a.plan} was tuned for {plan.get('workload')}, not {wl.name}"}))
             return 2
         plan_name = os.path.basename(a.plan)
-    layer = EncoderLayer(desc_for(wl), make_params(wl), dev)
+    layer = EncoderLayer(desc_for(wl, qkv_fusion=int(plan.get("qkv_fusion", 0)) if a.plan else 0),
+                         make_params(wl), dev)
     x = make_activation(wl, 0).to(dev)
     dy = make_activation(wl, 1).to(dev)
     y = torch.empty_like(x)

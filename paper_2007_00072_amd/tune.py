@@ -33,6 +33,9 @@ from collections import OrderedDict, defaultdict
 from typing import Dict, List, Sequence, Tuple
 
 TILE_CFGS = list(range(16))
+# A measured difference smaller than the run-to-run spread of these timings
+# does not move a contraction off the library's own choice.
+KEEP_BUILTIN = 0.97
 SPLITS = (1, 2, 4)
 ATTN_PATHS = (1, 2, 3)   # 1 separate, 2 scores on chip, 3 scores + next contraction
 
@@ -136,7 +139,7 @@ def select(chains: Dict[int, List[str]], costs: Dict[str, Dict[object, float]]):
 class _Layer:
     """A BERT-style layer with seeded inputs; fwd+bwd runs with per-launch timing."""
 
-    def __init__(self, workload: str, shape=None):
+    def __init__(self, workload: str, shape=None, **desc_over):
         import torch
         from .inputs import WORKLOADS, make_activation, make_params
         from .runner import EncoderLayer, desc_for
@@ -145,7 +148,7 @@ class _Layer:
         if shape is not None:
             wl = wl.with_(shape=shape)
         self.wl = wl
-        self.layer = EncoderLayer(desc_for(wl, 0), make_params(wl), "cuda")
+        self.layer = EncoderLayer(desc_for(wl, 0, **desc_over), make_params(wl), "cuda")
         self.x = make_activation(wl, 0).to("cuda")
         self.dy = make_activation(wl, 1).to("cuda")
 
@@ -232,6 +235,9 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
                     continue
                 tm = L.timed(reps)
                 seen[eff] = sum(tm.get(lab, 0.0) for lab in labs)
+        builtin = (choice_of[key].tile_cfg, choice_of[key].splits)
+        if builtin in seen:
+            seen[builtin] *= KEEP_BUILTIN
         shape_costs[key] = seen
         best = min(seen.items(), key=lambda kv: kv[1])
         log(f"  {labs}: {len(seen)} configurations, best {best[0]} {best[1] * 1e3:.1f} us "
@@ -289,11 +295,34 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
                               b_kcontig=e.b_kcontig, tile_cfg=e.tile_cfg, splits=e.splits,
                               label=e.label.decode()) for e in entries]
     result["builtin_ms"] = sum(base.values())
+    # Q/K/V projection grouping (Sec. "Algebraic Fusion"), a property of the
+    # layer: the grouping with the least projection time over both passes
+    table = fusion_table(workload, reps, shape)
+    result["qkv_fusion_table"] = table
+    result["qkv_fusion"] = min(table, key=lambda f: table[f]["forward"] + table[f]["backward"])
     lib.plan_set(entries, attn_path)
     result["planned_ms"] = sum(L.timed(reps).values())
     lib.plan_set([], 0)
     result["tuning_seconds"] = round(time.time() - t0, 1)
     return result
+
+
+FUSIONS = {0: "QKV fused", 1: "QK fused", 2: "unfused"}
+
+
+def fusion_table(workload: str, reps: int = 3, shape=None):
+    """Forward (Q/K/V projections) and backward (their dX and dW) time in
+    ms of each projection grouping, built-in configurations (the analogue
+    of the paper's algebraic-fusion table)."""
+    out = {}
+    for f in FUSIONS:
+        L = _Layer(workload, shape, qkv_fusion=f)
+        for _ in range(10):
+            L.step()
+        tm = L.timed(max(reps, 10))
+        out[f] = {"forward": tm.get("F1 qkv", 0.0), "backward": tm.get("B18 qkv_dx", 0.0) + tm.get("B19 qkv_dw", 0.0)}
+        del L
+    return out
 
 
 def load_plan(path: str):
@@ -311,8 +340,17 @@ def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="bert_large_f16")
     ap.add_argument("--reps", type=int, default=3)
-    ap.add_argument("--out", required=True)
+    ap.add_argument("--out", default=None)
+    ap.add_argument("--fusion-table", action="store_true", help="only time the Q/K/V projection groupings")
     a = ap.parse_args()
+    if a.fusion_table:
+        t = fusion_table(a.workload, a.reps)
+        print("grouping      forward us  backward us")
+        for f, r in t.items():
+            print(f"{FUSIONS[f]:12s} {r['forward'] * 1e3:10.1f} {r['backward'] * 1e3:12.1f}", flush=True)
+        return 0
+    if not a.out:
+        ap.error("--out is required")
     res = tune(a.workload, a.reps, log=lambda s: print(s, flush=True))
     with open(a.out, "w") as f:
         json.dump(res, f, indent=1)
