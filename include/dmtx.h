@@ -73,7 +73,9 @@ typedef struct {
     float p_ffn_act;         /* dropout after the activation (site 3; the paper's 4th)     */
     uint64_t seed;           /* dropout key                                                */
     uint32_t layer_id;       /* fourth counter word                                        */
-    int32_t self_attention;  /* attention only: 1 = q, k, v are one tensor (fused QKV)     */
+    int32_t self_attention;  /* attention only: 1 = q, k, v are one tensor (fused QKV);    */
+                             /* 2 = k, v are one memory tensor (fused KV, encoder/decoder */
+                             /* attention, W == P); 0 = three tensors                      */
     int32_t causal;          /* 1 = query j attends to keys k <= j only (decoder self-     */
                              /* attention, as in GPT-style layers); needs J == K; 0 = all  */
     int32_t qkv_fusion;      /* self-attention input projections (Sec. "Algebraic Fusion")*/
@@ -140,13 +142,17 @@ int mha_sizes(const dm_layer_desc* d, size_t* saved_bytes, size_t* fwd_ws_bytes,
  *   out = wo . (dropout(softmax(scaler * (wq q + bq)(wk k + bk))) . (wv v + bv)) + bo.
  * q: [I][B][J] or [B][J][I]; k, v: [I][B][K] or [B][K][I]; out like q.
  * With self_attention = 1, q == k == v is required (one fused projection);
- * k and v may then be NULL. */
+ * k and v may then be NULL.  With self_attention = 2, k is the memory that
+ * keys and values are both projected from ([Wk Wv] stacked, Sec.
+ * "Algebraic Fusion"); v must be NULL or equal to k. */
 int mha_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* q, const void* k,
             const void* v, void* out, void* saved, void* ws, size_t ws_bytes, void* stream);
 
 /* Multi-head attention backward.  Writes dq, dk, dv (layouts of q, k, v)
  * and the gradients of wq..bo.  With self_attention = 1, dq receives the
- * total input gradient (dq + dk + dv) and dk, dv must be NULL. */
+ * total input gradient (dq + dk + dv) and dk, dv must be NULL.  With
+ * self_attention = 2, dk receives the memory's total gradient (dk + dv)
+ * and dv must be NULL. */
 int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* q, const void* k,
             const void* v, const void* saved, const void* dout, void* dq, void* dk, void* dv,
             const dm_layer_grads* g, void* ws, size_t ws_bytes, void* stream);

@@ -89,7 +89,10 @@ int64_t max3(int64_t a, int64_t b, int64_t c) { return a > b ? (a > c ? a : c) :
 
 std::atomic<int> g_attn_path{0};  // plan_set's attn_path
 
-void plan_attention(const Dims& x, bool fused, Carver& sv, Carver& fw, Carver& bw, MhaPlan& p) {
+// Input-projection modes of attention (dm_layer_desc.self_attention).
+enum { PROJ_SEPARATE = 0, PROJ_QKV = 1, PROJ_KV = 2 };
+
+void plan_attention(const Dims& x, int mode, Carver& sv, Carver& fw, Carver& bw, MhaPlan& p) {
     const size_t es = x.es;
     p.q = sv.take(es * x.B * x.H * x.J * x.P);
     p.k = sv.take(es * x.B * x.H * x.K * x.P);
@@ -101,11 +104,17 @@ void plan_attention(const Dims& x, bool fused, Carver& sv, Carver& fw, Carver& b
     p.dgamma = bw.take(es * x.Tq * x.H * x.W);
     p.dalpha = bw.take(es * x.S);
     p.dbeta = bw.take(es * x.S);
-    if (fused) {
+    if (mode == PROJ_QKV) {
         p.ldq = p.ldk = p.ldv = 3 * x.H * x.P;
         p.dq = bw.take(es * x.Tq * p.ldq);
         p.dk = p.dq;  // column offsets are added at use
         p.dv = p.dq;
+    } else if (mode == PROJ_KV) {
+        p.ldq = x.H * x.P;
+        p.ldk = p.ldv = 2 * x.H * x.P;
+        p.dq = bw.take(es * x.Tq * p.ldq);
+        p.dk = bw.take(es * x.Tk * p.ldk);
+        p.dv = p.dk;  // column offset added at use
     } else {
         p.ldq = x.H * x.P; p.ldk = x.H * x.P; p.ldv = x.H * x.W;
         p.dq = bw.take(es * x.Tq * p.ldq);
@@ -117,7 +126,7 @@ void plan_attention(const Dims& x, bool fused, Carver& sv, Carver& fw, Carver& b
 EncPlan plan_encoder(const Dims& x) {
     EncPlan e{};
     Carver sv, fw, bw;
-    plan_attention(x, true, sv, fw, bw, e.m);
+    plan_attention(x, PROJ_QKV, sv, fw, bw, e.m);
     const size_t es = x.es, T = x.Tq;
     e.xhat1 = sv.take(es * x.N);
     e.rstd1 = sv.take(4 * T);
@@ -149,11 +158,11 @@ EncPlan plan_encoder(const Dims& x) {
 }
 
 struct MhaSizes { MhaPlan p; size_t saved, fwd, bwd, fwd_split, bwd_split; int64_t split_floats; };
-MhaSizes plan_mha(const Dims& x, bool fused) {
+MhaSizes plan_mha(const Dims& x, int mode) {
     MhaSizes s{};
     Carver sv, fw, bw;
-    plan_attention(x, fused, sv, fw, bw, s.p);
-    int64_t cols = max3(fused ? 3 * x.H * x.P : x.H * x.P, x.H * x.W, x.I);
+    plan_attention(x, mode, sv, fw, bw, s.p);
+    int64_t cols = max3(mode == PROJ_SEPARATE ? x.H * x.P : (3 - (mode == PROJ_KV)) * x.H * x.P, x.H * x.W, x.I);
     s.p.part = bw.take(colsum_ws_bytes(x.Tq > x.Tk ? x.Tq : x.Tk, (int32_t)cols) + 4 * x.I);
     s.split_floats = split_floats_for(3 * x.H * x.P * x.I, x.H * x.W * x.I, x.Tq * x.I);
     s.fwd_split = fw.take(4 * s.split_floats);
@@ -205,8 +214,12 @@ int check_desc(const dm_layer_desc* d, bool encoder) {
         if (d->act != DM_GELU && d->act != DM_RELU) return set_error(DM_ERR_UNSUPPORTED, "unknown activation");
         if (!(d->ln_eps > 0.f)) return set_error(DM_ERR_ARG, "ln_eps must be > 0");
     } else {
-        if (d->self_attention && (d->J != d->K || d->W != d->P))
+        if (d->self_attention < PROJ_SEPARATE || d->self_attention > PROJ_KV)
+            return set_error(DM_ERR_ARG, "self_attention must be 0, 1 or 2");
+        if (d->self_attention == PROJ_QKV && (d->J != d->K || d->W != d->P))
             return set_error(DM_ERR_ARG, "self-attention needs J == K and W == P");
+        if (d->self_attention == PROJ_KV && d->W != d->P)
+            return set_error(DM_ERR_ARG, "a fused K/V projection needs W == P");
         if (3 * d->H * d->P > 16384 || d->I > 16384) return set_error(DM_ERR_UNSUPPORTED, "width above 16384");
     }
     return DM_OK;
@@ -302,13 +315,13 @@ int project(const Dims& x, int layout, const void* in, int64_t L, int64_t n, con
     return launch_gemm(x.dtype, gemm(T, x.H * n, x.I, 1, A, Bw, c), st);
 }
 
-// Fused [Wq Wk Wv] projection of one input (self-attention, W == P): the
-// output columns (s, h, p) go to qkv + s*Nh with Nh = B*H*J*P.
-// Self-attention input projections (Sec. "Algebraic Fusion"): the stacked
-// weights [Wq Wk Wv] of segments [s0, s1) times X as one contraction, each
-// segment's output going to its own [B][H][J][P] tensor with its bias.
-// qkv_fusion picks the grouping: one stack, Q and K stacked plus V, or
-// three separate contractions.
+// Stacked input projections (Sec. "Algebraic Fusion"): the weights
+// [Wq Wk Wv] of segments [s0, s1) times one input X of L tokens per
+// sequence as one contraction, each segment's output going to its own
+// [B][H][L][P] tensor with its bias.  Self-attention stacks Q, K and V
+// (qkv_fusion picks the grouping: one stack, Q and K stacked plus V, or
+// three separate contractions); encoder/decoder attention stacks K and V of
+// the memory.
 struct ProjGroup { int s0, s1; const char* sub; };
 int proj_groups(int fusion, ProjGroup* g) {
     if (fusion == 1) { g[0] = {0, 2, ""}; g[1] = {2, 3, "v"}; return 2; }
@@ -317,16 +330,16 @@ int proj_groups(int fusion, ProjGroup* g) {
     return 1;
 }
 
-int project_segments(const Dims& x, int layout, const void* in, const dm_layer_params* prm, void* const* outs,
-                     int s0, int s1, hipStream_t st) {
-    const int64_t T = x.Tq, P = x.P, H = x.H;
+int project_segments(const Dims& x, int layout, const void* in, int64_t L, const dm_layer_params* prm,
+                     void* const* outs, int s0, int s1, hipStream_t st) {
+    const int64_t T = x.B * L, P = x.P, H = x.H;
     const void* w[3] = {prm->wq, prm->wk, prm->wv};
     const void* b[3] = {prm->bq, prm->bk, prm->bv};
     const int ns = s1 - s0;
     Operand A = act_mk(in, layout, T, x.I);
     Operand Bw = opnd(w[s0], true, make_map((uint32_t)P, (uint32_t)H, H * x.I, x.I, 0));
-    Epilogue c = epi(outs[s0], make_map((uint32_t)x.J, 0, P, H * x.J * P, 0),
-                     make_map((uint32_t)P, (uint32_t)H, 1, x.J * P, 0), true, false);
+    Epilogue c = epi(outs[s0], make_map((uint32_t)L, 0, P, H * L * P, 0),
+                     make_map((uint32_t)P, (uint32_t)H, 1, L * P, 0), true, false);
     for (int i = 0; i < ns; ++i) {
         Bw.ptr[i] = w[s0 + i];
         c.ptr[i] = outs[s0 + i];
@@ -345,7 +358,7 @@ int project_fused(const Dims& x, int layout, const void* in, const dm_layer_para
     const int n = proj_groups(x.qkv_fusion, grp);
     for (int i = 0; i < n; ++i) {
         if (i > 0) trace_next(grp[i].sub);
-        DM_TRY(project_segments(x, layout, in, prm, outs, grp[i].s0, grp[i].s1, st));
+        DM_TRY(project_segments(x, layout, in, x.J, prm, outs, grp[i].s0, grp[i].s1, st));
     }
     return DM_OK;
 }
@@ -507,19 +520,19 @@ int project_bwd(const Dims& x, int layout, const void* in, int64_t T, int64_t n,
                        st);
 }
 
-// Backward of project_fused on the token-major [T][3][H][P] gradient: per
-// group, dX += dqkv[:, segments] [Wq Wk Wv][segments] (the first group adds
+// Backward of stacked projections on a token-major [T][nseg][H][P]
+// gradient dstk whose segment 0 is weight segment `seg0`: per group,
+// dX += dstk[:, segments] [Wq Wk Wv][segments] (the first group adds
 // `resid`, later ones add the dX written so far, each output element read
-// and written by the same thread) and d[Wq Wk Wv][segments] = dqkv[:,
+// and written by the same thread) and d[Wq Wk Wv][segments] = dstk[:,
 // segments]^T X.
-int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqkv, const dm_layer_params* prm,
-                      void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st) {
-    const int64_t H = x.H, I = x.I, P = x.P, T = x.Tq, HP = H * P;
+int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, const void* dstk, int nseg, int seg0,
+                        const ProjGroup* grp, int n, const dm_layer_params* prm, void* dx, const dm_layer_grads* g,
+                        const void* resid, hipStream_t st) {
+    const int64_t H = x.H, I = x.I, P = x.P, HP = H * P, ld = nseg * HP;
     const IdxMap wmap = make_map((uint32_t)P, (uint32_t)H, H * I, I, 0);
     const void* w[3] = {prm->wq, prm->wk, prm->wv};
     float* dw[3] = {g->dwq, g->dwk, g->dwv};
-    ProjGroup grp[3];
-    const int n = proj_groups(x.qkv_fusion, grp);
     {
         TraceScope t_("B18 qkv_dx", st);
         for (int i = 0; i < n; ++i) {
@@ -530,8 +543,8 @@ int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqk
             Operand Bw = opnd(w[s0], false, wmap);
             for (int j = 0; j < ns; ++j) Bw.ptr[j] = w[s0 + j];
             Bw.nseg = ns;
-            const void* a = B8(dqkv, (size_t)x.es * s0 * HP);
-            DM_TRY(launch_gemm(x.dtype, gemm(T, I, ns * HP, 1, opnd(a, true, linear_map(3 * HP)), Bw, c), st));
+            const void* a = B8(dstk, (size_t)x.es * (s0 - seg0) * HP);
+            DM_TRY(launch_gemm(x.dtype, gemm(T, I, ns * HP, 1, opnd(a, true, linear_map(ld)), Bw, c), st));
         }
     }
     TraceScope t_("B19 qkv_dw", st);
@@ -541,12 +554,20 @@ int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqk
         Epilogue cw = epi(dw[s0], wmap, linear_map(1), true, true);
         for (int j = 0; j < ns; ++j) cw.ptr[j] = dw[s0 + j];
         cw.nseg = ns; cw.seg_on_m = 1;
-        const void* a = B8(dqkv, (size_t)x.es * s0 * HP);
+        const void* a = B8(dstk, (size_t)x.es * (s0 - seg0) * HP);
         DM_TRY(launch_gemm(x.dtype,
-                           gemm(ns * HP, I, T, 1, opnd(a, false, linear_map(3 * HP)), act_kn(in, layout, T, I), cw),
+                           gemm(ns * HP, I, T, 1, opnd(a, false, linear_map(ld)), act_kn(in, layout, T, I), cw),
                            st));
     }
     return DM_OK;
+}
+
+// Backward of project_fused on the token-major [T][3][H][P] gradient.
+int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqkv, const dm_layer_params* prm,
+                      void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st) {
+    ProjGroup grp[3];
+    const int n = proj_groups(x.qkv_fusion, grp);
+    return project_stacked_bwd(x, layout, in, x.Tq, dqkv, 3, 0, grp, n, prm, dx, g, resid, st);
 }
 
 }  // namespace
@@ -774,7 +795,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
 // ------------------------------------------------------------ attention only
 int mha_sizes(const dm_layer_desc* d, size_t* saved_bytes, size_t* fwd_ws_bytes, size_t* bwd_ws_bytes) {
     DM_TRY(check_desc(d, false));
-    MhaSizes s = plan_mha(dims_of(d), d->self_attention != 0);
+    MhaSizes s = plan_mha(dims_of(d), d->self_attention);
     if (saved_bytes) *saved_bytes = s.saved;
     if (fwd_ws_bytes) *fwd_ws_bytes = s.fwd;
     if (bwd_ws_bytes) *bwd_ws_bytes = s.bwd;
@@ -785,23 +806,34 @@ int mha_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
             void* out, void* saved, void* ws, size_t ws_bytes, void* stream) {
     DM_TRY(check_desc(d, false));
     DM_TRY(check_params(prm, false));
-    const bool fused = d->self_attention != 0;
+    const int mode = d->self_attention;
     DM_TRY(need(qin, "q")); DM_TRY(need(out, "out")); DM_TRY(need(saved, "saved")); DM_TRY(need(ws, "ws"));
-    if (fused) {
+    if (mode == PROJ_QKV) {
         if ((kin && kin != qin) || (vin && vin != qin))
             return set_error(DM_ERR_ARG, "self-attention needs k and v NULL or equal to q");
+    } else if (mode == PROJ_KV) {
+        DM_TRY(need(kin, "k"));
+        if (vin && vin != kin) return set_error(DM_ERR_ARG, "a fused K/V projection needs v NULL or equal to k");
     } else {
         DM_TRY(need(kin, "k")); DM_TRY(need(vin, "v"));
     }
     const Dims x = dims_of(d);
-    const MhaSizes s = plan_mha(x, fused);
+    const MhaSizes s = plan_mha(x, mode);
     if (ws_bytes < s.fwd) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     SplitScope split_(B8(ws, s.fwd_split), s.split_floats);
     void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);
-    if (fused) {
+    if (mode == PROJ_QKV) {
         TraceScope t_("F1 qkv", st);
         DM_TRY(project_fused(x, x.layout, qin, prm, q, k, v, st));
+    } else if (mode == PROJ_KV) {
+        // queries from q; keys and values of the one memory tensor k with
+        // [Wk Wv] stacked (one contraction)
+        TraceScope t_("F1 q,kv", st);
+        DM_TRY(project(x, x.layout, qin, x.J, x.P, prm->wq, prm->bq, q, st));
+        trace_next("kv");
+        void* outs[3] = {q, k, v};
+        DM_TRY(project_segments(x, x.layout, kin, x.K, prm, outs, 1, 3, st));
     } else {
         TraceScope t_("F1 q,k,v", st);
         DM_TRY(project(x, x.layout, qin, x.J, x.P, prm->wq, prm->bq, q, st));
@@ -820,18 +852,23 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     DM_TRY(check_desc(d, false));
     DM_TRY(check_params(prm, false));
     DM_TRY(check_grads(g, false));
-    const bool fused = d->self_attention != 0;
+    const int mode = d->self_attention;
+    const bool fused = mode == PROJ_QKV;
     DM_TRY(need(qin, "q")); DM_TRY(need(saved, "saved")); DM_TRY(need(dout, "dout")); DM_TRY(need(dq, "dq"));
     DM_TRY(need(ws, "ws"));
     if (fused) {
         if (dk || dv) return set_error(DM_ERR_ARG, "self-attention writes the total input gradient to dq; dk, dv must be NULL");
         if ((kin && kin != qin) || (vin && vin != qin))
             return set_error(DM_ERR_ARG, "self-attention needs k and v NULL or equal to q");
+    } else if (mode == PROJ_KV) {
+        DM_TRY(need(kin, "k")); DM_TRY(need(dk, "dk"));
+        if (vin && vin != kin) return set_error(DM_ERR_ARG, "a fused K/V projection needs v NULL or equal to k");
+        if (dv) return set_error(DM_ERR_ARG, "a fused K/V projection writes the memory gradient to dk; dv must be NULL");
     } else {
         DM_TRY(need(kin, "k")); DM_TRY(need(vin, "v")); DM_TRY(need(dk, "dk")); DM_TRY(need(dv, "dv"));
     }
     const Dims x = dims_of(d);
-    const MhaSizes s = plan_mha(x, fused);
+    const MhaSizes s = plan_mha(x, mode);
     if (ws_bytes < s.bwd) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     SplitScope split_(B8(ws, s.bwd_split), s.split_floats);
@@ -840,7 +877,8 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     const void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);
     void* bq = B8(ws, s.p.dq);
     void* bk = fused ? B8(ws, s.p.dq + (size_t)es * x.H * x.P) : B8(ws, s.p.dk);
-    void* bv = fused ? B8(ws, s.p.dq + (size_t)es * 2 * x.H * x.P) : B8(ws, s.p.dv);
+    void* bv = fused ? B8(ws, s.p.dq + (size_t)es * 2 * x.H * x.P)
+                     : mode == PROJ_KV ? B8(ws, s.p.dk + (size_t)es * x.H * x.P) : B8(ws, s.p.dv);
     float* part = (float*)B8(ws, s.p.part);
 
     // output-bias grad
@@ -864,6 +902,15 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
         run_colsum_partial(dt, x.Tq, (int)(3 * x.H * x.P), bq, part, st);
         trace_next("finish");
         run_colsum_finish_qkv(colsum_blocks(x.Tq), (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
+    } else if (mode == PROJ_KV) {
+        TraceScope t_("B18-20 q,kv_bwd", st);
+        DM_TRY(project_bwd(x, x.layout, qin, x.Tq, x.P, bq, s.p.ldq, prm->wq, dq, g->dwq, nullptr, st));
+        const ProjGroup kv = {1, 3, "kv"};
+        DM_TRY(project_stacked_bwd(x, x.layout, kin, x.Tk, bk, 2, 1, &kv, 1, prm, dk, g, nullptr, st));
+        run_colsum_partial(dt, x.Tq, (int)(x.H * x.P), bq, part, st);
+        run_colsum_finish_qkv(colsum_blocks(x.Tq), (int)x.H, (int)x.P, 1, part, g->dbq, nullptr, nullptr, st);
+        run_colsum_partial(dt, x.Tk, (int)(2 * x.H * x.P), bk, part, st);
+        run_colsum_finish_qkv(colsum_blocks(x.Tk), (int)x.H, (int)x.P, 2, part, g->dbk, g->dbv, nullptr, st);
     } else {
         TraceScope t_("B18-20 q,k,v_bwd", st);
         DM_TRY(project_bwd(x, x.layout, qin, x.Tq, x.P, bq, s.p.ldq, prm->wq, dq, g->dwq, nullptr, st));

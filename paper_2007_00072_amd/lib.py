@@ -170,12 +170,12 @@ def _drop(d):
 
 def make_desc(shape, dtype: str, layout: str = "bji", act: str = "gelu", scaler: float = 0.0,
               ln_eps: float = 1e-12, p_attn=0.0, p_attn_out=0.0, p_ffn_out=0.0, p_ffn_act=0.0,
-              seed: int = 0, layer_id: int = 0, self_attention: bool = True, causal: bool = False,
+              seed: int = 0, layer_id: int = 0, self_attention=True, causal: bool = False,
               qkv_fusion: int = 0) -> LayerDesc:
     return LayerDesc(shape.B, shape.J, shape.K, shape.H, shape.P, shape.W, shape.I, shape.F,
                      DTYPE_CODES[dtype], LAYOUT_CODES[layout], DM_GELU if act == "gelu" else DM_RELU,
                      scaler, ln_eps, p_attn, p_attn_out, p_ffn_out, p_ffn_act, seed, layer_id,
-                     1 if self_attention else 0, 1 if causal else 0, qkv_fusion)
+                     int(self_attention), 1 if causal else 0, qkv_fusion)
 
 
 def make_params(tensors) -> LayerParams:

@@ -85,8 +85,9 @@ class MultiHeadAttention:
     def backward(self, q, dout, k=None, v=None, dq=None, dk=None, dv=None):
         if dq is None:
             dq = torch.empty_like(q)
-        if not self.desc.self_attention:
+        if self.desc.self_attention != 1:
             dk = torch.empty_like(k) if dk is None else dk
+        if self.desc.self_attention == 0:
             dv = torch.empty_like(v) if dv is None else dv
         lib.mha_bwd(self.desc, self.cparams, q, k, v, self.saved, dout, dq, dk, dv, self.cgrads, self.ws,
                     self.ws.numel())

@@ -121,6 +121,34 @@ def test_mha_validation(lib):
     assert "k" in str(e.value)
 
 
+def test_mha_fused_kv_validation(lib):
+    from paper_2007_00072_amd.inputs import Shape
+    d = lib.make_desc(Shape(B=2, J=64, K=72, H=4, P=32, W=32, I=128), "f16", layout="bji", self_attention=2)
+    s2, f2, b2 = lib.mha_sizes(d)   # queries and memory of different lengths
+    d.self_attention = 0
+    s0, f0, b0 = lib.mha_sizes(d)
+    assert (s2, f2) == (s0, f0) and b2 >= b0   # dK and dV stacked; bias sums over 2HP columns
+    d.self_attention = 3
+    with pytest.raises(lib.DmError) as e:
+        lib.mha_sizes(d)
+    assert "self_attention" in str(e.value)
+    d = lib.make_desc(Shape(B=2, J=64, K=72, H=4, P=32, W=48, I=128), "f16", self_attention=2)
+    with pytest.raises(lib.DmError) as e:
+        lib.mha_sizes(d)
+    assert "W == P" in str(e.value)
+    d.W = 32
+    prm = lib.make_params({n: 0x10000 for n in lib._PNAMES[:8]})
+    g = lib.make_grads({n: 0x10000 for n in lib._PNAMES[:8]})
+    s, f, b = lib.mha_sizes(d)
+    with pytest.raises(lib.DmError) as e:   # v must be NULL or the memory itself
+        lib.mha_fwd(d, prm, 0x10000, 0x20000, 0x30000, 0x40000, 0x50000, 0x60000, f, stream=None)
+    assert "v NULL or equal to k" in str(e.value)
+    with pytest.raises(lib.DmError) as e:   # the memory gradient goes to dk only
+        lib.mha_bwd(d, prm, 0x10000, 0x20000, None, 0x50000, 0x40000, 0x70000, 0x80000, 0x90000, g, 0x60000, b,
+                    stream=None)
+    assert "dv must be NULL" in str(e.value)
+
+
 def test_fused_op_validation(lib):
     with pytest.raises(lib.DmError) as e:
         lib.bdrln_fwd(1, 16, 100, 0x10000, 0x10000, 0x10000, 0x10000, 0x10000, 1e-5, None, 0x10000, None, None,

@@ -147,9 +147,13 @@ def check_mha(wl, self_attention=True, causal=False, **desc_over):
     params = make_params(wl)
     q = make_activation(wl, 0)
     dout = make_activation(wl, 1)
-    if self_attention:
+    if self_attention is True:
         k = v = None
         kh = vh = q
+    elif self_attention == 2:
+        # encoder/decoder attention: keys and values from one memory tensor
+        kh = vh = make_activation(wl, 2, length=s.K)
+        k, v = kh.to(DEV), None
     else:
         kh = make_activation(wl, 2, length=s.K)
         vh = make_activation(wl, 3, length=s.K)
@@ -167,8 +171,12 @@ def check_mha(wl, self_attention=True, causal=False, **desc_over):
     rdq, rdk, rdv, rg, _ = OL.mha_backward_ibj(to_ibj(f64(dout)), cache, prm, cfg)
     dt = wl.dtype
     assert_close("out", out, from_ibj(rout), dt)
-    if self_attention:
+    if self_attention is True:
         assert_close("dx", dq, from_ibj(OL.store(rdq + rdk + rdv, dt)), dt)
+    elif self_attention == 2:
+        assert dv is None
+        assert_close("dq", dq, from_ibj(OL.store(rdq, dt)), dt)
+        assert_close("dmem", dk, from_ibj(OL.store(rdk + rdv, dt)), dt)
     else:
         assert_close("dq", dq, from_ibj(OL.store(rdq, dt)), dt)
         assert_close("dk", dk, from_ibj(OL.store(rdk, dt)), dt)
@@ -178,6 +186,24 @@ def check_mha(wl, self_attention=True, causal=False, **desc_over):
             assert_close("dbk", M.grads[n], rg[n], dt, zero_ref=True, scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
         else:
             assert_close("d" + n, M.grads[n], rg[n], dt, param_grad=True)
+
+
+@pytest.mark.parametrize("dtype,layout", [("f16", "bji"), ("bf16", "ibj"), ("f32", "bji")])
+def test_mha_fused_kv_cross_attention(dtype, layout):
+    # encoder/decoder attention with [Wk Wv] stacked over one memory tensor:
+    # query length 72 against memory length 128 (scores kept on chip) and
+    # the tiny fp32 case through the separate launches
+    shape = Shape(B=2, J=72, K=128, H=4, P=32, W=32, I=128) if dtype != "f32" else \
+        Shape(B=2, J=24, K=40, H=2, P=16, W=16, I=32)
+    wl = WORKLOADS["mha_large_f16"].with_(shape=shape, dtype=dtype, layout=layout, p_attn=0.1)
+    check_mha(wl, self_attention=2)
+
+
+def test_mha_fused_kv_full_size():
+    # BERT-large widths, 512 queries against a 384-token memory
+    wl = WORKLOADS["mha_large_f16"]
+    wl = wl.with_(shape=Shape(B=4, J=512, K=384, H=16, P=64, W=64, I=1024), layout="bji")
+    check_mha(wl, self_attention=2)
 
 
 def test_mha_full_size_ibj():
