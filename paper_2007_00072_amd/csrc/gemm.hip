@@ -1365,108 +1365,14 @@ __device__ __forceinline__ void lean_store(const GemmArgs& g, const LeanOut& o, 
     }
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean(GemmArgs g) {
-    constexpr int NT = 64 * WGM * WGN, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
-    constexpr int NQ = BKS / 16;  // 16-wide k slices per step
-    constexpr int AS = BM * BKS, BS = BN * BKS;
-    constexpr int STAGE = (AS + BS) * (int)sizeof(T);
-    static_assert(STAGES >= 3 && FM >= 1 && FN >= 1 && STAGES * STAGE <= 160 * 1024, "configuration");
-    __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
-    typedef typename LeanSel<T, BM, BKS, NT, AKC>::type DA;
-    typedef typename LeanSel<T, BN, BKS, NT, BKC>::type DB;
-    constexpr int NL = DA::NV + DB::NV;  // copies per thread per step
-    typedef typename Mfma32<T>::frag frag;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WGN, wn = wave % WGN;
-    int tm, tn;
-    int by;
-    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int splits = g.splits > 1 ? g.splits : 1;
-    const uint32_t z = (uint32_t)by / splits;
-    const int sidx = by - (int)z * splits;
-    const int kb = splits > 1 ? sidx * g.kper : 0;
-    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
+// Epilogue of a lean kernel for one wave's FM x FN accumulator blocks at
+// (mw, nw): split-k partials as row-major floats through the same store
+// routine as float outputs (one code path keeps registers few).
+template <typename T, int FM, int FN>
+__device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 (&acc)[FM][FN], int mw, int nw,
+                                              uint32_t z, int sidx, int splits) {
+    const int lane = threadIdx.x & 63, c = lane & 31;
     int dummy = 0;
-    const int64_t aoff = map_off(g.a.batch, z, 1, &dummy), boff = map_off(g.b.batch, z, 1, &dummy);
-    DA da;
-    DB db;
-    da.init(g.a, aoff, kb, m0, g.M);
-    db.init(g.b, boff, kb, n0, g.N);
-    const uint32_t base = lds_addr(smem);
-
-    floatx16 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    const int nk = (ke - kb) / BKS;
-    auto issue = [&](int s) {
-        const uint32_t st = base + (uint32_t)((s % STAGES) * STAGE);
-        da.issue(g.a, aoff, kb, s, st);
-        db.issue(g.b, boff, kb, s, st + (uint32_t)(AS * sizeof(T)));
-    };
-    frag a[2][FM], b[2][FN];
-    auto read = [&](int buf, int s, int q) {
-        const T* A = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
-        const T* B = A + AS;
-#pragma unroll
-        for (int i = 0; i < FM; ++i) a[buf][i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, q * 16, lane));
-#pragma unroll
-        for (int j = 0; j < FN; ++j) b[buf][j] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + j * 32, q * 16, lane));
-    };
-    auto mma = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j) acc[i][j] = Mfma32<T>::run(a[buf][i], b[buf][j], acc[i][j]);
-    };
-
-    if (nk > 0) {
-#pragma unroll
-        for (int s = 0; s < STAGES - 1; ++s)
-            if (s < nk) issue(s);
-        if (nk >= STAGES - 1) wait_vm<(STAGES - 2) * NL>();
-        else wait_vm<0>();
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        read(0, 0, 0);
-    }
-    // Every 16-wide slice: the next slice's fragments are read while this
-    // slice's MFMAs run.  Before the last slice of step s, once step s+1 has
-    // landed and this wave's reads of step s are done, one barrier lets the
-    // slot of step s-1 be refilled with step s+STAGES-1 (after the last step
-    // the read is of a stale slot, unused).
-    for (int s = 0; s < nk; ++s) {
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int cur = q & 1;
-            if (q + 1 < NQ) {
-                read(cur ^ 1, s, q + 1);
-            } else {
-                if (s + STAGES - 2 < nk) wait_vm<(STAGES - 3) * NL>();
-                else wait_vm<0>();
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                __builtin_amdgcn_s_barrier();
-                asm volatile("" ::: "memory");
-                if (s + STAGES - 1 < nk) issue(s + STAGES - 1);
-                read(cur ^ 1, s + 1, 0);
-            }
-            asm volatile("" ::: "memory");
-            __builtin_amdgcn_sched_barrier(0);
-            mma(cur);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    }
-
-    // epilogue: split-k partials as row-major floats through the same
-    // store routine as float outputs (one code path keeps registers few)
-    const int mw = m0 + wm * WM, nw = n0 + wn * WN, c = lane & 31;
     const Epilogue& e = g.c;
     const bool part = splits > 1;
     float bn[FN];
@@ -1533,6 +1439,162 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean(GemmArgs g) {
     else if (o.cn) lean_store<T, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
     else if (e.out_f32) lean_store<float, false, FM, FN>(g, o, acc, mw, nw, bn, alpha);
     else lean_store<T, false, FM, FN>(g, o, acc, mw, nw, bn, alpha);
+}
+
+
+// KG > 1 splits each k-step's 16-wide slices among KG groups of WGM x WGN
+// waves (group g takes slices g, g + KG, ...), so a wave holds a larger
+// tile of the output and reads fewer fragments per MFMA; the groups' fp32
+// partial tiles are added through LDS before the stores.
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG>
+__global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
+    constexpr int NT = 64 * WGM * WGN * KG, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
+    constexpr int NQ = BKS / 16;  // 16-wide k slices per step
+    constexpr int NQL = NQ / KG;  // of them, the slices of one wave
+    static_assert(NQL * KG == NQ && NQL % 2 == 0 && (KG == 1 || (KG == 2 && FM % 2 == 0)), "k groups");
+    constexpr int AS = BM * BKS, BS = BN * BKS;
+    constexpr int STAGE = (AS + BS) * (int)sizeof(T);
+    static_assert(STAGES >= 3 && FM >= 1 && FN >= 1 && STAGES * STAGE <= 160 * 1024, "configuration");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
+    typedef typename LeanSel<T, BM, BKS, NT, AKC>::type DA;
+    typedef typename LeanSel<T, BN, BKS, NT, BKC>::type DB;
+    constexpr int NL = DA::NV + DB::NV;  // copies per thread per step
+    typedef typename Mfma32<T>::frag frag;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kg = wave / (WGM * WGN), wl = wave - kg * (WGM * WGN);
+    const int wm = wl / WGN, wn = wl % WGN;
+    int tm, tn;
+    int by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int splits = g.splits > 1 ? g.splits : 1;
+    const uint32_t z = (uint32_t)by / splits;
+    const int sidx = by - (int)z * splits;
+    const int kb = splits > 1 ? sidx * g.kper : 0;
+    const int ke = splits > 1 ? min(g.K, kb + g.kper) : g.K;
+    int dummy = 0;
+    const int64_t aoff = map_off(g.a.batch, z, 1, &dummy), boff = map_off(g.b.batch, z, 1, &dummy);
+    DA da;
+    DB db;
+    da.init(g.a, aoff, kb, m0, g.M);
+    db.init(g.b, boff, kb, n0, g.N);
+    const uint32_t base = lds_addr(smem);
+
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int nk = (ke - kb) / BKS;
+    auto issue = [&](int s) {
+        const uint32_t st = base + (uint32_t)((s % STAGES) * STAGE);
+        da.issue(g.a, aoff, kb, s, st);
+        db.issue(g.b, boff, kb, s, st + (uint32_t)(AS * sizeof(T)));
+    };
+    frag a[2][FM], b[2][FN];
+    auto read = [&](int buf, int s, int q) {
+        const T* A = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
+        const T* B = A + AS;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[buf][i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, q * 16, lane));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[buf][j] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + j * 32, q * 16, lane));
+    };
+    auto mma = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = Mfma32<T>::run(a[buf][i], b[buf][j], acc[i][j]);
+    };
+
+    if (nk > 0) {
+#pragma unroll
+        for (int s = 0; s < STAGES - 1; ++s)
+            if (s < nk) issue(s);
+        if (nk >= STAGES - 1) wait_vm<(STAGES - 2) * NL>();
+        else wait_vm<0>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        read(0, 0, kg);
+    }
+    // Every 16-wide slice: the next slice's fragments are read while this
+    // slice's MFMAs run.  Before the last slice of step s, once step s+1 has
+    // landed and this wave's reads of step s are done, one barrier lets the
+    // slot of step s-1 be refilled with step s+STAGES-1 (after the last step
+    // the read is of a stale slot, unused).
+    for (int s = 0; s < nk; ++s) {
+#pragma unroll
+        for (int q = 0; q < NQL; ++q) {
+            const int cur = q & 1;
+            if (q + 1 < NQL) {
+                read(cur ^ 1, s, (q + 1) * KG + kg);
+            } else {
+                if (s + STAGES - 2 < nk) wait_vm<(STAGES - 3) * NL>();
+                else wait_vm<0>();
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                asm volatile("" ::: "memory");
+                if (s + STAGES - 1 < nk) issue(s + STAGES - 1);
+                read(cur ^ 1, s + 1, kg);
+            }
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_sched_barrier(0);
+            mma(cur);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    const int mw = m0 + wm * WM, nw = n0 + wn * WN;
+    if constexpr (KG == 1) {
+        lean_epilogue<T, FM, FN>(g, acc, mw, nw, z, sidx, splits);
+    } else {
+        // group 0 stores rows [0, FM/2) of the wave tile and group 1 the
+        // rest: each group first hands the other half of its partial tile
+        // to its partner wave through LDS (the stages are free once every
+        // wave has passed the barrier)
+        constexpr int FH = FM / 2, SLOT = FH * FN * 16 * 64;
+        float* red = reinterpret_cast<float*>(smem);
+        auto put = [&](float* dst, auto give_c) {
+            constexpr int give = decltype(give_c)::value;
+#pragma unroll
+            for (int i = 0; i < FH; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4) {
+                        floatx4 v = {acc[give + i][j][4 * r4], acc[give + i][j][4 * r4 + 1], acc[give + i][j][4 * r4 + 2],
+                                     acc[give + i][j][4 * r4 + 3]};
+                        *reinterpret_cast<floatx4*>(dst + (((i * FN + j) * 4 + r4) * 64 + lane) * 4) = v;
+                    }
+        };
+        floatx16 half[FH][FN];
+        auto take = [&](const float* src, auto keep_c) {
+            constexpr int keep = decltype(keep_c)::value;
+#pragma unroll
+            for (int i = 0; i < FH; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4) {
+                        const floatx4 v = *reinterpret_cast<const floatx4*>(src + (((i * FN + j) * 4 + r4) * 64 + lane) * 4);
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) half[i][j][4 * r4 + t] = acc[keep + i][j][4 * r4 + t] + v[t];
+                    }
+        };
+        __syncthreads();
+        float* to_partner = red + ((1 - kg) * (WGM * WGN) + wl) * SLOT;
+        if (kg == 0) put(to_partner, std::integral_constant<int, FH>{});
+        else put(to_partner, std::integral_constant<int, 0>{});
+        __syncthreads();
+        const float* mine = red + (kg * (WGM * WGN) + wl) * SLOT;
+        if (kg == 0) take(mine, std::integral_constant<int, 0>{});
+        else take(mine, std::integral_constant<int, FH>{});
+        lean_epilogue<T, FH, FN>(g, half, mw + kg * FH * 32, nw, z, sidx, splits);
+    }
 }
 
 // True when a lean kernel with k-steps of bks takes this contraction.
@@ -1632,12 +1694,13 @@ struct TileCfg {
 // 9-12: asynchronous kernel on 32x32x16 MFMAs; 13: lean 256x256 kernel
 // (8 waves of 128x64, four stages of 32-wide k-steps); 14: the general
 // 256x256 kernel with the same waves; 15: lean 128x128 kernel (8 waves of
-// 64x32, four stages of 64-wide k-steps).  Contractions a lean kernel does
-// not take run on 14 (for 13) or 11 (for 15).
+// 64x32, four stages of 64-wide k-steps); 16: lean 128x128 kernel with two
+// k groups of 4 waves of 64x64.  Contractions a lean kernel does not take
+// run on 14 (for 13) or 11 (for 15, 16).
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
-                            {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}};
+                            {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}, {128, 128, 2, 2}};
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
 template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH>
@@ -1682,18 +1745,18 @@ void launch_x32(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, false, false>), grid, block, 0, st, g);
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, int KG = 1>
 void launch_lean(const GemmArgs& g, hipStream_t st) {
     dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
-    dim3 block(64 * WGM * WGN);
+    dim3 block(64 * WGM * WGN * KG);
     if (g.a.kcontig && g.b.kcontig)
-        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true>), grid, block, 0, st, g);
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, KG>), grid, block, 0, st, g);
     else if (g.a.kcontig)
-        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, false>), grid, block, 0, st, g);
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, false, KG>), grid, block, 0, st, g);
     else if (g.b.kcontig)
-        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true>), grid, block, 0, st, g);
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, KG>), grid, block, 0, st, g);
     else
-        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false>), grid, block, 0, st, g);
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, KG>), grid, block, 0, st, g);
 }
 
 template <typename T, int WGM, int WGN>
@@ -1711,6 +1774,7 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
         case 13: launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st); break;
         case 15: launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st); break;
+        case 16: launch_lean<T, 128, 128, 2, 2, 64, 4, 2>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -1766,7 +1830,7 @@ void choose(GemmArgs& g) {
     // maps affine over 32-wide blocks; of them only the lean 128x128 kernel
     // takes a residual operand
     if (((g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
-    if (g.c.resid && g.cfg >= 9 && g.cfg != 15) g.cfg = 8;
+    if (g.c.resid && g.cfg >= 9 && g.cfg != 15 && g.cfg != 16) g.cfg = 8;
     if (g.splits <= 0) {
         int s = split_ok ? want_split : 1;
         while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
@@ -1778,7 +1842,7 @@ void choose(GemmArgs& g) {
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
     if (g.cfg == 13 && !lean_ok(g, 32)) g.cfg = 14;
-    if (g.cfg == 15 && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
+    if ((g.cfg == 15 || g.cfg == 16) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
     // tile counts of the configuration that runs (the fallback from 15 to 8
     // changes the tile width)
     const TileCfg& c = CFGS[g.cfg];

@@ -47,6 +47,19 @@ def test_plan_entry_changes_the_kernel_and_keeps_parity():
     check_encoder(wl, layer=1)
 
 
+def test_plan_every_contraction_on_the_k_group_kernel():
+    # every contraction of the layer that the lean kernels take runs on the
+    # 128x128 kernel with two k groups (the residual epilogue of the Q/K/V
+    # input gradient included); results still match the oracle
+    wl = small("bert_large_f16", B=2, J=96, K=96, H=4, P=64, W=64, I=256, F=512)
+    recs, _ = _launches(wl)
+    lib.plan_set([lib.ContractChoice(*k, 16, 1) for k in {r.key() for r in recs}], 3)
+    recs2, _ = _launches(wl)
+    assert sum(r.tile_cfg == 16 for r in recs2) >= 8
+    assert any(r.tile_cfg == 16 and r.label.decode() == "B18 qkv_dx" for r in recs2)
+    check_encoder(wl, layer=1)
+
+
 @pytest.mark.parametrize("path,fwd,bwd", [
     (1, ["F2 qkt", "F3 softmax", "F4 gamma"], ["B13 gamma_dx1", "B15 softmax_bwd", "B16 qkt_dx1"]),
     (2, ["F2-3 qkt_softmax", "F4 gamma"], ["B13-15 gamma_dx1_softmax_bwd", "B16 qkt_dx1"]),
@@ -75,7 +88,7 @@ def test_tuner_end_to_end(tmp_path):
                     shape=Shape(B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024),
                     tile_cfgs=(8, 13, 15), splits=(1, 2))
     assert res["attn_path"] in (1, 2, 3)
-    assert res["entries"] and all(0 <= e["tile_cfg"] <= 15 for e in res["entries"])
+    assert res["entries"] and all(0 <= e["tile_cfg"] <= 16 for e in res["entries"])
     for name in ("forward", "backward"):
         assert res["passes"][name]["predicted_ms"] > 0
     path = tmp_path / "plan.json"
