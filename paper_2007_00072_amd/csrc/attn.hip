@@ -106,8 +106,14 @@ __device__ __forceinline__ u32x4 stage_frag(const T* stg, int lane) {
 constexpr int STG_BYTES = 2048;  // per-wave staging slot: two 16 x 32 pieces
 constexpr int PF2 = 8;           // k16 steps of the second contraction loaded ahead into registers
 
+// chunk permutation mask of the score tile's rows (K a multiple of 8)
+__host__ __device__ inline int tile_swizzle_mask(int K) {
+    const int ch = K / 8, low = ch & -ch;
+    return (low < 16 ? low : 16) - 1;
+}
+
 inline size_t attn_lds_bytes(int K, int es, int nb2) {
-    const size_t s = ((size_t)32 * (K + 8) * es + 15) / 16 * 16;
+    const size_t s = (size_t)32 * K * es;
     if (nb2 == 0) return s;
     const size_t ks = 8 / nb2;
     return std::max(s + (size_t)(NTA / 64) * STG_BYTES, (ks - 1) * nb2 * 4096);
@@ -117,10 +123,13 @@ template <typename T, int LPR, int NV, int DK, bool BWD, int NB2>
 __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
     T* S = reinterpret_cast<T*>(smem_raw);
-    // rows 16 bytes apart in bank space: the 8-byte tile writes, the 16-byte
-    // fragment reads and the row operator's 16-byte accesses all spread over
-    // the 64 banks
-    const int K = g.K, J = g.J, pitch = K + 8;
+    // unpadded rows of K elements; the 16-byte chunks of row r are permuted
+    // by chunk ^ (r & swm) (swm + 1 = the largest power of two up to 16
+    // dividing K / 8), so the 8-byte tile writes, the 16-byte fragment reads
+    // and the row operator's 16-byte accesses spread over the 64 banks as
+    // padded rows would, while the tile takes no more than 32 K elements
+    const int K = g.K, J = g.J, swm = tile_swizzle_mask(K);
+    auto at = [&](int r, int col) { return r * K + ((((col >> 3) ^ (r & swm))) << 3) + (col & 7); };
     // Workgroups reach the 8 XCDs round-robin by linear id; the row blocks
     // of one (b, h) are given consecutive ids within one XCD's share, so
     // that XCD's L2 serves the head's key-side rows to all of them
@@ -183,7 +192,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
                 pk.x = bits16(from_f<T>(acc[4 * q] * g.out_scale)) | (bits16(from_f<T>(acc[4 * q + 1] * g.out_scale)) << 16);
                 pk.y = bits16(from_f<T>(acc[4 * q + 2] * g.out_scale)) |
                        (bits16(from_f<T>(acc[4 * q + 3] * g.out_scale)) << 16);
-                *reinterpret_cast<uint2*>(S + c * pitch + cb * 32 + 8 * q + 4 * hh) = pk;
+                *reinterpret_cast<uint2*>(S + at(c, cb * 32 + 8 * q + 4 * hh)) = pk;
             }
         }
     }
@@ -227,7 +236,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
             for (int i = 0; i < NV; ++i) {
                 const int col = (gl + i * LPR) * 8;
                 if (active && col < K) {
-                    V8<T>::unpack(*reinterpret_cast<const u32x4*>(S + lr * pitch + col), v[i]);
+                    V8<T>::unpack(*reinterpret_cast<const u32x4*>(S + at(lr, col)), v[i]);
                     if (g.causal) {
 #pragma unroll
                         for (int q = 0; q < 8; ++q)
@@ -260,7 +269,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
                     dropout8(g.dp, (uint64_t)(ebase + col), v[i]);
                     const u32x4 pk = V8<T>::pack(v[i]);
                     *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(g.out1) + base + col) = pk;
-                    if constexpr (NB2 > 0) *reinterpret_cast<u32x4*>(S + lr * pitch + col) = pk;
+                    if constexpr (NB2 > 0) *reinterpret_cast<u32x4*>(S + at(lr, col)) = pk;
                 }
             }
         } else {
@@ -271,7 +280,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
                 const int col = (gl + i * LPR) * 8;
                 if (active && col < K) {
                     V8<T>::unpack(pre[it][i], p[i]);
-                    V8<T>::unpack(*reinterpret_cast<const u32x4*>(S + lr * pitch + col), v[i]);
+                    V8<T>::unpack(*reinterpret_cast<const u32x4*>(S + at(lr, col)), v[i]);
                     dropout8(g.dp, (uint64_t)(ebase + col), v[i]);
 #pragma unroll
                     for (int q = 0; q < 8; ++q) dot += v[i][q] * p[i][q];
@@ -291,7 +300,7 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
                     for (int q = 0; q < 8; ++q) o[q] = g.sm_scale * p[i][q] * (v[i][q] - dot);
                     const u32x4 pk = V8<T>::pack(o);
                     *reinterpret_cast<u32x4*>(reinterpret_cast<T*>(g.out0) + base + col) = pk;
-                    if constexpr (NB2 > 0) *reinterpret_cast<u32x4*>(S + lr * pitch + col) = pk;
+                    if constexpr (NB2 > 0) *reinterpret_cast<u32x4*>(S + at(lr, col)) = pk;
                 }
             }
         }
@@ -302,12 +311,12 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
     if constexpr (NB2 > 0) {
         if constexpr (BWD) load_next(0);
         __syncthreads();
-        const size_t s_bytes = ((size_t)32 * pitch * sizeof(T) + 15) / 16 * 16;
+        const size_t s_bytes = (size_t)32 * K * sizeof(T);
         T* stg = reinterpret_cast<T*>(smem_raw + s_bytes + wave * STG_BYTES);
         floatx16 acc;
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-        const T* arow = S + c * pitch + 8 * hh;
+
         for (int g0 = 0; g0 < cnt; g0 += PF2) {
             if (g0 > 0) load_next(g0);
 #pragma unroll
@@ -319,10 +328,11 @@ __global__ __launch_bounds__(NTA) void attn_fused_k(AttnArgs g) {
                     if (g0 + i + 1 < cnt)
                         *reinterpret_cast<u32x4*>(stg + 512 + (lane >> 2) * 32 + 8 * (lane & 3)) = xr[i + 1];
                     const int s0 = 16 * (ks + KS * (g0 + i));
-                    acc = AMfma<T>::run(*reinterpret_cast<const u32x4*>(arow + s0), stage_frag(stg, lane), acc);
+                    acc = AMfma<T>::run(*reinterpret_cast<const u32x4*>(S + at(c, s0 + 8 * hh)), stage_frag(stg, lane), acc);
                     if (g0 + i + 1 < cnt) {
                         const int s1 = 16 * (ks + KS * (g0 + i + 1));
-                        acc = AMfma<T>::run(*reinterpret_cast<const u32x4*>(arow + s1), stage_frag(stg + 512, lane), acc);
+                        acc = AMfma<T>::run(*reinterpret_cast<const u32x4*>(S + at(c, s1 + 8 * hh)), stage_frag(stg + 512, lane),
+                                            acc);
                     }
                 }
             }
@@ -399,7 +409,7 @@ AttnOp attn_op(const void* p, int64_t outer, int64_t inner, int64_t ld) {
 }  // namespace
 
 bool attn_fused_ok(int dtype, int K, int D) {
-    // the score tile (32 rows of K + 16 elements) stays within 64 KB of LDS
+    // the score tile (32 rows of K elements) stays within 64 KB of LDS
     return (dtype == DM_F16 || dtype == DM_BF16) && K % 32 == 0 && K <= 960 &&
            (D == 16 || D == 32 || D == 48 || D == 64 || D == 96 || D == 128);
 }

@@ -78,7 +78,7 @@ def test_plan_set_validation():
     with pytest.raises(lib.DmError):
         lib.plan_set([], 4)
     with pytest.raises(lib.DmError):
-        lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 16, 1)], 0)
+        lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 17, 1)], 0)
     with pytest.raises(lib.DmError):
         lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 5, 0)], 0)
 
