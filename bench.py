@@ -3,12 +3,14 @@
 (fp16, B=8, L=512, I=1024, H=16, P=64, FFN 4096, three dropouts p=0.1) on
 one MI355X, through the library's C ABI.
 
-Prints one JSON line: ms per fwd+bwd step (inputs resident in HBM), the
-roofline position of the dominant kernel (per-launch durations measured
-with HIP events on the launch stream), the aggregate HBM rate of the fused
-memory-bound operators, and the CPU oracle timed on a bounded sample.
+Prints one JSON line: ms per fwd+bwd step (inputs resident in HBM; with
+--graph also the time of replaying the step captured as one HIP graph),
+the roofline position of the dominant kernel (per-launch durations
+measured with HIP events on the launch stream), the aggregate HBM rate of
+the fused memory-bound operators, and the CPU oracle timed on a bounded
+sample.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--graph] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -92,6 +94,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="sequences in the CPU-oracle sample (0: the whole batch)")
     ap.add_argument("--kernels-json", default=None, help="write the per-kernel table here")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time replays of the step captured as one HIP graph (reported beside the "
+                         "launch-by-launch time, after checking that a replay writes what an eager step writes)")
     ap.add_argument("--plan", default=None,
                     help="configuration plan written by paper_2007_00072_amd.tune (default: the built-in choices)")
     a = ap.parse_args()
@@ -133,15 +138,43 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    e0.record(st)
-    for _ in range(a.steps):
+
+    def timed(run):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(st)
+        for _ in range(a.steps):
+            run()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / a.steps, time.perf_counter() - t0
+
+    ms, wall = timed(step)
+    graph_ms, graph_check = None, None
+    if a.graph:
+        # the whole step (every launch of forward and backward) captured once
+        # and replayed; the library issues no allocation, copy or
+        # synchronisation inside a step, so capture records its kernels only
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        for _ in range(a.warmup):
+            graph.replay()
+        graph_ms, _ = timed(graph.replay)
+        # a replay writes exactly what an eager step writes
+        graph.replay()
+        torch.cuda.synchronize()
+        yg, dxg = y.clone(), dx.clone()
+        gg = {n: t.clone() for n, t in layer.grads.items()}
         step()
-    e1.record(st)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms = e0.elapsed_time(e1) / a.steps
+        torch.cuda.synchronize()
+        same = torch.equal(yg, y) and torch.equal(dxg, dx) and all(torch.equal(gg[n], layer.grads[n]) for n in gg)
+        graph_check = "replay bit-identical to an eager step" if same else "MISMATCH"
+        if not same:
+            print(json.dumps({"error": "graph replay differs from the eager step"}))
+            return 1
 
     # per-launch durations: the library brackets each launch with events on this stream
     lib.dm_trace_enable(True)
@@ -218,6 +251,8 @@ def main() -> int:
         "contractions": {"tflops_all": round(cf / ct / 1e12, 1), "us_per_step": round(ct * 1e6, 1),
                          "mfma_bound_tflops": round(mff / mft / 1e12, 1),
                          "mfma_bound_frac": round(mff / mft / 1e12 / dataflow.MFMA_PEAK_TFLOPS[wl.dtype], 4)},
+        "graph_ms_per_step": round(graph_ms, 4) if graph_ms is not None else None,
+        "graph_check": graph_check,
         "traced_ms_per_step": round(traced_ms, 4),
         "wall_s": round(wall, 3),
     }
