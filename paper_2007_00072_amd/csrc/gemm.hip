@@ -405,13 +405,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& g, const floatx4 (&acc)
 // that XCD's L2.  Within a batch entry tiles go in groups of GM tile rows
 // (column-major inside a group) so concurrently running tiles reuse both
 // operand panels.
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn, int& by) {
-    const int nt = tiles_m * tiles_n;
-    const int total = nt * (int)gridDim.y;
-    int lid = (int)blockIdx.y * nt + (int)blockIdx.x;
-    if ((total & 7) == 0) lid = (lid & 7) * (total >> 3) + (lid >> 3);
-    by = lid / nt;
-    const int t = lid - by * nt;
+__device__ __forceinline__ int xcd_order(int lid, int total) {
+    return (total & 7) == 0 ? (lid & 7) * (total >> 3) + (lid >> 3) : lid;
+}
+__device__ __forceinline__ void tile_in(int t, int tiles_m, int tiles_n, int& tm, int& tn) {
     constexpr int GM = 4;
     const int per_group = GM * tiles_n;
     const int grp = t / per_group;
@@ -420,6 +417,12 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& 
     const int r = t - grp * per_group;
     tm = first + r % gm;
     tn = r / gm;
+}
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn, int& by) {
+    const int nt = tiles_m * tiles_n;
+    const int lid = xcd_order((int)blockIdx.y * nt + (int)blockIdx.x, nt * (int)gridDim.y);
+    by = lid / nt;
+    tile_in(lid - by * nt, tiles_m, tiles_n, tm, tn);
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH, bool AKC, bool BKC>
@@ -1447,7 +1450,7 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
 // tile of the output and reads fewer fragments per MFMA; the groups' fp32
 // partial tiles are added through LDS before the stores.
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG>
-__global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
+__device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int by) {
     constexpr int NT = 64 * WGM * WGN * KG, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
     constexpr int NQ = BKS / 16;  // 16-wide k slices per step
     constexpr int NQL = NQ / KG;  // of them, the slices of one wave
@@ -1464,9 +1467,6 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int kg = wave / (WGM * WGN), wl = wave - kg * (WGM * WGN);
     const int wm = wl / WGN, wn = wl % WGN;
-    int tm, tn;
-    int by;
-    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
     const int m0 = tm * BM, n0 = tn * BN;
     const int splits = g.splits > 1 ? g.splits : 1;
     const uint32_t z = (uint32_t)by / splits;
@@ -1594,6 +1594,31 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
         if (kg == 0) take(mine, std::integral_constant<int, 0>{});
         else take(mine, std::integral_constant<int, FH>{});
         lean_epilogue<T, FH, FN>(g, half, mw + kg * FH * 32, nw, z, sidx, splits);
+    }
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG>
+__global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
+    int tm, tn, by;
+    tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
+    lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, KG>(g, tm, tn, by);
+}
+
+// Two unbatched, unsplit contractions in one launch: blocks (renumbered
+// over the 8 XCDs as a whole) below g0's tile count take g0's tiles, the
+// rest g1's, so two contractions that each leave CUs idle fill the chip
+// together.
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean_pair(GemmArgs g0, GemmArgs g1) {
+    const int n0 = g0.tiles_m * g0.tiles_n, total = n0 + g1.tiles_m * g1.tiles_n;
+    const int lid = xcd_order((int)blockIdx.x, total);
+    int tm, tn;
+    if (lid < n0) {
+        tile_in(lid, g0.tiles_m, g0.tiles_n, tm, tn);
+        lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, 1>(g0, tm, tn, 0);
+    } else {
+        tile_in(lid - n0, g1.tiles_m, g1.tiles_n, tm, tn);
+        lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, 1>(g1, tm, tn, 0);
     }
 }
 
@@ -1757,6 +1782,20 @@ void launch_lean(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, KG>), grid, block, 0, st, g);
     else
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, KG>), grid, block, 0, st, g);
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+void launch_lean_pair(const GemmArgs& g0, const GemmArgs& g1, hipStream_t st) {
+    dim3 grid(g0.tiles_m * g0.tiles_n + g1.tiles_m * g1.tiles_n);
+    dim3 block(64 * WGM * WGN);
+    if (g0.a.kcontig && g0.b.kcontig)
+        hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, true, true>), grid, block, 0, st, g0, g1);
+    else if (g0.a.kcontig)
+        hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, true, false>), grid, block, 0, st, g0, g1);
+    else if (g0.b.kcontig)
+        hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, false, true>), grid, block, 0, st, g0, g1);
+    else
+        hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, false, false>), grid, block, 0, st, g0, g1);
 }
 
 template <typename T, int WGM, int WGN>
@@ -1925,6 +1964,25 @@ int plan_log_copy(dm_contract_choice* out, int cap) {
     return (int)g_log.size();
 }
 
+// Validation, plan and configuration of a 16-bit contraction; `pair`: when
+// no plan entry fixes the configuration, ask for the lean 128x128 kernel
+// unsplit (what a paired launch runs).
+int prepare(GemmArgs& g, int dtype, bool pair) {
+    if (g.K % 8 || g.M % 8 || g.N % 8)
+        return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
+    if (g.c.bias[0] && ((g.c.bias_on_m != 0) == (g.c.contig_n == 0)) && g.c.bias_map.r0 % 8 != 0)
+        return set_error(DM_ERR_UNSUPPORTED, "bias map radix along the output vector must be a multiple of 8");
+    if (!g.split_ws) g.splits = 1;
+    set_affine(g);
+    if (g.cfg < 0) apply_plan(g, dtype);
+    if (pair && g.cfg < 0) { g.cfg = 15; g.splits = 1; }
+    choose(g);
+    if (g.splits > 1 && (int64_t)g.splits * g.batch * g.M * g.N > g.split_cap)
+        return set_error(DM_ERR_WORKSPACE, "split-k scratch too small");
+    if ((int64_t)g.batch * g.splits > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction grid too large");
+    return 0;
+}
+
 int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     GemmArgs g = args;
     if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
@@ -1940,17 +1998,7 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
         g.cfg = -1;
         log_launch(g, dtype);
     } else {
-        if (g.K % 8 || g.M % 8 || g.N % 8)
-            return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
-        if (g.c.bias[0] && ((g.c.bias_on_m != 0) == (g.c.contig_n == 0)) && g.c.bias_map.r0 % 8 != 0)
-            return set_error(DM_ERR_UNSUPPORTED, "bias map radix along the output vector must be a multiple of 8");
-        if (!g.split_ws) g.splits = 1;
-        set_affine(g);
-        if (g.cfg < 0) apply_plan(g, dtype);
-        choose(g);
-        if (g.splits > 1 && (int64_t)g.splits * g.batch * g.M * g.N > g.split_cap)
-            return set_error(DM_ERR_WORKSPACE, "split-k scratch too small");
-        if ((int64_t)g.batch * g.splits > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction grid too large");
+        if (int rc = prepare(g, dtype, false)) return rc;
         if (dtype == G_F16) launch_t<half_t>(g, st);
         else launch_t<bf16_t>(g, st);
         log_launch(g, dtype);
@@ -1958,6 +2006,29 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return set_error(DM_ERR_DEVICE, "contraction launch: %s", hipGetErrorString(err));
     return 0;
+}
+
+int launch_gemm_pair(int dtype, const GemmArgs& x0, const GemmArgs& x1, hipStream_t st) {
+    constexpr int64_t CUS = 256;
+    if (dtype != G_F32 && x0.batch == 1 && x1.batch == 1 && x0.M > 0 && x0.N > 0 && x0.K > 0 && x1.M > 0 &&
+        x1.N > 0 && x1.K > 0 && x0.a.kcontig == x1.a.kcontig && x0.b.kcontig == x1.b.kcontig) {
+        GemmArgs g0 = x0, g1 = x1;
+        if (int rc = prepare(g0, dtype, true)) return rc;
+        if (int rc = prepare(g1, dtype, true)) return rc;
+        if (g0.cfg == 15 && g1.cfg == 15 && g0.splits == 1 && g1.splits == 1 &&
+            (int64_t)g0.tiles_m * g0.tiles_n + (int64_t)g1.tiles_m * g1.tiles_n <= CUS) {
+            if (dtype == G_F16) launch_lean_pair<half_t, 128, 128, 2, 4, 64, 4>(g0, g1, st);
+            else launch_lean_pair<bf16_t, 128, 128, 2, 4, 64, 4>(g0, g1, st);
+            log_launch(g0, dtype);
+            log_launch(g1, dtype);
+            hipError_t err = hipGetLastError();
+            if (err != hipSuccess) return set_error(DM_ERR_DEVICE, "contraction launch: %s", hipGetErrorString(err));
+            return 0;
+        }
+    }
+    if (int rc = launch_gemm(dtype, x0, st)) return rc;
+    trace_next("2");
+    return launch_gemm(dtype, x1, st);
 }
 
 }  // namespace dm

@@ -103,5 +103,9 @@ enum GemmDtype { G_F32 = 0, G_F16 = 1, G_BF16 = 2 };
 // Validates and launches one contraction; returns 0 on success, else a
 // message is stored for dm_last_error and a nonzero code returned.
 int launch_gemm(int dtype, const GemmArgs& args, hipStream_t stream);
+// Two contractions in one launch when both take the lean 128x128 kernel
+// unsplit with the same operand contiguity and their tiles together fit one
+// block per CU; otherwise launch_gemm on each, in order.
+int launch_gemm_pair(int dtype, const GemmArgs& a, const GemmArgs& b, hipStream_t stream);
 
 }  // namespace dm

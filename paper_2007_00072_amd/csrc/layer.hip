@@ -421,6 +421,15 @@ int out_projection(const Dims& x, const void* gamma, const void* wo, const void*
 // Backward of attention from d(out) (layout `layout`) down to the gradients
 // of Q, K, V (written token-major into dq/dk/dv at row strides ldq/ldk/ldv),
 // plus dwo.
+// Out dW: dwo[w][h][i] = sum_t gamma[t][(h,w)] dout(t,i)
+GemmArgs out_dw_args(const Dims& x, const void* gamma, const void* dout, int layout, float* dwo) {
+    const int64_t HW = x.H * x.W, I = x.I;
+    return gemm(HW, I, x.Tq, 1, opnd(gamma, false, linear_map(HW)), act_kn(dout, layout, x.Tq, I),
+                epi(dwo, make_map((uint32_t)x.W, 0, x.H * I, I, 0), linear_map(1), true, true));
+}
+
+// dwo == nullptr: the caller launches the output-projection weight gradient
+// itself (the encoder pairs it with the Q/K/V weight gradient).
 int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const void* dout, int layout,
                        const void* q, const void* k, const void* v, const void* prob, const void* alpha,
                        const void* gamma, const void* wo, float* dwo, void* dgamma, void* dalpha, void* dbeta,
@@ -434,14 +443,11 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
                             epi(dgamma, linear_map(HW), linear_map(1), true, false)),
                        st));
     t11.stop();
-    // Out dW: dwo[w][h][i] = sum_t gamma[t][(h,w)] dout(t,i)
-    TraceScope t12("B12 out_dw", st);
-    DM_TRY(launch_gemm(x.dtype,
-                       gemm(HW, I, x.Tq, 1, opnd(gamma, false, linear_map(HW)), act_kn(dout, layout, x.Tq, I),
-                            epi(dwo, make_map((uint32_t)W, 0, H * I, I, 0), linear_map(1), true, true)),
-                       st));
+    if (dwo) {
+        TraceScope t12("B12 out_dw", st);
+        DM_TRY(launch_gemm(x.dtype, out_dw_args(x, gamma, dout, layout, dwo), st));
+    }
     const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
-    t12.stop();
     const int path = g_attn_path.load(std::memory_order_relaxed);
     const bool fused = path != 1 && attn_fused_ok(x.dtype, (int)K, (int)W);
     AttnNext nq;
@@ -526,9 +532,11 @@ int project_bwd(const Dims& x, int layout, const void* in, int64_t T, int64_t n,
 // `resid`, later ones add the dX written so far, each output element read
 // and written by the same thread) and d[Wq Wk Wv][segments] = dstk[:,
 // segments]^T X.
+// pair: a further contraction launched together with the first group's
+// weight gradient (one launch when both fit the chip at once).
 int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, const void* dstk, int nseg, int seg0,
                         const ProjGroup* grp, int n, const dm_layer_params* prm, void* dx, const dm_layer_grads* g,
-                        const void* resid, hipStream_t st) {
+                        const void* resid, hipStream_t st, const GemmArgs* pair = nullptr) {
     const int64_t H = x.H, I = x.I, P = x.P, HP = H * P, ld = nseg * HP;
     const IdxMap wmap = make_map((uint32_t)P, (uint32_t)H, H * I, I, 0);
     const void* w[3] = {prm->wq, prm->wk, prm->wv};
@@ -547,7 +555,7 @@ int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, co
             DM_TRY(launch_gemm(x.dtype, gemm(T, I, ns * HP, 1, opnd(a, true, linear_map(ld)), Bw, c), st));
         }
     }
-    TraceScope t_("B19 qkv_dw", st);
+    TraceScope t_(pair ? "B12+19 out_dw+qkv_dw" : "B19 qkv_dw", st);
     for (int i = 0; i < n; ++i) {
         const int s0 = grp[i].s0, ns = grp[i].s1 - grp[i].s0;
         if (i > 0) trace_next(grp[i].sub);
@@ -555,19 +563,20 @@ int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, co
         for (int j = 0; j < ns; ++j) cw.ptr[j] = dw[s0 + j];
         cw.nseg = ns; cw.seg_on_m = 1;
         const void* a = B8(dstk, (size_t)x.es * (s0 - seg0) * HP);
-        DM_TRY(launch_gemm(x.dtype,
-                           gemm(ns * HP, I, T, 1, opnd(a, false, linear_map(ld)), act_kn(in, layout, T, I), cw),
-                           st));
+        const GemmArgs gw = gemm(ns * HP, I, T, 1, opnd(a, false, linear_map(ld)), act_kn(in, layout, T, I), cw);
+        if (i == 0 && pair) DM_TRY(launch_gemm_pair(x.dtype, gw, *pair, st));
+        else DM_TRY(launch_gemm(x.dtype, gw, st));
     }
     return DM_OK;
 }
 
 // Backward of project_fused on the token-major [T][3][H][P] gradient.
 int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqkv, const dm_layer_params* prm,
-                      void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st) {
+                      void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st,
+                      const GemmArgs* pair = nullptr) {
     ProjGroup grp[3];
     const int n = proj_groups(x.qkv_fusion, grp);
-    return project_stacked_bwd(x, layout, in, x.Tq, dqkv, 3, 0, grp, n, prm, dx, g, resid, st);
+    return project_stacked_bwd(x, layout, in, x.Tq, dqkv, 3, 0, grp, n, prm, dx, g, resid, st, pair);
 }
 
 }  // namespace
@@ -770,11 +779,14 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     DM_TRY(check_launch("LayerNorm-1 backward"));
     // attention backward into the token-major [T][3][H][P] gradient
     const int64_t ld = 3 * I;
+    // (the output-projection weight gradient waits for the Q/K/V weight
+    // gradient: the two contractions share one launch)
     DM_TRY(attention_core_bwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), dAO, DM_BJI, q, k, v,
-                              prob, alpha, gamma, prm->wo, g->dwo, dgamma, dalpha, dbeta, dqkv, ld,
+                              prob, alpha, gamma, prm->wo, nullptr, dgamma, dalpha, dbeta, dqkv, ld,
                               B8(dqkv, (size_t)es * I), ld, B8(dqkv, (size_t)es * 2 * I), ld, st));
-    // Q, K, V dX (fused) + encoder-input residual; Q, K, V dW (fused)
-    DM_TRY(project_fused_bwd(x, DM_BJI, x_in, dqkv, prm, dx, g, dS1, st));
+    // Q, K, V dX (fused) + encoder-input residual; Q, K, V dW (fused) with Out dW
+    const GemmArgs out_dw = out_dw_args(x, gamma, dAO, DM_BJI, g->dwo);
+    DM_TRY(project_fused_bwd(x, DM_BJI, x_in, dqkv, prm, dx, g, dS1, st, &out_dw));
     // input-bias grads
     {
         TraceScope t20("B20 qkv_bias_grad", st);

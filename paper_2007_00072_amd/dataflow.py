@@ -52,6 +52,9 @@ REPLACES = {
     "B13-15 gamma_dx1_softmax_bwd": ("B13 gamma_dx1", "B15 softmax_bwd"),
     "B13+15+16 score_bwd_dq": ("B13 gamma_dx1", "B15 softmax_bwd", "B16 qkt_dx1"),
 }
+# Contractions the encoder layer issues as one launch (their tiles together
+# fill the chip): the backward's output-projection and Q/K/V weight gradients.
+PAIRED = {"B12+19 out_dw+qkv_dw": ("B12 out_dw", "B19 qkv_dw")}
 # The launch sets one layer can run: every score step separate, scores on
 # chip, and scores on chip with the next contraction in the same launch.
 PATHS = {
@@ -64,7 +67,7 @@ PATHS = {
 def path_groups(w: Dict[str, "Work"], path: str) -> Dict[str, "Work"]:
     """The launch groups of `w` that path `path` runs."""
     fused = PATHS[path]
-    gone = {p for f in fused for p in REPLACES[f]}
+    gone = {p for f in fused for p in REPLACES[f]} | {p for parts in PAIRED.values() for p in parts}
     return {k: v for k, v in w.items() if (k not in REPLACES or k in fused) and k not in gone}
 
 
@@ -116,6 +119,8 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read
     w["B19 qkv_dw"] = g(3 * I, I, T, 3 * N, N, 3 * I * I, c_es=4)
+    for lab, parts in PAIRED.items():
+        w[lab] = Work(sum(w[p].flop for p in parts), sum(w[p].bytes for p in parts), "mfma", "contraction")
     w["B20 qkv_bias_grad"] = m(3 * N * es + 3 * I * 4)
     # column-sum partials of B1-2, B5, B8-10 and B20 finished in one launch
     w["B colsum finish"] = m(0)

@@ -29,12 +29,14 @@ def short_name(sym: str) -> str:
         dt = "f16" if m.group(1) == "DF16_" else "bf16"
         mode = lambda b: "k" if b == "1" else "o"
         return f"gemm_dma<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},A:{mode(m.group(6))},B:{mode(m.group(7))}>"
-    m = re.search(r"gemm_leanI(DF16_|DF16b)Li(\d+)ELi(\d+)ELi(\d)ELi(\d)ELi(\d+)ELi(\d)ELb(\d)ELb(\d)", sym)
+    m = re.search(r"gemm_lean(_pair)?I(DF16_|DF16b)Li(\d+)ELi(\d+)ELi(\d)ELi(\d)ELi(\d+)ELi(\d)ELb(\d)ELb(\d)"
+                  r"(?:ELi(\d))?", sym)
     if m:
-        dt = "f16" if m.group(1) == "DF16_" else "bf16"
+        dt = "f16" if m.group(2) == "DF16_" else "bf16"
         mode = lambda b: "k" if b == "1" else "o"
-        return (f"gemm_lean<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},bk {m.group(6)},"
-                f"A:{mode(m.group(8))},B:{mode(m.group(9))}>")
+        kg = f",k groups {m.group(11)}" if m.group(11) and m.group(11) != "1" else ""
+        return (f"gemm_lean{m.group(1) or ''}<{dt},{m.group(3)}x{m.group(4)},waves {m.group(5)}x{m.group(6)},"
+                f"bk {m.group(7)}{kg},A:{mode(m.group(9))},B:{mode(m.group(10))}>")
     m = re.search(r"gemm_(x32|big)I(DF16_|DF16b)", sym)
     if m:
         return f"gemm_{m.group(1)}<{'f16' if m.group(2) == 'DF16_' else 'bf16'}>"

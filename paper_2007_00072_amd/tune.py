@@ -320,7 +320,11 @@ def fusion_table(workload: str, reps: int = 3, shape=None):
         for _ in range(10):
             L.step()
         tm = L.timed(max(reps, 10))
-        out[f] = {"forward": tm.get("F1 qkv", 0.0), "backward": tm.get("B18 qkv_dx", 0.0) + tm.get("B19 qkv_dw", 0.0)}
+        # backward: dX and dW of the projections (the encoder launches the
+        # first group's dW together with the output projection's dW)
+        out[f] = {"forward": tm.get("F1 qkv", 0.0),
+                  "backward": tm.get("B18 qkv_dx", 0.0) + tm.get("B19 qkv_dw", 0.0) +
+                  tm.get("B12+19 out_dw+qkv_dw", 0.0)}
         del L
     return out
 

@@ -28,6 +28,9 @@ def test_layer_model_flops_consistent():
         assert sum(x.flop for x in groups.values()) / 1e9 == pytest.approx(table3, rel=1e-12), path
     assert "F4 gamma" in dataflow.path_groups(w, "scores")
     assert "F4 gamma" not in dataflow.path_groups(w, "scores_next")
+    for k, v in dataflow.PAIRED.items():
+        assert w[k].flop == sum(w[p].flop for p in v) and w[k].bytes == sum(w[p].bytes for p in v)
+        assert all(p not in dataflow.path_groups(w, "scores_next") for p in v)
     for k, v in dataflow.REPLACES.items():
         assert w[k].flop == sum(w[p].flop for p in v)
         assert w[k].cls == "fused"

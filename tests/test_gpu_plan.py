@@ -60,6 +60,26 @@ def test_plan_every_contraction_on_the_k_group_kernel():
     check_encoder(wl, layer=1)
 
 
+def test_weight_gradients_share_one_launch():
+    # the output-projection and Q/K/V weight gradients (both reduce over the
+    # tokens) run as one launch of the lean 128x128 kernel; a plan entry
+    # that gives one of them another kernel separates the launches again;
+    # parity either way
+    wl = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
+    lab = "B12+19 out_dw+qkv_dw"
+    recs, labels = _launches(wl)
+    pair = [r for r in recs if r.label.decode() == lab]
+    assert len(pair) == 2 and all((r.tile_cfg, r.splits) == (15, 1) for r in pair), pair
+    assert labels.count(lab) == 1
+    check_encoder(wl, layer=1)
+    out_dw = next(r for r in pair if r.M == wl.shape.H * wl.shape.W)
+    lib.plan_set([lib.ContractChoice(*out_dw.key(), 6, 1)], 0)
+    recs2, labels2 = _launches(wl)
+    assert labels2.count(lab) == 2   # two launches under the one label
+    assert any(r.label.decode() == lab and (r.tile_cfg, r.splits) == (6, 1) for r in recs2)
+    check_encoder(wl, layer=1)
+
+
 @pytest.mark.parametrize("path,fwd,bwd", [
     (1, ["F2 qkt", "F3 softmax", "F4 gamma"], ["B13 gamma_dx1", "B15 softmax_bwd", "B16 qkt_dx1"]),
     (2, ["F2-3 qkt_softmax", "F4 gamma"], ["B13-15 gamma_dx1_softmax_bwd", "B16 qkt_dx1"]),
