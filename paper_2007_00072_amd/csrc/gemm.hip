@@ -2015,8 +2015,12 @@ int launch_gemm_pair(int dtype, const GemmArgs& x0, const GemmArgs& x1, hipStrea
         GemmArgs g0 = x0, g1 = x1;
         if (int rc = prepare(g0, dtype, true)) return rc;
         if (int rc = prepare(g1, dtype, true)) return rc;
-        if (g0.cfg == 15 && g1.cfg == 15 && g0.splits == 1 && g1.splits == 1 &&
-            (int64_t)g0.tiles_m * g0.tiles_n + (int64_t)g1.tiles_m * g1.tiles_n <= CUS) {
+        // together the two fill the chip with one block per CU (fewer tiles
+        // would leave CUs idle for the whole reduction, where separate
+        // launches split it)
+        const int64_t tiles = (int64_t)g0.tiles_m * g0.tiles_n + (int64_t)g1.tiles_m * g1.tiles_n;
+        if (g0.cfg == 15 && g1.cfg == 15 && g0.splits == 1 && g1.splits == 1 && tiles >= CUS * 3 / 4 &&
+            tiles <= CUS) {
             if (dtype == G_F16) launch_lean_pair<half_t, 128, 128, 2, 4, 64, 4>(g0, g1, st);
             else launch_lean_pair<bf16_t, 128, 128, 2, 4, 64, 4>(g0, g1, st);
             log_launch(g0, dtype);

@@ -104,8 +104,9 @@ enum GemmDtype { G_F32 = 0, G_F16 = 1, G_BF16 = 2 };
 // message is stored for dm_last_error and a nonzero code returned.
 int launch_gemm(int dtype, const GemmArgs& args, hipStream_t stream);
 // Two contractions in one launch when both take the lean 128x128 kernel
-// unsplit with the same operand contiguity and their tiles together fit one
-// block per CU; otherwise launch_gemm on each, in order.
+// unsplit with the same operand contiguity and their tiles together give
+// between 3/4 of the CUs and all of them one block; otherwise launch_gemm on
+// each, in order.
 int launch_gemm_pair(int dtype, const GemmArgs& a, const GemmArgs& b, hipStream_t stream);
 
 }  // namespace dm

@@ -65,7 +65,8 @@ def test_weight_gradients_share_one_launch():
     # tokens) run as one launch of the lean 128x128 kernel; a plan entry
     # that gives one of them another kernel separates the launches again;
     # parity either way
-    wl = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
+    # (BERT-large widths: 192 + 64 tiles of 128 x 128, one per CU)
+    wl = small("bert_large_f16", B=1, J=128, K=128, H=16, P=64, W=64, I=1024, F=1024)
     lab = "B12+19 out_dw+qkv_dw"
     recs, labels = _launches(wl)
     pair = [r for r in recs if r.label.decode() == lab]
@@ -78,6 +79,11 @@ def test_weight_gradients_share_one_launch():
     assert labels2.count(lab) == 2   # two launches under the one label
     assert any(r.label.decode() == lab and (r.tile_cfg, r.splits) == (6, 1) for r in recs2)
     check_encoder(wl, layer=1)
+    # narrower layers (fewer tiles than 3/4 of the CUs) keep separate launches
+    lib.plan_set([], 0)
+    wl2 = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
+    recs3, labels3 = _launches(wl2)
+    assert labels3.count(lab) >= 2
 
 
 @pytest.mark.parametrize("path,fwd,bwd", [
