@@ -85,6 +85,25 @@ def cpu_baseline(wl, sample_b: int):
             "sample_seconds": round(dt, 2)}
 
 
+def copy_rate_gbs(torch, dev, reps: int = 10) -> float:
+    """HBM rate of a plain device-to-device copy of 1 GiB (read + write
+    bytes over time), the practical ceiling beside the 8 TB/s peak."""
+    n = 1 << 28
+    src = torch.empty(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    rate = 2.0 * 4 * n * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return rate
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -219,9 +238,11 @@ def main() -> int:
         achieved = dw.bytes / dom_s / 1e9
         peak = dataflow.HBM_PEAK_GBS
         unit = "GB/s"
+    copy_gbs = copy_rate_gbs(torch, dev)
     roof = {"bound": dw.bound, "kernel": dom["kernel"], "achieved": round(achieved, 1), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(dom["kernel"]),
-            "per_launch_us": dom["us"],
+            "per_launch_us": dom["us"], "copy_GBs": round(copy_gbs, 1),
+            "frac_of_copy": round(achieved / copy_gbs, 4) if unit == "GB/s" else None,
             "algorithmic_per_launch": dw.flop if dw.bound == "mfma" else dw.bytes}
     # operator classes; second launches (reduce / finish) count with their operator
     is_fused = lambda r: work.get(r["op"]) is not None and work[r["op"]].cls == "fused"
