@@ -3,13 +3,16 @@
     python -m paper_2007_00072_amd.build [--jobs N]
 
 Each .hip source is compiled separately with hipcc and the objects are
-linked into paper_2007_00072_amd/libdmtx.so.
+linked into paper_2007_00072_amd/libdmtx.so, which exports exactly the C
+functions that include/dmtx.h declares (a linker version script keeps
+everything else local).
 """
 from __future__ import annotations
 
 import argparse
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -20,6 +23,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdmtx.so")
 SOURCES = ["gemm.hip", "fused.hip", "attn.hip", "abi.hip", "layer.hip"]
+HEADER = os.path.join(ROOT, "include", "dmtx.h")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
@@ -49,12 +53,27 @@ def _compile(src: str) -> str:
     return obj
 
 
+def abi_names(header: str = HEADER) -> list:
+    """Names of the functions the C header declares (declarations start at
+    column 0 with a return type; comments and typedefs are skipped)."""
+    text = re.sub(r"/\*.*?\*/", "", open(header).read(), flags=re.S)
+    names = []
+    for ln in text.splitlines():
+        m = re.match(r"^(?:const\s+)?(?:int|int32_t|size_t|void|char)\s*\**\s*(\w+)\s*\(", ln)
+        if m:
+            names.append(m.group(1))
+    return names
+
+
 def build(jobs: int = 4, verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+    vscript = os.path.join(BUILD, "exports.map")
+    with open(vscript, "w") as f:
+        f.write("{\n  global:\n" + "".join(f"    {n};\n" for n in abi_names()) + "  local: *;\n};\n")
+    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,--version-script=" + vscript, "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

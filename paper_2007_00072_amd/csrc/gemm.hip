@@ -1967,7 +1967,7 @@ int plan_log_copy(dm_contract_choice* out, int cap) {
 // Validation, plan and configuration of a 16-bit contraction; `pair`: when
 // no plan entry fixes the configuration, ask for the lean 128x128 kernel
 // unsplit (what a paired launch runs).
-int prepare(GemmArgs& g, int dtype, bool pair) {
+static int prepare(GemmArgs& g, int dtype, bool pair) {
     if (g.K % 8 || g.M % 8 || g.N % 8)
         return set_error(DM_ERR_UNSUPPORTED, "contraction sizes must be multiples of 8");
     if (g.c.bias[0] && ((g.c.bias_on_m != 0) == (g.c.contig_n == 0)) && g.c.bias_map.r0 % 8 != 0)

@@ -42,6 +42,22 @@ def test_library_exports_every_header_symbol(lib):
     assert sorted(lib.EXPORTED) == header_functions()
 
 
+def test_library_exports_nothing_else(lib):
+    # the version script keeps the C++ internals local: the dynamic symbol
+    # table defines exactly the header's functions (read with binutils' nm
+    # on this repository's own build)
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--defined-only", lib.LIB_PATH], capture_output=True, text=True, check=True)
+    funcs = sorted(ln.split()[-1] for ln in out.stdout.splitlines() if ln.split()[-2:-1] == ["T"])
+    assert funcs == header_functions()
+    from paper_2007_00072_amd.build import abi_names
+    assert sorted(abi_names()) == header_functions()
+
+
 def _desc(lib, **kw):
     from paper_2007_00072_amd.inputs import WORKLOADS
     d = lib.make_desc(WORKLOADS["bert_large_f16"].shape, "f16", p_attn=0.1, p_attn_out=0.1, p_ffn_out=0.1)
