@@ -126,3 +126,15 @@ def test_tuner_end_to_end(tmp_path):
     assert plan["attn_path"] == res["attn_path"]
     wl = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
     check_encoder(wl, layer=0)
+
+
+def test_saved_bert_base_plan_keeps_parity():
+    # the tuned BERT-base plan (weight gradients split on the 256x256
+    # kernel, dV/dK on the register-staged tile) at its full size
+    import os
+    from paper_2007_00072_amd.inputs import WORKLOADS
+    path = os.path.join(os.path.dirname(tune.__file__), "plans", "bert_base_bf16.json")
+    tune.load_plan(path)
+    recs, _ = _launches(WORKLOADS["bert_base_bf16"])
+    assert any((r.tile_cfg, r.splits) == (13, 4) for r in recs)
+    check_encoder(WORKLOADS["bert_base_bf16"])

@@ -61,3 +61,23 @@ def test_shortest_path_rejects_negative_weights():
     with pytest.raises(ValueError):
         tune.shortest_path(2, [(0, 1, -1.0, None)], 0, 1)
     assert tune.shortest_path(3, [(0, 1, 1.0, "e")], 0, 2) == (math.inf, [])
+
+
+def test_saved_plans_are_well_formed():
+    # every plan shipped with the package names a known workload and only
+    # valid configurations (what plan_set accepts)
+    import glob
+    import json
+    import os
+    from paper_2007_00072_amd.inputs import WORKLOADS
+    plans = glob.glob(os.path.join(os.path.dirname(tune.__file__), "plans", "*.json"))
+    assert len(plans) >= 2
+    for path in plans:
+        plan = json.load(open(path))
+        assert plan["workload"] in WORKLOADS, path
+        assert os.path.basename(path) == plan["workload"] + ".json"
+        assert 0 <= int(plan["attn_path"]) <= 3 and int(plan.get("qkv_fusion", 0)) in (0, 1, 2)
+        assert plan["entries"]
+        for e in plan["entries"]:
+            assert 0 <= e["tile_cfg"] <= 16 and 1 <= e["splits"] <= 64, (path, e)
+            assert e["M"] > 0 and e["N"] > 0 and e["K"] > 0 and e["batch"] >= 1
