@@ -625,6 +625,11 @@ __global__ __launch_bounds__(NTL) void ln_bwd_cs_k(LnBwdArgs a, int nblk) {
     constexpr int RPP = 64 / LG;       // rows per pass of one wave
     constexpr int NP = LN_TILE / RPP;  // passes per tile
     __shared__ float rowred[2][LN_TILE][NW][2];
+    // transposed copy of the tile's dsub (16-bit types): column c's LN_TILE
+    // rows at tb[c * LN_TILE ..], written out as 32-byte row pieces of
+    // dsub_t[c][t0 ..]
+    __shared__ __attribute__((aligned(16))) uint16_t tb[1024 * LN_TILE];
+    static_assert(LN_TILE == 16, "a tile column is written as two 16-byte pieces");
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int gi = lane / LG, v = lane % LG;
@@ -714,11 +719,45 @@ __global__ __launch_bounds__(NTL) void ln_bwd_cs_k(LnBwdArgs a, int nblk) {
             if (a.dsub) {
                 dropout8(a.dp, (uint64_t)off, o);
                 V8<T>::store(reinterpret_cast<T*>(a.dsub) + off, o);
+                if constexpr (sizeof(T) == 2) {
+                    if (a.dsub_t) {
+                        const int r = p * RPP + gi;  // row within the tile
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) tb[(c + q) * LN_TILE + r] = __builtin_bit_cast(uint16_t, from_f<T>(o[q]));
+                    }
+                }
                 if (do_part && a.want_dsub_sum) {
                     // sum the stored (rounded) values that later consumers see
 #pragma unroll
                     for (int q = 0; q < 8; ++q) p_dsub[q] += to_f(from_f<T>(o[q]));
                 }
+            }
+        }
+        if constexpr (sizeof(T) == 2) {
+            if (a.dsub_t && a.dsub && do_ds) {
+                // the tile's transposed dsub: each column's (up to) LN_TILE
+                // rows as one 32-byte piece of dsub_t[c][t0 ..] (rows and t0
+                // multiples of 8 keep the pieces 16-byte aligned); the last,
+                // partial tile element by element
+                __syncthreads();
+                const int nr = (int)min<int64_t>(LN_TILE, a.rows - t0);
+                uint16_t* dtr = reinterpret_cast<uint16_t*>(a.dsub_t);
+                if (nr == LN_TILE && (a.rows & 7) == 0) {
+                    // lanes 2i and 2i+1 store the two halves of one column's
+                    // 32 bytes, so each store instruction writes 32-byte runs
+                    for (int idx = (int)threadIdx.x; idx < 2 * cols; idx += NTL) {
+                        const int col = idx >> 1, h8 = (idx & 1) * 8;
+                        *reinterpret_cast<u32x4*>(dtr + (int64_t)col * a.rows + t0 + h8) =
+                            *reinterpret_cast<const u32x4*>(tb + col * LN_TILE + h8);
+                    }
+                } else {
+                    for (int col = (int)threadIdx.x; col < cols; col += NTL) {
+                        const uint16_t* src = tb + col * LN_TILE;
+                        uint16_t* dst = dtr + (int64_t)col * a.rows + t0;
+                        for (int r = 0; r < nr; ++r) dst[r] = src[r];
+                    }
+                }
+                __syncthreads();  // the next tile rewrites tb
             }
         }
     }

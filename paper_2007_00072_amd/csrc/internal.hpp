@@ -129,6 +129,7 @@ struct LnBwdArgs {
     void* dsub;
     float* part;  // null: no column sums
     int want_dsub_sum;
+    void* dsub_t;  // optional [cols][rows] copy of dsub (written when ln_bwd_split_ok(cols, dtype))
 };
 void run_ln_bwd(const LnBwdArgs& a, hipStream_t st);
 

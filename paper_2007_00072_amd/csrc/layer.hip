@@ -67,7 +67,7 @@ struct EncPlan {
     MhaPlan m;
     size_t xhat1, rstd1, y1, h, a, xhat2, rstd2, saved_total;
     size_t ao, o, fwd_split, fwd_total;
-    size_t dS2, dO, dA, dH, dY1f, dS1, dAO, bwd_split, bwd_total;
+    size_t dS2, dO, dOT, dA, dH, dY1f, dS1, dAO, bwd_split, bwd_total;
     size_t part_ln2, part_act, part_ln1;  // column partials finished together at the end of the backward
     int64_t split_floats;
 };
@@ -143,6 +143,7 @@ EncPlan plan_encoder(const Dims& x) {
     e.fwd_total = fw.total;
     e.dS2 = bw.take(es * x.N);
     e.dO = bw.take(es * x.N);
+    e.dOT = bw.take(es * x.N);  // dO transposed, [I][T]
     e.dA = bw.take(es * T * x.F);
     e.dH = bw.take(es * T * x.F);
     e.dY1f = bw.take(es * x.N);
@@ -725,6 +726,11 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     l2.dtype = dt; l2.rows = T; l2.cols = (int)I; l2.dya = dy; l2.xhat = xhat2; l2.gamma = prm->g2; l2.rstd = rstd2;
     l2.dp = make_drop(d->p_ffn_out, d->seed, 2, d->layer_id); l2.ds = dS2; l2.dsub = dO; l2.part = part_ln2;
     l2.want_dsub_sum = 1;
+    // the column-split LayerNorm backward also writes dO transposed, so the
+    // Linear-2 weight gradient reads one operand contiguous along the tokens
+    void* dOT = B8(ws, e.dOT);
+    const bool have_dOT = ln_bwd_split_ok((int)I, dt);
+    l2.dsub_t = have_dOT ? dOT : nullptr;
     {
         TraceScope t_("B1-2 ln2_bwd", st);
         run_ln_bwd(l2, st);
@@ -740,8 +746,9 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     }
     {
         TraceScope t_("B4 linear2_dw", st);
+        const Operand a_op = have_dOT ? opnd(dOT, true, linear_map(T)) : opnd(dO, false, linear_map(I));
         DM_TRY(launch_gemm(dt,
-                           gemm(I, F, T, 1, opnd(dO, false, linear_map(I)), opnd(abuf, false, linear_map(F)),
+                           gemm(I, F, T, 1, a_op, opnd(abuf, false, linear_map(F)),
                                 epi(g->dw2, linear_map(F), linear_map(1), true, true)),
                            st));
     }

@@ -98,7 +98,11 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["F9 linear2"] = g(T, I, F, Fh, I * F, N)
     w["F10 bdrln2"] = m(4 * N * es + 4 * T + 3 * I * es)
     # backward
-    w["B1-2 ln2_bwd"] = m(4 * N * es + 4 * T + I * es + 3 * I * 4)
+    # (+ dO transposed for the Linear-2 weight gradient where the
+    # column-split LayerNorm backward runs: 16-bit, I a multiple of 64 in
+    # 320..1024)
+    dot = N * es if es == 2 and I % 64 == 0 and 320 <= I <= 1024 else 0
+    w["B1-2 ln2_bwd"] = m(4 * N * es + 4 * T + I * es + 3 * I * 4 + dot)
     w["B3 linear2_dx"] = g(T, F, I, N, I * F, Fh)
     w["B4 linear2_dw"] = g(I, F, T, N, Fh, I * F, c_es=4)
     w["B5 act_bwd"] = m(3 * Fh * es + F * es + F * 4)

@@ -74,6 +74,13 @@ def test_encoder_reduced_ragged(name):
 
 
 @pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
+def test_encoder_transposed_grad_ragged_tile(name):
+    # 40 tokens: the LayerNorm-2 backward's transposed dO copy (read by the
+    # Linear-2 weight gradient) ends with a partial 8-row tile
+    check_encoder(small(name, B=1, J=40, K=40, H=6, P=64, W=64, I=384, F=768))
+
+
+@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
 def test_encoder_saved_tensors(name):
     wl = small(name, B=2, J=64, K=64, H=2, P=64, W=64, I=128, F=512)
     L, params, x, dy, y, dx = run_encoder(wl)
