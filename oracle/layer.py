@@ -194,35 +194,57 @@ def f64(t) -> np.ndarray:
     return np.asarray(t, dtype=np.float64)
 
 
-# --------------------------------------------------------- attention (Fig. 1a)
+# ------------------------------------------------------ attention (Fig. 1a)
 def mha_forward(q, k, v, prm: Dict[str, np.ndarray], cfg: Config, out_bias: bool = True):
-    """Multi-head attention on q [I,B,J], k [I,B,K], v [I,B,K] (Fig. 1a).
+    """Multi-head attention on q [I,B,J], k [I,B,K], v [I,B,K].
 
-    Returns (out [I,B,J], cache).  With out_bias=False the output bias bo
-    is left out (the encoder layer adds it in its bias/dropout/residual/
-    LayerNorm operator, Table 3)."""
+    Computed one sequence b and one head h at a time as plain matrix
+    products, from the index definitions of the attention (Fig. 1a): the
+    head's query, key and value rows are its slices of the projection
+    weights applied to the token vectors plus the input bias; the scores are
+    the scaled query-key dot products; the probabilities are their softmax
+    over the keys; the head's context is the dropped-out probabilities
+    times the value rows; the output sums every head's context through its
+    slice of the output weights.
+
+    Returns (out [I,B,J], cache); cached tensors are kept in the paper's
+    index orders (qq, kk [P,H,B,len], vv and gamma [W,H,B,len], beta, prob
+    and alpha [H,B,J,K]).  With out_bias=False the output bias bo is left
+    out (the encoder layer adds it in its bias/dropout/residual/LayerNorm
+    operator, Table 3)."""
     r = lambda x: store(x, cfg.store_dtype)
-    wq, wk, wv, wo = prm["wq"], prm["wk"], prm["wv"], prm["wo"]
-    # Q, K, V projections with the input bias (rows "Q, K, V" and "Input bias").
-    qq = r(contract("phi,ibj->phbj", wq, q) + prm["bq"][:, :, None, None])
-    kk = r(contract("phi,ibk->phbk", wk, k) + prm["bk"][:, :, None, None])
-    vv = r(contract("whi,ibk->whbk", wv, v) + prm["bv"][:, :, None, None])
-    # QK^T, scaled.
-    beta = r(cfg.s * contract("phbk,phbj->hbjk", kk, qq))
-    # Softmax over k (keys after the query masked out when causal), then
-    # dropout on the probabilities.
-    prob_x = softmax_k(beta, cfg.causal)
-    prob = r(prob_x)
-    m_attn = attn_dropout(cfg)
-    alpha = r(prob_x * m_attn)
-    # Gamma and Out.
-    gamma = r(contract("whbk,hbjk->whbj", vv, alpha))
-    out = contract("whi,whbj->ibj", wo, gamma)
+    B, J, K = q.shape[1], q.shape[2], k.shape[2]
+    H, P, W, I = cfg.H, cfg.P, cfg.W, q.shape[0]
+    m_attn = attn_dropout(cfg)                                  # [H,B,J,K]
+    causal_ok = np.tril(np.ones((J, K), dtype=bool)) if cfg.causal else None
+    head_q, head_k = np.empty((P, H, B, J)), np.empty((P, H, B, K))
+    head_v, ctx = np.empty((W, H, B, K)), np.empty((W, H, B, J))
+    scores, probs, dropped = np.empty((H, B, J, K)), np.empty((H, B, J, K)), np.empty((H, B, J, K))
+    out = np.zeros((I, B, J))
+    for b in range(B):
+        tq, tk, tv = q[:, b, :].T, k[:, b, :].T, v[:, b, :].T   # token vectors, [len, I]
+        for h in range(H):
+            # rows "Q, K, V" and "Input bias" of Table 3
+            Qh = r(tq @ prm["wq"][:, h, :].T + prm["bq"][:, h])    # [J, P]
+            Kh = r(tk @ prm["wk"][:, h, :].T + prm["bk"][:, h])    # [K, P]
+            Vh = r(tv @ prm["wv"][:, h, :].T + prm["bv"][:, h])    # [K, W]
+            Sh = r(cfg.s * (Qh @ Kh.T))                             # [J, K]
+            if causal_ok is not None:
+                Sh_m = np.where(causal_ok, Sh, -np.inf)
+            else:
+                Sh_m = Sh
+            e = np.exp(Sh_m - Sh_m.max(axis=1, keepdims=True))
+            Ph = e / e.sum(axis=1, keepdims=True)                  # softmax over the keys
+            Ah = r(Ph * m_attn[h, b])                              # dropout of the probabilities
+            Ch = r(Ah @ Vh)                                         # [J, W]
+            out[:, b, :] += (Ch @ prm["wo"][:, h, :]).T             # the head's share of Out
+            head_q[:, h, b, :], head_k[:, h, b, :], head_v[:, h, b, :] = Qh.T, Kh.T, Vh.T
+            scores[h, b], probs[h, b], dropped[h, b], ctx[:, h, b, :] = Sh, r(Ph), Ah, Ch.T
     if out_bias:
         out = out + prm["bo"][:, None, None]
     out = r(out)
-    cache = dict(q=q, k=k, v=v, qq=qq, kk=kk, vv=vv, beta=beta, prob=prob,
-                 m_attn=m_attn, alpha=alpha, gamma=gamma)
+    cache = dict(q=q, k=k, v=v, qq=head_q, kk=head_k, vv=head_v, beta=scores, prob=probs,
+                 m_attn=m_attn, alpha=dropped, gamma=ctx)
     return out, cache
 
 
