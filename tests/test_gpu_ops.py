@@ -43,6 +43,25 @@ def test_dropout_mask_bit_exact(lib, site, layer, p, seed, offset):
     np.testing.assert_array_equal(got, ref)
 
 
+@pytest.mark.parametrize("p", [1e-20, 2.0 ** -33, 2.0 ** -24])
+def test_dropout_mask_tiny_p(lib, p):
+    # 1e-20: 1 - p rounds to 1 in double, so the threshold is 2^32 and every
+    # element is kept; 2^-33: threshold 2^32 - 1, only the all-ones word drops
+    n = 1 << 16
+    out = torch.empty(n, dtype=torch.uint8, device=DEV)
+    lib.dropout_mask(3, 1, 2, p, 0, n, out)
+    np.testing.assert_array_equal(out.cpu().numpy().astype(bool), philox.keep_mask(3, 1, 2, p, n))
+    if p == 1e-20:
+        x = make_tensor((16, 64), "f16", 7)
+        ys = []
+        for pp in (0.0, p):
+            y = torch.empty((16, 64), dtype=x.dtype, device=DEV)
+            lib.bias_act_fwd(DT["f16"], 16, 64, dev(x), dev(make_tensor((64,), "f16", 8)), 1, (pp, 3, 0, 5), y)
+            ys.append(y)
+        torch.cuda.synchronize()
+        assert torch.equal(ys[0], ys[1])
+
+
 def test_dropout_mask_p0_all_ones(lib):
     out = torch.zeros(1024, dtype=torch.uint8, device=DEV)
     lib.dropout_mask(1, 0, 0, 0.0, 0, 1024, out)
@@ -69,7 +88,7 @@ def test_bdrln_fwd(lib, dt, rows, cols):
     xhat, rstd = OL.layernorm_i(s.T, 1e-5)
     ref_y = rnd(f64(g)[:, None] * xhat + f64(be)[:, None], dt).T
     assert_close("y", y, ref_y, dt)
-    assert_close("xhat", xh, rnd(xhat, dt).T, dt, scale=4.0)
+    assert_close("xhat", xh, rnd(xhat, dt).T, dt)
     assert_close("rstd", rs, rstd, "f32" if dt == "f32" else dt)
 
 
@@ -140,9 +159,9 @@ def test_ln_dropout_bwd(lib, dt, rows, cols):
     lib.ln_dropout_bwd(DT[dt], rows, cols, dev(dy), dev(xh), dev(g), dev(rs), (0.1, 2, 0, 3), ds, dsub)
     torch.cuda.synchronize()
     ref = OL.layernorm_i_bwd(f64(dy).T[:, :, None], f64(xh).T[:, :, None], f64(rs)[:, None], f64(g))[:, :, 0].T
-    assert_close("ds", ds, rnd(ref, dt), dt, scale=float(np.abs(ref).max()))
+    assert_close("ds", ds, rnd(ref, dt), dt)
     ref_sub = rnd(ref, dt) * philox.dropout_factor(3, 2, 0, 0.1, (rows, cols))
-    assert_close("dsub", dsub, rnd(ref_sub, dt), dt, scale=float(np.abs(ref).max()))
+    assert_close("dsub", dsub, rnd(ref_sub, dt), dt)
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
@@ -270,9 +289,8 @@ def _contract_case(lib, dt, a_trans, b_trans, batch, M, N, K, cfg=-1, splits=0):
     a = f64(A).transpose(0, 2, 1) if a_trans else f64(A)
     b = f64(B).transpose(0, 2, 1) if b_trans else f64(B)
     ref = np.matmul(a, b)
-    scale = float(np.sqrt(K))
-    assert_close("C", C, rnd(0.5 * ref + f64(bias), dt), dt, scale=scale)
-    assert_close("Cf", Cf, ref, "f32" if dt == "f32" else dt, scale=scale)
+    assert_close("C", C, rnd(0.5 * ref + f64(bias), dt), dt)
+    assert_close("Cf", Cf, ref, "f32" if dt == "f32" else dt)
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
