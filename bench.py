@@ -134,16 +134,15 @@ def main() -> int:
     s = wl.shape
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    plan_name = "built-in"
+    plan_name, plan, cplan = "built-in", {}, None
     if a.plan:
         from paper_2007_00072_amd.tune import load_plan
-        plan = load_plan(a.plan)
+        plan, cplan = load_plan(a.plan)
         if plan.get("workload") != wl.name:
             print(json.dumps({"error": f"plan {a.plan} was tuned for {plan.get('workload')}, not {wl.name}"}))
             return 2
         plan_name = os.path.basename(a.plan)
-    layer = EncoderLayer(desc_for(wl, qkv_fusion=int(plan.get("qkv_fusion", 0)) if a.plan else 0),
-                         make_params(wl), dev)
+    layer = EncoderLayer(desc_for(wl, qkv_fusion=int(plan.get("qkv_fusion", 0)), plan=cplan), make_params(wl), dev)
     x = make_activation(wl, 0).to(dev)
     dy = make_activation(wl, 1).to(dev)
     y = torch.empty_like(x)

@@ -23,6 +23,10 @@
  *    of 8.  dm_last_error() describes the last failure of the calling thread.
  *  - Parameter gradients are float32 and are overwritten, not accumulated.
  *  - Outputs must not alias inputs.
+ *  - Calls are thread-safe.  The library keeps no mutable process-wide
+ *    state: configuration plans are immutable objects named by each call's
+ *    descriptor, and the optional launch records (plan_log, dm_trace_*)
+ *    belong to the calling thread.
  *  - Dropout masks are never stored: each is regenerated from a
  *    counter-based generator (Philox4x32-10, Salmon et al., SC'11) as a
  *    function of (seed, site, layer, logical element index), so a mask is
@@ -58,6 +62,11 @@ typedef enum { DM_BJI = 0, DM_IBJ = 1 } dm_layout;
 
 typedef enum { DM_GELU = 0, DM_RELU = 1 } dm_act;
 
+/* Configuration plan (opaque, host memory; see plan_create).  A layer or
+ * attention call uses the plan its descriptor points to; NULL selects the
+ * library's built-in choices. */
+typedef struct dm_plan dm_plan;
+
 /* Layer description.  Encoder layer: I == H*P, W == P, J == K, layout BJI.
  * Attention only: any J, K; layout BJI or IBJ. */
 typedef struct {
@@ -81,6 +90,8 @@ typedef struct {
     int32_t qkv_fusion;      /* self-attention input projections (Sec. "Algebraic Fusion")*/
                              /* 0: [Wq Wk Wv] X as one contraction each way; 1: [Wq Wk] X */
                              /* and Wv X; 2: three separate contractions                   */
+    const dm_plan* plan;     /* configuration plan (plan_create), read during the call    */
+                             /* only; NULL = built-in choices                              */
 } dm_layer_desc;
 
 /* Parameters in the paper's index order (Fig. 1a), row-major, dtype of the
@@ -288,26 +299,30 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
  * The configuration-selection step (Sec. "Configuration Selection"): the
  * layer and attention entry points choose each contraction's kernel, tile
  * and split factor from its shape, and the attention-score steps' launch
- * grouping by itself; a plan replaces those choices.  A contraction is
- * identified by its sizes, dtype and which operands are contiguous along
- * the contraction index (dm_contract_choice without the label); a plan
- * entry sets its tile_cfg (0..16, as for contract) and split factor (1 =
- * none; larger values are cut to what the call's split-k scratch holds).
- * Entries that a contraction's operands or epilogue do not allow fall back
- * the way contract's tile_cfg does, so a plan never changes results beyond
- * the order of the fp32 accumulation.  attn_path: 0 = automatic, 1 = QK^T,
- * softmax + dropout and Gamma (and their backward steps) as separate
- * launches, 2 = scores kept on chip (QK^T with softmax + dropout, Gamma dX1
- * with its backward), 3 = as 2 with Gamma and QK^T dX1 in the same
- * launches; a grouping a shape does not allow falls back to the next
- * smaller one.  plan_set(NULL, 0, 0) restores the built-in choices.  The
- * plan is process-wide: set it while no layer call is being enqueued.
+ * grouping by itself; a plan replaces those choices for the calls whose
+ * descriptor names it.  A contraction is identified by its sizes, dtype and
+ * which operands are contiguous along the contraction index
+ * (dm_contract_choice without the label); a plan entry sets its tile_cfg
+ * (0..16, as for contract) and split factor (1 = none; larger values are cut
+ * to what the call's split-k scratch holds).  Entries that a contraction's
+ * operands or epilogue do not allow fall back the way contract's tile_cfg
+ * does, so a plan never changes results beyond the order of the fp32
+ * accumulation.  attn_path: 0 = automatic, 1 = QK^T, softmax + dropout and
+ * Gamma (and their backward steps) as separate launches, 2 = scores kept on
+ * chip (QK^T with softmax + dropout, Gamma dX1 with its backward), 3 = as 2
+ * with Gamma and QK^T dX1 in the same launches; a grouping a shape does not
+ * allow falls back to the next smaller one.
  *
- * plan_log(1) clears and starts a record of the contractions the entry
- * points launch (sizes, dtype, operand contiguity, the tile_cfg and splits
- * that ran, and the kernel-timing label when timing is on); plan_log(0)
- * stops it; plan_log_read copies up to `cap` records and sets *count to
- * the number recorded. */
+ * plan_create copies the entries into a new immutable plan (host memory,
+ * owned by the caller until plan_destroy); it may be shared by any number
+ * of descriptors and threads.  Destroy a plan only when no call that names
+ * it is running.
+ *
+ * plan_log(1) clears and starts a record of the contractions the calling
+ * thread's layer and attention calls launch (sizes, dtype, operand
+ * contiguity, the tile_cfg and splits that ran, and the kernel-timing label
+ * when timing is on); plan_log(0) stops it; plan_log_read copies up to `cap`
+ * records of the calling thread and sets *count to the number recorded. */
 typedef struct {
     int64_t M, N, K, batch;        /* contraction sizes; batch: contractions in one launch */
     int32_t dtype;                 /* dm_dtype                                             */
@@ -316,7 +331,8 @@ typedef struct {
     int32_t splits;                /* split-k factor, 1 = none                             */
     char label[48];                /* log only: kernel-timing label, "" when timing is off */
 } dm_contract_choice;
-int plan_set(const dm_contract_choice* entries, int32_t n, int32_t attn_path);
+int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path, dm_plan** plan);
+int plan_destroy(dm_plan* plan);
 int plan_log(int32_t on);
 int plan_log_read(dm_contract_choice* out, int32_t cap, int32_t* count);
 
@@ -330,8 +346,8 @@ int plan_log_read(dm_contract_choice* out, int32_t cap, int32_t* count);
  * records per launch; leave it off outside measurement.
  * dm_trace_enable(1) clears earlier records; dm_trace_get waits for the
  * i-th record to complete and returns its label and sub-label (static
- * storage) and its duration in milliseconds.  Not for concurrent use from
- * several threads. */
+ * storage) and its duration in milliseconds.  Switch, records and events
+ * belong to the calling thread: each thread times its own calls. */
 int dm_trace_enable(int32_t on);
 int32_t dm_trace_count(void);
 int dm_trace_get(int32_t i, const char** label, const char** sub, float* ms);

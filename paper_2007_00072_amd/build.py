@@ -40,8 +40,17 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def _compile(src: str) -> str:
+def _deps_mtime(src: str) -> float:
+    """Newest modification time of a source and the headers it may include."""
+    paths = [os.path.join(CSRC, src), HEADER] + [os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                                                  if f.endswith(".hpp")]
+    return max(os.path.getmtime(p) for p in paths)
+
+
+def _compile(src: str, incremental: bool = False) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+    if incremental and os.path.exists(obj) and os.path.getmtime(obj) > _deps_mtime(src):
+        return obj
     cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -65,10 +74,12 @@ def abi_names(header: str = HEADER) -> list:
     return names
 
 
-def build(jobs: int = 4, verbose: bool = False) -> str:
+def build(jobs: int = 4, verbose: bool = False, incremental: bool = False) -> str:
+    """Compiles every source (incremental: only those whose object is older
+    than the source or a header) and links the library."""
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        objs = list(ex.map(lambda s: _compile(s, incremental), SOURCES))
     tmp = LIB + ".tmp"
     vscript = os.path.join(BUILD, "exports.map")
     with open(vscript, "w") as f:
@@ -86,8 +97,9 @@ def build(jobs: int = 4, verbose: bool = False) -> str:
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=min(4, os.cpu_count() or 1))
+    ap.add_argument("--incremental", action="store_true", help="recompile only sources newer than their objects")
     a = ap.parse_args()
-    build(a.jobs, verbose=True)
+    build(a.jobs, verbose=True, incremental=a.incremental)
 
 
 if __name__ == "__main__":

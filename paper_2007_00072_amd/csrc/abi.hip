@@ -5,8 +5,7 @@
 #include <stdio.h>
 #include <math.h>
 
-#include <atomic>
-#include <mutex>
+#include <new>
 #include <vector>
 
 #include "gemm.hpp"
@@ -37,12 +36,12 @@ struct TraceRec {
     const char* sub;
     hipEvent_t a, b;
 };
+// Timing switch, records and event pool of the calling thread.
 thread_local TraceScope* g_active = nullptr;
-std::atomic<bool> g_trace_on{false};
-std::mutex g_trace_mu;
-std::vector<TraceRec> g_trace;     // records of the current session
-std::vector<hipEvent_t> g_events;  // event pool, reused across sessions
-size_t g_events_used = 0;
+thread_local bool g_trace_on = false;
+thread_local std::vector<TraceRec> g_trace;     // records of the current session
+thread_local std::vector<hipEvent_t> g_events;  // event pool, reused across sessions
+thread_local size_t g_events_used = 0;
 
 hipEvent_t pooled_event() {
     if (g_events_used == g_events.size()) {
@@ -55,7 +54,6 @@ hipEvent_t pooled_event() {
 }  // namespace
 
 static int trace_open(const char* label, const char* sub, hipStream_t st) {
-    std::lock_guard<std::mutex> lk(g_trace_mu);
     hipEvent_t a = pooled_event(), b = pooled_event();
     if (!a || !b) return -1;
     (void)hipEventRecord(a, st);
@@ -66,7 +64,7 @@ static int trace_open(const char* label, const char* sub, hipStream_t st) {
 const char* trace_current_label() { return g_active ? g_active->label : ""; }
 
 TraceScope::TraceScope(const char* lab, hipStream_t s) : idx(-1), st(s), label(lab), outer(nullptr) {
-    if (!g_trace_on.load(std::memory_order_relaxed)) return;
+    if (!g_trace_on) return;
     idx = trace_open(label, "", st);
     if (idx >= 0) {
         outer = g_active;
@@ -76,20 +74,14 @@ TraceScope::TraceScope(const char* lab, hipStream_t s) : idx(-1), st(s), label(l
 
 void TraceScope::stop() {
     if (idx < 0) return;
-    {
-        std::lock_guard<std::mutex> lk(g_trace_mu);
-        (void)hipEventRecord(g_trace[idx].b, st);
-    }
+    (void)hipEventRecord(g_trace[idx].b, st);
     idx = -1;
     if (g_active == this) g_active = outer;
 }
 
 void TraceScope::next(const char* sub) {
     if (idx < 0) return;
-    {
-        std::lock_guard<std::mutex> lk(g_trace_mu);
-        (void)hipEventRecord(g_trace[idx].b, st);
-    }
+    (void)hipEventRecord(g_trace[idx].b, st);
     idx = trace_open(label, sub, st);
     if (idx < 0 && g_active == this) g_active = outer;
 }
@@ -103,11 +95,12 @@ DropParams make_drop(float p, uint64_t seed, uint32_t site, uint32_t layer) {
     d.seed = seed;
     d.site = site;
     d.layer = layer;
-    d.enabled = p > 0.f;
-    double thr = floor((1.0 - (double)p) * 4294967296.0);
-    d.thr = (uint64_t)thr;
-    d.scale = (float)(1.0 / (1.0 - (double)p));
-    if (!d.enabled) { d.thr = 1ull << 32; d.scale = 1.f; }
+    const double thr = floor((1.0 - (double)p) * 4294967296.0);
+    // a p so small that 1 - p rounds to 1 keeps every word (thr = 2^32),
+    // which a 32-bit threshold cannot express: no draws at all then
+    d.enabled = p > 0.f && thr < 4294967296.0;
+    d.thr = d.enabled ? (uint64_t)thr : (1ull << 32);
+    d.scale = d.enabled ? (float)(1.0 / (1.0 - (double)p)) : 1.f;
     return d;
 }
 
@@ -158,7 +151,9 @@ extern "C" {
 
 const char* dm_last_error(void) { return g_err; }
 
-int plan_set(const dm_contract_choice* entries, int32_t n, int32_t attn_path) {
+int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path, dm_plan** plan) {
+    if (!plan) return set_error(DM_ERR_ARG, "plan output pointer is NULL");
+    *plan = nullptr;
     if (n < 0 || (n > 0 && !entries)) return set_error(DM_ERR_ARG, "plan entries missing");
     if (attn_path < 0 || attn_path > 3) return set_error(DM_ERR_ARG, "attn_path %d outside [0, 3]", attn_path);
     for (int i = 0; i < n; ++i) {
@@ -167,8 +162,16 @@ int plan_set(const dm_contract_choice* entries, int32_t n, int32_t attn_path) {
         if (e.splits < 1 || e.splits > 64) return set_error(DM_ERR_ARG, "plan entry %d: splits %d", i, e.splits);
         if (e.M <= 0 || e.N <= 0 || e.K <= 0 || e.batch <= 0) return set_error(DM_ERR_ARG, "plan entry %d: sizes", i);
     }
-    plan_contracts(entries, n);
-    set_attn_path(attn_path);
+    dm_plan* p = new (std::nothrow) dm_plan;
+    if (!p) return set_error(DM_ERR_ARG, "out of host memory for the plan");
+    p->entries.assign(entries, entries + n);
+    p->attn_path = attn_path;
+    *plan = p;
+    return DM_OK;
+}
+
+int plan_destroy(dm_plan* plan) {
+    delete plan;
     return DM_OK;
 }
 
@@ -184,22 +187,19 @@ int plan_log_read(dm_contract_choice* out, int32_t cap, int32_t* count) {
 }
 
 int dm_trace_enable(int32_t on) {
-    std::lock_guard<std::mutex> lk(g_trace_mu);
     if (on) {
         g_trace.clear();
         g_events_used = 0;
     }
-    g_trace_on.store(on != 0);
+    g_trace_on = on != 0;
     return DM_OK;
 }
 
 int32_t dm_trace_count(void) {
-    std::lock_guard<std::mutex> lk(g_trace_mu);
     return (int32_t)g_trace.size();
 }
 
 int dm_trace_get(int32_t i, const char** label, const char** sub, float* ms) {
-    std::lock_guard<std::mutex> lk(g_trace_mu);
     if (i < 0 || i >= (int32_t)g_trace.size()) return set_error(DM_ERR_ARG, "trace index %d out of range", i);
     hipError_t e = hipEventSynchronize(g_trace[i].b);
     float t = 0.f;

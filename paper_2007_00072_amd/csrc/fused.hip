@@ -34,7 +34,11 @@ __global__ __launch_bounds__(NT) void bdrln_fwd_k(int64_t rows, int cols, const 
     const bool active = row < rows;
     const int64_t base = row * cols;
     float v[NV][8];
-    float sum = 0.f;
+    // v holds the row minus its first residual value r0: r - r0 is exact
+    // for nearby values, so a row far from zero keeps its fp32 precision
+    // (the sum a + r itself would lose it); the statistics and x_hat use
+    // the shifted row throughout
+    const float r0 = active ? to_f(resid[base]) : 0.f;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
         const int c = (gl + i * LPR) * 8;
@@ -47,14 +51,23 @@ __global__ __launch_bounds__(NT) void bdrln_fwd_k(int64_t rows, int cols, const 
             for (int q = 0; q < 8; ++q) a[q] += b[q];
             dropout8(dp, (uint64_t)(base + c), a);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) { v[i][q] = a[q] + r[q]; sum += v[i][q]; }
+            for (int q = 0; q < 8; ++q) v[i][q] = (r[q] - r0) + a[q];
         } else {
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[i][q] = 0.f;
         }
     }
     const float inv = 1.0f / (float)cols;
-    const float mean = group_sum<LPR>(sum) * inv;
+    float ssum = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const int c = (gl + i * LPR) * 8;
+        if (active && c < cols) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) ssum += v[i][q];
+        }
+    }
+    const float mean = group_sum<LPR>(ssum) * inv;  // of the shifted row
     float sq = 0.f;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {

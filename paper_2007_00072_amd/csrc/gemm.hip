@@ -1907,12 +1907,11 @@ void set_affine(GemmArgs& g) {
     g.affine = 1;
 }
 
-// Configuration plan (entries keyed by sizes, dtype and operand
-// contiguity) and the launch record.
-std::mutex g_plan_mu;
-std::vector<dm_contract_choice> g_plan;
-bool g_log_on = false;
-std::vector<dm_contract_choice> g_log;
+// The plan of the running call (entries keyed by sizes, dtype and operand
+// contiguity) and this thread's launch record.
+thread_local const dm_plan* t_plan = nullptr;
+thread_local bool t_log_on = false;
+thread_local std::vector<dm_contract_choice> t_log;
 
 bool same_contraction(const dm_contract_choice& e, const GemmArgs& g, int dtype) {
     return e.M == g.M && e.N == g.N && e.K == g.K && e.batch == g.batch && e.dtype == dtype &&
@@ -1922,8 +1921,8 @@ bool same_contraction(const dm_contract_choice& e, const GemmArgs& g, int dtype)
 // A plan entry's tile and split factor for an automatically configured
 // contraction; the split factor is cut to what the scratch holds.
 void apply_plan(GemmArgs& g, int dtype) {
-    std::lock_guard<std::mutex> lk(g_plan_mu);
-    for (const dm_contract_choice& e : g_plan) {
+    if (!t_plan) return;
+    for (const dm_contract_choice& e : t_plan->entries) {
         if (!same_contraction(e, g, dtype)) continue;
         g.cfg = e.tile_cfg;
         int s = e.splits > 1 ? e.splits : 1;
@@ -1935,33 +1934,30 @@ void apply_plan(GemmArgs& g, int dtype) {
 }
 
 void log_launch(const GemmArgs& g, int dtype) {
-    std::lock_guard<std::mutex> lk(g_plan_mu);
-    if (!g_log_on) return;
+    if (!t_log_on) return;
     dm_contract_choice r{};
     r.M = g.M; r.N = g.N; r.K = g.K; r.batch = g.batch; r.dtype = dtype;
     r.a_kcontig = g.a.kcontig ? 1 : 0; r.b_kcontig = g.b.kcontig ? 1 : 0;
     r.tile_cfg = g.cfg; r.splits = g.splits > 1 ? g.splits : 1;
     strncpy(r.label, trace_current_label(), sizeof(r.label) - 1);
-    g_log.push_back(r);
+    t_log.push_back(r);
 }
 
 }  // namespace
 
-void plan_contracts(const dm_contract_choice* e, int n) {
-    std::lock_guard<std::mutex> lk(g_plan_mu);
-    g_plan.assign(e, e + n);
-}
+const dm_plan* current_plan() { return t_plan; }
+PlanScope::PlanScope(const dm_plan* p) : prev(t_plan) { t_plan = p; }
+PlanScope::~PlanScope() { t_plan = prev; }
+int current_attn_path() { return t_plan ? t_plan->attn_path : 0; }
 
 void plan_log_set(bool on) {
-    std::lock_guard<std::mutex> lk(g_plan_mu);
-    g_log_on = on;
-    if (on) g_log.clear();
+    t_log_on = on;
+    if (on) t_log.clear();
 }
 
 int plan_log_copy(dm_contract_choice* out, int cap) {
-    std::lock_guard<std::mutex> lk(g_plan_mu);
-    for (int i = 0; i < cap && i < (int)g_log.size(); ++i) out[i] = g_log[i];
-    return (int)g_log.size();
+    for (int i = 0; i < cap && i < (int)t_log.size(); ++i) out[i] = t_log[i];
+    return (int)t_log.size();
 }
 
 // Validation, plan and configuration of a 16-bit contraction; `pair`: when

@@ -6,8 +6,16 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "../../include/dmtx.h"
 #include "common.hpp"
+
+// A configuration plan (plan_create): immutable once made.
+struct dm_plan {
+    std::vector<dm_contract_choice> entries;
+    int attn_path;
+};
 
 namespace dm {
 
@@ -32,11 +40,19 @@ struct TraceScope {
 void trace_next(const char* sub);
 // label of the innermost active scope ("" when timing is off)
 const char* trace_current_label();
-// attention-score launch grouping: 0 automatic, 1 separate, 2 scores on
-// chip, 3 scores and the next contraction together (plan_set's attn_path)
-void set_attn_path(int path);
-// contraction configuration plan and launch record (plan_set / plan_log)
-void plan_contracts(const dm_contract_choice* entries, int n);
+// The configuration plan of the entry-point call running on this thread
+// (its descriptor's plan; nullptr = built-in choices), set for the call's
+// duration by a PlanScope.
+const dm_plan* current_plan();
+struct PlanScope {
+    explicit PlanScope(const dm_plan* p);
+    ~PlanScope();
+    const dm_plan* prev;
+};
+// attention-score launch grouping of the current plan: 0 automatic,
+// 1 separate, 2 scores on chip, 3 scores and the next contraction together
+int current_attn_path();
+// launch record of the calling thread (plan_log)
 void plan_log_set(bool on);
 int plan_log_copy(dm_contract_choice* out, int cap);
 

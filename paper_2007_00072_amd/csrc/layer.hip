@@ -12,8 +12,6 @@
 // index maps inside the contraction kernel, never by a transpose pass.
 #include <math.h>
 
-#include <atomic>
-
 #include "gemm.hpp"
 #include "internal.hpp"
 
@@ -87,16 +85,23 @@ struct SplitScope {
 
 int64_t max3(int64_t a, int64_t b, int64_t c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
 
-std::atomic<int> g_attn_path{0};  // plan_set's attn_path
-
 // Input-projection modes of attention (dm_layer_desc.self_attention).
 enum { PROJ_SEPARATE = 0, PROJ_QKV = 1, PROJ_KV = 2 };
 
 void plan_attention(const Dims& x, int mode, Carver& sv, Carver& fw, Carver& bw, MhaPlan& p) {
     const size_t es = x.es;
-    p.q = sv.take(es * x.B * x.H * x.J * x.P);
-    p.k = sv.take(es * x.B * x.H * x.K * x.P);
-    p.v = sv.take(es * x.B * x.H * x.K * x.W);
+    if (mode == PROJ_QKV) {
+        // one [3][B][H][J][P] block (the saved-tensor view of Q, K, V);
+        // every piece stays 16-byte aligned since J and P are multiples of 8
+        const size_t one = es * x.B * x.H * x.J * x.P;
+        p.q = sv.take(3 * one);
+        p.k = p.q + one;
+        p.v = p.k + one;
+    } else {
+        p.q = sv.take(es * x.B * x.H * x.J * x.P);
+        p.k = sv.take(es * x.B * x.H * x.K * x.P);
+        p.v = sv.take(es * x.B * x.H * x.K * x.W);
+    }
     p.prob = sv.take(es * x.S);
     p.alpha = sv.take(es * x.S);
     p.gamma = sv.take(es * x.Tq * x.H * x.W);
@@ -368,7 +373,7 @@ int project_fused(const Dims& x, int layout, const void* in, const dm_layer_para
 int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const void* q, const void* k,
                        const void* v, void* beta, void* prob, void* alpha, void* gamma, hipStream_t st) {
     const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, HW = x.H * x.W;
-    const int path = g_attn_path.load(std::memory_order_relaxed);
+    const int path = current_attn_path();
     if (path != 1 && attn_fused_ok(x.dtype, (int)K, (int)P)) {
         // QK^T and the softmax + dropout in one launch (beta stays on chip),
         // and Gamma in the same launch when its shape allows
@@ -449,7 +454,7 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
         DM_TRY(launch_gemm(x.dtype, out_dw_args(x, gamma, dout, layout, dwo), st));
     }
     const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
-    const int path = g_attn_path.load(std::memory_order_relaxed);
+    const int path = current_attn_path();
     const bool fused = path != 1 && attn_fused_ok(x.dtype, (int)K, (int)W);
     AttnNext nq;
     nq.x = k; nq.x_outer = H * K * P; nq.x_inner = K * P; nq.x_ld = P;
@@ -582,8 +587,6 @@ int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqk
 
 }  // namespace
 
-void dm::set_attn_path(int path) { g_attn_path.store(path, std::memory_order_relaxed); }
-
 extern "C" {
 
 // ------------------------------------------------------------ encoder layer
@@ -630,6 +633,7 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     const EncPlan e = plan_encoder(x);
     if (ws_bytes < e.fwd_total) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    PlanScope plan_(d->plan);
     SplitScope split_(B8(ws, e.fwd_split), e.split_floats);
     const int dt = x.dtype;
     const int64_t T = x.Tq;
@@ -700,6 +704,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     const EncPlan e = plan_encoder(x);
     if (ws_bytes < e.bwd_total) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    PlanScope plan_(d->plan);
     SplitScope split_(B8(ws, e.bwd_split), e.split_floats);
     const int dt = x.dtype;
     const int64_t T = x.Tq, I = x.I, F = x.F;
@@ -840,6 +845,7 @@ int mha_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     const MhaSizes s = plan_mha(x, mode);
     if (ws_bytes < s.fwd) return set_error(DM_ERR_WORKSPACE, "forward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    PlanScope plan_(d->plan);
     SplitScope split_(B8(ws, s.fwd_split), s.split_floats);
     void *q = B8(saved, s.p.q), *k = B8(saved, s.p.k), *v = B8(saved, s.p.v);
     if (mode == PROJ_QKV) {
@@ -890,6 +896,7 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     const MhaSizes s = plan_mha(x, mode);
     if (ws_bytes < s.bwd) return set_error(DM_ERR_WORKSPACE, "backward workspace too small");
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    PlanScope plan_(d->plan);
     SplitScope split_(B8(ws, s.bwd_split), s.split_floats);
     const int dt = x.dtype;
     const int es = x.es;

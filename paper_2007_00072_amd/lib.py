@@ -44,7 +44,7 @@ EXPORTED = [
     "softmax_dropout_bwd", "bias_grad", "attn_input_bias_grad", "residual_add",
     "dropout_mask", "saved_tensor_view", "contract", "dm_last_error",
     "dm_trace_enable", "dm_trace_count", "dm_trace_get",
-    "plan_set", "plan_log", "plan_log_read",
+    "plan_create", "plan_destroy", "plan_log", "plan_log_read",
 ]
 
 
@@ -71,7 +71,8 @@ class LayerDesc(C.Structure):
                 ("scaler", C.c_float), ("ln_eps", C.c_float),
                 ("p_attn", C.c_float), ("p_attn_out", C.c_float), ("p_ffn_out", C.c_float),
                 ("p_ffn_act", C.c_float), ("seed", C.c_uint64), ("layer_id", C.c_uint32),
-                ("self_attention", C.c_int32), ("causal", C.c_int32), ("qkv_fusion", C.c_int32)]
+                ("self_attention", C.c_int32), ("causal", C.c_int32), ("qkv_fusion", C.c_int32),
+                ("plan", C.c_void_p)]
 
 
 _PNAMES = ["wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "g1", "be1", "w1", "b1", "w2", "b2",
@@ -131,7 +132,8 @@ _f["dm_trace_enable"] = _sig("dm_trace_enable", I32, I32)
 _f["dm_trace_count"] = _sig("dm_trace_count", I32)
 _f["dm_trace_get"] = _sig("dm_trace_get", I32, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_char_p),
                           C.POINTER(C.c_float))
-_f["plan_set"] = _sig("plan_set", I32, C.POINTER(ContractChoice), I32, I32)
+_f["plan_create"] = _sig("plan_create", I32, C.POINTER(ContractChoice), I32, I32, C.POINTER(C.c_void_p))
+_f["plan_destroy"] = _sig("plan_destroy", I32, C.c_void_p)
 _f["plan_log"] = _sig("plan_log", I32, I32)
 _f["plan_log_read"] = _sig("plan_log_read", I32, C.POINTER(ContractChoice), I32, C.POINTER(I32))
 
@@ -171,11 +173,20 @@ def _drop(d):
 def make_desc(shape, dtype: str, layout: str = "bji", act: str = "gelu", scaler: float = 0.0,
               ln_eps: float = 1e-12, p_attn=0.0, p_attn_out=0.0, p_ffn_out=0.0, p_ffn_act=0.0,
               seed: int = 0, layer_id: int = 0, self_attention=True, causal: bool = False,
-              qkv_fusion: int = 0) -> LayerDesc:
-    return LayerDesc(shape.B, shape.J, shape.K, shape.H, shape.P, shape.W, shape.I, shape.F,
-                     DTYPE_CODES[dtype], LAYOUT_CODES[layout], DM_GELU if act == "gelu" else DM_RELU,
-                     scaler, ln_eps, p_attn, p_attn_out, p_ffn_out, p_ffn_act, seed, layer_id,
-                     int(self_attention), 1 if causal else 0, qkv_fusion)
+              qkv_fusion: int = 0, plan: "Optional[Plan]" = None) -> LayerDesc:
+    d = LayerDesc(shape.B, shape.J, shape.K, shape.H, shape.P, shape.W, shape.I, shape.F,
+                  DTYPE_CODES[dtype], LAYOUT_CODES[layout], DM_GELU if act == "gelu" else DM_RELU,
+                  scaler, ln_eps, p_attn, p_attn_out, p_ffn_out, p_ffn_act, seed, layer_id,
+                  int(self_attention), 1 if causal else 0, qkv_fusion, None)
+    set_plan(d, plan)
+    return d
+
+
+def set_plan(desc: LayerDesc, plan: "Optional[Plan]") -> None:
+    """Points the descriptor at a plan (None: built-in choices); the
+    descriptor keeps the Plan object alive."""
+    desc.plan = plan.handle if plan is not None else None
+    desc._plan_ref = plan
 
 
 def make_params(tensors) -> LayerParams:
@@ -322,13 +333,25 @@ def trace_records():
     return [dm_trace_get(i) for i in range(dm_trace_count())]
 
 
-def plan_set(entries, attn_path: int = 0) -> None:
-    """Install a configuration plan: entries are ContractChoice records
-    (or (M, N, K, batch, dtype, a_kcontig, b_kcontig, tile_cfg, splits)
-    tuples); plan_set([]) restores the built-in choices."""
-    recs = [e if isinstance(e, ContractChoice) else ContractChoice(*e) for e in entries]
-    arr = (ContractChoice * max(1, len(recs)))(*recs)
-    _call("plan_set", arr if recs else None, len(recs), attn_path)
+class Plan:
+    """A configuration plan (plan_create) owned by Python: entries are
+    ContractChoice records (or (M, N, K, batch, dtype, a_kcontig, b_kcontig,
+    tile_cfg, splits) tuples).  Name it in a descriptor (make_desc(plan=...)
+    or set_plan) to use it; destroyed with the object."""
+
+    def __init__(self, entries=(), attn_path: int = 0):
+        recs = [e if isinstance(e, ContractChoice) else ContractChoice(*e) for e in entries]
+        arr = (ContractChoice * max(1, len(recs)))(*recs)
+        h = C.c_void_p()
+        _call("plan_create", arr if recs else None, len(recs), attn_path, C.byref(h))
+        self.handle = h.value
+        self.entries = recs
+        self.attn_path = attn_path
+
+    def __del__(self):
+        h, self.handle = getattr(self, "handle", None), None
+        if h is not None and _f is not None:
+            _f["plan_destroy"](h)
 
 
 def plan_log(on: bool) -> None:

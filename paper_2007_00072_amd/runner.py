@@ -17,6 +17,7 @@ TORCH_DTYPES = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat
 
 
 def desc_for(wl: Workload, layer: int = 0, **over) -> lib.LayerDesc:
+    """Descriptor of a workload's layer; `plan=` names a lib.Plan."""
     kw = dict(layout=wl.layout, p_attn=wl.p_attn, p_attn_out=wl.p_attn_out, p_ffn_out=wl.p_ffn_out,
               seed=wl.seed, layer_id=layer, ln_eps=1e-12, self_attention=True)
     kw.update(over)

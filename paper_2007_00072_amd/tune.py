@@ -9,7 +9,7 @@ the output, and saves the path to a configuration file used when training
 starts.  Forward and backward passes are optimised separately.
 
 Here the knobs a caller can change are each contraction's kernel, tile and
-split factor (``plan_set`` entries) and the grouping of the attention-score
+split factor (plan entries, ``lib.Plan``) and the grouping of the attention-score
 steps (``attn_path``: separate launches, scores kept on chip, or scores with
 the next contraction in the same launch).  The tensors between operators
 keep one layout whatever the configuration, so the graph's layout nodes are
@@ -152,6 +152,11 @@ class _Layer:
         self.x = make_activation(wl, 0).to("cuda")
         self.dy = make_activation(wl, 1).to("cuda")
 
+    def use(self, entries=(), attn_path: int = 0):
+        """Runs the layer with this plan from now on (nothing: built-in choices)."""
+        from . import lib
+        lib.set_plan(self.layer.desc, lib.Plan(entries, attn_path) if (entries or attn_path) else None)
+
     def step(self):
         self.layer.forward(self.x)
         self.layer.backward(self.x, self.dy)
@@ -196,7 +201,7 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
     candidates tried for every contraction."""
     from . import lib
     L = _Layer(workload, shape)
-    lib.plan_set([], 0)
+    L.use()
     t0 = time.time()
     for _ in range(5):  # clocks and caches settle before anything is timed
         L.step()
@@ -204,11 +209,11 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
     # attention groupings: which labels each produces, and their times
     grouping_times, grouping_labels = {}, {}
     for p in ATTN_PATHS:
-        lib.plan_set([], p)
+        L.use((), p)
         tm = L.timed(reps)
         grouping_times[p] = tm
         grouping_labels[p] = list(tm.keys())
-    lib.plan_set([], 0)
+    L.use()
     base = L.timed(reps)
     launches = L.launches()
     # contraction shapes and the labels at which each occurs
@@ -226,7 +231,7 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
         for cfg in tile_cfgs:
             for sp in splits:
                 e = lib.ContractChoice(*key, cfg, sp)
-                lib.plan_set([e], 0)
+                L.use([e], 0)
                 ran = {(r.tile_cfg, r.splits) for lab, r in L.launches() if r.key() == key}
                 if len(ran) != 1:
                     continue
@@ -243,7 +248,7 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
         log(f"  {labs}: {len(seen)} configurations, best {best[0]} {best[1] * 1e3:.1f} us "
             f"(built-in {(choice_of[key].tile_cfg, choice_of[key].splits)} "
             f"{sum(base.get(l, 0.0) for l in labs) * 1e3:.1f} us)")
-    lib.plan_set([], 0)
+    L.use()
     # one graph per pass; contraction stages carry their shape's candidates
     # at the first occurrence, later occurrences cost nothing
     label_key = {}
@@ -300,9 +305,9 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
     table = fusion_table(workload, reps, shape)
     result["qkv_fusion_table"] = table
     result["qkv_fusion"] = min(table, key=lambda f: table[f]["forward"] + table[f]["backward"])
-    lib.plan_set(entries, attn_path)
+    L.use(entries, attn_path)
     result["planned_ms"] = sum(L.timed(reps).values())
-    lib.plan_set([], 0)
+    L.use()
     result["tuning_seconds"] = round(time.time() - t0, 1)
     return result
 
@@ -330,14 +335,14 @@ def fusion_table(workload: str, reps: int = 3, shape=None):
 
 
 def load_plan(path: str):
-    """Install the plan a tuning run saved (returns its dict)."""
+    """The plan a tuning run saved: (its dict, a lib.Plan to name in a
+    descriptor)."""
     from . import lib
     with open(path) as f:
         plan = json.load(f)
     entries = [lib.ContractChoice(e["M"], e["N"], e["K"], e["batch"], e["dtype"], e["a_kcontig"], e["b_kcontig"],
                                   e["tile_cfg"], e["splits"]) for e in plan["entries"]]
-    lib.plan_set(entries, int(plan["attn_path"]))
-    return plan
+    return plan, lib.Plan(entries, int(plan["attn_path"]))
 
 
 def main() -> int:

@@ -42,7 +42,7 @@ def check_encoder(wl, layer=0, x=None, dy=None, act="gelu", p_ffn_act=0.0, causa
     assert_close("dx", dx, rdx, dt)
     for n in GRAD_NAMES:
         if n == "bk":   # exactly zero: softmax is invariant to a per-row shift
-            assert_close("dbk", L.grads[n], rg[n], dt, zero_ref=True, scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
+            assert_close("dbk", L.grads[n], rg[n], dt, zero_ref=True, zero_scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
         else:
             assert_close("d" + n, L.grads[n], rg[n], dt, param_grad=True)
     return L, cache
@@ -80,9 +80,14 @@ def test_encoder_transposed_grad_ragged_tile(name):
     check_encoder(small(name, B=1, J=40, K=40, H=6, P=64, W=64, I=384, F=768))
 
 
-@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
-def test_encoder_saved_tensors(name):
-    wl = small(name, B=2, J=64, K=64, H=2, P=64, W=64, I=128, F=512)
+@pytest.mark.parametrize("name,shape", [
+    ("bert_large_f16", dict(B=2, J=64, K=64, H=2, P=64, W=64, I=128, F=512)),
+    ("bert_base_bf16", dict(B=2, J=64, K=64, H=2, P=64, W=64, I=128, F=512)),
+    # 2 * B*H*J*P = 384 bytes per projection: not a multiple of 256
+    ("bert_large_f16", dict(B=1, J=8, K=8, H=3, P=8, W=8, I=24, F=32)),
+])
+def test_encoder_saved_tensors(name, shape):
+    wl = small(name, **shape)
     L, params, x, dy, y, dx = run_encoder(wl)
     cfg = oracle_config(wl)
     _, c = OL.encoder_forward(f64(x), params64(params), cfg)
@@ -113,38 +118,6 @@ def test_encoder_deterministic():
     assert torch.equal(y1, y2) and torch.equal(dx1, dx2)
     for n in g1:
         assert torch.equal(g1[n], L2.grads[n]), n
-
-
-def test_encoder_stack_sampled_layers():
-    # 24-layer BERT-large stack, bf16: layers run in sequence on the GPU; a
-    # sample of layers is checked against the oracle on the GPU's own input.
-    from paper_2007_00072_amd.runner import EncoderLayer, desc_for
-    wl = WORKLOADS["bert_large_stack24_bf16"]
-    check = {0, 11, 23}
-    x = make_activation(wl, 0).to(DEV)
-    layers, inputs = [], []
-    for li in range(wl.n_layers):
-        L = EncoderLayer(desc_for(wl, li), make_params(wl, layer=li), DEV,
-                         workspace=layers[0].ws if layers else None)
-        inputs.append(x)
-        x = L.forward(x)
-        layers.append(L)
-    dy = make_activation(wl, 1).to(DEV)
-    dys = [None] * wl.n_layers
-    for li in reversed(range(wl.n_layers)):
-        dys[li] = dy
-        dy = layers[li].backward(inputs[li], dy)
-        if li in check:
-            torch.cuda.synchronize()
-            cfg = oracle_config(wl, li)
-            prm = params64(make_params(wl, layer=li))
-            ry, cache = OL.encoder_forward(f64(inputs[li]), prm, cfg)
-            rdx, rg, _ = OL.encoder_backward(f64(dys[li]), cache, prm, cfg)
-            assert_close(f"dx[{li}]", dy, rdx, wl.dtype)
-            for n in ("wq", "w1", "w2", "g2"):
-                assert_close(f"d{n}[{li}]", layers[li].grads[n], rg[n], wl.dtype, param_grad=True)
-    torch.cuda.synchronize()
-    assert torch.isfinite(x.float()).all() and torch.isfinite(dy.float()).all()
 
 
 # ----------------------------------------------------------- attention only
@@ -190,7 +163,7 @@ def check_mha(wl, self_attention=True, causal=False, **desc_over):
         assert_close("dv", dv, from_ibj(OL.store(rdv, dt)), dt)
     for n in ("wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo"):
         if n == "bk":
-            assert_close("dbk", M.grads[n], rg[n], dt, zero_ref=True, scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
+            assert_close("dbk", M.grads[n], rg[n], dt, zero_ref=True, zero_scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
         else:
             assert_close("d" + n, M.grads[n], rg[n], dt, param_grad=True)
 

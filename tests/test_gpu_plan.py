@@ -13,16 +13,10 @@ from test_gpu_layer import check_encoder, run_encoder, small
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(autouse=True)
-def _builtin_plan_after():
-    yield
-    lib.plan_set([], 0)
-
-
-def _launches(wl):
+def _launches(wl, plan=None):
     lib.dm_trace_enable(True)
     lib.plan_log(True)
-    run_encoder(wl)
+    run_encoder(wl, plan=plan)
     recs = lib.plan_log_read()
     lib.plan_log(False)
     labels = [lab for lab, _, _ in lib.trace_records()]
@@ -36,15 +30,15 @@ def test_plan_entry_changes_the_kernel_and_keeps_parity():
     lin1 = next(r for r in recs if r.label.decode() == "F7 linear1")
     builtin = (lin1.tile_cfg, lin1.splits)
     want = 6 if builtin[0] != 6 else 2
-    lib.plan_set([lib.ContractChoice(*lin1.key(), want, 1)], 0)
-    recs2, _ = _launches(wl)
+    plan = lib.Plan([lib.ContractChoice(*lin1.key(), want, 1)], 0)
+    recs2, _ = _launches(wl, plan)
     got = next(r for r in recs2 if r.label.decode() == "F7 linear1")
     assert (got.tile_cfg, got.splits) == (want, 1)
     # every other contraction kept its built-in choice
     for a, b in zip(recs, recs2):
         if a.label.decode() != "F7 linear1":
             assert (a.tile_cfg, a.splits) == (b.tile_cfg, b.splits)
-    check_encoder(wl, layer=1)
+    check_encoder(wl, layer=1, plan=plan)
 
 
 def test_plan_every_contraction_on_the_k_group_kernel():
@@ -53,11 +47,11 @@ def test_plan_every_contraction_on_the_k_group_kernel():
     # input gradient included); results still match the oracle
     wl = small("bert_large_f16", B=2, J=96, K=96, H=4, P=64, W=64, I=256, F=512)
     recs, _ = _launches(wl)
-    lib.plan_set([lib.ContractChoice(*k, 16, 1) for k in {r.key() for r in recs}], 3)
-    recs2, _ = _launches(wl)
+    plan = lib.Plan([lib.ContractChoice(*k, 16, 1) for k in {r.key() for r in recs}], 3)
+    recs2, _ = _launches(wl, plan)
     assert sum(r.tile_cfg == 16 for r in recs2) >= 8
     assert any(r.tile_cfg == 16 and r.label.decode() == "B18 qkv_dx" for r in recs2)
-    check_encoder(wl, layer=1)
+    check_encoder(wl, layer=1, plan=plan)
 
 
 @pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
@@ -77,13 +71,12 @@ def test_weight_gradients_share_one_launch(name):
     assert labels.count(lab) == 1
     check_encoder(wl, layer=1)
     out_dw = next(r for r in pair if r.M == wl.shape.H * wl.shape.W)
-    lib.plan_set([lib.ContractChoice(*out_dw.key(), 6, 1)], 0)
-    recs2, labels2 = _launches(wl)
+    plan = lib.Plan([lib.ContractChoice(*out_dw.key(), 6, 1)], 0)
+    recs2, labels2 = _launches(wl, plan)
     assert labels2.count(lab) == 2   # two launches under the one label
     assert any(r.label.decode() == lab and (r.tile_cfg, r.splits) == (6, 1) for r in recs2)
-    check_encoder(wl, layer=1)
+    check_encoder(wl, layer=1, plan=plan)
     # narrower layers (fewer tiles than 3/4 of the CUs) keep separate launches
-    lib.plan_set([], 0)
     wl2 = small(name, B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
     recs3, labels3 = _launches(wl2)
     assert labels3.count(lab) >= 2
@@ -96,20 +89,11 @@ def test_weight_gradients_share_one_launch(name):
 ])
 def test_attention_groupings(path, fwd, bwd):
     wl = small("bert_base_bf16", B=2, J=64, K=64, H=4, P=64, W=64, I=256, F=512).with_(p_attn=0.1)
-    lib.plan_set([], path)
-    _, labels = _launches(wl)
+    plan = lib.Plan([], path)
+    _, labels = _launches(wl, plan)
     for lab in fwd + bwd:
         assert lab in labels, (lab, labels)
-    check_encoder(wl, layer=2)
-
-
-def test_plan_set_validation():
-    with pytest.raises(lib.DmError):
-        lib.plan_set([], 4)
-    with pytest.raises(lib.DmError):
-        lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 17, 1)], 0)
-    with pytest.raises(lib.DmError):
-        lib.plan_set([(64, 64, 64, 1, lib.DM_F16, 1, 1, 5, 0)], 0)
+    check_encoder(wl, layer=2, plan=plan)
 
 
 def test_tuner_end_to_end(tmp_path):
@@ -122,10 +106,10 @@ def test_tuner_end_to_end(tmp_path):
         assert res["passes"][name]["predicted_ms"] > 0
     path = tmp_path / "plan.json"
     path.write_text(json.dumps(res))
-    plan = tune.load_plan(str(path))
-    assert plan["attn_path"] == res["attn_path"]
+    plan, cplan = tune.load_plan(str(path))
+    assert plan["attn_path"] == res["attn_path"] == cplan.attn_path
     wl = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
-    check_encoder(wl, layer=0)
+    check_encoder(wl, layer=0, plan=cplan, qkv_fusion=int(plan["qkv_fusion"]))
 
 
 def test_saved_bert_base_plan_keeps_parity():
@@ -134,7 +118,7 @@ def test_saved_bert_base_plan_keeps_parity():
     import os
     from paper_2007_00072_amd.inputs import WORKLOADS
     path = os.path.join(os.path.dirname(tune.__file__), "plans", "bert_base_bf16.json")
-    tune.load_plan(path)
-    recs, _ = _launches(WORKLOADS["bert_base_bf16"])
+    plan, cplan = tune.load_plan(path)
+    recs, _ = _launches(WORKLOADS["bert_base_bf16"], cplan)
     assert any((r.tile_cfg, r.splits) == (13, 4) for r in recs)
-    check_encoder(WORKLOADS["bert_base_bf16"])
+    check_encoder(WORKLOADS["bert_base_bf16"], plan=cplan, qkv_fusion=int(plan.get("qkv_fusion", 0)))

@@ -65,7 +65,7 @@ def test_shortest_path_rejects_negative_weights():
 
 def test_saved_plans_are_well_formed():
     # every plan shipped with the package names a known workload and only
-    # valid configurations (what plan_set accepts)
+    # valid configurations (what plan_create accepts)
     import glob
     import json
     import os
