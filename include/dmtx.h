@@ -237,6 +237,20 @@ int softmax_dropout_bwd(int32_t dtype, int32_t B, int32_t H, int32_t J, int32_t 
 int bias_grad(int32_t dtype, int64_t rows, int32_t cols, const void* x, float* db, void* ws,
               size_t ws_bytes, void* stream);
 
+/* [baob] as bias_grad, for callers that cannot allocate device memory
+ * (work recorded under stream capture, tight serving loops, harnesses that
+ * forbid allocation): no workspace argument; the column partial sums live
+ * in a fixed 8 MiB device array inside the library (one per GPU, held until
+ * the process ends), enough for colsum_blocks(rows) * cols <= 2^21 floats,
+ * i.e. up to 2048 columns at any row count or 4096 columns up to 4096
+ * rows; larger shapes return DM_ERR_UNSUPPORTED before any launch.  The
+ * call allocates nothing.  `stream` must belong to the current device.
+ * Every call on one GPU shares that GPU's array: calls that overlap on a
+ * GPU (on different streams, or from different threads) race; serialize
+ * them.  Results are bit-identical to bias_grad's. */
+int bias_grad_noalloc(int32_t dtype, int64_t rows, int32_t cols, const void* x, float* db,
+                      void* stream);
+
 /* [baib] input-bias gradients from a token-major [rows][3][H][P] gradient:
  * db_s[p][h] = sum_r x[r][s][h][p] for s = q, k, v (float, paper order). */
 int attn_input_bias_grad(int32_t dtype, int64_t rows, int32_t H, int32_t P, const void* x,

@@ -22,7 +22,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdmtx.so")
-SOURCES = ["gemm.hip", "fused.hip", "attn.hip", "abi.hip", "layer.hip"]
+SOURCES = ["gemm.hip", "fused.hip", "attn.hip", "abi.hip", "layer.hip", "noalloc.hip"]
 HEADER = os.path.join(ROOT, "include", "dmtx.h")
 
 HIPCC_FLAGS = [

@@ -41,7 +41,7 @@ EXPORTED = [
     "mha_sizes", "mha_fwd", "mha_bwd",
     "colsum_ws_bytes", "bdrln_fwd", "softmax_dropout_fwd", "bias_act_fwd", "attn_input_bias",
     "ln_param_bwd", "ln_dropout_bwd", "residual_ln_param_bwd", "act_bias_bwd",
-    "softmax_dropout_bwd", "bias_grad", "attn_input_bias_grad", "residual_add",
+    "softmax_dropout_bwd", "bias_grad", "bias_grad_noalloc", "attn_input_bias_grad", "residual_add",
     "dropout_mask", "saved_tensor_view", "contract", "dm_last_error",
     "dm_trace_enable", "dm_trace_count", "dm_trace_get",
     "plan_create", "plan_destroy", "plan_log", "plan_log_read",
@@ -121,6 +121,7 @@ _f["residual_ln_param_bwd"] = _sig("residual_ln_param_bwd", I32, I32, I64, I32, 
 _f["act_bias_bwd"] = _sig("act_bias_bwd", I32, I32, I64, I32, I32, P_, P_, P_, I32, PDROP, P_, P_, P_, P_, P_, SZ, P_)
 _f["softmax_dropout_bwd"] = _sig("softmax_dropout_bwd", I32, I32, I32, I32, I32, I32, F32, P_, P_, PDROP, P_, P_)
 _f["bias_grad"] = _sig("bias_grad", I32, I32, I64, I32, P_, P_, P_, SZ, P_)
+_f["bias_grad_noalloc"] = _sig("bias_grad_noalloc", I32, I32, I64, I32, P_, P_, P_)
 _f["attn_input_bias_grad"] = _sig("attn_input_bias_grad", I32, I32, I64, I32, I32, P_, P_, P_, P_, P_, SZ, P_)
 _f["residual_add"] = _sig("residual_add", I32, I32, I64, P_, P_, P_, P_)
 _f["dropout_mask"] = _sig("dropout_mask", I32, U64, U32, U32, F32, U64, U64, P_, P_)
@@ -291,6 +292,10 @@ def softmax_dropout_bwd(dtype, B, H, J, K, scale, dalpha, prob, drop, dbeta, str
 
 def bias_grad(dtype, rows, cols, x, db, ws, ws_bytes, stream=None):
     return _call("bias_grad", dtype, rows, cols, ptr(x), ptr(db), ptr(ws), ws_bytes, _st(stream))
+
+
+def bias_grad_noalloc(dtype, rows, cols, x, db, stream=None):
+    return _call("bias_grad_noalloc", dtype, rows, cols, ptr(x), ptr(db), _st(stream))
 
 
 def attn_input_bias_grad(dtype, rows, H, P, x, dbq, dbk, dbv, ws, ws_bytes, stream=None):
