@@ -299,7 +299,11 @@ int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t
  * otherwise run as 14), 14: 256x256 with 8 waves of 128x64, 15: lean
  * 128x128 kernel with 8 waves of 64x32 and 64-wide k-steps (K a multiple
  * of 64; otherwise run as 11), 16: the same tile with two groups of 4
- * waves of 64x64 each taking half of every k-step (otherwise run as 11);
+ * waves of 64x64 each taking half of every k-step (otherwise run as 11),
+ * 17: lean 256x256 kernel with 4 waves of 128x128 (as 13 otherwise 14),
+ * 18: lean 128x128 kernel with 4 waves of 64x64 (as 15 otherwise 11),
+ * 19: lean 256x192 kernel with 4 waves of 128x96, for a B operand
+ * contiguous along k (otherwise run as 13);
  * -1: chosen from the shape; other values are
  * DM_ERR_ARG); splits > 1 splits k, using `ws` (ws_bytes >=
  * splits*batch*M*N*4) for partial sums; splits = 0 chooses (no split
@@ -317,7 +321,7 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
  * descriptor names it.  A contraction is identified by its sizes, dtype and
  * which operands are contiguous along the contraction index
  * (dm_contract_choice without the label); a plan entry sets its tile_cfg
- * (0..16, as for contract) and split factor (1 = none; larger values are cut
+ * (0..19, as for contract) and split factor (1 = none; larger values are cut
  * to what the call's split-k scratch holds).  Entries that a contraction's
  * operands or epilogue do not allow fall back the way contract's tile_cfg
  * does, so a plan never changes results beyond the order of the fp32
@@ -341,7 +345,7 @@ typedef struct {
     int64_t M, N, K, batch;        /* contraction sizes; batch: contractions in one launch */
     int32_t dtype;                 /* dm_dtype                                             */
     int32_t a_kcontig, b_kcontig;  /* 1: operand contiguous along the contraction index   */
-    int32_t tile_cfg;              /* 0..16 (contract's list)                              */
+    int32_t tile_cfg;              /* 0..19 (contract's list)                              */
     int32_t splits;                /* split-k factor, 1 = none                             */
     char label[48];                /* log only: kernel-timing label, "" when timing is off */
 } dm_contract_choice;

@@ -158,7 +158,8 @@ int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path,
     if (attn_path < 0 || attn_path > 3) return set_error(DM_ERR_ARG, "attn_path %d outside [0, 3]", attn_path);
     for (int i = 0; i < n; ++i) {
         const dm_contract_choice& e = entries[i];
-        if (e.tile_cfg < 0 || e.tile_cfg > 16) return set_error(DM_ERR_ARG, "plan entry %d: tile_cfg %d", i, e.tile_cfg);
+        if (e.tile_cfg < 0 || e.tile_cfg > GEMM_MAX_CFG)
+            return set_error(DM_ERR_ARG, "plan entry %d: tile_cfg %d", i, e.tile_cfg);
         if (e.splits < 1 || e.splits > 64) return set_error(DM_ERR_ARG, "plan entry %d: splits %d", i, e.splits);
         if (e.M <= 0 || e.N <= 0 || e.K <= 0 || e.batch <= 0) return set_error(DM_ERR_ARG, "plan entry %d: sizes", i);
     }
@@ -413,7 +414,8 @@ int contract(int32_t dtype, int32_t batch, int32_t M, int32_t N, int32_t K, floa
         return set_error(DM_ERR_UNSUPPORTED, "M, N, K must be multiples of 8");
     DM_TRY(check_ptr(A, "A")); DM_TRY(check_ptr(B, "B")); DM_TRY(check_ptr(C, "C"));
     if (bias) DM_TRY(check_ptr(bias, "bias"));
-    if (tile_cfg < -1 || tile_cfg > 16) return set_error(DM_ERR_ARG, "tile_cfg %d outside [-1, 16]", tile_cfg);
+    if (tile_cfg < -1 || tile_cfg > GEMM_MAX_CFG)
+        return set_error(DM_ERR_ARG, "tile_cfg %d outside [-1, %d]", tile_cfg, GEMM_MAX_CFG);
     if (splits < 0 || splits > 64) return set_error(DM_ERR_ARG, "splits %d outside [0, 64]", splits);
     if (splits > 1 && (!ws || ws_bytes < gemm_split_ws_bytes(M, N, batch, splits)))
         return set_error(DM_ERR_WORKSPACE, "split-k workspace too small");

@@ -1401,7 +1401,7 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
         o.mmap = e.mmap; o.nmap = e.nmap;
     }
     const float alpha = part ? 1.0f : e.alpha;
-    if constexpr (FM * FN <= 2) {
+    if constexpr (FM * FN <= 4) {
         // residual operand (same addressing as the output, along n, input
         // dtype): every value of the wave's tile is loaded before the first
         // store, since vector-memory waits count loads and stores together
@@ -1721,11 +1721,21 @@ struct TileCfg {
 // 256x256 kernel with the same waves; 15: lean 128x128 kernel (8 waves of
 // 64x32, four stages of 64-wide k-steps); 16: lean 128x128 kernel with two
 // k groups of 4 waves of 64x64.  Contractions a lean kernel does not take
-// run on 14 (for 13) or 11 (for 15, 16).
+// run on 14 (for 13) or 11 (for 15, 16).  17: lean 256x256 kernel with 4
+// waves of 128x128 (one per SIMD); 18: lean 128x128 kernel with 4 waves of
+// 64x64 (one per SIMD): each SIMD's wave then reads every fragment of its
+// region once per k-step, where two waves per SIMD read the shared operand
+// twice.  Contractions they do not take run on 14 (17) or 11 (18).
+// 19: lean 256x192 kernel (4 waves of 128x96) for outputs whose width is a
+// multiple of 192 but leaves 256x256 tiles short of the CU count (3072
+// columns: 16 x 16 tiles instead of 16 x 12); the 192-wide operand must be
+// contiguous along k (else run as 13).
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
-                            {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}, {128, 128, 2, 2}};
+                            {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}, {128, 128, 2, 2},
+                            {256, 256, 2, 2}, {128, 128, 2, 2}, {256, 192, 2, 2}};
+static_assert(sizeof(CFGS) / sizeof(CFGS[0]) == GEMM_MAX_CFG + 1, "configuration table");
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
 template <typename T, int BM, int BN, int WGM, int WGN, int DEPTH>
@@ -1784,6 +1794,17 @@ void launch_lean(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, KG>), grid, block, 0, st, g);
 }
 
+// Lean kernels whose B tile width only suits a k-contiguous B operand.
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+void launch_lean_bk(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1>), grid, block, 0, st, g);
+    else
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, 1>), grid, block, 0, st, g);
+}
+
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean_pair(const GemmArgs& g0, const GemmArgs& g1, hipStream_t st) {
     dim3 grid(g0.tiles_m * g0.tiles_n + g1.tiles_m * g1.tiles_n);
@@ -1814,6 +1835,9 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
         case 13: launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st); break;
         case 15: launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st); break;
         case 16: launch_lean<T, 128, 128, 2, 2, 64, 4, 2>(g, st); break;
+        case 17: launch_lean<T, 256, 256, 2, 2, 32, 4>(g, st); break;
+        case 18: launch_lean<T, 128, 128, 2, 2, 64, 4>(g, st); break;
+        case 19: launch_lean_bk<T, 256, 192, 2, 2, 32, 4>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -1859,6 +1883,15 @@ void choose(GemmArgs& g) {
             g.cfg = 8;
         } else if (ntiles(CFGS[13], g) * 4 >= CUS * 3) {
             g.cfg = 13;
+            // 256x192 tiles where they need fewer rounds of the CUs for the
+            // width: estimated time = rounds x tile width, the 4-wave
+            // kernel's lower rate per tile counted as 0.8 (measured 0.79-0.82
+            // on 4096x3072 and 12288x3072 outputs)
+            if (g.N % 192 == 0 && g.b.kcontig) {
+                const int64_t r13 = (ntiles(CFGS[13], g) + CUS - 1) / CUS;
+                const int64_t r19 = (ntiles(CFGS[19], g) + CUS - 1) / CUS;
+                if (r19 * 192 * 10 < r13 * 256 * 8) g.cfg = 19;
+            }
         } else {
             g.cfg = 15;
             const int64_t t = ntiles(CFGS[15], g);
@@ -1869,7 +1902,7 @@ void choose(GemmArgs& g) {
     // maps affine over 32-wide blocks; of them only the lean 128x128 kernel
     // takes a residual operand
     if (((g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
-    if (g.c.resid && g.cfg >= 9 && g.cfg != 15 && g.cfg != 16) g.cfg = 8;
+    if (g.c.resid && g.cfg >= 9 && g.cfg != 15 && g.cfg != 16 && g.cfg != 18) g.cfg = 8;
     if (g.splits <= 0) {
         int s = split_ok ? want_split : 1;
         while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
@@ -1880,8 +1913,9 @@ void choose(GemmArgs& g) {
         g.kper = (ksteps + g.splits - 1) / g.splits * BK;
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
-    if (g.cfg == 13 && !lean_ok(g, 32)) g.cfg = 14;
-    if ((g.cfg == 15 || g.cfg == 16) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
+    if (g.cfg == 19 && !g.b.kcontig) g.cfg = 13;
+    if ((g.cfg == 13 || g.cfg == 17 || g.cfg == 19) && !lean_ok(g, 32)) g.cfg = 14;
+    if ((g.cfg == 15 || g.cfg == 16 || g.cfg == 18) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
     // tile counts of the configuration that runs (the fallback from 15 to 8
     // changes the tile width)
     const TileCfg& c = CFGS[g.cfg];

@@ -89,6 +89,9 @@ struct GemmArgs {
     int blk32;
 };
 
+// Largest tile configuration index (contract's tile_cfg, plan entries).
+constexpr int GEMM_MAX_CFG = 19;
+
 // Scratch bytes for a split-K contraction.
 inline size_t gemm_split_ws_bytes(int64_t M, int64_t N, int64_t batch, int splits) {
     return splits > 1 ? (size_t)splits * batch * M * N * sizeof(float) : 0;

@@ -27,6 +27,7 @@ class Work:
     bytes: float
     bound: str     # "mfma" or "hbm"
     cls: str = ""  # "fused" (memory-bound fused operator) or "contraction"; default from flop
+    overhead: float = 0.0  # bytes the launch moves by design beyond the algorithmic minimum
 
     def __post_init__(self):
         if not self.cls:
@@ -71,11 +72,16 @@ def path_groups(w: Dict[str, "Work"], path: str) -> Dict[str, "Work"]:
     return {k: v for k, v in w.items() if (k not in REPLACES or k in fused) and k not in gone}
 
 
-def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
+def encoder_layer(s: Shape, dtype: str, elements: bool = False) -> Dict[str, Work]:
     """Work of each labelled launch group of one encoder-layer forward + backward.
 
-    Holds both forms of the attention-score steps (see REPLACES)."""
+    Holds both forms of the attention-score steps (see REPLACES).  With
+    elements=True the `bytes` fields count elements instead (every tensor
+    element once, whatever its type), the unit of the paper's I/O columns."""
     es = 4 if dtype == "f32" else 2
+    f4 = 4
+    if elements:
+        es = f4 = 1
     T, I, F, H, P, W = s.B * s.J, s.I, s.F, s.H, s.P, s.W
     Z, J, K = s.B * s.H, s.J, s.K
     N, S, Fh = T * I, s.B * s.H * s.J * s.K, T * F
@@ -92,25 +98,26 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["F2-4 qkt_softmax_gamma"] = Work(2.0 * Z * J * K * (P + W), float((4 * N + 2 * S) * es), "hbm", "fused")
     w["F4 gamma"] = _att(Z, J, W, K, es, dtype, S, N)
     w["F5 out"] = g(T, I, I, N, I * I, N)
-    w["F6 bdrln1"] = m(4 * N * es + 4 * T + 3 * I * es)
+    w["F6 bdrln1"] = m(4 * N * es + f4 * T + 3 * I * es)
     w["F7 linear1"] = g(T, F, I, N, F * I, Fh)
     w["F8 bias_act"] = m(2 * Fh * es + F * es)
     w["F9 linear2"] = g(T, I, F, Fh, I * F, N)
-    w["F10 bdrln2"] = m(4 * N * es + 4 * T + 3 * I * es)
+    w["F10 bdrln2"] = m(4 * N * es + f4 * T + 3 * I * es)
     # backward
-    # (+ dO transposed for the Linear-2 weight gradient where the
-    # column-split LayerNorm backward runs: 16-bit, I a multiple of 64 in
-    # 320..1024)
-    dot = N * es if es == 2 and I % 64 == 0 and 320 <= I <= 1024 else 0
-    w["B1-2 ln2_bwd"] = m(4 * N * es + 4 * T + I * es + 3 * I * 4 + dot)
+    # (the column-split LayerNorm backward also writes dO transposed for the
+    # Linear-2 weight gradient: 16-bit, I a multiple of 64 in 320..1024; the
+    # dataflow needs dO once, so that copy is overhead, not algorithmic)
+    dot = N * es if dtype != "f32" and I % 64 == 0 and 320 <= I <= 1024 else 0
+    w["B1-2 ln2_bwd"] = m(4 * N * es + f4 * T + I * es + 3 * I * f4)
+    w["B1-2 ln2_bwd"].overhead = dot
     w["B3 linear2_dx"] = g(T, F, I, N, I * F, Fh)
-    w["B4 linear2_dw"] = g(I, F, T, N, Fh, I * F, c_es=4)
-    w["B5 act_bwd"] = m(3 * Fh * es + F * es + F * 4)
+    w["B4 linear2_dw"] = g(I, F, T, N, Fh, I * F, c_es=f4)
+    w["B5 act_bwd"] = m(3 * Fh * es + F * es + F * f4)
     w["B6 linear1_dx"] = g(T, I, F, Fh, F * I, N)
-    w["B7 linear1_dw"] = g(F, I, T, Fh, N, F * I, c_es=4)
-    w["B8-10 ln1_bwd"] = m(5 * N * es + 4 * T + I * es + 3 * I * 4)
+    w["B7 linear1_dw"] = g(F, I, T, Fh, N, F * I, c_es=f4)
+    w["B8-10 ln1_bwd"] = m(5 * N * es + f4 * T + I * es + 3 * I * f4)
     w["B11 out_dx"] = g(T, I, I, N, I * I, N)
-    w["B12 out_dw"] = g(I, I, T, N, N, I * I, c_es=4)
+    w["B12 out_dw"] = g(I, I, T, N, N, I * I, c_es=f4)
     w["B13 gamma_dx1"] = _att(Z, J, K, W, es, dtype, S, N)
     w["B14 gamma_dx2"] = _att(Z, K, W, J, es, dtype, S, N)
     w["B15 softmax_bwd"] = m(3 * S * es)
@@ -122,10 +129,10 @@ def encoder_layer(s: Shape, dtype: str) -> Dict[str, Work]:
     w["B16 qkt_dx1"] = _att(Z, J, P, K, es, dtype, S, N)
     w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read
-    w["B19 qkv_dw"] = g(3 * I, I, T, 3 * N, N, 3 * I * I, c_es=4)
+    w["B19 qkv_dw"] = g(3 * I, I, T, 3 * N, N, 3 * I * I, c_es=f4)
     for lab, parts in PAIRED.items():
         w[lab] = Work(sum(w[p].flop for p in parts), sum(w[p].bytes for p in parts), "mfma", "contraction")
-    w["B20 qkv_bias_grad"] = m(3 * N * es + 3 * I * 4)
+    w["B20 qkv_bias_grad"] = m(3 * N * es + 3 * I * f4)
     # column-sum partials of B1-2, B5, B8-10 and B20 finished in one launch
     w["B colsum finish"] = m(0)
     return w
@@ -152,3 +159,71 @@ def contraction_gflop(s: Shape) -> Dict[str, float]:
         "bwd Out dX": out, "bwd Out dW": out, "bwd Gamma dX1": att, "bwd Gamma dX2": att,
         "bwd QK^T dX1": att, "bwd QK^T dX2": att, "bwd Q,K,V dX": qkv, "bwd Q,K,V dW": qkv,
     }
+
+
+def mha(s: Shape, dtype: str, layout: str = "ibj", elements: bool = False) -> Dict[str, Work]:
+    """Work of each labelled launch group of multi-head self-attention alone
+    (fused Q/K/V projection, output bias in the output projection's
+    epilogue), forward + backward: the encoder layer's attention launches,
+    with the output-bias gradient as its own launch and the Q/K/V input
+    gradient written without a residual."""
+    w = encoder_layer(s, dtype, elements)
+    es = 1 if elements else (4 if dtype == "f32" else 2)
+    f4 = 1 if elements else 4
+    T, I = s.B * s.J, s.I
+    N = T * I
+    keep = ("F1 qkv", "F2 qkt", "F3 softmax", "F2-3 qkt_softmax", "F2-4 qkt_softmax_gamma", "F4 gamma",
+            "F5 out", "B11 out_dx", "B12 out_dw", "B13 gamma_dx1", "B14 gamma_dx2", "B15 softmax_bwd",
+            "B13-15 gamma_dx1_softmax_bwd", "B13+15+16 score_bwd_dq", "B16 qkt_dx1", "B17 qkt_dx2",
+            "B18 qkv_dx", "B19 qkv_dw", "B20 qkv_bias_grad")
+    out = {k: w[k] for k in keep}
+    f5 = w["F5 out"]
+    out["F5 out"] = Work(f5.flop, f5.bytes + I * es, f5.bound)
+    b18 = w["B18 qkv_dx"]
+    out["B18 qkv_dx"] = Work(b18.flop, b18.bytes - N * es, b18.bound)
+    out["B10 out_bias_grad"] = Work(0.0, float(N * es + I * f4), "hbm")
+    return out
+
+
+def unfused_table3(s: Shape, act_dropout: bool = False):
+    """The layer's operators one by one, as the paper's Table 3 lists them
+    (each its own kernel: every input read, every output written, dropout
+    masks stored and read back as tensors of their own), with input and
+    output element counts derived from the shapes.  The activation is the
+    workload's; act_dropout adds the dropout after it (the paper's fourth).
+    Returns [(row, inputs, outputs)]."""
+    T, I, F, H, P = s.B * s.J, s.I, s.F, s.H, s.P
+    N, S, Fh, I2 = T * I, s.B * s.H * s.J * s.K, T * F, I * I
+    r = [("Q, K, V", N + 3 * I2, 3 * N), ("Input bias", 3 * N + 3 * I, 3 * N), ("QK^T", 2 * N, S),
+         ("Scaled softmax", S, 3 * S), ("Gamma", S + N, N), ("Out", N + I2, N)]
+    ln_block = lambda: [("Bias", N + I, N), ("Dropout", N, 2 * N), ("Residual", 2 * N, N), ("LayerNorm", N + 2 * I, N)]
+    r += ln_block()
+    r += [("Linear", N + I * F, Fh), ("Bias", Fh + F, Fh), ("Activation", Fh, Fh)]
+    if act_dropout:
+        r += [("Dropout", Fh, 2 * Fh)]
+    r += [("Linear", Fh + I * F, N)]
+    r += ln_block()
+    # backward
+    # (LayerNorm dX reads dY, x_hat, its scale and the per-token statistics)
+    r += [("LayerNorm dW", 2 * N, 2 * I), ("LayerNorm dX", 2 * N + I + 2 * T, N), ("Dropout dX", 2 * N, N),
+          ("Linear+Bias dX", N + I * F, Fh), ("Linear dW", N + Fh, I * F), ("Bias dW", N, I)]
+    if act_dropout:
+        r += [("Dropout dX", 2 * Fh, Fh)]
+    r += [("Activation dX", 2 * Fh, Fh), ("Bias dW", Fh, F), ("Linear+Bias dX", Fh + I * F, N),
+          ("Linear dW", Fh + N, I * F), ("Residual", 2 * N, N), ("LayerNorm dW", 2 * N, 2 * I),
+          ("LayerNorm dX", 2 * N + I + 2 * T, N), ("Dropout dX", 2 * N, N), ("Output bias dW", N, I),
+          ("Out dX", N + I2, N), ("Out dW", 2 * N, I2), ("Gamma dX1", 2 * N, S), ("Gamma dX2", S + N, N),
+          ("Scaled softmax dX", 3 * S, S), ("QK^T dX1", S + N, N), ("QK^T dX2", S + N, N),
+          ("Q, K, V dX", 3 * N + 3 * I2, N), ("Q, K, V dW", 4 * N, 3 * I2), ("Input bias dW", 3 * N, 3 * I),
+          ("Residual", 2 * N, N)]
+    return r
+
+
+def data_movement(s: Shape, dtype: str, path: str = "scores_next", act_dropout: bool = False) -> Dict[str, float]:
+    """The data-movement reduction of the fused layer against the operators
+    one by one (the analogue of the paper's figure, from its Table 3 I/O
+    columns): elements moved per forward + backward step, both ways."""
+    unf = sum(i + o for _, i, o in unfused_table3(s, act_dropout))
+    fused = sum(w.bytes for w in path_groups(encoder_layer(s, dtype, elements=True), path).values())
+    return {"unfused_Melem": round(unf / 1e6, 2), "fused_Melem": round(fused / 1e6, 2),
+            "reduction": round(1.0 - fused / unf, 4)}

@@ -197,7 +197,7 @@ def test_plan_objects_host_only(lib):
     assert d.plan == p.handle and d._plan_ref is p
     lib.set_plan(d, None)
     assert not d.plan
-    for bad in [((), 4), ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 17, 1)], 0),
+    for bad in [((), 4), ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 20, 1)], 0),
                 ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 5, 0)], 0), ([(0, 64, 64, 1, lib.DM_F16, 1, 1, 5, 1)], 0)]:
         with pytest.raises(lib.DmError):
             lib.Plan(*bad)

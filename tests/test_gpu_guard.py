@@ -154,15 +154,16 @@ def test_fused_operators_write_stay_inside(lib, dt):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("cfg,splits", [(-1, 0), (13, 1), (15, 2), (16, 1), (8, 3), (11, 1)])
-def test_contract_writes_stay_inside(lib, dt, cfg, splits):
+@pytest.mark.parametrize("cfg,splits", [(-1, 0), (13, 1), (15, 2), (16, 1), (8, 3), (11, 1), (17, 1), (18, 2), (19, 1)])
+@pytest.mark.parametrize("bt", [0, 1])
+def test_contract_writes_stay_inside(lib, dt, cfg, splits, bt):
     g = Guard()
-    batch, M, N, K = 2, 264, 328, 256
+    batch, M, N, K = 2, 264, 392, 256
     A = make_tensor((batch, M, K), dt, 1).to(DEV)
-    Bm = make_tensor((batch, K, N), dt, 2).to(DEV)
+    Bm = make_tensor((batch, N, K) if bt else (batch, K, N), dt, 2).to(DEV)
     C = g.tensor((batch, M, N), TDT[dt])
     wsb = max(1, splits) * batch * M * N * 4
     ws = g.bytes(wsb) if splits > 1 else None
-    lib.contract(DT[dt], batch, M, N, K, 1.0, A, 0, M * K, Bm, 0, N * K, None, C, 0, M * N, cfg, splits, ws,
+    lib.contract(DT[dt], batch, M, N, K, 1.0, A, 0, M * K, Bm, bt, N * K, None, C, 0, M * N, cfg, splits, ws,
                  wsb if splits > 1 else 0)
     g.check()
