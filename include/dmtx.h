@@ -349,7 +349,31 @@ typedef struct {
     int32_t splits;                /* split-k factor, 1 = none                             */
     char label[48];                /* log only: kernel-timing label, "" when timing is off */
 } dm_contract_choice;
-int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path, dm_plan** plan);
+/* Layout and reduction choices of the memory-bound fused operators, the
+ * plan's counterpart of the contraction entries (Sec. "Data Layout -- Fused
+ * Operators"): which producers also write their output transposed, so
+ * that the weight-gradient contraction consuming it reads it contiguous
+ * along the tokens, and the reduction width of the LayerNorm kernels.
+ * -1 in any field keeps the library's choice.  None of them changes
+ * results beyond the order of fp32 sums. */
+typedef struct {
+    int32_t dO_transposed;  /* 1: the LayerNorm-2 backward also writes dO^T ([I][T]) and the    */
+                            /* Linear-2 weight gradient reads it (column-split form only);     */
+                            /* 0: not.  Library: 1 wherever the column-split form runs          */
+    int32_t dH_transposed;  /* 1: the activation backward also writes dH^T ([F][T]) and the    */
+                            /* Linear-1 weight gradient reads it (16-bit types); 0: not.        */
+                            /* Library: 0                                                       */
+    int32_t ln_bwd_form;    /* LayerNorm backward: 1 = one lane group per row, reduced across  */
+                            /* its lanes; 2 = column slices of 16-row tiles (16-bit types, I a */
+                            /* multiple of 64 in 320..1024).  Library: 2 where allowed         */
+    int32_t ln_lanes;       /* lanes per row of the row-form LayerNorm kernels (the forward,   */
+                            /* and the backward in form 1): 16, 32 or 64 for rows of 257..1024  */
+                            /* elements (each lane holding 8-element vectors of its row).       */
+                            /* Library: 64                                                      */
+} dm_layout_choice;
+/* layout: NULL keeps the library's choice for every field. */
+int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path,
+                const dm_layout_choice* layout, dm_plan** plan);
 int plan_destroy(dm_plan* plan);
 int plan_log(int32_t on);
 int plan_log_read(dm_contract_choice* out, int32_t cap, int32_t* count);

@@ -151,7 +151,8 @@ extern "C" {
 
 const char* dm_last_error(void) { return g_err; }
 
-int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path, dm_plan** plan) {
+int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path, const dm_layout_choice* layout,
+                dm_plan** plan) {
     if (!plan) return set_error(DM_ERR_ARG, "plan output pointer is NULL");
     *plan = nullptr;
     if (n < 0 || (n > 0 && !entries)) return set_error(DM_ERR_ARG, "plan entries missing");
@@ -163,10 +164,21 @@ int plan_create(const dm_contract_choice* entries, int32_t n, int32_t attn_path,
         if (e.splits < 1 || e.splits > 64) return set_error(DM_ERR_ARG, "plan entry %d: splits %d", i, e.splits);
         if (e.M <= 0 || e.N <= 0 || e.K <= 0 || e.batch <= 0) return set_error(DM_ERR_ARG, "plan entry %d: sizes", i);
     }
+    dm_layout_choice lc = {-1, -1, -1, -1};
+    if (layout) {
+        lc = *layout;
+        if (lc.dO_transposed < -1 || lc.dO_transposed > 1 || lc.dH_transposed < -1 || lc.dH_transposed > 1)
+            return set_error(DM_ERR_ARG, "layout: transposed-copy fields must be -1, 0 or 1");
+        if (lc.ln_bwd_form < -1 || lc.ln_bwd_form > 2)
+            return set_error(DM_ERR_ARG, "layout: ln_bwd_form %d outside [-1, 2]", lc.ln_bwd_form);
+        if (lc.ln_lanes != -1 && lc.ln_lanes != 0 && lc.ln_lanes != 16 && lc.ln_lanes != 32 && lc.ln_lanes != 64)
+            return set_error(DM_ERR_ARG, "layout: ln_lanes %d not one of 16, 32, 64", lc.ln_lanes);
+    }
     dm_plan* p = new (std::nothrow) dm_plan;
     if (!p) return set_error(DM_ERR_ARG, "out of host memory for the plan");
     p->entries.assign(entries, entries + n);
     p->attn_path = attn_path;
+    p->layout = lc;
     *plan = p;
     return DM_OK;
 }

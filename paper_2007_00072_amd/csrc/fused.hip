@@ -393,6 +393,65 @@ __global__ __launch_bounds__(NT) void act_bwd_k(int64_t rows, int F, const T* __
     V8<float>::store(part + (int64_t)blockIdx.x * F + v * 8, acc);
 }
 
+// The same, also writing dh transposed (dht[f][row], the layout in which
+// the Linear-1 weight gradient reads it contiguous along the tokens): rows
+// go in groups of 8, so each lane writes every one of its 8 columns as one
+// 16-byte piece of 8 consecutive rows.  Blocks are numbered so that each
+// XCD takes one contiguous eighth of the rows: the pieces of one 128-byte
+// line of dht (64 rows, 8 row blocks) are then written through one L2,
+// which merges them before they reach HBM.  Needs rows and
+// rows_per_block multiples of 8.
+template <typename T>
+__global__ __launch_bounds__(NT) void act_bwd_t_k(int64_t rows, int F, const T* __restrict__ da,
+                                                  const T* __restrict__ h, const T* __restrict__ b1, int act,
+                                                  DropParams dp, T* __restrict__ dh, T* __restrict__ dht,
+                                                  float* __restrict__ part, int rows_per_block, int nrb) {
+    const int lid = (int)blockIdx.x, total = (int)gridDim.x;
+    int rb, cb;
+    if ((nrb & 7) == 0 && (total & 7) == 0) {
+        const int per = nrb >> 3, i = lid >> 3;
+        cb = i / per;
+        rb = (lid & 7) * per + (i - cb * per);
+    } else {
+        cb = lid / nrb;
+        rb = lid - cb * nrb;
+    }
+    const int v = cb * NT + threadIdx.x;
+    if (v >= F / 8) return;
+    const int64_t r0 = (int64_t)rb * rows_per_block;
+    const int64_t r1 = min<int64_t>(rows, r0 + rows_per_block);
+    float bb[8], acc[8];
+    V8<T>::load(b1 + v * 8, bb);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int64_t r = r0; r < r1; r += 8) {
+        float g[8][8], u[8][8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            V8<T>::load(da + (r + j) * F + v * 8, g[j]);
+            V8<T>::load(h + (r + j) * F + v * 8, u[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int64_t off = (r + j) * F + v * 8;
+            dropout8(dp, (uint64_t)off, g[j]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) g[j][q] = to_f(from_f<T>(g[j][q] * act_grad(u[j][q] + bb[q], act)));
+            V8<T>::store(dh + off, g[j]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[q] += g[j][q];
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            float col[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) col[j] = g[j][q];
+            V8<T>::store(dht + (int64_t)(v * 8 + q) * rows + r, col);
+        }
+    }
+    V8<float>::store(part + (int64_t)rb * F + v * 8, acc);
+}
+
 template <typename T>
 __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, const T* __restrict__ x,
                                                        float* __restrict__ part, int rows_per_block) {
@@ -574,10 +633,25 @@ int grid_for(int64_t nvec) {
     else if (len <= 2048) { LAUNCH(64, 4); }                                   \
     else { LAUNCH(64, 8); }
 
+// Lanes per row chosen by a configuration plan (the reduction width of a
+// row operator): 32 or 16 lanes per row for rows of 257..1024 elements, each
+// lane holding proportionally more vectors; anything else takes the table
+// above.
+#define DM_ROW_CASES_LANES(lanes, LAUNCH)                                          \
+    if ((lanes) == 32 && len > 256 && len <= 1024) {                               \
+        if (len <= 512) { LAUNCH(32, 2); }                                         \
+        else if (len <= 768) { LAUNCH(32, 3); }                                    \
+        else { LAUNCH(32, 4); }                                                    \
+    } else if ((lanes) == 16 && len > 256 && len <= 1024) {                        \
+        if (len <= 512) { LAUNCH(16, 4); }                                         \
+        else if (len <= 768) { LAUNCH(16, 6); }                                    \
+        else { LAUNCH(16, 8); }                                                    \
+    } else { DM_ROW_CASES(LAUNCH) }
+
 template <typename T>
 void bdrln_t(int64_t rows, int len, const void* x, const void* bias, const void* resid, const void* gamma,
              const void* beta, float eps, const DropParams& dp, void* y, void* xhat, float* rstd,
-             hipStream_t st) {
+             int lanes, hipStream_t st) {
 #define L(LPR, NV)                                                                              \
     {                                                                                           \
         int64_t rpb = 4 * (64 / LPR);                                                           \
@@ -585,7 +659,7 @@ void bdrln_t(int64_t rows, int len, const void* x, const void* bias, const void*
                            st, rows, len, (const T*)x, (const T*)bias, (const T*)resid,         \
                            (const T*)gamma, (const T*)beta, eps, dp, (T*)y, (T*)xhat, rstd);    \
     }
-    DM_ROW_CASES(L)
+    DM_ROW_CASES_LANES(lanes, L)
 #undef L
 }
 
@@ -792,9 +866,9 @@ __global__ __launch_bounds__(NTL) void ln_bwd_cs_k(LnBwdArgs a, int nblk) {
 
 template <typename T>
 void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
-    const int nblk = ln_bwd_blocks(a.rows, a.cols, a.dtype);
+    const int nblk = ln_bwd_blocks(a.rows, a.cols, a.dtype, a.form);
     if constexpr (sizeof(T) == 2) {
-        if (ln_bwd_split_ok(a.cols, a.dtype)) {
+        if (ln_bwd_uses_split(a.cols, a.dtype, a.form)) {
             if (a.cols / 64 <= 8) hipLaunchKernelGGL((ln_bwd_cs_k<T, 8>), dim3(nblk), dim3(NTL), 0, st, a, nblk);
             else hipLaunchKernelGGL((ln_bwd_cs_k<T, 16>), dim3(nblk), dim3(NTL), 0, st, a, nblk);
             return;
@@ -804,11 +878,18 @@ void ln_bwd_t(const LnBwdArgs& a, hipStream_t st) {
     const int rpb = (int)((a.rows + nblk - 1) / nblk);
 #define L(LPR, NV) \
     { hipLaunchKernelGGL((ln_bwd_k<T, LPR, NV>), dim3(nblk), dim3(NTL), 0, st, a, rpb, nblk); }
-    DM_ROW_CASES(L)
+    DM_ROW_CASES_LANES(a.lanes, L)
 #undef L
 }
 
 }  // namespace
+
+int act_bwd_blocks(int64_t rows, bool transposed) {
+    const int nblk = colsum_blocks(rows);
+    if (!transposed) return nblk;
+    const int rpb = (int)((rows + nblk - 1) / nblk + 7) / 8 * 8;
+    return (int)((rows + rpb - 1) / rpb);
+}
 
 int colsum_blocks(int64_t rows) {
     int64_t b = (rows + 7) / 8;
@@ -816,8 +897,8 @@ int colsum_blocks(int64_t rows) {
     return (int)(b < 1 ? 1 : b);
 }
 
-int ln_bwd_blocks(int64_t rows, int cols, int dtype) {
-    if (!ln_bwd_split_ok(cols, dtype)) return colsum_blocks(rows);
+int ln_bwd_blocks(int64_t rows, int cols, int dtype, int form) {
+    if (!ln_bwd_uses_split(cols, dtype, form)) return colsum_blocks(rows);
     int64_t b = (rows + LN_TILE - 1) / LN_TILE;
     if (b > 512) b = 512;
     return (int)(b < 1 ? 1 : b);
@@ -832,8 +913,8 @@ int ln_bwd_blocks(int64_t rows, int cols, int dtype) {
 
 void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias, const void* resid,
                    const void* gamma, const void* beta, float eps, const DropParams& dp, void* y, void* xhat,
-                   float* rstd, hipStream_t st) {
-    DM_DTYPE_SWITCH(dtype, bdrln_t<T>(rows, cols, x, bias, resid, gamma, beta, eps, dp, y, xhat, rstd, st));
+                   float* rstd, hipStream_t st, int lanes) {
+    DM_DTYPE_SWITCH(dtype, bdrln_t<T>(rows, cols, x, bias, resid, gamma, beta, eps, dp, y, xhat, rstd, lanes, st));
 }
 
 void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta, const DropParams& dp,
@@ -864,8 +945,20 @@ void run_attn_input_bias(int dtype, int64_t rows, int H, int P, const void* x, c
 }
 
 void run_act_bwd(int dtype, int64_t rows, int F, const void* da, const void* h, const void* b1, int act,
-                 const DropParams& dp, void* dh, float* part, hipStream_t st) {
+                 const DropParams& dp, void* dh, float* part, hipStream_t st, void* dht) {
     const int nblk = colsum_blocks(rows);
+    if (dht) {
+        // whole groups of 8 rows per block (the caller checked rows % 8 == 0)
+        const int rpb = (int)((rows + nblk - 1) / nblk + 7) / 8 * 8;
+        const int nrb = (int)((rows + rpb - 1) / rpb);
+        const int ncb = (F / 8 + NT - 1) / NT;
+        DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((act_bwd_t_k<T>), dim3(nrb * ncb), dim3(NT), 0, st, rows, F,
+                                                  (const T*)da, (const T*)h, (const T*)b1, act, dp, (T*)dh,
+                                                  (T*)dht, part, rpb, nrb));
+        // row blocks past nrb (up to colsum_blocks) would leave their
+        // partial rows unwritten: the finish reads nrb rows (act_bwd_blocks)
+        return;
+    }
     const int rpb = (int)((rows + nblk - 1) / nblk);
     const dim3 grid(nblk, (F / 8 + NT - 1) / NT);
     DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((act_bwd_k<T>), grid, dim3(NT), 0, st, rows, F, (const T*)da,

@@ -1984,6 +1984,17 @@ PlanScope::PlanScope(const dm_plan* p) : prev(t_plan) { t_plan = p; }
 PlanScope::~PlanScope() { t_plan = prev; }
 int current_attn_path() { return t_plan ? t_plan->attn_path : 0; }
 
+FusedLayout fused_layout(int dtype, int64_t T, int I, int F) {
+    (void)F;
+    FusedLayout f{};
+    const dm_layout_choice c = t_plan ? t_plan->layout : dm_layout_choice{-1, -1, -1, -1};
+    f.ln_form = c.ln_bwd_form > 0 ? c.ln_bwd_form : 0;
+    f.ln_lanes = c.ln_lanes > 0 ? c.ln_lanes : 0;
+    f.dO_t = ln_bwd_uses_split(I, dtype, f.ln_form) && c.dO_transposed != 0;
+    f.dH_t = dtype != DM_F32 && T % 8 == 0 && c.dH_transposed == 1;
+    return f;
+}
+
 void plan_log_set(bool on) {
     t_log_on = on;
     if (on) t_log.clear();

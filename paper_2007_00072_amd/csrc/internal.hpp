@@ -15,6 +15,7 @@
 struct dm_plan {
     std::vector<dm_contract_choice> entries;
     int attn_path;
+    dm_layout_choice layout;
 };
 
 namespace dm {
@@ -67,19 +68,38 @@ inline DropParams make_drop(const dm_dropout* d) {
 // the column-sum and activation-backward kernels, ln_bwd_blocks for the
 // LayerNorm backward; never more than colsum_blocks(rows)).
 int colsum_blocks(int64_t rows);
-int ln_bwd_blocks(int64_t rows, int cols, int dtype);
-// LayerNorm backward takes its column-split form for these row lengths
+// LayerNorm backward can take its column-split form for these row lengths
 // (16-bit storage types)
 inline bool ln_bwd_split_ok(int cols, int dtype) {
     return dtype != DM_F32 && cols % 64 == 0 && cols >= 320 && cols <= 1024;
 }
+// form: 0 = the library's choice (column split where allowed), 1 = one lane
+// group per row, 2 = column split (where allowed)
+inline bool ln_bwd_uses_split(int cols, int dtype, int form) {
+    return form != 1 && ln_bwd_split_ok(cols, dtype);
+}
+int ln_bwd_blocks(int64_t rows, int cols, int dtype, int form = 0);
+// partial rows of the activation backward (with the transposed copy, whole
+// groups of 8 rows per block)
+int act_bwd_blocks(int64_t rows, bool transposed);
+
+// Layout and reduction choices of the fused operators for the running call:
+// its plan's, with every "library's choice" field resolved for this shape.
+struct FusedLayout {
+    bool dO_t;      // LayerNorm-2 backward writes dO^T, the Linear-2 weight gradient reads it
+    bool dH_t;      // activation backward writes dH^T, the Linear-1 weight gradient reads it
+    int ln_form;    // LayerNorm backward reduction form (0/1/2 as ln_bwd_uses_split)
+    int ln_lanes;   // lanes per row of the row-form LayerNorm kernels (0 = by length)
+};
+FusedLayout fused_layout(int dtype, int64_t T, int I, int F);
 
 // ------------------------------------------------------- kernel launchers
 // All take element counts, device pointers and a stream, and assume the
 // caller validated alignment and sizes.  dtype: DM_F32 / DM_F16 / DM_BF16.
+// lanes: lanes per row (0 = by row length; 16, 32 for rows of 257..1024)
 void run_bdrln_fwd(int dtype, int64_t rows, int cols, const void* x, const void* bias,
                    const void* resid, const void* gamma, const void* beta, float eps,
-                   const DropParams& dp, void* y, void* xhat, float* rstd, hipStream_t st);
+                   const DropParams& dp, void* y, void* xhat, float* rstd, hipStream_t st, int lanes = 0);
 
 // Attention scores without the score tensor in HBM (attn.hip).  Operand
 // element (z = b*H + h, row r, contraction index d) sits at
@@ -145,16 +165,20 @@ struct LnBwdArgs {
     void* dsub;
     float* part;  // null: no column sums
     int want_dsub_sum;
-    void* dsub_t;  // optional [cols][rows] copy of dsub (written when ln_bwd_split_ok(cols, dtype))
+    void* dsub_t;  // optional [cols][rows] copy of dsub (written when the column-split form runs)
+    int form;      // 0 library's choice, 1 row form, 2 column split (ln_bwd_uses_split)
+    int lanes;     // row form: lanes per row (0 = by row length)
 };
 void run_ln_bwd(const LnBwdArgs& a, hipStream_t st);
 
 void run_softmax_bwd(int dtype, int B, int H, int J, int K, float scale, const void* dalpha,
                      const void* prob, const DropParams& dp, void* dbeta, hipStream_t st);
 
-// dh = dropout'(da) * act'(h + b1) with column partials of dh into part.
+// dh = dropout'(da) * act'(h + b1) with column partials of dh into part
+// (act_bwd_blocks(rows, dht != nullptr) partial rows); with dht also dh
+// transposed, [F][rows] (rows a multiple of 8).
 void run_act_bwd(int dtype, int64_t rows, int F, const void* da, const void* h, const void* b1,
-                 int act, const DropParams& dp, void* dh, float* part, hipStream_t st);
+                 int act, const DropParams& dp, void* dh, float* part, hipStream_t st, void* dht = nullptr);
 
 // Column partial sums of x (rows x cols) into part[nblk][cols].
 void run_colsum_partial(int dtype, int64_t rows, int cols, const void* x, float* part,

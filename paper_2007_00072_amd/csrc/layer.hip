@@ -65,7 +65,7 @@ struct EncPlan {
     MhaPlan m;
     size_t xhat1, rstd1, y1, h, a, xhat2, rstd2, saved_total;
     size_t ao, o, fwd_split, fwd_total;
-    size_t dS2, dO, dOT, dA, dH, dY1f, dS1, dAO, bwd_split, bwd_total;
+    size_t dS2, dO, dOT, dA, dH, dHT, dY1f, dS1, dAO, bwd_split, bwd_total;
     size_t part_ln2, part_act, part_ln1;  // column partials finished together at the end of the backward
     int64_t split_floats;
 };
@@ -151,12 +151,14 @@ EncPlan plan_encoder(const Dims& x) {
     e.dOT = bw.take(es * x.N);  // dO transposed, [I][T]
     e.dA = bw.take(es * T * x.F);
     e.dH = bw.take(es * T * x.F);
+    e.dHT = bw.take(es * T * x.F);  // dH transposed, [F][T] (when a plan asks for it)
     e.dY1f = bw.take(es * x.N);
     e.dS1 = bw.take(es * x.N);
     e.dAO = bw.take(es * x.N);
-    e.part_ln2 = bw.take(colsum_part_bytes(ln_bwd_blocks(T, (int)x.I, x.dtype), x.I, 3));
+    // (either LayerNorm-backward form: colsum_blocks bounds both partial counts)
+    e.part_ln2 = bw.take(colsum_part_bytes(colsum_blocks(T), x.I, 3));
     e.part_act = bw.take(colsum_part_bytes(colsum_blocks(T), x.F, 1));
-    e.part_ln1 = bw.take(colsum_part_bytes(ln_bwd_blocks(T, (int)x.I, x.dtype), x.I, 3));
+    e.part_ln1 = bw.take(colsum_part_bytes(colsum_blocks(T), x.I, 3));
     e.m.part = bw.take(colsum_part_bytes(colsum_blocks(T), 3 * x.I, 1));
     e.bwd_split = bw.take(4 * e.split_floats);
     e.bwd_total = bw.total;
@@ -654,11 +656,12 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
                               alpha, gamma, st));
     // Out
     DM_TRY(out_projection(x, gamma, prm->wo, nullptr, ao, DM_BJI, st));
+    const FusedLayout fl = fused_layout(dt, T, (int)x.I, (int)x.F);
     // bias + dropout + residual + LayerNorm 1
     {
         TraceScope t_("F6 bdrln1", st);
         run_bdrln_fwd(dt, T, (int)x.I, ao, prm->bo, x_in, prm->g1, prm->be1, d->ln_eps,
-                      make_drop(d->p_attn_out, d->seed, 1, d->layer_id), y1, xhat1, rstd1, st);
+                      make_drop(d->p_attn_out, d->seed, 1, d->layer_id), y1, xhat1, rstd1, st, fl.ln_lanes);
     }
     DM_TRY(check_launch("bdrln 1"));
     // Linear 1
@@ -689,7 +692,7 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     // bias + dropout + residual + LayerNorm 2
     TraceScope t10("F10 bdrln2", st);
     run_bdrln_fwd(dt, T, (int)x.I, o, prm->b2, y1, prm->g2, prm->be2, d->ln_eps,
-                  make_drop(d->p_ffn_out, d->seed, 2, d->layer_id), y, xhat2, rstd2, st);
+                  make_drop(d->p_ffn_out, d->seed, 2, d->layer_id), y, xhat2, rstd2, st, fl.ln_lanes);
     return check_launch("bdrln 2");
 }
 
@@ -726,15 +729,18 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     float* part_act = (float*)B8(ws, e.part_act);
     float* part_ln1 = (float*)B8(ws, e.part_ln1);
 
+    const FusedLayout fl = fused_layout(dt, T, (int)I, (int)F);
     // LayerNorm-2 scale/shift grads, LayerNorm-2 dX, dropout dX, Linear-2 bias grad
     LnBwdArgs l2{};
+    l2.form = fl.ln_form; l2.lanes = fl.ln_lanes;
     l2.dtype = dt; l2.rows = T; l2.cols = (int)I; l2.dya = dy; l2.xhat = xhat2; l2.gamma = prm->g2; l2.rstd = rstd2;
     l2.dp = make_drop(d->p_ffn_out, d->seed, 2, d->layer_id); l2.ds = dS2; l2.dsub = dO; l2.part = part_ln2;
     l2.want_dsub_sum = 1;
-    // the column-split LayerNorm backward also writes dO transposed, so the
-    // Linear-2 weight gradient reads one operand contiguous along the tokens
+    // the column-split LayerNorm backward can also write dO transposed, so
+    // the Linear-2 weight gradient reads one operand contiguous along the
+    // tokens (the plan's layout choice; on by default)
     void* dOT = B8(ws, e.dOT);
-    const bool have_dOT = ln_bwd_split_ok((int)I, dt);
+    const bool have_dOT = fl.dO_t;
     l2.dsub_t = have_dOT ? dOT : nullptr;
     {
         TraceScope t_("B1-2 ln2_bwd", st);
@@ -758,10 +764,13 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
                            st));
     }
     // dropout / activation backward, Linear-1 bias grad
+    // (with the plan's layout choice, also dH transposed for the Linear-1
+    // weight gradient)
+    void* dHT = fl.dH_t ? B8(ws, e.dHT) : nullptr;
     {
         TraceScope t_("B5 act_bwd", st);
         run_act_bwd(dt, T, (int)F, dA, hbuf, prm->b1, d->act, make_drop(d->p_ffn_act, d->seed, 3, d->layer_id), dH,
-                    part_act, st);
+                    part_act, st, dHT);
     }
     DM_TRY(check_launch("activation backward"));
     // Linear 1 dX and dW
@@ -774,8 +783,9 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     }
     {
         TraceScope t_("B7 linear1_dw", st);
+        const Operand a_op = dHT ? opnd(dHT, true, linear_map(T)) : opnd(dH, false, linear_map(F));
         DM_TRY(launch_gemm(dt,
-                           gemm(F, I, T, 1, opnd(dH, false, linear_map(F)), opnd(y1, false, linear_map(I)),
+                           gemm(F, I, T, 1, a_op, opnd(y1, false, linear_map(I)),
                                 epi(g->dw1, linear_map(I), linear_map(1), true, true)),
                            st));
     }
@@ -783,7 +793,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     LnBwdArgs l1{};
     l1.dtype = dt; l1.rows = T; l1.cols = (int)I; l1.dya = dY1f; l1.dyb = dS2; l1.xhat = xhat1; l1.gamma = prm->g1;
     l1.rstd = rstd1; l1.dp = make_drop(d->p_attn_out, d->seed, 1, d->layer_id); l1.ds = dS1; l1.dsub = dAO;
-    l1.part = part_ln1; l1.want_dsub_sum = 1;
+    l1.part = part_ln1; l1.want_dsub_sum = 1; l1.form = fl.ln_form; l1.lanes = fl.ln_lanes;
     {
         TraceScope t_("B8-10 ln1_bwd", st);
         run_ln_bwd(l1, st);
@@ -806,9 +816,9 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     }
     // LayerNorm-2 (dgamma2, dbeta2, db2), activation (db1), LayerNorm-1
     // (dgamma1, dbeta1, dbo) and input-bias (dbq, dbk, dbv) column sums
-    const int nln = ln_bwd_blocks(T, (int)I, dt), ncs = colsum_blocks(T);
+    const int nln = ln_bwd_blocks(T, (int)I, dt, fl.ln_form), ncs = colsum_blocks(T);
     const FinishJob jobs[4] = {finish_job3(part_ln2, nln, (int)I, g->dg2, g->dbe2, g->db2),
-                               finish_job(part_act, ncs, (int)F, g->db1),
+                               finish_job(part_act, act_bwd_blocks(T, dHT != nullptr), (int)F, g->db1),
                                finish_job3(part_ln1, nln, (int)I, g->dg1, g->dbe1, g->dbo),
                                finish_job_qkv(part, ncs, (int)x.H, (int)x.P, 3, g->dbq, g->dbk, g->dbv)};
     TraceScope tf("B colsum finish", st);

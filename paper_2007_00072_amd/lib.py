@@ -57,6 +57,15 @@ class ContractChoice(C.Structure):
         return (self.M, self.N, self.K, self.batch, self.dtype, self.a_kcontig, self.b_kcontig)
 
 
+class LayoutChoice(C.Structure):
+    """Layout and reduction choices of the fused operators (-1: library's choice)."""
+    _fields_ = [("dO_transposed", C.c_int32), ("dH_transposed", C.c_int32), ("ln_bwd_form", C.c_int32),
+                ("ln_lanes", C.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 class DmError(RuntimeError):
     def __init__(self, code: int, fn: str):
         self.code = code
@@ -133,7 +142,8 @@ _f["dm_trace_enable"] = _sig("dm_trace_enable", I32, I32)
 _f["dm_trace_count"] = _sig("dm_trace_count", I32)
 _f["dm_trace_get"] = _sig("dm_trace_get", I32, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_char_p),
                           C.POINTER(C.c_float))
-_f["plan_create"] = _sig("plan_create", I32, C.POINTER(ContractChoice), I32, I32, C.POINTER(C.c_void_p))
+_f["plan_create"] = _sig("plan_create", I32, C.POINTER(ContractChoice), I32, I32, C.POINTER(LayoutChoice),
+                         C.POINTER(C.c_void_p))
 _f["plan_destroy"] = _sig("plan_destroy", I32, C.c_void_p)
 _f["plan_log"] = _sig("plan_log", I32, I32)
 _f["plan_log_read"] = _sig("plan_log_read", I32, C.POINTER(ContractChoice), I32, C.POINTER(I32))
@@ -341,17 +351,22 @@ def trace_records():
 class Plan:
     """A configuration plan (plan_create) owned by Python: entries are
     ContractChoice records (or (M, N, K, batch, dtype, a_kcontig, b_kcontig,
-    tile_cfg, splits) tuples).  Name it in a descriptor (make_desc(plan=...)
+    tile_cfg, splits) tuples); layout a LayoutChoice or a dict of its fields
+    (missing ones: the library's choice).  Name it in a descriptor (make_desc(plan=...)
     or set_plan) to use it; destroyed with the object."""
 
-    def __init__(self, entries=(), attn_path: int = 0):
+    def __init__(self, entries=(), attn_path: int = 0, layout=None):
         recs = [e if isinstance(e, ContractChoice) else ContractChoice(*e) for e in entries]
         arr = (ContractChoice * max(1, len(recs)))(*recs)
+        if isinstance(layout, dict):
+            layout = LayoutChoice(**{f: int(layout.get(f, -1)) for f, _ in LayoutChoice._fields_})
         h = C.c_void_p()
-        _call("plan_create", arr if recs else None, len(recs), attn_path, C.byref(h))
+        _call("plan_create", arr if recs else None, len(recs), attn_path,
+              C.byref(layout) if layout is not None else None, C.byref(h))
         self.handle = h.value
         self.entries = recs
         self.attn_path = attn_path
+        self.layout = layout
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None

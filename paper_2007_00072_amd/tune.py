@@ -9,15 +9,22 @@ the output, and saves the path to a configuration file used when training
 starts.  Forward and backward passes are optimised separately.
 
 Here the knobs a caller can change are each contraction's kernel, tile and
-split factor (plan entries, ``lib.Plan``) and the grouping of the attention-score
+split factor (plan entries, ``lib.Plan``), the grouping of the attention-score
 steps (``attn_path``: separate launches, scores kept on chip, or scores with
-the next contraction in the same launch).  The tensors between operators
-keep one layout whatever the configuration, so the graph's layout nodes are
-the points between consecutive operators; the attention-score groupings are
-alternative chains of operators between the same two points.  Timings come
-from the library's per-launch events.  A contraction shape that occurs at
-several points of a pass is one decision: its candidates are timed over all
-its occurrences together, and its node sits at the first occurrence.
+the next contraction in the same launch), and the fused operators' layout
+and reduction choices (``lib.LayoutChoice``): whether the LayerNorm-2
+backward and the activation backward also write their output transposed
+for the weight-gradient contraction that reads it (which then reads it
+contiguous along the tokens: a different contraction, with its own
+candidates), the LayerNorm backward's reduction form, and the lanes per
+row of the LayerNorm kernels.  The graph's nodes are the points between
+consecutive operators; each attention grouping and each layout combination
+is an alternative chain of operators between shared points (a stage whose
+time depends on the layout appears once per layout as its own stage).
+Timings come from the library's per-launch events.  A contraction shape
+that occurs at several points of a pass is one decision: its candidates are
+timed over all its occurrences together, and its node sits at the first
+occurrence.
 
 Usage (on the GPU):
     python -m paper_2007_00072_amd.tune --workload bert_large_f16 --out plan.json
@@ -38,6 +45,7 @@ TILE_CFGS = list(range(20))
 KEEP_BUILTIN = 0.97
 SPLITS = (1, 2, 4)
 ATTN_PATHS = (1, 2, 3)   # 1 separate, 2 scores on chip, 3 scores + next contraction
+SWEEP_PATH = 3           # the grouping under which contraction candidates are swept
 
 
 # --------------------------------------------------------------- the graph
@@ -152,10 +160,11 @@ class _Layer:
         self.x = make_activation(wl, 0).to("cuda")
         self.dy = make_activation(wl, 1).to("cuda")
 
-    def use(self, entries=(), attn_path: int = 0):
+    def use(self, entries=(), attn_path: int = 0, layout=None):
         """Runs the layer with this plan from now on (nothing: built-in choices)."""
         from . import lib
-        lib.set_plan(self.layer.desc, lib.Plan(entries, attn_path) if (entries or attn_path) else None)
+        lib.set_plan(self.layer.desc, lib.Plan(entries, attn_path, layout)
+                     if (entries or attn_path or layout) else None)
 
     def step(self):
         self.layer.forward(self.x)
@@ -195,6 +204,38 @@ def _is_fwd(label: str) -> bool:
     return label.startswith("F")
 
 
+# Stages whose time depends on a layout choice, and the fields it depends on
+# (the stage appears once per value of those fields in the graph).
+LAYOUT_STAGES = {
+    "F6 bdrln1": ("ln_lanes",), "F10 bdrln2": ("ln_lanes",),
+    "B1-2 ln2_bwd": ("ln_bwd_form", "dO_transposed", "ln_lanes"), "B8-10 ln1_bwd": ("ln_bwd_form", "ln_lanes"),
+    "B4 linear2_dw": ("dO_transposed",), "B5 act_bwd": ("dH_transposed",), "B7 linear1_dw": ("dH_transposed",),
+    "B colsum finish": ("ln_bwd_form", "dH_transposed"),
+}
+
+
+def layout_options(I: int, dtype: str, T: int):
+    """(forward lane counts, backward layout combinations) a layer of width
+    I in storage type dtype can take; every combination is complete
+    (ln_lanes filled in later from the forward's choice)."""
+    sixteen = dtype != "f32"
+    split_ok = sixteen and I % 64 == 0 and 320 <= I <= 1024
+    lanes = [64, 32, 16] if 256 < I <= 1024 else [64]
+    combos = []
+    for form in ([2, 1] if split_ok else [1]):
+        for dot in ([1, 0] if form == 2 else [0]):
+            for dht in ([0, 1] if sixteen and T % 8 == 0 else [0]):
+                combos.append({"ln_bwd_form": form, "dO_transposed": dot, "dH_transposed": dht})
+    return lanes, combos
+
+
+def stage_name(label: str, layout: dict) -> str:
+    fields = LAYOUT_STAGES.get(label)
+    if not fields:
+        return label
+    return label + " [" + ",".join(f"{f}={layout[f]}" for f in fields) + "]"
+
+
 def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFGS, splits=SPLITS):
     """Measure and select; returns the plan as a dict (see load_plan).
     shape: run the workload's layer at other sizes; tile_cfgs / splits: the
@@ -206,32 +247,70 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
     for _ in range(5):  # clocks and caches settle before anything is timed
         L.step()
     L.torch.cuda.synchronize()
-    # attention groupings: which labels each produces, and their times
-    grouping_times, grouping_labels = {}, {}
-    for p in ATTN_PATHS:
-        L.use((), p)
+    s = L.wl.shape
+    lanes_opts, combos = layout_options(s.I, L.wl.dtype, s.B * s.J)
+    # forward: each lane count (the LayerNorm forward's reduction width)
+    lane_times = {}
+    for ln in lanes_opts:
+        L.use((), 0, {"ln_lanes": ln})
         tm = L.timed(reps)
-        grouping_times[p] = tm
-        grouping_labels[p] = list(tm.keys())
+        lane_times[ln] = tm.get("F6 bdrln1", 0.0) + tm.get("F10 bdrln2", 0.0)
+    lanes = min(lane_times, key=lane_times.get)
+    for c in combos:
+        c["ln_lanes"] = lanes
+    fwd_layout = dict(combos[0])
+    # every (attention grouping, layout combination): per-stage times and
+    # the contractions each stage launches
+    runs = {}
+    for p in ATTN_PATHS:
+        for li, lay in enumerate(combos):
+            L.use((), p, lay)
+            tm = L.timed(reps)
+            runs[(p, li)] = (tm, L.launches())
+    builtin_layout = {"ln_bwd_form": -1, "dO_transposed": -1, "dH_transposed": -1, "ln_lanes": -1}
     L.use()
     base = L.timed(reps)
-    launches = L.launches()
-    # contraction shapes and the labels at which each occurs
+    # stage names per run, fixed-cost stage times (averaged over the runs
+    # that have the stage), and where each contraction shape occurs
+    # (contractions are swept where they run under the library's own
+    # grouping; those of the other groupings keep their measured time)
+    chains_f, chains_b = {}, {}
+    fixed = defaultdict(list)
     where: Dict[tuple, List[str]] = OrderedDict()
-    choice_of = {}
-    for lab, r in launches:
-        where.setdefault(r.key(), [])
-        if lab not in where[r.key()]:
-            where[r.key()].append(lab)
-        choice_of[r.key()] = r
+    occurs_in: Dict[tuple, int] = {}
+    label_key = {}
+    for (p, li), (tm, launches) in runs.items():
+        lay = combos[li]
+        names = {lab: stage_name(lab, lay) for lab in tm}
+        if p == SWEEP_PATH:
+            for lab, r in launches:
+                st = names.get(lab, stage_name(lab, lay))
+                label_key[st] = r.key()
+                where.setdefault(r.key(), [])
+                if st not in where[r.key()]:
+                    where[r.key()].append(st)
+                occurs_in.setdefault(r.key(), li)
+    for (p, li), (tm, launches) in runs.items():
+        lay = combos[li]
+        names = {lab: stage_name(lab, lay) for lab in tm}
+        for lab, t in tm.items():
+            if names[lab] not in label_key:
+                fixed[names[lab]].append(t)
+        fwd = [names[l] for l in tm if _is_fwd(l)]
+        bwd = [names[l] for l in tm if not _is_fwd(l)]
+        if li == 0:
+            chains_f[p] = fwd
+        chains_b[(p, li)] = bwd
     # candidates of every contraction shape, timed over all its occurrences
+    # under a layout where it occurs
     shape_costs: Dict[tuple, Dict[tuple, float]] = {}
-    for key, labs in where.items():
+    for key, sts in where.items():
+        lay = combos[occurs_in[key]]
         seen = {}
         for cfg in tile_cfgs:
             for sp in splits:
                 e = lib.ContractChoice(*key, cfg, sp)
-                L.use([e], 0)
+                L.use([e], 0, lay)
                 ran = {(r.tile_cfg, r.splits) for lab, r in L.launches() if r.key() == key}
                 if len(ran) != 1:
                     continue
@@ -239,63 +318,74 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
                 if eff in seen:
                     continue
                 tm = L.timed(reps)
-                seen[eff] = sum(tm.get(lab, 0.0) for lab in labs)
-        builtin = (choice_of[key].tile_cfg, choice_of[key].splits)
+                names = {lab: stage_name(lab, lay) for lab in tm}
+                seen[eff] = sum(t for lab, t in tm.items() if names[lab] in sts)
+        L.use((), 0, lay)
+        builtin = next(((r.tile_cfg, r.splits) for lab, r in L.launches() if r.key() == key), None)
         if builtin in seen:
             seen[builtin] *= KEEP_BUILTIN
         shape_costs[key] = seen
         best = min(seen.items(), key=lambda kv: kv[1])
-        log(f"  {labs}: {len(seen)} configurations, best {best[0]} {best[1] * 1e3:.1f} us "
-            f"(built-in {(choice_of[key].tile_cfg, choice_of[key].splits)} "
-            f"{sum(base.get(l, 0.0) for l in labs) * 1e3:.1f} us)")
+        log(f"  {sts}: {len(seen)} configurations, best {best[0]} {best[1] * 1e3:.1f} us (built-in {builtin})")
     L.use()
-    # one graph per pass; contraction stages carry their shape's candidates
-    # at the first occurrence, later occurrences cost nothing
-    label_key = {}
-    for key, labs in where.items():
-        for lab in labs:
-            label_key[lab] = key
-    first = {labs[0] for labs in where.values()}
+
+    def costs_for(chains):
+        # a contraction shape carries its candidates at its first stage of a
+        # chain; its later stages in the same chain cost nothing more
+        costs, firsts, laters = {}, set(), set()
+        for stages in chains.values():
+            seen_keys = set()
+            for st in stages:
+                k = label_key.get(st)
+                if k in shape_costs:
+                    (laters if k in seen_keys else firsts).add(st)
+                    seen_keys.add(k)
+        if firsts & laters:
+            raise RuntimeError(f"stages both first and repeated: {sorted(firsts & laters)}")
+        for stages in chains.values():
+            for st in stages:
+                if st in firsts:
+                    costs[st] = {("cfg",) + c: t for c, t in shape_costs[label_key[st]].items()}
+                elif st in laters:
+                    costs[st] = {("same",): 0.0}
+                else:
+                    costs[st] = {("fixed",): sum(fixed[st]) / len(fixed[st])}
+        return costs
+
     result = {"workload": workload, "passes": {}}
     chosen = {}
-    attn_total = {p: 0.0 for p in ATTN_PATHS}
-    per_pass = {}
-    for pass_name, in_pass in (("forward", _is_fwd), ("backward", lambda l: not _is_fwd(l))):
-        chains, costs = {}, {}
-        for p in ATTN_PATHS:
-            stages = [l for l in grouping_labels[p] if in_pass(l)]
-            chains[p] = stages
-            for st in stages:
-                if st in label_key and label_key[st] in shape_costs:
-                    # a shape's occurrence inside one grouping only is timed per grouping
-                    if st in first:
-                        costs[st] = {("cfg",) + c: t for c, t in shape_costs[label_key[st]].items()}
-                    else:
-                        costs[st] = {("same",): 0.0}
-                else:
-                    costs[st] = {("fixed", p): grouping_times[p][st]}
-        t, grouping, cfgs = select(chains, costs)
-        per_pass[pass_name] = (t, grouping, cfgs)
+    # one grouping knob and one layout serve both passes: per grouping, the
+    # forward's best and the backward's best over the layouts; the grouping
+    # with the lower total wins
+    cf, cb = costs_for(chains_f), costs_for(chains_b)
+    totals = {}
+    for p in ATTN_PATHS:
+        tf, _, cfg_f = select({p: chains_f[p]}, cf)
+        tb, key_b, cfg_b = select({k: v for k, v in chains_b.items() if k[0] == p}, cb)
+        totals[p] = (tf + tb, tf, tb, key_b[1], cfg_f, cfg_b)
+    attn_path = min(totals, key=lambda q: totals[q][0])
+    _, tf, tb, li, cfg_f, cfg_b = totals[attn_path]
+    layout = dict(combos[li])
+    for pass_name, t, cfgs in (("forward", tf, cfg_f), ("backward", tb, cfg_b)):
         for st, c in cfgs.items():
             if c[0] == "cfg" and st in label_key:
                 chosen[label_key[st]] = c[1:]
-        result["passes"][pass_name] = {"predicted_ms": t, "attn_path": grouping,
+        result["passes"][pass_name] = {"predicted_ms": t, "attn_path": attn_path,
                                         "stages": {st: list(c) for st, c in cfgs.items()}}
-        for p in ATTN_PATHS:
-            sub = {p: chains[p]}
-            try:
-                attn_total[p] += select(sub, costs)[0]
-            except RuntimeError:
-                attn_total[p] = math.inf
-    # one grouping knob serves both passes: the one with the lower total
-    groupings = {v[1] for v in per_pass.values()}
-    attn_path = groupings.pop() if len(groupings) == 1 else min(attn_total, key=attn_total.get)
+    # the backward's best time under each layout (this grouping): the
+    # measured value of each layout choice
+    result["layout_table"] = []
+    for k in sorted(k for k in chains_b if k[0] == attn_path):
+        t, _, _ = select({k: chains_b[k]}, cb)
+        result["layout_table"].append(dict(combos[k[1]], backward_ms=round(t, 4)))
+    result["lane_table"] = {str(k): round(v, 4) for k, v in lane_times.items()}
     entries = []
     for key, (cfg, sp) in chosen.items():
         e = lib.ContractChoice(*key, cfg, sp)
         e.label = ",".join(where[key]).encode()[:47]
         entries.append(e)
     result["attn_path"] = attn_path
+    result["layout"] = layout
     result["entries"] = [dict(M=e.M, N=e.N, K=e.K, batch=e.batch, dtype=e.dtype, a_kcontig=e.a_kcontig,
                               b_kcontig=e.b_kcontig, tile_cfg=e.tile_cfg, splits=e.splits,
                               label=e.label.decode()) for e in entries]
@@ -305,7 +395,7 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
     table = fusion_table(workload, reps, shape)
     result["qkv_fusion_table"] = table
     result["qkv_fusion"] = min(table, key=lambda f: table[f]["forward"] + table[f]["backward"])
-    L.use(entries, attn_path)
+    L.use(entries, attn_path, layout)
     result["planned_ms"] = sum(L.timed(reps).values())
     L.use()
     result["tuning_seconds"] = round(time.time() - t0, 1)
@@ -342,7 +432,7 @@ def load_plan(path: str):
         plan = json.load(f)
     entries = [lib.ContractChoice(e["M"], e["N"], e["K"], e["batch"], e["dtype"], e["a_kcontig"], e["b_kcontig"],
                                   e["tile_cfg"], e["splits"]) for e in plan["entries"]]
-    return plan, lib.Plan(entries, int(plan["attn_path"]))
+    return plan, lib.Plan(entries, int(plan["attn_path"]), plan.get("layout"))
 
 
 def main() -> int:
@@ -364,7 +454,8 @@ def main() -> int:
     with open(a.out, "w") as f:
         json.dump(res, f, indent=1)
     print(f"built-in {res['builtin_ms']:.3f} ms, planned {res['planned_ms']:.3f} ms (sum of launches), "
-          f"attn_path {res['attn_path']}, {len(res['entries'])} entries, {res['tuning_seconds']} s", flush=True)
+          f"attn_path {res['attn_path']}, layout {res['layout']}, {len(res['entries'])} entries, "
+          f"{res['tuning_seconds']} s", flush=True)
     return 0
 
 

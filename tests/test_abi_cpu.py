@@ -190,14 +190,15 @@ def test_fused_op_validation(lib):
 
 def test_plan_objects_host_only(lib):
     # plan_create / plan_destroy are host code: validation and ownership
-    p = lib.Plan([(64, 64, 64, 1, lib.DM_F16, 1, 1, 13, 2)], 3)
-    assert p.handle and p.attn_path == 3
+    p = lib.Plan([(64, 64, 64, 1, lib.DM_F16, 1, 1, 13, 2)], 3, {"dH_transposed": 1, "ln_lanes": 32})
+    assert p.handle and p.attn_path == 3 and p.layout.ln_lanes == 32 and p.layout.ln_bwd_form == -1
     d = lib.make_desc(__import__("paper_2007_00072_amd.inputs", fromlist=["Shape"]).Shape(
         B=1, J=8, K=8, H=1, P=8, W=8, I=8, F=8), "f16", plan=p)
     assert d.plan == p.handle and d._plan_ref is p
     lib.set_plan(d, None)
     assert not d.plan
-    for bad in [((), 4), ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 20, 1)], 0),
+    for bad in [((), 0, {"ln_lanes": 24}), ((), 0, {"ln_bwd_form": 3}), ((), 0, {"dH_transposed": 2}),
+                ((), 4), ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 20, 1)], 0),
                 ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 5, 0)], 0), ([(0, 64, 64, 1, lib.DM_F16, 1, 1, 5, 1)], 0)]:
         with pytest.raises(lib.DmError):
             lib.Plan(*bad)

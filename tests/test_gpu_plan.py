@@ -108,6 +108,8 @@ def test_tuner_end_to_end(tmp_path):
     path.write_text(json.dumps(res))
     plan, cplan = tune.load_plan(str(path))
     assert plan["attn_path"] == res["attn_path"] == cplan.attn_path
+    assert set(plan["layout"]) == {"ln_bwd_form", "dO_transposed", "dH_transposed", "ln_lanes"}
+    assert len(res["layout_table"]) >= 2
     wl = small("bert_large_f16", B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
     check_encoder(wl, layer=0, plan=cplan, qkv_fusion=int(plan["qkv_fusion"]))
 
@@ -122,3 +124,35 @@ def test_saved_bert_base_plan_keeps_parity():
     recs, _ = _launches(WORKLOADS["bert_base_bf16"], cplan)
     assert any((r.tile_cfg, r.splits) == (13, 4) for r in recs)
     check_encoder(WORKLOADS["bert_base_bf16"], plan=cplan, qkv_fusion=int(plan.get("qkv_fusion", 0)))
+
+
+@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
+@pytest.mark.parametrize("layout", [
+    {"dO_transposed": 0},
+    {"dH_transposed": 1},
+    {"ln_bwd_form": 1},
+    {"ln_bwd_form": 1, "ln_lanes": 32},
+    {"ln_lanes": 16, "dH_transposed": 1, "dO_transposed": 1},
+])
+def test_layout_choices_keep_parity(name, layout):
+    # the fused operators' layout and reduction choices (transposed copies
+    # for the weight gradients, LayerNorm backward form, lanes per row):
+    # the contraction reading a transposed copy changes operand layout,
+    # results match the oracle at every choice (144 tokens: ragged tiles)
+    wl = small(name, B=2, J=72, K=72, H=6, P=64, W=64, I=384, F=768)
+    plan = lib.Plan([], 0, layout)
+    recs, _ = _launches(wl, plan)
+    by = {r.label.decode(): r for r in recs}
+    dot = layout.get("dO_transposed", -1) != 0 and layout.get("ln_bwd_form", -1) != 1
+    assert by["B4 linear2_dw"].a_kcontig == (1 if dot else 0)
+    assert by["B7 linear1_dw"].a_kcontig == (1 if layout.get("dH_transposed") == 1 else 0)
+    check_encoder(wl, layer=1, plan=plan)
+
+
+def test_layout_choice_validation():
+    with pytest.raises(lib.DmError):
+        lib.Plan([], 0, {"ln_lanes": 24})
+    with pytest.raises(lib.DmError):
+        lib.Plan([], 0, {"ln_bwd_form": 3})
+    with pytest.raises(lib.DmError):
+        lib.Plan([], 0, {"dH_transposed": 2})

@@ -81,3 +81,46 @@ def test_saved_plans_are_well_formed():
         for e in plan["entries"]:
             assert 0 <= e["tile_cfg"] <= 19 and 1 <= e["splits"] <= 64, (path, e)
             assert e["M"] > 0 and e["N"] > 0 and e["K"] > 0 and e["batch"] >= 1
+
+
+def layout_case(rng):
+    # chains keyed by (attention grouping, layout combination): layout
+    # choices rename the stages whose time they change, as the tuner does
+    pre = ["F1", "F2"]
+    groupings = {1: ["a1", "a2"], 2: ["b1"], 3: ["c1"]}
+    layouts = [{"d": 1, "f": 2}, {"d": 0, "f": 2}, {"d": 0, "f": 1}]
+    chains = {}
+    for p, mid in groupings.items():
+        for li, lay in enumerate(layouts):
+            stages = pre + [f"LN [{lay['f']},{lay['d']}]", "W", f"Wd [{lay['d']}]"] + mid + ["G", f"fin [{lay['f']}]"]
+            chains[(p, li)] = stages
+    costs = {}
+    for stages in chains.values():
+        for st in stages:
+            if st not in costs:
+                costs[st] = {(k,): rng.uniform(0.1, 10.0) for k in range(rng.randint(1, 3))}
+    return chains, costs
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_layout_selection_equals_brute_force(seed):
+    rng = random.Random(1000 + seed)
+    chains, costs = layout_case(rng)
+    t, key, cfgs = tune.select(chains, costs)
+    bt, bkey, _ = brute_force(chains, costs)
+    assert t == pytest.approx(bt, rel=1e-12)
+    assert set(cfgs) == set(chains[key])
+
+
+def test_layout_options_and_stage_names():
+    lanes, combos = tune.layout_options(1024, "f16", 4096)
+    assert lanes == [64, 32, 16]
+    # column-split form with and without dO^T, row form without it; dH^T on or off
+    assert len(combos) == 6
+    assert {(c["ln_bwd_form"], c["dO_transposed"]) for c in combos} == {(2, 1), (2, 0), (1, 0)}
+    assert all(c["dO_transposed"] == 0 for c in combos if c["ln_bwd_form"] == 1)
+    lanes, combos = tune.layout_options(32, "f32", 64)
+    assert lanes == [64] and combos == [{"ln_bwd_form": 1, "dO_transposed": 0, "dH_transposed": 0}]
+    lay = {"ln_bwd_form": 2, "dO_transposed": 1, "dH_transposed": 0, "ln_lanes": 64}
+    assert tune.stage_name("B4 linear2_dw", lay) == "B4 linear2_dw [dO_transposed=1]"
+    assert tune.stage_name("B3 linear2_dx", lay) == "B3 linear2_dx"
