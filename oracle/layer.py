@@ -235,7 +235,9 @@ def mha_forward(q, k, v, prm: Dict[str, np.ndarray], cfg: Config, out_bias: bool
                 Sh_m = Sh
             e = np.exp(Sh_m - Sh_m.max(axis=1, keepdims=True))
             Ph = e / e.sum(axis=1, keepdims=True)                  # softmax over the keys
-            Ah = r(Ph * m_attn[h, b])                              # dropout of the probabilities
+            # dropout of the probabilities as the operator stores them (rounded):
+            # alpha is a function of the stored P and the mask alone
+            Ah = r(r(Ph) * m_attn[h, b])
             Ch = r(Ah @ Vh)                                         # [J, W]
             out[:, b, :] += (Ch @ prm["wo"][:, h, :]).T             # the head's share of Out
             head_q[:, h, b, :], head_k[:, h, b, :], head_v[:, h, b, :] = Qh.T, Kh.T, Vh.T

@@ -107,8 +107,8 @@ def test_softmax_dropout_fwd(lib, dt, K):
     fac = philox.dropout_factor(9, 0, 4, 0.2, (H, B, J, K)).transpose(1, 0, 2, 3)
     assert_close("prob", prob, rnd(p, dt), dt)
     a = f64(alpha)
-    np.testing.assert_array_equal(a == 0, (fac == 0) | (rnd(p * fac, dt) == 0))
-    assert_close("alpha", alpha, rnd(p * fac, dt), dt)
+    np.testing.assert_array_equal(a == 0, (fac == 0) | (rnd(rnd(p, dt) * fac, dt) == 0))
+    assert_close("alpha", alpha, rnd(rnd(p, dt) * fac, dt), dt)
 
 
 # ------------------------------------------------------------ bias + act

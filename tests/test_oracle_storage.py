@@ -15,8 +15,8 @@ arithmetic:
   the oracle's value bit for bit; every value the emulation keeps inside a
   fused operator must not be rounded.  A rounding that is missing,
   misplaced (taken before instead of after a bias or a dropout) or taken
-  from the wrong operand (alpha from the rounded instead of the unrounded
-  probabilities) fails one of these comparisons.
+  from the wrong operand (alpha from the unrounded instead of the stored,
+  rounded probabilities) fails one of these comparisons.
 """
 import numpy as np
 import pytest
@@ -110,7 +110,7 @@ def test_rounding_points(dt, act):
     same("beta", beta, R(cfg.s * torch.einsum("bhjp,bhkp->bhjk", qq, kk)))
     pr = torch.softmax(beta, dim=-1)                                   # unrounded inside `sm`
     same("prob", prob, R(pr))
-    same("alpha", alpha, R(pr * m_attn))                               # from the unrounded probabilities
+    same("alpha", alpha, R(R(pr) * m_attn))                            # from the rounded (stored) probabilities
     same("gamma", gamma, R(torch.einsum("bhjk,bhkw->bhjw", alpha, vv)))
     ctx = gamma.permute(0, 2, 1, 3).reshape(B, J, H * cfg.W)
     same("ao", ao, R(ctx @ p["wo"].permute(1, 0, 2).reshape(H * cfg.W, I)))
