@@ -261,13 +261,18 @@ def mha_backward(dout, cache, prm, cfg: Config, out_bias: bool = True):
     # Out dX and dW.
     dgamma = r(contract("whi,ibj->whbj", wo, dout))
     g["wo"] = contract("whbj,ibj->whi", cache["gamma"], dout)
-    # Gamma dX1 (w.r.t. alpha) and dX2 (w.r.t. vv).
-    dalpha = r(contract("whbk,whbj->hbjk", cache["vv"], dgamma))
+    # Gamma dX1 (w.r.t. alpha) and dX2 (w.r.t. vv).  d(alpha) feeds only the
+    # softmax backward, which takes it inside the same fused operator: it is
+    # not rounded.
+    dalpha = contract("whbk,whbj->hbjk", cache["vv"], dgamma)
     dvv = r(contract("hbjk,whbj->whbk", cache["alpha"], dgamma))
-    # Scaled softmax dX: dropout backward, softmax backward, scaling.
+    # Scaled softmax dX: dropout backward, softmax backward, scaling.  The
+    # softmax backward's row term sum_k dP P equals sum_k d(alpha) alpha
+    # (dP = m d(alpha) and alpha = m P, m the dropout factor); it is taken
+    # with alpha as stored.
     prob = cache["prob"]
     dprob = dalpha * cache["m_attn"]
-    dbeta = r(cfg.s * prob * (dprob - (dprob * prob).sum(axis=-1, keepdims=True)))
+    dbeta = r(cfg.s * prob * (dprob - (dalpha * cache["alpha"]).sum(axis=-1, keepdims=True)))
     # QK^T dX1 (w.r.t. qq) and dX2 (w.r.t. kk).
     dqq = r(contract("hbjk,phbk->phbj", dbeta, cache["kk"]))
     dkk = r(contract("hbjk,phbj->phbk", dbeta, cache["qq"]))

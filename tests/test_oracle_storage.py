@@ -157,12 +157,15 @@ def test_rounding_points(dt, act):
     dgamma = head(it["dgamma"])
     wo_hw = p["wo"].permute(1, 0, 2)                                   # [h,w,i]
     same("dgamma", dgamma, R(torch.einsum("bji,hwi->bhjw", dAO, wo_hw)))
-    dalpha = hbjk(it["dalpha"])
-    same("dalpha", dalpha, R(torch.einsum("bhjw,bhkw->bhjk", dgamma, vv)))
+    dalpha = hbjk(it["dalpha"])                                        # inside the fused score backward
+    assert torch.allclose(dalpha, torch.einsum("bhjw,bhkw->bhjk", dgamma, vv), rtol=1e-12, atol=1e-14)
     same("dvv", head(it["dvv"]), R(torch.einsum("bhjk,bhjw->bhkw", alpha, dgamma)))
     dprob = dalpha * m_attn                                            # inside `bs`
     dbeta = hbjk(it["dbeta"])
-    same("dbeta", dbeta, R(cfg.s * prob * (dprob - (dprob * prob).sum(-1, keepdim=True))))
+    # row term: sum_k d(alpha) alpha with alpha as stored (= sum_k dP P exactly)
+    same("dbeta", dbeta, R(cfg.s * prob * (dprob - (dalpha * alpha).sum(-1, keepdim=True))))
+    # ... which is a different rounding reading from sum_k dP P over the stored P
+    assert not torch.equal(dbeta, R(cfg.s * prob * (dprob - (dprob * prob).sum(-1, keepdim=True))))
     dqq, dkk = head(it["dqq"]), head(it["dkk"])
     same("dqq", dqq, R(torch.einsum("bhjk,bhkp->bhjp", dbeta, kk)))
     same("dkk", dkk, R(torch.einsum("bhjk,bhjp->bhkp", dbeta, qq)))
@@ -172,7 +175,8 @@ def test_rounding_points(dt, act):
     same("dx", _t(dx), R(dXa + dS1))                                   # `bei` in the Q/K/V dX epilogue
 
     # values kept inside one fused operator are not rounded
-    for name, v in (("s1", s1), ("u", u), ("s2", s2), ("dY1", dY1), ("dXa", dXa), ("dprob", dprob[m_attn != 0])):
+    for name, v in (("s1", s1), ("u", u), ("s2", s2), ("dY1", dY1), ("dXa", dXa), ("dalpha", dalpha),
+                    ("dprob", dprob[m_attn != 0])):
         v = v.numpy()
         frac = float(np.mean(L.store(v, dt) == v))
         assert frac < 0.5, (name, frac)
