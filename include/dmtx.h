@@ -272,7 +272,7 @@ int dropout_mask(uint64_t seed, uint32_t site, uint32_t layer, float p, uint64_t
 typedef enum {
     DM_SAVED_QKV = 0,    /* [3][B][H][J][P]: projections with input bias (head-major) */
     DM_SAVED_PROB = 1,   /* [B][H][J][K] softmax output                                */
-    DM_SAVED_ALPHA = 2,  /* [B][H][J][K] after dropout                                 */
+    DM_SAVED_ALPHA = 2,  /* not saved (DM_ERR_ARG): re-formed from P and the mask      */
     DM_SAVED_GAMMA = 3,  /* [B][J][H][W] attention context                             */
     DM_SAVED_XHAT1 = 4,  /* [B][J][I]                                                  */
     DM_SAVED_RSTD1 = 5,  /* float [B*J]                                                */
@@ -284,6 +284,15 @@ typedef enum {
     DM_SAVED_COUNT = 11
 } dm_saved_id;
 int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t* bytes);
+
+/* Which attention-score backward the calls with this descriptor take (its
+ * shape, dtype and plan decide): *key_blocks = 1 for the key-block form
+ * (Gamma dX1, the softmax + dropout backward and both QK^T gradients in
+ * one pass over key blocks: d(alpha) is never stored and the softmax
+ * backward's row term is sum_k d(alpha) alpha, formed as d(gamma) . gamma
+ * before gamma's rounding), 0 for the row form (d(alpha) stored in the
+ * storage type, row term sum_k dP P).  The two differ only in rounding. */
+int attn_backward_form(const dm_layer_desc* d, int32_t* key_blocks);
 
 /* General contraction on the library's MFMA kernel, for op-level tests:
  * C[z][m][n] = alpha * sum_k A[z][m][k] * B[z][k][n] (+ bias[n]) with

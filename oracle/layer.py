@@ -168,6 +168,12 @@ class Config:
     act: str = "gelu"
     store_dtype: str = "f64"
     causal: bool = False     # decoder self-attention: query j attends to keys k <= j
+    # Storage emulation of the attention-score backward (no effect without
+    # storage rounding): False, d(alpha) stays inside the fused score
+    # backward (not rounded) and the softmax backward's row term is
+    # sum_k d(alpha) alpha; True, Gamma dX1 stores d(alpha) in the storage
+    # type and the row term is sum_k dP P over it.
+    dalpha_stored: bool = False
 
     @property
     def s(self) -> float:
@@ -261,18 +267,22 @@ def mha_backward(dout, cache, prm, cfg: Config, out_bias: bool = True):
     # Out dX and dW.
     dgamma = r(contract("whi,ibj->whbj", wo, dout))
     g["wo"] = contract("whbj,ibj->whi", cache["gamma"], dout)
-    # Gamma dX1 (w.r.t. alpha) and dX2 (w.r.t. vv).  d(alpha) feeds only the
-    # softmax backward, which takes it inside the same fused operator: it is
-    # not rounded.
+    # Gamma dX1 (w.r.t. alpha) and dX2 (w.r.t. vv).
     dalpha = contract("whbk,whbj->hbjk", cache["vv"], dgamma)
+    if cfg.dalpha_stored:
+        dalpha = r(dalpha)
     dvv = r(contract("hbjk,whbj->whbk", cache["alpha"], dgamma))
     # Scaled softmax dX: dropout backward, softmax backward, scaling.  The
-    # softmax backward's row term sum_k dP P equals sum_k d(alpha) alpha
-    # (dP = m d(alpha) and alpha = m P, m the dropout factor); it is taken
-    # with alpha as stored.
+    # row term sum_k dP P equals sum_k d(alpha) alpha (dP = m d(alpha) and
+    # alpha = m P, m the dropout factor); with d(alpha) kept inside the
+    # fused operator it is taken in that form, with alpha as stored.
     prob = cache["prob"]
     dprob = dalpha * cache["m_attn"]
-    dbeta = r(cfg.s * prob * (dprob - (dalpha * cache["alpha"]).sum(axis=-1, keepdims=True)))
+    if cfg.dalpha_stored:
+        row = (dprob * prob).sum(axis=-1, keepdims=True)
+    else:
+        row = (dalpha * cache["alpha"]).sum(axis=-1, keepdims=True)
+    dbeta = r(cfg.s * prob * (dprob - row))
     # QK^T dX1 (w.r.t. qq) and dX2 (w.r.t. kk).
     dqq = r(contract("hbjk,phbk->phbj", dbeta, cache["kk"]))
     dkk = r(contract("hbjk,phbj->phbk", dbeta, cache["qq"]))

@@ -146,7 +146,7 @@ __global__ __launch_bounds__(NT) void softmax_fwd_k(int64_t rows, int B, int H, 
         const int c = (gl + i * LPR) * 8;
         if (c < K) {
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v[i][q] *= rinv;
+            for (int q = 0; q < 8; ++q) v[i][q] = to_f(from_f<T>(v[i][q] * rinv));  // P as stored
             V8<T>::store(prob + base + c, v[i]);
             dropout8(dp, (uint64_t)(ebase + c), v[i]);
             V8<T>::store(alpha + base + c, v[i]);
@@ -200,6 +200,28 @@ __global__ __launch_bounds__(NT) void softmax_bwd_k(int64_t rows, int B, int H, 
             V8<T>::store(dbeta + base + c, o);
         }
     }
+}
+
+// ------------------------------------------------------ alpha from the stored P
+// alpha = dropout(P) re-formed from the saved probabilities (the forward
+// forms it from the same rounded values and the same keep decisions, so the
+// result is bit-identical); thread t handles 8 consecutive keys of one row.
+template <typename T>
+__global__ __launch_bounds__(256) void alpha_from_prob_k(int64_t n8, int B, int H, int J, int K,
+                                                         const T* __restrict__ prob, DropParams dp,
+                                                         T* __restrict__ alpha) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= n8) return;
+    const int64_t e = t * 8;
+    const int64_t row = e / K;  // (b, h, j)
+    const int c = (int)(e - row * K);
+    const int j = (int)(row % J);
+    const int64_t bh = row / J;
+    const int h = (int)(bh % H), b = (int)(bh / H);
+    float v[8];
+    V8<T>::load(prob + e, v);
+    dropout8(dp, (uint64_t)((((int64_t)h * B + b) * J + j) * (int64_t)K + c), v);
+    V8<T>::store(alpha + e, v);
 }
 
 // ------------------------------------------------------ LayerNorm backward family
@@ -925,6 +947,13 @@ void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const v
 void run_softmax_bwd(int dtype, int B, int H, int J, int K, float scale, const void* dalpha, const void* prob,
                      const DropParams& dp, void* dbeta, hipStream_t st) {
     DM_DTYPE_SWITCH(dtype, softmax_bwd_t<T>(B, H, J, K, scale, dalpha, prob, dp, dbeta, st));
+}
+
+void run_alpha_from_prob(int dtype, int B, int H, int J, int K, const void* prob, const DropParams& dp, void* alpha,
+                         hipStream_t st) {
+    const int64_t n8 = (int64_t)B * H * J * K / 8;
+    DM_DTYPE_SWITCH(dtype, hipLaunchKernelGGL((alpha_from_prob_k<T>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0,
+                                              st, n8, B, H, J, K, (const T*)prob, dp, (T*)alpha));
 }
 
 void run_ln_bwd(const LnBwdArgs& a, hipStream_t st) { DM_DTYPE_SWITCH(a.dtype, ln_bwd_t<T>(a, st)); }

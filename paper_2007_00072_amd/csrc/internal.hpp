@@ -120,6 +120,7 @@ struct AttnNext {
     void* out = nullptr;
     int64_t o_outer = 0, o_inner = 0, o_ld = 0;
     int N = 0;
+    float* out_f32 = nullptr;  // optional fp32 copy of out before rounding (same strides)
 };
 bool attn_next_ok(int dtype, int K, int D, const AttnNext& n);
 // P = softmax_k(round(scaler * Q K^T)), alpha = dropout(P); with `next`,
@@ -134,6 +135,27 @@ void run_attn_scores_bwd(int dtype, int B, int H, int J, int K, int D, float sca
                          int64_t dg_outer, int64_t dg_inner, int64_t dg_ld, const void* v, int64_t v_outer,
                          int64_t v_inner, int64_t v_ld, const void* prob, const DropParams& dp, void* dbeta,
                          const AttnNext* next, hipStream_t st);
+
+// Key-block backward of the attention scores (attn.hip): from d(gamma),
+// gamma (fp32, before rounding), P and Q, K, V it writes dQ, dK, dV (the
+// rows of Table 3 from Gamma dX1 to QK^T dX2) without materialising
+// d(alpha), alpha or d(beta).
+// Row operands as for the score kernels: element (z = b*H + h, row r, d) at
+// ptr + b*outer + h*inner + r*ld + d.  attn_keys_ok: fp16 / bf16, P = W =
+// 64, K a multiple of 128 (all rows 16-byte aligned).  part: fp32 scratch of
+// attn_keys_part_bytes (nullptr allowed when that is 0).
+struct AttnRows {
+    const void* ptr;
+    int64_t outer, inner, ld;
+};
+bool attn_keys_ok(int dtype, int K, int P, int W);
+size_t attn_keys_part_bytes(int B, int H, int J, int K);
+void run_attn_bwd_keys(int dtype, int B, int H, int J, int K, float scaler, AttnRows q, AttnRows k, AttnRows v,
+                       AttnRows dgamma, AttnRows gamma, const void* prob, const DropParams& dp, AttnRows dq,
+                       AttnRows dk, AttnRows dv, float* part, hipStream_t st);
+// alpha = dropout(P) from the stored probabilities [B][H][J][K] (K % 8 == 0)
+void run_alpha_from_prob(int dtype, int B, int H, int J, int K, const void* prob, const DropParams& dp, void* alpha,
+                         hipStream_t st);
 
 // causal: query row j sees keys k <= j only (probabilities after it exactly 0)
 void run_softmax_fwd(int dtype, int B, int H, int J, int K, float scale, const void* beta,

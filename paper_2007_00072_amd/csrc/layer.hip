@@ -51,12 +51,15 @@ struct Carver {
 };
 
 struct MhaPlan {
-    // saved
-    size_t q, k, v, prob, alpha, gamma;
-    // forward workspace
-    size_t beta;
-    // backward workspace
-    size_t dgamma, dalpha, dbeta, dq, dk, dv, part;
+    // saved (alpha is not: it is re-formed from P and the dropout keep
+    // decisions where a step needs it); gamma32: gamma before rounding, in
+    // fp32, for the key-block backward's row term (0 = not saved)
+    size_t q, k, v, prob, gamma, gamma32;
+    // forward workspace (alpha for the launch groupings that read it back)
+    size_t beta, alpha_f;
+    // backward workspace (alpha re-formed for the groupings that read it;
+    // the key-block backward keeps its dQ partial sums in dalpha)
+    size_t dgamma, dalpha, dbeta, alpha_b, dq, dk, dv, part;
     int64_t ldq, ldk, ldv;  // row strides (elements) of the Q/K/V gradient buffers
     size_t fused_dqkv;      // self-attention: one [T][3][H][P] buffer at dq
 };
@@ -103,12 +106,18 @@ void plan_attention(const Dims& x, int mode, Carver& sv, Carver& fw, Carver& bw,
         p.v = sv.take(es * x.B * x.H * x.K * x.W);
     }
     p.prob = sv.take(es * x.S);
-    p.alpha = sv.take(es * x.S);
     p.gamma = sv.take(es * x.Tq * x.H * x.W);
+    p.gamma32 = attn_keys_ok(x.dtype, (int)x.K, (int)x.P, (int)x.W) ? sv.take(4 * x.Tq * x.H * x.W) : 0;
     p.beta = fw.take(es * x.S);
+    p.alpha_f = fw.take(es * x.S);
     p.dgamma = bw.take(es * x.Tq * x.H * x.W);
-    p.dalpha = bw.take(es * x.S);
+    // (dQ partials of the key-block backward: at most 4 B x 64 per query
+    // row and 128-key block, no more than 2 B per score)
+    p.dalpha = bw.take(es * x.S > attn_keys_part_bytes((int)x.B, (int)x.H, (int)x.J, (int)x.K)
+                           ? es * x.S
+                           : attn_keys_part_bytes((int)x.B, (int)x.H, (int)x.J, (int)x.K));
     p.dbeta = bw.take(es * x.S);
+    p.alpha_b = bw.take(es * x.S);
     if (mode == PROJ_QKV) {
         p.ldq = p.ldk = p.ldv = 3 * x.H * x.P;
         p.dq = bw.take(es * x.Tq * p.ldq);
@@ -371,9 +380,11 @@ int project_fused(const Dims& x, int layout, const void* in, const dm_layer_para
     return DM_OK;
 }
 
-// QK^T -> softmax + dropout -> alpha.V ; gamma token-major [Tq][H][W].
+// QK^T -> softmax + dropout -> alpha.V ; gamma token-major [Tq][H][W]
+// (and, when gamma32 is not null, the same in fp32 before rounding).
 int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const void* q, const void* k,
-                       const void* v, void* beta, void* prob, void* alpha, void* gamma, hipStream_t st) {
+                       const void* v, void* beta, void* prob, void* alpha, void* gamma, float* gamma32,
+                       hipStream_t st) {
     const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, HW = x.H * x.W;
     const int path = current_attn_path();
     if (path != 1 && attn_fused_ok(x.dtype, (int)K, (int)P)) {
@@ -382,10 +393,13 @@ int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const 
         AttnNext nx;
         nx.x = v; nx.x_outer = x.H * K * W; nx.x_inner = K * W; nx.x_ld = W;
         nx.out = gamma; nx.o_outer = J * HW; nx.o_inner = W; nx.o_ld = HW; nx.N = (int)W;
+        nx.out_f32 = gamma32;
         const bool with_gamma = path != 2 && attn_next_ok(x.dtype, (int)K, (int)P, nx);
         TraceScope t_(with_gamma ? "F2-4 qkt_softmax_gamma" : "F2-3 qkt_softmax", st);
+        // (with Gamma in the same launch alpha stays on chip)
         run_attn_scores_fwd(x.dtype, (int)x.B, (int)x.H, (int)J, (int)K, (int)P, scaler, q, x.H * J * P, J * P, P, k,
-                            x.H * K * P, K * P, P, dp, prob, alpha, with_gamma ? &nx : nullptr, st, x.causal);
+                            x.H * K * P, K * P, P, dp, prob, with_gamma ? nullptr : alpha, with_gamma ? &nx : nullptr,
+                            st, x.causal);
         DM_TRY(check_launch("attention scores"));
         if (with_gamma) return DM_OK;
     } else {
@@ -406,12 +420,17 @@ int attention_core_fwd(const Dims& x, float scaler, const DropParams& dp, const 
     DM_TRY(check_launch("softmax"));
     }
     // gamma[(b,j)][(h,w)] = sum_k alpha[z][j][k] V[z][k][w]
-    Epilogue cg = epi(gamma, linear_map(HW), linear_map(1), true, false, make_map((uint32_t)x.H, 0, W, J * HW, 0));
     TraceScope t_("F4 gamma", st);
-    return launch_gemm(x.dtype,
-                       gemm(J, W, K, Z, opnd(alpha, true, linear_map(K), linear_map(J * K)),
-                            opnd(v, false, linear_map(W), linear_map(K * W)), cg),
-                       st);
+    for (int f32 = 0; f32 < (gamma32 ? 2 : 1); ++f32) {
+        if (f32) trace_next("fp32");
+        Epilogue cg = epi(f32 ? static_cast<void*>(gamma32) : gamma, linear_map(HW), linear_map(1), true, f32 != 0,
+                          make_map((uint32_t)x.H, 0, W, J * HW, 0));
+        DM_TRY(launch_gemm(x.dtype,
+                           gemm(J, W, K, Z, opnd(alpha, true, linear_map(K), linear_map(J * K)),
+                                opnd(v, false, linear_map(W), linear_map(K * W)), cg),
+                           st));
+    }
+    return DM_OK;
 }
 
 // out(t, i) = sum_{h,w} gamma[t][(h,w)] wo[w][h][i] (+ bo)
@@ -437,10 +456,13 @@ GemmArgs out_dw_args(const Dims& x, const void* gamma, const void* dout, int lay
 }
 
 // dwo == nullptr: the caller launches the output-projection weight gradient
-// itself (the encoder pairs it with the Q/K/V weight gradient).
+// itself (the encoder pairs it with the Q/K/V weight gradient).  alpha:
+// workspace of B*H*J*K elements where the groupings that read alpha
+// re-form it from P.
 int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const void* dout, int layout,
-                       const void* q, const void* k, const void* v, const void* prob, const void* alpha,
-                       const void* gamma, const void* wo, float* dwo, void* dgamma, void* dalpha, void* dbeta,
+                       const void* q, const void* k, const void* v, const void* prob, void* alpha,
+                       const void* gamma, const float* gamma32, const void* wo, float* dwo, void* dgamma,
+                       void* dalpha, void* dbeta,
                        void* dq, int64_t ldq, void* dk, int64_t ldk, void* dv, int64_t ldv, hipStream_t st) {
     const int64_t Z = x.B * x.H, J = x.J, K = x.K, P = x.P, W = x.W, H = x.H, HW = x.H * x.W, I = x.I;
     // Out dX: dgamma[t][(h,w)] = sum_i dout(t,i) wo[w][h][i]
@@ -457,6 +479,23 @@ int attention_core_bwd(const Dims& x, float scaler, const DropParams& dp, const 
     }
     const IdxMap zg = make_map((uint32_t)H, 0, W, J * HW, 0);  // z=(b,h) -> gamma-like token-major offset
     const int path = current_attn_path();
+    if ((path == 0 || path == 3) && gamma32 && attn_keys_ok(x.dtype, (int)K, (int)P, (int)W)) {
+        // Gamma dX1, the softmax + dropout backward, Gamma dX2 and both QK^T
+        // gradients in one launch over key blocks, reading P once (dQ
+        // partial sums of several key blocks added by a second launch)
+        TraceScope t_("B13-17 score_bwd_keys", st);
+        run_attn_bwd_keys(x.dtype, (int)x.B, (int)H, (int)J, (int)K, scaler, AttnRows{q, H * J * P, J * P, P},
+                          AttnRows{k, H * K * P, K * P, P}, AttnRows{v, H * K * W, K * W, W},
+                          AttnRows{dgamma, J * HW, W, HW}, AttnRows{gamma32, J * HW, W, HW}, prob, dp,
+                          AttnRows{dq, J * ldq, P, ldq}, AttnRows{dk, K * ldk, P, ldk}, AttnRows{dv, K * ldv, W, ldv},
+                          reinterpret_cast<float*>(dalpha), st);
+        return check_launch("attention key-block backward");
+    }
+    {
+        TraceScope t_("B14a alpha", st);
+        run_alpha_from_prob(x.dtype, (int)x.B, (int)H, (int)J, (int)K, prob, dp, alpha, st);
+    }
+    DM_TRY(check_launch("alpha from P"));
     const bool fused = path != 1 && attn_fused_ok(x.dtype, (int)K, (int)W);
     AttnNext nq;
     nq.x = k; nq.x_outer = H * K * P; nq.x_inner = K * P; nq.x_ld = P;
@@ -601,6 +640,15 @@ int encoder_layer_sizes(const dm_layer_desc* d, size_t* saved_bytes, size_t* fwd
     return DM_OK;
 }
 
+int attn_backward_form(const dm_layer_desc* d, int32_t* key_blocks) {
+    DM_TRY(check_desc(d, false));
+    if (!key_blocks) return set_error(DM_ERR_ARG, "key_blocks is NULL");
+    PlanScope plan_(d->plan);
+    const int path = current_attn_path();
+    *key_blocks = (path == 0 || path == 3) && attn_keys_ok(d->dtype, d->K, d->P, d->W);
+    return DM_OK;
+}
+
 int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t* bytes) {
     DM_TRY(check_desc(d, true));
     const Dims x = dims_of(d);
@@ -610,7 +658,8 @@ int saved_tensor_view(const dm_layer_desc* d, int32_t id, size_t* offset, size_t
     switch (id) {
         case DM_SAVED_QKV: o = e.m.q; b = 3 * es * x.N; break;
         case DM_SAVED_PROB: o = e.m.prob; b = es * x.S; break;
-        case DM_SAVED_ALPHA: o = e.m.alpha; b = es * x.S; break;
+        case DM_SAVED_ALPHA:
+            return set_error(DM_ERR_ARG, "alpha is not saved: the backward re-forms it from P and the dropout mask");
         case DM_SAVED_GAMMA: o = e.m.gamma; b = es * x.N; break;
         case DM_SAVED_XHAT1: o = e.xhat1; b = es * x.N; break;
         case DM_SAVED_RSTD1: o = e.rstd1; b = 4 * x.Tq; break;
@@ -640,7 +689,7 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     const int dt = x.dtype;
     const int64_t T = x.Tq;
     void *q = B8(saved, e.m.q), *k = B8(saved, e.m.k), *v = B8(saved, e.m.v);
-    void *prob = B8(saved, e.m.prob), *alpha = B8(saved, e.m.alpha), *gamma = B8(saved, e.m.gamma);
+    void *prob = B8(saved, e.m.prob), *gamma = B8(saved, e.m.gamma), *alpha = B8(ws, e.m.alpha_f);
     void *xhat1 = B8(saved, e.xhat1), *y1 = B8(saved, e.y1), *hbuf = B8(saved, e.h), *abuf = B8(saved, e.a);
     void* xhat2 = B8(saved, e.xhat2);
     float *rstd1 = (float*)B8(saved, e.rstd1), *rstd2 = (float*)B8(saved, e.rstd2);
@@ -652,8 +701,9 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
         DM_TRY(project_fused(x, DM_BJI, x_in, prm, q, k, v, st));
     }
     // QK^T, scaled softmax + dropout, Gamma
+    float* gamma32 = e.m.gamma32 ? reinterpret_cast<float*>(B8(saved, e.m.gamma32)) : nullptr;
     DM_TRY(attention_core_fwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), q, k, v, beta, prob,
-                              alpha, gamma, st));
+                              alpha, gamma, gamma32, st));
     // Out
     DM_TRY(out_projection(x, gamma, prm->wo, nullptr, ao, DM_BJI, st));
     const FusedLayout fl = fused_layout(dt, T, (int)x.I, (int)x.F);
@@ -713,7 +763,9 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     const int64_t T = x.Tq, I = x.I, F = x.F;
     const int es = x.es;
     const void *q = B8(saved, e.m.q), *k = B8(saved, e.m.k), *v = B8(saved, e.m.v);
-    const void *prob = B8(saved, e.m.prob), *alpha = B8(saved, e.m.alpha), *gamma = B8(saved, e.m.gamma);
+    const void *prob = B8(saved, e.m.prob), *gamma = B8(saved, e.m.gamma);
+    const float* gamma32 = e.m.gamma32 ? reinterpret_cast<const float*>(B8(saved, e.m.gamma32)) : nullptr;
+    void* alpha = B8(ws, e.m.alpha_b);
     const void *xhat1 = B8(saved, e.xhat1), *y1 = B8(saved, e.y1), *hbuf = B8(saved, e.h), *abuf = B8(saved, e.a);
     const void* xhat2 = B8(saved, e.xhat2);
     const float *rstd1 = (const float*)B8(saved, e.rstd1), *rstd2 = (const float*)B8(saved, e.rstd2);
@@ -804,7 +856,7 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     // (the output-projection weight gradient waits for the Q/K/V weight
     // gradient: the two contractions share one launch)
     DM_TRY(attention_core_bwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), dAO, DM_BJI, q, k, v,
-                              prob, alpha, gamma, prm->wo, nullptr, dgamma, dalpha, dbeta, dqkv, ld,
+                              prob, alpha, gamma, gamma32, prm->wo, nullptr, dgamma, dalpha, dbeta, dqkv, ld,
                               B8(dqkv, (size_t)es * I), ld, B8(dqkv, (size_t)es * 2 * I), ld, st));
     // Q, K, V dX (fused) + encoder-input residual; Q, K, V dW (fused) with Out dW
     const GemmArgs out_dw = out_dw_args(x, gamma, dAO, DM_BJI, g->dwo);
@@ -876,8 +928,8 @@ int mha_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
         DM_TRY(project(x, x.layout, vin, x.K, x.W, prm->wv, prm->bv, v, st));
     }
     DM_TRY(attention_core_fwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), q, k, v,
-                              B8(ws, s.p.beta), B8(saved, s.p.prob), B8(saved, s.p.alpha), B8(saved, s.p.gamma),
-                              st));
+                              B8(ws, s.p.beta), B8(saved, s.p.prob), B8(ws, s.p.alpha_f), B8(saved, s.p.gamma),
+                              s.p.gamma32 ? reinterpret_cast<float*>(B8(saved, s.p.gamma32)) : nullptr, st));
     return out_projection(x, B8(saved, s.p.gamma), prm->wo, prm->bo, out, x.layout, st);
 }
 
@@ -929,7 +981,9 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
     DM_TRY(check_launch("output-bias backward"));
     t10.stop();
     DM_TRY(attention_core_bwd(x, scaler_of(d), make_drop(d->p_attn, d->seed, 0, d->layer_id), dout, x.layout, q, k, v,
-                              B8(saved, s.p.prob), B8(saved, s.p.alpha), B8(saved, s.p.gamma), prm->wo, g->dwo,
+                              B8(saved, s.p.prob), B8(ws, s.p.alpha_b), B8(saved, s.p.gamma),
+                              s.p.gamma32 ? reinterpret_cast<const float*>(B8(saved, s.p.gamma32)) : nullptr,
+                              prm->wo, g->dwo,
                               B8(ws, s.p.dgamma), B8(ws, s.p.dalpha), B8(ws, s.p.dbeta), bq, s.p.ldq, bk, s.p.ldk, bv,
                               s.p.ldv, st));
     if (fused) {

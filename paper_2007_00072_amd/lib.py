@@ -42,7 +42,7 @@ EXPORTED = [
     "colsum_ws_bytes", "bdrln_fwd", "softmax_dropout_fwd", "bias_act_fwd", "attn_input_bias",
     "ln_param_bwd", "ln_dropout_bwd", "residual_ln_param_bwd", "act_bias_bwd",
     "softmax_dropout_bwd", "bias_grad", "bias_grad_noalloc", "attn_input_bias_grad", "residual_add",
-    "dropout_mask", "saved_tensor_view", "contract", "dm_last_error",
+    "dropout_mask", "saved_tensor_view", "attn_backward_form", "contract", "dm_last_error",
     "dm_trace_enable", "dm_trace_count", "dm_trace_get",
     "plan_create", "plan_destroy", "plan_log", "plan_log_read",
 ]
@@ -135,6 +135,7 @@ _f["attn_input_bias_grad"] = _sig("attn_input_bias_grad", I32, I32, I64, I32, I3
 _f["residual_add"] = _sig("residual_add", I32, I32, I64, P_, P_, P_, P_)
 _f["dropout_mask"] = _sig("dropout_mask", I32, U64, U32, U32, F32, U64, U64, P_, P_)
 _f["saved_tensor_view"] = _sig("saved_tensor_view", I32, PDESC, I32, PSZ, PSZ)
+_f["attn_backward_form"] = _sig("attn_backward_form", I32, PDESC, C.POINTER(C.c_int32))
 _f["contract"] = _sig("contract", I32, I32, I32, I32, I32, I32, F32, P_, I32, I64, P_, I32, I64, P_, P_, I32, I64,
                       I32, I32, P_, SZ, P_)
 _f["dm_last_error"] = _sig("dm_last_error", C.c_char_p)
@@ -246,6 +247,14 @@ def saved_tensor_view(desc, name: str):
     o, b = C.c_size_t(), C.c_size_t()
     _call("saved_tensor_view", C.byref(desc), SAVED_IDS[name], C.byref(o), C.byref(b))
     return o.value, b.value
+
+
+def attn_backward_form(desc) -> bool:
+    """True when this descriptor's backward takes the key-block form of the
+    attention-score backward (d(alpha) never stored), False for the row form."""
+    kb = C.c_int32()
+    _call("attn_backward_form", C.byref(desc), C.byref(kb))
+    return bool(kb.value)
 
 
 # ----------------------------------------------------- fused operators

@@ -70,7 +70,8 @@ def test_sizes_valid(lib):
     d = _desc(lib)
     saved, fwd, bwd = lib.encoder_layer_sizes(d)
     N, S, Fh = 8 * 512 * 1024, 8 * 16 * 512 * 512, 8 * 512 * 4096
-    assert saved >= 2 * (7 * N + 2 * S + 2 * Fh)       # Q,K,V,gamma,xhat1,y1,xhat2 + prob,alpha + H,A
+    assert saved >= 2 * (7 * N + S + 2 * Fh)           # Q,K,V,gamma,xhat1,y1,xhat2 + prob + H,A
+    assert saved < 2 * (7 * N + 2 * S + 2 * Fh)        # alpha is not saved
     assert fwd >= 2 * (S + 2 * N)
     assert bwd >= 2 * (2 * S + 9 * N + 2 * Fh)
 
@@ -203,3 +204,16 @@ def test_plan_objects_host_only(lib):
         with pytest.raises(lib.DmError):
             lib.Plan(*bad)
     del p
+
+
+def test_saved_views_inside_and_alpha_not_saved(lib):
+    d = _desc(lib)
+    saved, _, _ = lib.encoder_layer_sizes(d)
+    for name in lib.SAVED_IDS:
+        if name == "alpha":
+            with pytest.raises(lib.DmError) as e:
+                lib.saved_tensor_view(d, name)
+            assert e.value.code == lib.DM_ERR_ARG and "not saved" in str(e.value)
+            continue
+        off, nbytes = lib.saved_tensor_view(d, name)
+        assert off % 256 == 0 and nbytes > 0 and off + nbytes <= saved, name

@@ -17,16 +17,16 @@ import torch
 from oracle import layer as OL
 from oracle import philox
 from paper_2007_00072_amd.inputs import WORKLOADS, Shape, make_activation, make_params, make_tensor
-from _util import assert_close, f64, oracle_config, params64
+from _util import assert_close, encoder_dx_scale, f64, oracle_config, params64
 from test_gpu_layer import GRAD_NAMES, check_encoder, check_mha, run_encoder, small
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-def _compare_layer(tag, y, dx, grads, ry, rdx, rg, dt):
+def _compare_layer(tag, y, dx, grads, ry, rdx, rg, dt, dx_scale=None):
     assert_close(f"y{tag}", y, ry, dt)
-    assert_close(f"dx{tag}", dx, rdx, dt)
+    assert_close(f"dx{tag}", dx, rdx, dt, scale=dx_scale)
     for n in GRAD_NAMES:
         if n == "bk":
             assert_close(f"dbk{tag}", grads[n], rg[n], dt, zero_ref=True,
@@ -47,11 +47,11 @@ def test_encoder_stack_layer_parity(li):
     x = make_activation(wl, 10 + 2 * li)
     dy = make_activation(wl, 11 + 2 * li)
     L, params, x, dy, y, dx = run_encoder(wl, layer=li, x=x, dy=dy)
-    cfg = oracle_config(wl, li)
+    cfg = oracle_config(wl, li, desc=L.desc)
     prm = params64(params)
     ry, cache = OL.encoder_forward(f64(x), prm, cfg)
-    rdx, rg, _ = OL.encoder_backward(f64(dy), cache, prm, cfg)
-    _compare_layer(f"[{li}]", y, dx, L.grads, ry, rdx, rg, wl.dtype)
+    rdx, rg, inter = OL.encoder_backward(f64(dy), cache, prm, cfg)
+    _compare_layer(f"[{li}]", y, dx, L.grads, ry, rdx, rg, wl.dtype, encoder_dx_scale(cache, inter, prm))
 
 
 def test_encoder_stack_chained_equals_standalone():
@@ -107,7 +107,7 @@ def check_encoder_relu(wl, layer=0, p_ffn_act=0.1):
     those branches, and every output must match it at the parity bar."""
     L, params, x, dy, y, dx = run_encoder(wl, layer, act="relu", p_ffn_act=p_ffn_act)
     dt = wl.dtype
-    cfg = oracle_config(wl, layer, act="relu", p_ffn_act=p_ffn_act)
+    cfg = oracle_config(wl, layer, desc=L.desc, act="relu", p_ffn_act=p_ffn_act)
     prm = params64(params)
     ry, cache = OL.encoder_forward(f64(x), prm, cfg)
     assert_close("y", y, ry, dt)
@@ -146,8 +146,9 @@ def check_encoder_relu(wl, layer=0, p_ffn_act=0.1):
         for f, t in flips:
             u2[f, t] = -np.sign(u2d[f, t]) * 1e-30 if u2d[f, t] != 0 else 1e-30
         c2 = dict(cache, u=u2.reshape(u.shape))
-        rdx, rg, _ = OL.encoder_backward(f64(dy), c2, prm, cfg)
-    assert_close(f"dx (ambiguous ReLU branches {n_amb}, taken the other way {len(flips)})", dx, rdx, dt)
+        rdx, rg, inter = OL.encoder_backward(f64(dy), c2, prm, cfg)
+    assert_close(f"dx (ambiguous ReLU branches {n_amb}, taken the other way {len(flips)})", dx, rdx, dt,
+                 scale=encoder_dx_scale(cache, inter, prm))
     for n in GRAD_NAMES:
         if n == "bk":
             assert_close("dbk", L.grads[n], rg[n], dt, zero_ref=True, zero_scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
@@ -173,11 +174,11 @@ def test_encoder_full_size_vs_plain_f64():
     # "f64": nothing rounded inside the oracle), at the stated bar
     wl = WORKLOADS["bert_large_f16"]
     L, params, x, dy, y, dx = run_encoder(wl)
-    cfg = oracle_config(wl, store_dtype="f64")
+    cfg = oracle_config(wl, desc=L.desc, store_dtype="f64")
     prm = params64(params)
     ry, cache = OL.encoder_forward(f64(x), prm, cfg)
-    rdx, rg, _ = OL.encoder_backward(f64(dy), cache, prm, cfg)
-    _compare_layer("(f64)", y, dx, L.grads, ry, rdx, rg, "f16")
+    rdx, rg, inter = OL.encoder_backward(f64(dy), cache, prm, cfg)
+    _compare_layer("(f64)", y, dx, L.grads, ry, rdx, rg, "f16", encoder_dx_scale(cache, inter, prm))
 
 
 # --------------------------------------------------------- extreme inputs
@@ -248,7 +249,7 @@ def test_mha_extreme_logits_exact_scores(dtype):
     out = M.forward(q.to(DEV), k.to(DEV), v.to(DEV))
     dq, dk, dv = M.backward(q.to(DEV), dout.to(DEV), k.to(DEV), v.to(DEV))
     torch.cuda.synchronize()
-    cfg = oracle_config(wl)
+    cfg = oracle_config(wl, desc=M.desc)
     prm = params64(params)
     t = lambda a: f64(a).transpose(2, 0, 1)
     back = lambda a: a.transpose(1, 2, 0)

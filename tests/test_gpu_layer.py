@@ -8,7 +8,7 @@ import torch
 
 from oracle import layer as OL
 from paper_2007_00072_amd.inputs import WORKLOADS, Shape, make_activation, make_params
-from _util import assert_close, f64, oracle_config, params64
+from _util import assert_close, encoder_dx_scale, f64, oracle_config, params64
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -33,13 +33,13 @@ def run_encoder(wl, layer=0, x=None, dy=None, **desc_over):
 def check_encoder(wl, layer=0, x=None, dy=None, act="gelu", p_ffn_act=0.0, causal=False, **desc_over):
     L, params, x, dy, y, dx = run_encoder(wl, layer, x, dy, act=act, p_ffn_act=p_ffn_act, causal=causal,
                                           **desc_over)
-    cfg = oracle_config(wl, layer, act=act, p_ffn_act=p_ffn_act, causal=causal)
+    cfg = oracle_config(wl, layer, desc=L.desc, act=act, p_ffn_act=p_ffn_act, causal=causal)
     prm = params64(params)
     ry, cache = OL.encoder_forward(f64(x), prm, cfg)
-    rdx, rg, _ = OL.encoder_backward(f64(dy), cache, prm, cfg)
+    rdx, rg, inter = OL.encoder_backward(f64(dy), cache, prm, cfg)
     dt = wl.dtype
     assert_close("y", y, ry, dt)
-    assert_close("dx", dx, rdx, dt)
+    assert_close("dx", dx, rdx, dt, scale=encoder_dx_scale(cache, inter, prm))
     for n in GRAD_NAMES:
         if n == "bk":   # exactly zero: softmax is invariant to a per-row shift
             assert_close("dbk", L.grads[n], rg[n], dt, zero_ref=True, zero_scale=float(np.sqrt(np.mean(rg["bq"] ** 2))))
@@ -98,11 +98,35 @@ def test_encoder_saved_tensors(name, shape):
         assert_close(key, qkv[i], c[key].transpose(2, 1, 3, 0), wl.dtype)   # [p,h,b,j] -> [b,h,j,p]
     prob = L.saved_tensor("prob", (s.B, s.H, s.J, s.K), tdt)
     assert_close("prob", prob, c["prob"].transpose(1, 0, 2, 3), wl.dtype)
-    alpha = L.saved_tensor("alpha", (s.B, s.H, s.J, s.K), tdt)
-    ref_alpha = c["alpha"].transpose(1, 0, 2, 3)
-    np.testing.assert_array_equal(f64(alpha) == 0, ref_alpha == 0)     # masks bit-exact
     y1 = L.saved_tensor("y1", (s.B, s.J, s.I), tdt)
     assert_close("y1", y1, c["y1"].transpose(1, 2, 0), wl.dtype)
+    from paper_2007_00072_amd import lib
+    with pytest.raises(lib.DmError):
+        L.saved_tensor("alpha", (s.B, s.H, s.J, s.K), tdt)   # re-formed from P where needed, never saved
+
+
+@pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
+def test_encoder_attention_masks_bit_exact(name):
+    # alpha is not saved, but with one-hot token inputs and the identity as
+    # value weights (V = I, no bias) the saved context gamma = alpha V is
+    # alpha itself: the forward's dropout keep decisions show element by
+    # element and must match the oracle's bit for bit
+    from paper_2007_00072_amd.runner import EncoderLayer, desc_for
+    wl = small(name, B=2, J=64, K=64, H=1, P=64, W=64, I=64, F=128).with_(p_attn=0.3)
+    params = make_params(wl)
+    tdt = params["wq"].dtype
+    params["wv"] = torch.eye(64, dtype=tdt).reshape(64, 1, 64)
+    params["bv"] = torch.zeros(64, 1, dtype=tdt)
+    x = torch.eye(64, dtype=tdt).expand(2, 64, 64).contiguous()
+    L = EncoderLayer(desc_for(wl, 0), params, DEV)
+    L.forward(x.to(DEV))
+    torch.cuda.synchronize()
+    got = f64(L.saved_tensor("gamma", (2, 64, 1, 64), tdt))[:, :, 0, :]   # [B][J][H][W] -> [B][J][K]
+    _, c = OL.encoder_forward(f64(x), params64(params), oracle_config(wl))
+    ref = c["alpha"][0]                                                  # [H][B][J][K], H = 1
+    assert (ref == 0).any() and (ref != 0).any()
+    np.testing.assert_array_equal(got == 0, ref == 0)
+    assert_close("alpha", got, ref, wl.dtype)
 
 
 @pytest.mark.parametrize("name", ["bert_large_f16", "bert_base_bf16"])
@@ -143,7 +167,7 @@ def check_mha(wl, self_attention=True, causal=False, **desc_over):
     out = M.forward(qd, k, v)
     dq, dk, dv = M.backward(qd, dout.to(DEV), k, v)
     torch.cuda.synchronize()
-    cfg = oracle_config(wl, causal=causal)
+    cfg = oracle_config(wl, desc=M.desc, causal=causal)
     prm = params64(params)
     to_ibj = (lambda a: a) if wl.layout == "ibj" else (lambda a: a.transpose(2, 0, 1))
     from_ibj = (lambda a: a) if wl.layout == "ibj" else (lambda a: a.transpose(1, 2, 0))

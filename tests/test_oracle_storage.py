@@ -76,9 +76,11 @@ def _t(a):
     return torch.from_numpy(np.ascontiguousarray(a))
 
 
-@pytest.mark.parametrize("dt,act", [("f16", "gelu"), ("bf16", "gelu"), ("f16", "relu")])
-def test_rounding_points(dt, act):
+@pytest.mark.parametrize("dt,act,dalpha_stored", [("f16", "gelu", False), ("bf16", "gelu", False),
+                                                  ("f16", "relu", False), ("bf16", "gelu", True)])
+def test_rounding_points(dt, act, dalpha_stored):
     cfg, prm, x, dy = _setup(dt, act)
+    cfg.dalpha_stored = dalpha_stored
     y, c = L.encoder_forward(x, prm, cfg)
     dx, g, it = L.encoder_backward(dy, c, prm, cfg)
     B, J, H, P, I = cfg.B, cfg.J, cfg.H, cfg.P, cfg.I
@@ -157,15 +159,20 @@ def test_rounding_points(dt, act):
     dgamma = head(it["dgamma"])
     wo_hw = p["wo"].permute(1, 0, 2)                                   # [h,w,i]
     same("dgamma", dgamma, R(torch.einsum("bji,hwi->bhjw", dAO, wo_hw)))
-    dalpha = hbjk(it["dalpha"])                                        # inside the fused score backward
-    assert torch.allclose(dalpha, torch.einsum("bhjw,bhkw->bhjk", dgamma, vv), rtol=1e-12, atol=1e-14)
+    dalpha = hbjk(it["dalpha"])
+    dalpha_x = torch.einsum("bhjw,bhkw->bhjk", dgamma, vv)
+    if dalpha_stored:                                                  # written by Gamma dX1
+        same("dalpha", dalpha, R(dalpha_x))
+    else:                                                              # inside the fused score backward
+        assert torch.allclose(dalpha, dalpha_x, rtol=1e-12, atol=1e-14)
     same("dvv", head(it["dvv"]), R(torch.einsum("bhjk,bhjw->bhkw", alpha, dgamma)))
     dprob = dalpha * m_attn                                            # inside `bs`
     dbeta = hbjk(it["dbeta"])
-    # row term: sum_k d(alpha) alpha with alpha as stored (= sum_k dP P exactly)
-    same("dbeta", dbeta, R(cfg.s * prob * (dprob - (dalpha * alpha).sum(-1, keepdim=True))))
-    # ... which is a different rounding reading from sum_k dP P over the stored P
-    assert not torch.equal(dbeta, R(cfg.s * prob * (dprob - (dprob * prob).sum(-1, keepdim=True))))
+    row_dp = (dprob * prob).sum(-1, keepdim=True)                      # sum_k dP P over the stored P
+    row_da = (dalpha * alpha).sum(-1, keepdim=True)                    # sum_k d(alpha) alpha, alpha as stored
+    same("dbeta", dbeta, R(cfg.s * prob * (dprob - (row_dp if dalpha_stored else row_da))))
+    # the two row terms are different rounding readings of one number
+    assert not torch.equal(R(cfg.s * prob * (dprob - row_dp)), R(cfg.s * prob * (dprob - row_da)))
     dqq, dkk = head(it["dqq"]), head(it["dkk"])
     same("dqq", dqq, R(torch.einsum("bhjk,bhkp->bhjp", dbeta, kk)))
     same("dkk", dkk, R(torch.einsum("bhjk,bhjp->bhkp", dbeta, qq)))
@@ -175,8 +182,10 @@ def test_rounding_points(dt, act):
     same("dx", _t(dx), R(dXa + dS1))                                   # `bei` in the Q/K/V dX epilogue
 
     # values kept inside one fused operator are not rounded
-    for name, v in (("s1", s1), ("u", u), ("s2", s2), ("dY1", dY1), ("dXa", dXa), ("dalpha", dalpha),
-                    ("dprob", dprob[m_attn != 0])):
+    kept = [("s1", s1), ("u", u), ("s2", s2), ("dY1", dY1), ("dXa", dXa), ("dprob", dprob[m_attn != 0])]
+    if not dalpha_stored:
+        kept.append(("dalpha", dalpha))
+    for name, v in kept:
         v = v.numpy()
         frac = float(np.mean(L.store(v, dt) == v))
         assert frac < 0.5, (name, frac)
