@@ -360,8 +360,10 @@ def main() -> int:
         # the fused step's algorithmic elements against the same layer's
         # operators one by one (every input read, every output and stored
         # dropout mask written), per layer
-        path = "scores_next" if any(r["op"] == "F2-4 qkt_softmax_gamma" for r in table) else (
-            "scores" if any(r["op"] == "F2-3 qkt_softmax" for r in table) else "separate")
+        ops = {r["op"] for r in table}
+        path = ("keys" if "B13-17 score_bwd_keys" in ops else
+                "scores_next" if "F2-4 qkt_softmax_gamma" in ops else
+                "scores" if "F2-3 qkt_softmax" in ops else "separate")
         out["data_movement"] = dict(dataflow.data_movement(s, wl.dtype, path), per="layer fwd+bwd",
                                     paper="22.91% (V100; see paper_context)")
     if a.kernels_json:

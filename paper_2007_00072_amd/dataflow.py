@@ -52,17 +52,28 @@ REPLACES = {
     "F2-4 qkt_softmax_gamma": ("F2 qkt", "F3 softmax", "F4 gamma"),
     "B13-15 gamma_dx1_softmax_bwd": ("B13 gamma_dx1", "B15 softmax_bwd"),
     "B13+15+16 score_bwd_dq": ("B13 gamma_dx1", "B15 softmax_bwd", "B16 qkt_dx1"),
+    "B13-17 score_bwd_keys": ("B13 gamma_dx1", "B14 gamma_dx2", "B15 softmax_bwd", "B16 qkt_dx1", "B17 qkt_dx2"),
 }
 # Contractions the encoder layer issues as one launch (their tiles together
 # fill the chip): the backward's output-projection and Q/K/V weight gradients.
 PAIRED = {"B12+19 out_dw+qkv_dw": ("B12 out_dw", "B19 qkv_dw")}
 # The launch sets one layer can run: every score step separate, scores on
-# chip, and scores on chip with the next contraction in the same launch.
+# chip, scores on chip with the next contraction in the same launch, and
+# that forward with the key-block backward (head size 64, K a multiple of 128).
 PATHS = {
     "separate": (),
     "scores": ("F2-3 qkt_softmax", "B13-15 gamma_dx1_softmax_bwd"),
     "scores_next": ("F2-4 qkt_softmax_gamma", "B13+15+16 score_bwd_dq"),
+    "keys": ("F2-4 qkt_softmax_gamma", "B13-17 score_bwd_keys"),
 }
+
+
+def key_blocks(s: Shape, dtype: str):
+    """Key-block backward of the shape: (possible, key blocks per head)."""
+    if dtype == "f32" or s.P != 64 or s.W != 64 or s.K % 128:
+        return False, 0
+    kg = 8 if s.K % 256 == 0 and s.B * s.H * (s.K // 256) >= 192 else 4
+    return True, s.K // (32 * kg)
 
 
 def path_groups(w: Dict[str, "Work"], path: str) -> Dict[str, "Work"]:
@@ -94,8 +105,13 @@ def encoder_layer(s: Shape, dtype: str, elements: bool = False) -> Dict[str, Wor
     w["F3 softmax"] = m(3 * S * es)
     # QK^T and softmax + dropout in one launch: Q, K read; P and alpha written
     w["F2-3 qkt_softmax"] = Work(2.0 * Z * J * K * P, float((2 * N + 2 * S) * es), "hbm", "fused")
-    # ... and Gamma = alpha V in the same launch: V read and Gamma written too
-    w["F2-4 qkt_softmax_gamma"] = Work(2.0 * Z * J * K * (P + W), float((4 * N + 2 * S) * es), "hbm", "fused")
+    # ... and Gamma = alpha V in the same launch: V read, Gamma written, alpha
+    # kept on chip (when the key-block backward can run, Gamma is also
+    # written in fp32 before rounding: overhead)
+    keys, nkb = key_blocks(s, dtype)
+    w["F2-4 qkt_softmax_gamma"] = Work(2.0 * Z * J * K * (P + W), float((4 * N + S) * es), "hbm", "fused")
+    if keys:
+        w["F2-4 qkt_softmax_gamma"].overhead = f4 * N
     w["F4 gamma"] = _att(Z, J, W, K, es, dtype, S, N)
     w["F5 out"] = g(T, I, I, N, I * I, N)
     w["F6 bdrln1"] = m(4 * N * es + f4 * T + 3 * I * es)
@@ -126,6 +142,12 @@ def encoder_layer(s: Shape, dtype: str, elements: bool = False) -> Dict[str, Wor
     w["B13-15 gamma_dx1_softmax_bwd"] = Work(2.0 * Z * J * K * W, float((2 * N + 2 * S) * es), "hbm", "fused")
     # ... and dQ = dbeta K in the same launch: K read and dQ written too
     w["B13+15+16 score_bwd_dq"] = Work(2.0 * Z * J * K * (W + P), float((4 * N + 2 * S) * es), "hbm", "fused")
+    # the key-block backward: dGamma, gamma, P, Q, K, V read; dQ, dK, dV
+    # written (gamma read in fp32, and with several key blocks per head the
+    # fp32 dQ partials written and read back: overhead)
+    w["B13-17 score_bwd_keys"] = Work(2.0 * Z * J * K * 2 * (W + P), float((9 * N + S) * es), "hbm", "fused")
+    if keys:
+        w["B13-17 score_bwd_keys"].overhead = (f4 - es) * N + (2 * nkb * f4 * N if nkb > 1 else 0)
     w["B16 qkt_dx1"] = _att(Z, J, P, K, es, dtype, S, N)
     w["B17 qkt_dx2"] = _att(Z, K, P, J, es, dtype, S, N)
     w["B18 qkv_dx"] = g(T, I, 3 * I, 3 * N, 3 * I * I, N, extra=N * es)      # + residual read
@@ -174,7 +196,8 @@ def mha(s: Shape, dtype: str, layout: str = "ibj", elements: bool = False) -> Di
     N = T * I
     keep = ("F1 qkv", "F2 qkt", "F3 softmax", "F2-3 qkt_softmax", "F2-4 qkt_softmax_gamma", "F4 gamma",
             "F5 out", "B11 out_dx", "B12 out_dw", "B13 gamma_dx1", "B14 gamma_dx2", "B15 softmax_bwd",
-            "B13-15 gamma_dx1_softmax_bwd", "B13+15+16 score_bwd_dq", "B16 qkt_dx1", "B17 qkt_dx2",
+            "B13-15 gamma_dx1_softmax_bwd", "B13+15+16 score_bwd_dq", "B13-17 score_bwd_keys", "B16 qkt_dx1",
+            "B17 qkt_dx2",
             "B18 qkv_dx", "B19 qkv_dw", "B20 qkv_bias_grad")
     out = {k: w[k] for k in keep}
     f5 = w["F5 out"]

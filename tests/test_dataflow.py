@@ -28,6 +28,10 @@ def test_layer_model_flops_consistent():
         assert sum(x.flop for x in groups.values()) / 1e9 == pytest.approx(table3, rel=1e-12), path
     assert "F4 gamma" in dataflow.path_groups(w, "scores")
     assert "F4 gamma" not in dataflow.path_groups(w, "scores_next")
+    assert "B14 gamma_dx2" not in dataflow.path_groups(w, "keys") and "B17 qkt_dx2" not in dataflow.path_groups(w, "keys")
+    # the key-block backward reads P once and writes no score-sized tensor
+    N, S2 = s.B * s.J * s.I, s.B * s.H * s.J * s.K
+    assert w["B13-17 score_bwd_keys"].bytes == (9 * N + S2) * 2
     for k, v in dataflow.PAIRED.items():
         assert w[k].flop == sum(w[p].flop for p in v) and w[k].bytes == sum(w[p].bytes for p in v)
         assert all(p not in dataflow.path_groups(w, "scores_next") for p in v)
