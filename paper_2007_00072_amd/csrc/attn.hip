@@ -487,8 +487,11 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
     constexpr int ROWB = KB * 2;
     constexpr int AB = JB * ROWB;  // bytes of the alpha tile (as of d(beta))
     constexpr int HDT = JB * 128;  // bytes of one staged [JB][64] tile
-    constexpr int OFF_A = 0, OFF_DB = AB, OFF_DG = 2 * AB, OFF_Q = OFF_DG + HDT, OFF_D = OFF_Q + HDT;
-    constexpr int OFF_RED = OFF_D + JB * 4;
+    // two staging buffers (one step's d(gamma) and Q rows and D values):
+    // the row operator of step i writes step i + 1's while step i's are read
+    constexpr int SB = 2 * HDT + JB * 4;
+    constexpr int OFF_A = 0, OFF_DB = AB, OFF_STG = 2 * AB;
+    constexpr int OFF_RED = OFF_STG + 2 * SB;
     constexpr int LDS = OFF_RED + (8 - NT2) * 4096;
     // the K staging and the final query-group sums reuse the alpha / d(beta) tiles
     static_assert(KB * 128 <= 2 * AB && (QG - 1) * KG * 2 * 4096 <= 2 * AB, "LDS reuse");
@@ -557,7 +560,8 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
         sgm1 = *reinterpret_cast<const floatx4*>(GMz + (int64_t)j * g.gm.ld + sc + 4);
         sq = *reinterpret_cast<const u32x4*>(Qz + (int64_t)j * g.q.ld + sc);
     };
-    auto stage_store = [&](int j0) {
+    auto stage_store = [&](int j0, int buf) {
+        const int OFF_DG = OFF_STG + buf * SB, OFF_Q = OFF_DG + HDT, OFF_D = OFF_Q + HDT;
         float dd = 0.f;
         if (stager) {
             if (j0 + srow >= g.J) {  // rows past the end are zeros
@@ -584,6 +588,7 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
         pf[0] = *reinterpret_cast<const u32x4*>(pr);
         pf[1] = *reinterpret_cast<const u32x4*>(pr + 8);
     };
+    const int nit = (g.J + JB - 1) / JB;
     stage_load(0);
     p_load(0);
     __syncthreads();
@@ -591,7 +596,8 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
     u32x4 kf[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) kf[s] = frag_hd(OFF_A, 64 * ch + 16 * s, 32 * pt);
-    stage_store(0);
+    stage_store(0, 0);
+    if (nit > 1) stage_load(JB);
     __syncthreads();
 
     floatx16 accV[2], accK[2];
@@ -599,7 +605,6 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
     for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) { accV[t][r] = 0.f; accK[t][r] = 0.f; }
-    const int nit = (g.J + JB - 1) / JB;
     const int64_t erow0 = ((int64_t)h * g.B + b) * g.J;  // dropout logical row of (h, b, j = 0)
     const bool drop = g.dp.enabled != 0;
     const float dscale = drop ? g.dp.scale : 1.0f;
@@ -610,6 +615,7 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
 
     for (int it = 0; it < nit; ++it) {
         const int j0 = it * JB;
+        const int OFF_DG = OFF_STG + (it & 1) * SB, OFF_Q = OFF_DG + HDT, OFF_D = OFF_Q + HDT;
         // ---- d(alpha)^T: 32 keys x 32 queries
         floatx16 da;
 #pragma unroll
@@ -648,9 +654,12 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
         *reinterpret_cast<u32x4*>(lds + OFF_A + ab_off<ROWB>(jl, kl + 8)) = V8<T>::pack(al + 8);
         *reinterpret_cast<u32x4*>(lds + OFF_DB + ab_off<ROWB>(jl, kl)) = V8<T>::pack(db);
         *reinterpret_cast<u32x4*>(lds + OFF_DB + ab_off<ROWB>(jl, kl + 8)) = V8<T>::pack(db + 8);
+        // next step: its staged rows (loaded one step ahead) into the other
+        // buffer, then the loads for the step after
         if (it + 1 < nit) {
+            stage_store(j0 + JB, (it + 1) & 1);
             p_load(j0 + JB);
-            stage_load(j0 + JB);
+            if (it + 2 < nit) stage_load(j0 + 2 * JB);
         }
         __syncthreads();
 
@@ -697,8 +706,6 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
                 }
             }
         }
-        if (it + 1 < nit) stage_store(j0 + JB);
-        __syncthreads();
     }
 
     // ---- dV, dK of the block's keys (query groups added in order first)
