@@ -434,8 +434,9 @@ void attn_fused_t(const AttnArgs& g, hipStream_t st) {
 //     dK += d(beta)^T Q accumulate over all query steps in registers, their
 //     operands read k-contiguous with the gfx950 transposing LDS read;
 //   dQ = d(beta) K for the step's rows: each wave takes one 32 x 32 output
-//     tile over a 64-key chunk (K fragments held in registers) and the
-//     chunks' fp32 tiles are added through LDS in chunk order.
+//     tile over a 64-key chunk (K fragments held in registers); the chunks'
+//     fp32 tiles meet in LDS, where every wave adds up (in chunk order) and
+//     stores an equal share of the step's rows.
 // With more than one key block per head (nkb > 1) the block's dQ rows are
 // an fp32 partial over its keys, added in key-block order by
 // attn_dq_reduce_k; the sums are deterministic either way.
@@ -492,7 +493,7 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
     constexpr int SB = 2 * HDT + JB * 4;
     constexpr int OFF_A = 0, OFF_DB = AB, OFF_STG = 2 * AB;
     constexpr int OFF_RED = OFF_STG + 2 * SB;
-    constexpr int LDS = OFF_RED + (8 - NT2) * 4096;
+    constexpr int LDS = OFF_RED + NCH * NT2 * 4096;
     // the K staging and the final query-group sums reuse the alpha / d(beta) tiles
     static_assert(KB * 128 <= 2 * AB && (QG - 1) * KG * 2 * 4096 <= 2 * AB, "LDS reuse");
     __shared__ __attribute__((aligned(16))) unsigned char lds[LDS];
@@ -633,18 +634,25 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
         const float Dj = *reinterpret_cast<const float*>(lds + OFF_D + 4 * jl);
         const uint64_t blk0 = ((uint64_t)(erow0 + j) * (uint64_t)g.K + (uint64_t)(k0 + kl)) >> 2;
         float al[16], db[16];
+        // the four draws in one straight run, so their round chains interleave
+        u32x4 w[4];
+        if (drop) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint64_t blk = blk0 + q;
+                w[q] = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), g.dp.site, g.dp.layer, sk0, sk1);
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w[q] = u32x4{0, 0, 0, 0};
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            u32x4 w = {0, 0, 0, 0};
-            if (drop) {
-                const uint64_t blk = blk0 + q;
-                w = Philox::gen((uint32_t)blk, (uint32_t)(blk >> 32), g.dp.site, g.dp.layer, sk0, sk1);
-            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int r = 4 * q + i;
                 const float pv = valid ? p[r] : 0.f;
-                const bool keep = !drop || w[i] < thr;
+                const bool keep = !drop || w[q][i] < thr;
                 const float dpv = keep ? da[r] * dscale : 0.f;
                 db[r] = g.sm_scale * pv * (dpv - Dj);
                 al[r] = keep ? pv * dscale : 0.f;
@@ -682,27 +690,38 @@ __global__ __launch_bounds__(NTA) void attn_bwd_keys_k(KeysArgs g) {
         for (int s = 0; s < 4; ++s)
             aq = AMfma<T>::run(*reinterpret_cast<const u32x4*>(lds + OFF_DB + ab_off<ROWB>(32 * qt + c32, 64 * ch + 16 * s + 8 * hh)),
                                kf[s], aq);
-        if (ch > 0) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) red[((ch - 1) * NT2 + tq) * 1024 + r * 64 + lane] = aq[r];
-        }
+        for (int r = 0; r < 16; ++r) red[(ch * NT2 + tq) * 1024 + r * 64 + lane] = aq[r];
         __syncthreads();
-        if (ch == 0) {
-#pragma unroll 1
-            for (int c2 = 1; c2 < NCH; ++c2) {
+        // every wave adds up (in chunk order) and stores 16 / NCH accumulator
+        // rows of one dQ tile: wave w takes tile w % NT2, rows part w / NT2
+        {
+            constexpr int RPP = 16 / NCH;
+            const int tt = wave % NT2, part = wave / NT2;
+            const int pc = 32 * (tt & 1) + c32;
+            float v[RPP];
 #pragma unroll
-                for (int r = 0; r < 16; ++r) aq[r] += red[((c2 - 1) * NT2 + tq) * 1024 + r * 64 + lane];
+            for (int i = 0; i < RPP; ++i) {
+                const int r = part * RPP + i;
+                v[i] = red[tt * 1024 + r * 64 + lane];
+#pragma unroll
+                for (int c2 = 1; c2 < NCH; ++c2) v[i] += red[(c2 * NT2 + tt) * 1024 + r * 64 + lane];
             }
-            const int pc = 32 * pt + c32;
+            const int jrow = j0 + 32 * (tt >> 1) + 4 * hh;  // row of accumulator r: + 8 (r / 4) + r % 4
+            const bool full = j0 + JB <= g.J;
+            if (g.nkb == 1) {
+                T* dst = reinterpret_cast<T*>(const_cast<void*>(g.dq.ptr)) + b * g.dq.outer + h * g.dq.inner + pc;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int jq = j0 + 32 * qt + 8 * (r >> 2) + 4 * hh + (r & 3);
-                if (jq < g.J) {
-                    if (g.nkb == 1)
-                        reinterpret_cast<T*>(const_cast<void*>(g.dq.ptr))[b * g.dq.outer + h * g.dq.inner +
-                                                                         (int64_t)jq * g.dq.ld + pc] = from_f<T>(aq[r]);
-                    else
-                        g.part[(((int64_t)kb * nz + z) * g.J + jq) * KV_HD + pc] = aq[r];
+                for (int i = 0; i < RPP; ++i) {
+                    const int r = part * RPP + i, jq = jrow + 8 * (r >> 2) + (r & 3);
+                    if (full || jq < g.J) dst[(int64_t)jq * g.dq.ld] = from_f<T>(v[i]);
+                }
+            } else {
+                float* dst = g.part + ((int64_t)kb * nz + z) * g.J * KV_HD + pc;
+#pragma unroll
+                for (int i = 0; i < RPP; ++i) {
+                    const int r = part * RPP + i, jq = jrow + 8 * (r >> 2) + (r & 3);
+                    if (full || jq < g.J) dst[(int64_t)jq * KV_HD] = v[i];
                 }
             }
         }
