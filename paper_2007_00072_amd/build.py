@@ -94,12 +94,80 @@ def build(jobs: int = 4, verbose: bool = False, incremental: bool = False) -> st
     return LIB
 
 
+# Host-side AddressSanitizer + UndefinedBehaviorSanitizer build of the
+# same sources, for checking the host code (argument validation, workspace
+# carving, plan objects) on a machine without a GPU.  The sanitizers apply
+# to host code only; device code is compiled unoptimised (its kernels are
+# never launched from this build).  Load it with the sanitizer runtime
+# preloaded (hostsan_runtime()) and DMTX_LIB pointing at it.
+HOSTSAN_DIR = os.path.join(BUILD, "hostsan")
+HOSTSAN_LIB = os.path.join(HOSTSAN_DIR, "libdmtx_hostsan.so")
+HOSTSAN_FLAGS = [
+    "--offload-arch=gfx950", "-g", "-std=c++17", "-fPIC", "-fno-omit-frame-pointer",
+    "-Xarch_host", "-O1", "-Xarch_device", "-O0",
+    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=all",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I" + os.path.join(ROOT, "include"),
+]
+
+
+def hostsan_runtime() -> str:
+    """Path of clang's shared ASan runtime (which carries UBSan too)."""
+    out = subprocess.run([hipcc(), "--offload-host-only", "-print-file-name=libclang_rt.asan-x86_64.so"],
+                         capture_output=True, text=True).stdout.strip()
+    if out and os.path.isabs(out) and os.path.exists(out):
+        return out
+    llvm = os.path.join(os.path.dirname(os.path.dirname(os.path.realpath(hipcc()))), "lib", "llvm", "lib", "clang")
+    for ver in sorted(os.listdir(llvm)) if os.path.isdir(llvm) else []:
+        cand = os.path.join(llvm, ver, "lib", "linux", "libclang_rt.asan-x86_64.so")
+        if os.path.exists(cand):
+            return cand
+    raise RuntimeError("clang's shared ASan runtime not found")
+
+
+def hostsan_stale() -> bool:
+    if not os.path.exists(HOSTSAN_LIB):
+        return True
+    t = os.path.getmtime(HOSTSAN_LIB)
+    return any(_deps_mtime(src) > t for src in SOURCES)
+
+
+def build_hostsan(jobs: int = 4, verbose: bool = False) -> str:
+    """Builds the host-sanitized library (every source, then the link)."""
+    os.makedirs(HOSTSAN_DIR, exist_ok=True)
+
+    def one(src):
+        obj = os.path.join(HOSTSAN_DIR, os.path.splitext(src)[0] + ".o")
+        cmd = [hipcc(), *HOSTSAN_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"sanitized compile of {src} failed:\n{' '.join(cmd)}\n{r.stderr}")
+        return obj
+
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(one, SOURCES))
+    tmp = HOSTSAN_LIB + ".tmp"
+    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-shared-libsan",
+           "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-o", tmp, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{' '.join(cmd)}\n{r.stderr}")
+    os.replace(tmp, HOSTSAN_LIB)
+    if verbose:
+        print("built", HOSTSAN_LIB)
+    return HOSTSAN_LIB
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=min(4, os.cpu_count() or 1))
     ap.add_argument("--incremental", action="store_true", help="recompile only sources newer than their objects")
+    ap.add_argument("--hostsan", action="store_true", help="also build the host-sanitized library")
     a = ap.parse_args()
     build(a.jobs, verbose=True, incremental=a.incremental)
+    if a.hostsan:
+        build_hostsan(a.jobs, verbose=True)
 
 
 if __name__ == "__main__":

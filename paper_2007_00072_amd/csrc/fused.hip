@@ -504,8 +504,8 @@ __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, c
 // each block finds its job from the jobs' first-block table, then covers
 // columns 32x .. 32x+31 of one partial set (a whole 128-byte line of every
 // partial row) as 8 four-column groups x 32 row phases; each phase sums
-// rows ph, ph+32, ... with four loads in flight, and the 32 phase sums are
-// added in phase order.  Set y of a job is part + y*nblk*cols -> out[y].
+// rows ph, ph+32, ... with eight loads in flight (one memory round trip
+// for 256 partial rows), and the 32 phase sums are added in phase order.  Set y of a job is part + y*nblk*cols -> out[y].
 // With qkv_H > 0 the columns are (s, h, p) of a fused projection and land
 // in out[s][p * qkv_H + h] (single partial set).
 constexpr int FIN_COLS = 32;
@@ -525,21 +525,22 @@ __global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
     const int cg = threadIdx.x % (FIN_COLS / 4), ph = threadIdx.x / (FIN_COLS / 4);
     const int c = cbk * FIN_COLS + cg * 4;
     const float* base = job.part + (int64_t)set * nblk * cols;
-    floatx4 s[4];
+    constexpr int U = 8;
+    floatx4 s[U];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) s[u] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < U; ++u) s[u] = floatx4{0.f, 0.f, 0.f, 0.f};
     if (c < cols) {
-        int b = ph;
-        for (; b + 3 * NPH < nblk; b += 4 * NPH) {
+        for (int b = ph; b < nblk; b += U * NPH) {
+            floatx4 t[U];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + NPH * u) * cols + c);
+            for (int u = 0; u < U; ++u)
+                t[u] = b + NPH * u < nblk ? *reinterpret_cast<const floatx4*>(base + (int64_t)(b + NPH * u) * cols + c)
+                                          : floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int u = 0; u < U; ++u) s[u] += t[u];
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (b + NPH * u < nblk) s[u] += *reinterpret_cast<const floatx4*>(base + (int64_t)(b + NPH * u) * cols + c);
     }
-    red[ph][cg] = (s[0] + s[1]) + (s[2] + s[3]);
+    red[ph][cg] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
     __syncthreads();
     if (ph == 0 && c < cols) {
         floatx4 t = red[0][cg];

@@ -1449,7 +1449,8 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
 // waves (group g takes slices g, g + KG, ...), so a wave holds a larger
 // tile of the output and reads fewer fragments per MFMA; the groups' fp32
 // partial tiles are added through LDS before the stores.
-template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG>
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG,
+          bool RS = false>
 __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int by) {
     constexpr int NT = 64 * WGM * WGN * KG, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
     constexpr int NQ = BKS / 16;  // 16-wide k slices per step
@@ -1488,6 +1489,20 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
         for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    // RS: partial row sums of A over the contraction (Epilogue::rsum).  The
+    // waves of one tile row (tiles_n blocks x WGN waves that read the same
+    // A rows) share its 16-wide k slices round robin: wave wn of block tn
+    // adds up the A fragments of slices u = s * NQL + q with
+    // u % (tiles_n * WGN) == tn * WGN + wn (a fragment covers 16 k of 32
+    // rows, the two lane halves complementary k) and writes partial row
+    // tn * WGN + wn.
+    static_assert(!RS || KG == 1, "row sums need a single k group");
+    const bool rsum = RS && g.c.rsum != nullptr;
+    const int rs_nw = g.tiles_n * WGN;
+    int rs_next = tn * WGN + wn;
+    float rs[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) rs[i] = 0.f;
 
     const int nk = (ke - kb) / BKS;
     auto issue = [&](int s) {
@@ -1545,11 +1560,29 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
             __builtin_amdgcn_sched_barrier(0);
             mma(cur);
             __builtin_amdgcn_sched_barrier(0);
+            if constexpr (RS) {
+                if (rsum && s * NQL + q == rs_next) {
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) rs[i] += (float)a[cur][i][t];
+                    rs_next += rs_nw;
+                }
+            }
         }
     }
 
     const int mw = m0 + wm * WM, nw = n0 + wn * WN;
     if constexpr (KG == 1) {
+        if (RS && rsum) {
+            float* prow = g.c.rsum + (int64_t)(tn * WGN + wn) * g.c.rsum_ld;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const float v = rs[i] + __shfl_xor(rs[i], 32, 64);
+                const int m = mw + i * 32 + lane;
+                if (lane < 32 && m < g.M) prow[m] = v;
+            }
+        }
         lean_epilogue<T, FM, FN>(g, acc, mw, nw, z, sidx, splits);
     } else {
         // group 0 stores rows [0, FM/2) of the wave tile and group 1 the
@@ -1597,28 +1630,30 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
     }
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG>
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG,
+          bool RS = false>
 __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
     int tm, tn, by;
     tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
-    lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, KG>(g, tm, tn, by);
+    lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, KG, RS>(g, tm, tn, by);
 }
 
 // Two unbatched, unsplit contractions in one launch: blocks (renumbered
 // over the 8 XCDs as a whole) below g0's tile count take g0's tiles, the
 // rest g1's, so two contractions that each leave CUs idle fill the chip
 // together.
-template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC>
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, bool RS = false>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lean_pair(GemmArgs g0, GemmArgs g1) {
     const int n0 = g0.tiles_m * g0.tiles_n, total = n0 + g1.tiles_m * g1.tiles_n;
     const int lid = xcd_order((int)blockIdx.x, total);
     int tm, tn;
     if (lid < n0) {
         tile_in(lid, g0.tiles_m, g0.tiles_n, tm, tn);
-        lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, 1>(g0, tm, tn, 0);
+        lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, 1, RS>(g0, tm, tn, 0);
     } else {
         tile_in(lid - n0, g1.tiles_m, g1.tiles_n, tm, tn);
-        lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, 1>(g1, tm, tn, 0);
+        // (same instance as g0's, so that both share one LDS allocation)
+        lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, 1, RS>(g1, tm, tn, 0);
     }
 }
 
@@ -1780,10 +1815,20 @@ void launch_x32(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_x32<T, BM, BN, WGM, WGN, STAGES, false, false>), grid, block, 0, st, g);
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, int KG = 1>
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, int KG = 1, bool RS = false>
 void launch_lean(const GemmArgs& g, hipStream_t st) {
     dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
     dim3 block(64 * WGM * WGN * KG);
+    if constexpr (RS) {
+        // row sums are produced for an outer-contiguous A only
+        if (g.b.kcontig)
+            hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, KG, true>), grid, block, 0,
+                               st, g);
+        else
+            hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, KG, true>), grid, block, 0,
+                               st, g);
+        return;
+    }
     if (g.a.kcontig && g.b.kcontig)
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, KG>), grid, block, 0, st, g);
     else if (g.a.kcontig)
@@ -1809,6 +1854,16 @@ template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean_pair(const GemmArgs& g0, const GemmArgs& g1, hipStream_t st) {
     dim3 grid(g0.tiles_m * g0.tiles_n + g1.tiles_m * g1.tiles_n);
     dim3 block(64 * WGM * WGN);
+    if (g0.c.rsum) {
+        // row sums of g0's A (outer-contiguous) are produced
+        if (g0.b.kcontig)
+            hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, true>), grid, block, 0,
+                               st, g0, g1);
+        else
+            hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, true>), grid, block,
+                               0, st, g0, g1);
+        return;
+    }
     if (g0.a.kcontig && g0.b.kcontig)
         hipLaunchKernelGGL((gemm_lean_pair<T, BM, BN, WGM, WGN, BKS, STAGES, true, true>), grid, block, 0, st, g0, g1);
     else if (g0.a.kcontig)
@@ -1832,8 +1887,14 @@ void launch_big(const GemmArgs& g, hipStream_t st) {
 template <typename T>
 void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
-        case 13: launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st); break;
-        case 15: launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st); break;
+        case 13:
+            if (g.c.rsum) launch_lean<T, 256, 256, 2, 4, 32, 4, 1, true>(g, st);
+            else launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st);
+            break;
+        case 15:
+            if (g.c.rsum) launch_lean<T, 128, 128, 2, 4, 64, 4, 1, true>(g, st);
+            else launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st);
+            break;
         case 16: launch_lean<T, 128, 128, 2, 2, 64, 4, 2>(g, st); break;
         case 17: launch_lean<T, 256, 256, 2, 2, 32, 4>(g, st); break;
         case 18: launch_lean<T, 128, 128, 2, 2, 64, 4>(g, st); break;
@@ -1967,6 +2028,21 @@ void apply_plan(GemmArgs& g, int dtype) {
     }
 }
 
+thread_local int t_rsum_parts = 0;
+
+// Keeps the row-sum request only where the kernel that runs produces it
+// (the lean 256x256 and 128x128 tiles, both 4 wave tiles wide, unsplit, A
+// outer-contiguous) and its partial rows fit.
+void settle_rowsums(GemmArgs& g) {
+    constexpr int WGN = 4;
+    const bool lean1 = g.cfg == 13 || g.cfg == 15;
+    const int nw = g.tiles_n * WGN;
+    const bool ok = g.c.rsum != nullptr && lean1 && g.splits <= 1 && !g.a.kcontig && g.batch == 1 &&
+                    nw <= g.c.rsum_cap && g.c.rsum_ld >= g.M;
+    t_rsum_parts = ok ? nw : 0;
+    if (!ok) g.c.rsum = nullptr;
+}
+
 void log_launch(const GemmArgs& g, int dtype) {
     if (!t_log_on) return;
     dm_contract_choice r{};
@@ -1980,6 +2056,7 @@ void log_launch(const GemmArgs& g, int dtype) {
 }  // namespace
 
 const dm_plan* current_plan() { return t_plan; }
+int gemm_rowsum_parts() { return t_rsum_parts; }
 PlanScope::PlanScope(const dm_plan* p) : prev(t_plan) { t_plan = p; }
 PlanScope::~PlanScope() { t_plan = prev; }
 int current_attn_path() { return t_plan ? t_plan->attn_path : 0; }
@@ -2025,6 +2102,7 @@ static int prepare(GemmArgs& g, int dtype, bool pair) {
 }
 
 int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
+    t_rsum_parts = 0;
     GemmArgs g = args;
     if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
     if (g.K <= 0) return set_error(DM_ERR_ARG, "contraction with K <= 0");
@@ -2040,6 +2118,7 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
         log_launch(g, dtype);
     } else {
         if (int rc = prepare(g, dtype, false)) return rc;
+        settle_rowsums(g);
         if (dtype == G_F16) launch_t<half_t>(g, st);
         else launch_t<bf16_t>(g, st);
         log_launch(g, dtype);
@@ -2051,6 +2130,7 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
 
 int launch_gemm_pair(int dtype, const GemmArgs& x0, const GemmArgs& x1, hipStream_t st) {
     constexpr int64_t CUS = 256;
+    t_rsum_parts = 0;
     if (dtype != G_F32 && x0.batch == 1 && x1.batch == 1 && x0.M > 0 && x0.N > 0 && x0.K > 0 && x1.M > 0 &&
         x1.N > 0 && x1.K > 0 && x0.a.kcontig == x1.a.kcontig && x0.b.kcontig == x1.b.kcontig) {
         GemmArgs g0 = x0, g1 = x1;
@@ -2062,6 +2142,10 @@ int launch_gemm_pair(int dtype, const GemmArgs& x0, const GemmArgs& x1, hipStrea
         const int64_t tiles = (int64_t)g0.tiles_m * g0.tiles_n + (int64_t)g1.tiles_m * g1.tiles_n;
         if (g0.cfg == 15 && g1.cfg == 15 && g0.splits == 1 && g1.splits == 1 && tiles >= CUS * 3 / 4 &&
             tiles <= CUS) {
+            // the pair runs lean 128x128 tiles unsplit: row sums of either
+            // operand A are produced (the first contraction's are reported)
+            settle_rowsums(g1);
+            settle_rowsums(g0);
             if (dtype == G_F16) launch_lean_pair<half_t, 128, 128, 2, 4, 64, 4>(g0, g1, st);
             else launch_lean_pair<bf16_t, 128, 128, 2, 4, 64, 4>(g0, g1, st);
             log_launch(g0, dtype);
@@ -2072,8 +2156,11 @@ int launch_gemm_pair(int dtype, const GemmArgs& x0, const GemmArgs& x1, hipStrea
         }
     }
     if (int rc = launch_gemm(dtype, x0, st)) return rc;
+    const int first_parts = t_rsum_parts;
     trace_next("2");
-    return launch_gemm(dtype, x1, st);
+    const int rc = launch_gemm(dtype, x1, st);
+    t_rsum_parts = first_parts;
+    return rc;
 }
 
 }  // namespace dm

@@ -67,6 +67,15 @@ struct Epilogue {
     IdxMap bias_map;
     const void* resid;  // optional, same addressing as C (single pointer)
     int out_f32;        // C (and resid) stored as float instead of the input dtype
+    // optional: partial fp32 sums of A's rows over the contraction, as
+    // rows of rsum (row stride rsum_ld >= M, at most rsum_cap rows); the sum
+    // of partial rows 0 .. n-1 at column m is row m of A summed over k, with
+    // n = gemm_rowsum_parts() after the launch (0: not produced, and rsum
+    // untouched).  Only the lean 256x256 and 128x128 tiles, unsplit, with A
+    // outer-contiguous produce them.
+    float* rsum;
+    int rsum_ld;
+    int rsum_cap;
 };
 
 struct GemmArgs {
@@ -88,6 +97,10 @@ struct GemmArgs {
     // rows and columns (offsets then computed once per block)
     int blk32;
 };
+
+// Number of Epilogue::rsum partial rows the last launch_gemm on this
+// thread wrote (for launch_gemm_pair: its first contraction's), 0 if none.
+int gemm_rowsum_parts();
 
 // Largest tile configuration index (contract's tile_cfg, plan entries).
 constexpr int GEMM_MAX_CFG = 19;

@@ -581,9 +581,20 @@ int project_bwd(const Dims& x, int layout, const void* in, int64_t T, int64_t n,
 // segments]^T X.
 // pair: a further contraction launched together with the first group's
 // weight gradient (one launch when both fit the chip at once).
+// bias (optional, a single group of all nseg segments only): the weight
+// gradient contraction also takes the input-bias gradients, as partial row
+// sums of its dstk^T operand over the tokens (bias->part, at most
+// bias->cap rows of nseg * H * P floats) where its kernel allows;
+// bias->parts is the number of partial rows written (0: none).
+struct BiasParts {
+    float* part;
+    int cap;
+    int parts;
+};
 int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, const void* dstk, int nseg, int seg0,
                         const ProjGroup* grp, int n, const dm_layer_params* prm, void* dx, const dm_layer_grads* g,
-                        const void* resid, hipStream_t st, const GemmArgs* pair = nullptr) {
+                        const void* resid, hipStream_t st, const GemmArgs* pair = nullptr,
+                        BiasParts* bias = nullptr) {
     const int64_t H = x.H, I = x.I, P = x.P, HP = H * P, ld = nseg * HP;
     const IdxMap wmap = make_map((uint32_t)P, (uint32_t)H, H * I, I, 0);
     const void* w[3] = {prm->wq, prm->wk, prm->wv};
@@ -603,16 +614,23 @@ int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, co
         }
     }
     TraceScope t_(pair ? "B12+19 out_dw+qkv_dw" : "B19 qkv_dw", st);
+    if (bias) bias->parts = 0;
+    const bool want_bias = bias && n == 1 && grp[0].s1 - grp[0].s0 == nseg;
     for (int i = 0; i < n; ++i) {
         const int s0 = grp[i].s0, ns = grp[i].s1 - grp[i].s0;
         if (i > 0) trace_next(grp[i].sub);
         Epilogue cw = epi(dw[s0], wmap, linear_map(1), true, true);
         for (int j = 0; j < ns; ++j) cw.ptr[j] = dw[s0 + j];
         cw.nseg = ns; cw.seg_on_m = 1;
+        if (want_bias) {
+            // row (s, h, p) of dstk^T, partial sums in the same column order
+            cw.rsum = bias->part; cw.rsum_ld = (int)(ns * HP); cw.rsum_cap = bias->cap;
+        }
         const void* a = B8(dstk, (size_t)x.es * (s0 - seg0) * HP);
         const GemmArgs gw = gemm(ns * HP, I, T, 1, opnd(a, false, linear_map(ld)), act_kn(in, layout, T, I), cw);
         if (i == 0 && pair) DM_TRY(launch_gemm_pair(x.dtype, gw, *pair, st));
         else DM_TRY(launch_gemm(x.dtype, gw, st));
+        if (want_bias) bias->parts = gemm_rowsum_parts();
     }
     return DM_OK;
 }
@@ -620,10 +638,10 @@ int project_stacked_bwd(const Dims& x, int layout, const void* in, int64_t T, co
 // Backward of project_fused on the token-major [T][3][H][P] gradient.
 int project_fused_bwd(const Dims& x, int layout, const void* in, const void* dqkv, const dm_layer_params* prm,
                       void* dx, const dm_layer_grads* g, const void* resid, hipStream_t st,
-                      const GemmArgs* pair = nullptr) {
+                      const GemmArgs* pair = nullptr, BiasParts* bias = nullptr) {
     ProjGroup grp[3];
     const int n = proj_groups(x.qkv_fusion, grp);
-    return project_stacked_bwd(x, layout, in, x.Tq, dqkv, 3, 0, grp, n, prm, dx, g, resid, st, pair);
+    return project_stacked_bwd(x, layout, in, x.Tq, dqkv, 3, 0, grp, n, prm, dx, g, resid, st, pair, bias);
 }
 
 }  // namespace
@@ -860,19 +878,24 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
                               B8(dqkv, (size_t)es * I), ld, B8(dqkv, (size_t)es * 2 * I), ld, st));
     // Q, K, V dX (fused) + encoder-input residual; Q, K, V dW (fused) with Out dW
     const GemmArgs out_dw = out_dw_args(x, gamma, dAO, DM_BJI, g->dwo);
-    DM_TRY(project_fused_bwd(x, DM_BJI, x_in, dqkv, prm, dx, g, dS1, st, &out_dw));
-    // input-bias grads
-    {
+    // (the Q/K/V weight gradient also takes partial column sums of dQKV for
+    // the input-bias gradients (B20), where its kernel allows)
+    const int ncs = colsum_blocks(T);
+    BiasParts bias = {part, ncs, 0};
+    DM_TRY(project_fused_bwd(x, DM_BJI, x_in, dqkv, prm, dx, g, dS1, st, &out_dw, &bias));
+    // input-bias partial sums otherwise
+    if (bias.parts == 0) {
         TraceScope t20("B20 qkv_bias_grad", st);
         run_colsum_partial(dt, T, (int)(3 * I), dqkv, part, st);
     }
     // LayerNorm-2 (dgamma2, dbeta2, db2), activation (db1), LayerNorm-1
     // (dgamma1, dbeta1, dbo) and input-bias (dbq, dbk, dbv) column sums
-    const int nln = ln_bwd_blocks(T, (int)I, dt, fl.ln_form), ncs = colsum_blocks(T);
+    const int nln = ln_bwd_blocks(T, (int)I, dt, fl.ln_form);
     const FinishJob jobs[4] = {finish_job3(part_ln2, nln, (int)I, g->dg2, g->dbe2, g->db2),
                                finish_job(part_act, act_bwd_blocks(T, dHT != nullptr), (int)F, g->db1),
                                finish_job3(part_ln1, nln, (int)I, g->dg1, g->dbe1, g->dbo),
-                               finish_job_qkv(part, ncs, (int)x.H, (int)x.P, 3, g->dbq, g->dbk, g->dbv)};
+                               finish_job_qkv(part, bias.parts ? bias.parts : ncs, (int)x.H, (int)x.P, 3, g->dbq,
+                                              g->dbk, g->dbv)};
     TraceScope tf("B colsum finish", st);
     run_colsum_finish_jobs(jobs, 4, st);
     return check_launch("input-bias backward");
@@ -987,11 +1010,15 @@ int mha_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const void* qin,
                               B8(ws, s.p.dgamma), B8(ws, s.p.dalpha), B8(ws, s.p.dbeta), bq, s.p.ldq, bk, s.p.ldk, bv,
                               s.p.ldv, st));
     if (fused) {
-        DM_TRY(project_fused_bwd(x, x.layout, qin, bq, prm, dq, g, nullptr, st));
+        BiasParts bias = {part, colsum_blocks(x.Tq), 0};
+        DM_TRY(project_fused_bwd(x, x.layout, qin, bq, prm, dq, g, nullptr, st, nullptr, &bias));
         TraceScope t_("B20 qkv_bias_grad", st);
-        run_colsum_partial(dt, x.Tq, (int)(3 * x.H * x.P), bq, part, st);
-        trace_next("finish");
-        run_colsum_finish_qkv(colsum_blocks(x.Tq), (int)x.H, (int)x.P, 3, part, g->dbq, g->dbk, g->dbv, st);
+        if (bias.parts == 0) {
+            run_colsum_partial(dt, x.Tq, (int)(3 * x.H * x.P), bq, part, st);
+            trace_next("finish");
+        }
+        run_colsum_finish_qkv(bias.parts ? bias.parts : colsum_blocks(x.Tq), (int)x.H, (int)x.P, 3, part, g->dbq,
+                              g->dbk, g->dbv, st);
     } else if (mode == PROJ_KV) {
         TraceScope t_("B18-20 q,kv_bwd", st);
         DM_TRY(project_bwd(x, x.layout, qin, x.Tq, x.P, bq, s.p.ldq, prm->wq, dq, g->dwq, nullptr, st));

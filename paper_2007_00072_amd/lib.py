@@ -15,7 +15,9 @@ import os
 from typing import Optional
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libdmtx.so")
+# DMTX_LIB names another build of the same library (the host-sanitized one
+# used by the CPU validation checks); by default the in-tree libdmtx.so
+LIB_PATH = os.environ.get("DMTX_LIB") or os.path.join(PKG, "libdmtx.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2007_00072_amd.build` "
