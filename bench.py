@@ -364,8 +364,10 @@ def main() -> int:
         path = ("keys" if "B13-17 score_bwd_keys" in ops else
                 "scores_next" if "F2-4 qkt_softmax_gamma" in ops else
                 "scores" if "F2-3 qkt_softmax" in ops else "separate")
-        out["data_movement"] = dict(dataflow.data_movement(s, wl.dtype, path), per="layer fwd+bwd",
-                                    paper="22.91% (V100; see paper_context)")
+        out["data_movement"] = dict(dataflow.data_movement(s, wl.dtype, path,
+                                                           epilogue="F7+8 linear1_bias_act" in ops,
+                                                           folded="B20 qkv_bias_grad" not in ops),
+                                    per="layer fwd+bwd", paper="22.91% (V100; see paper_context)")
     if a.kernels_json:
         with open(a.kernels_json, "w") as f:
             json.dump({"workload": wl.name, "ms_per_step": ms, "kernels": table}, f, indent=1)

@@ -503,16 +503,19 @@ __global__ __launch_bounds__(NT) void colsum_partial_k(int64_t rows, int cols, c
 // a list of jobs (partial sets of several operators, finished together);
 // each block finds its job from the jobs' first-block table, then covers
 // columns 32x .. 32x+31 of one partial set (a whole 128-byte line of every
-// partial row) as 8 four-column groups x 32 row phases; each phase sums
-// rows ph, ph+32, ... with eight loads in flight (one memory round trip
-// for 256 partial rows), and the 32 phase sums are added in phase order.  Set y of a job is part + y*nblk*cols -> out[y].
-// With qkv_H > 0 the columns are (s, h, p) of a fused projection and land
-// in out[s][p * qkv_H + h] (single partial set).
+// partial row) as 8 four-column groups x 64 row phases; each phase sums
+// rows ph, ph+64, ... with eight loads in flight (one memory round trip
+// for 512 partial rows).  The phase sums are added as a fixed tree: the 8
+// phases of a wave by butterfly shuffles, then the 8 waves' sums in wave
+// order.  Set y of a job is part + y*nblk*cols -> out[y].  With qkv_H > 0
+// the columns are (s, h, p) of a fused projection and land in
+// out[s][p * qkv_H + h] (single partial set).
 constexpr int FIN_COLS = 32;
+constexpr int FIN_NT = 512;
 
-__global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
-    constexpr int NPH = NT / (FIN_COLS / 4);  // row phases
-    __shared__ floatx4 red[NPH][FIN_COLS / 4];
+__global__ __launch_bounds__(FIN_NT) void colsum_finish_k(FinishJobs fj) {
+    constexpr int CG = FIN_COLS / 4, NPH = FIN_NT / CG, NWV = FIN_NT / 64;  // column groups, row phases, waves
+    __shared__ floatx4 red[NWV][CG];
     int jb = 0;
 #pragma unroll
     for (int i = 1; i < MAX_FINISH_JOBS; ++i)
@@ -522,7 +525,7 @@ __global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
     const int local = (int)blockIdx.x - fj.first[jb];
     const int ncb = (cols + FIN_COLS - 1) / FIN_COLS;
     const int set = local / ncb, cbk = local - set * ncb;
-    const int cg = threadIdx.x % (FIN_COLS / 4), ph = threadIdx.x / (FIN_COLS / 4);
+    const int cg = threadIdx.x % CG, ph = threadIdx.x / CG, wave = threadIdx.x / 64;
     const int c = cbk * FIN_COLS + cg * 4;
     const float* base = job.part + (int64_t)set * nblk * cols;
     constexpr int U = 8;
@@ -540,11 +543,18 @@ __global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
             for (int u = 0; u < U; ++u) s[u] += t[u];
         }
     }
-    red[ph][cg] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
+    floatx4 t = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
+    // the wave's 8 phases of this column group (lanes cg, cg + 8, ..., cg + 56)
+#pragma unroll
+    for (int d = CG; d < 64; d <<= 1)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) t[q] += __shfl_xor(t[q], d, 64);
+    if ((threadIdx.x & 63) < CG) red[wave][cg] = t;
     __syncthreads();
-    if (ph == 0 && c < cols) {
-        floatx4 t = red[0][cg];
-        for (int i = 1; i < NPH; ++i) t += red[i][cg];
+    if (threadIdx.x < CG && c < cols) {
+        floatx4 tot = red[0][cg];
+#pragma unroll
+        for (int w = 1; w < NWV; ++w) tot += red[w][cg];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int cc = c + q;
@@ -552,9 +562,9 @@ __global__ __launch_bounds__(NT) void colsum_finish_k(FinishJobs fj) {
                 // column (s, h, p) of a fused projection -> bias gradient b_s[p][h]
                 const int I = job.qkv_H * job.qkv_P;
                 const int sg = cc / I, hp = cc - sg * I, hh = hp / job.qkv_P, pp = hp - hh * job.qkv_P;
-                job.out[sg][pp * job.qkv_H + hh] = t[q];
+                job.out[sg][pp * job.qkv_H + hh] = tot[q];
             } else {
-                job.out[set][cc] = t[q];
+                job.out[set][cc] = tot[q];
             }
         }
     }
@@ -1012,7 +1022,7 @@ void run_colsum_finish_jobs(const FinishJob* jobs, int n, hipStream_t st) {
         fj.first[i] = blocks;
         blocks += (jobs[i].cols + FIN_COLS - 1) / FIN_COLS * jobs[i].nsets;
     }
-    hipLaunchKernelGGL(colsum_finish_k, dim3(blocks), dim3(NT), 0, st, fj);
+    hipLaunchKernelGGL(colsum_finish_k, dim3(blocks), dim3(FIN_NT), 0, st, fj);
 }
 
 void run_colsum_finish(int nblk, int cols, const float* part, float* out, hipStream_t st) {

@@ -1266,6 +1266,11 @@ struct LeanK {
         for (int i = 0; i < NV; ++i) lds_dma16(src[i] + s * BKS, st + (uint32_t)(i * NT + w * 64) * 16u);
         (void)kb;
     }
+    // the same copies one at a time (prep once per step, then copy i)
+    __device__ __forceinline__ const T* prep(const Operand&, int64_t, int, int) const { return nullptr; }
+    __device__ __forceinline__ void copy(const T*, int s, int i, uint32_t st) const {
+        lds_dma16(src[i] + s * BKS, st + (uint32_t)(i * NT + (threadIdx.x >> 6) * 64) * 16u);
+    }
     // lane l: row ob + l % 32, k = kk + 8 (l / 32) .. +7
     __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
         const int r = ob + (lane & 31);
@@ -1298,6 +1303,14 @@ struct LeanO {
         const T* base = reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off;
 #pragma unroll
         for (int i = 0; i < NV; ++i) lds_dma16(base + poff[i], st + (uint32_t)(i * NT + w * 64) * 16u);
+    }
+    __device__ __forceinline__ const T* prep(const Operand& op, int64_t boff, int kb, int s) const {
+        int seg = 0;
+        const int64_t off = map_off(op.row, (uint32_t)(kb + s * BKS), op.nseg, &seg);
+        return reinterpret_cast<const T*>(seg_ptr(op.ptr, seg)) + boff + off;
+    }
+    __device__ __forceinline__ void copy(const T* base, int, int i, uint32_t st) const {
+        lds_dma16(base + poff[i], st + (uint32_t)(i * NT + (threadIdx.x >> 6) * 64) * 16u);
     }
     __device__ __forceinline__ static u32x4 frag(const T* lds, int ob, int kk, int lane) {
         return Frag32<T, R, false>::read(lds, ob, kk, lane);
@@ -1368,12 +1381,82 @@ __device__ __forceinline__ void lean_store(const GemmArgs& g, const LeanOut& o, 
     }
 }
 
+// Stores through LDS (row-major output, one pointer, N and the row pitch
+// multiples of 8): each 32-row block of the wave's tile is written to the
+// wave's own LDS region in its accumulator layout (rows padded by 32 bytes,
+// so the two half-waves' rows fall on disjoint banks), then read back as
+// 16-byte row pieces, so every global store instruction writes whole
+// 128-byte lines.  A wave's LDS accesses run in order, so no barrier is
+// needed between its writes and reads.
+// ACT: also the activation output (Epilogue::act_out) of each stored
+// piece; its read-back loop is not unrolled, so the accumulator loop stays
+// small enough to unroll (the accumulators must stay in registers).
+template <typename OutT, int FM, int FN, bool ACT = false>
+__device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanOut& o, const floatx16 (&acc)[FM][FN],
+                                                  int mw, int nw, const float (&bn)[FN], float alpha,
+                                                  unsigned char* region) {
+    constexpr int WN = FN * 32, LDR = WN + 32 / (int)sizeof(OutT);  // row pitch in elements
+    // rows per read pass (lanes past RPI * VPR idle when VPR does not divide 64)
+    constexpr int EPV = 16 / (int)sizeof(OutT), VPR = WN / EPV, RPI = 64 / VPR, NPASS = (32 + RPI - 1) / RPI;
+    static_assert(VPR <= 64 && WN % EPV == 0, "staged store shape");
+    OutT* sm = reinterpret_cast<OutT*>(region);
+    const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
+    const int rr0 = lane / VPR, vc = (lane % VPR) * EPV;
+    OutT* out = reinterpret_cast<OutT*>(o.ptr[0]) + o.coff;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int mb = mw + i * 32;
+        if (mb >= g.M) break;
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rr = 8 * (r >> 2) + 4 * h + (r & 3);
+                sm[rr * LDR + j * 32 + c] = from_f<OutT>(acc[i][j][r] * alpha + bn[j]);
+            }
+        const int n = nw + vc;
+        if constexpr (!ACT) {
+#pragma unroll
+            for (int p = 0; p < NPASS; ++p) {
+                const int rr = p * RPI + rr0;
+                if (lane < RPI * VPR && rr < 32) {
+                    const u32x4 v = *reinterpret_cast<const u32x4*>(sm + rr * LDR + vc);
+                    if (mb + rr < g.M && n < g.N) *reinterpret_cast<u32x4*>(out + (int64_t)(mb + rr) * o.ldc + n) = v;
+                }
+            }
+        } else {
+            static_assert(sizeof(OutT) == 2, "activation output in a 16-bit type");
+#pragma unroll 1
+            for (int p = 0; p < NPASS; ++p) {
+                const int rr = p * RPI + rr0;
+                if (lane < RPI * VPR && rr < 32) {
+                    const u32x4 v = *reinterpret_cast<const u32x4*>(sm + rr * LDR + vc);
+                    if (mb + rr < g.M && n < g.N) {
+                        const int64_t off = (int64_t)(mb + rr) * o.ldc + n;
+                        *reinterpret_cast<u32x4*>(out + off) = v;
+                        // activation of the stored values (the bias + activation
+                        // operator's arithmetic, element index off .. off+7)
+                        float a[8], b[8];
+                        V8<OutT>::unpack(v, a);
+                        V8<OutT>::load(reinterpret_cast<const OutT*>(g.c.act_bias) + n, b);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) a[q] = act_fwd(a[q] + b[q], g.c.act);
+                        dropout8(g.c.act_dp, (uint64_t)off, a);
+                        V8<OutT>::store(reinterpret_cast<OutT*>(g.c.act_out) + o.coff + off, a);
+                    }
+                }
+            }
+        }
+    }
+}
+
 // Epilogue of a lean kernel for one wave's FM x FN accumulator blocks at
 // (mw, nw): split-k partials as row-major floats through the same store
-// routine as float outputs (one code path keeps registers few).
-template <typename T, int FM, int FN>
+// routine as float outputs (one code path keeps registers few).  region:
+// this wave's LDS for the staged stores (nullptr: straight stores).
+template <typename T, int FM, int FN, bool ACT = false>
 __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 (&acc)[FM][FN], int mw, int nw,
-                                              uint32_t z, int sidx, int splits) {
+                                              uint32_t z, int sidx, int splits, unsigned char* region = nullptr) {
     const int lane = threadIdx.x & 63, c = lane & 31;
     int dummy = 0;
     const Epilogue& e = g.c;
@@ -1438,6 +1521,12 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
             return;
         }
     }
+    if (region) {
+        if constexpr (ACT) lean_store_staged<T, FM, FN, true>(g, o, acc, mw, nw, bn, alpha, region);
+        else if (part || e.out_f32) lean_store_staged<float, FM, FN>(g, o, acc, mw, nw, bn, alpha, region);
+        else lean_store_staged<T, FM, FN>(g, o, acc, mw, nw, bn, alpha, region);
+        return;
+    }
     if (part || (o.cn && e.out_f32)) lean_store<float, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
     else if (o.cn) lean_store<T, true, FM, FN>(g, o, acc, mw, nw, bn, alpha);
     else if (e.out_f32) lean_store<float, false, FM, FN>(g, o, acc, mw, nw, bn, alpha);
@@ -1450,7 +1539,7 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
 // tile of the output and reads fewer fragments per MFMA; the groups' fp32
 // partial tiles are added through LDS before the stores.
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG,
-          bool RS = false>
+          bool RS = false, bool IL = false, bool ACT = false>
 __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int by) {
     constexpr int NT = 64 * WGM * WGN * KG, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
     constexpr int NQ = BKS / 16;  // 16-wide k slices per step
@@ -1536,6 +1625,69 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
         asm volatile("" ::: "memory");
         read(0, 0, kg);
     }
+    // IL (one wave per SIMD): every MFMA of a slice is issued next to its
+    // share of the next slice's fragment reads (and, in the last slice of
+    // a step, of the next step's copies), so the wave keeps its MFMA unit
+    // busy while LDS and memory work proceed.  Half of the last slice's
+    // MFMAs go before the step barrier.  No LDS wait is needed at the
+    // barrier: the slot refilled is that of step s-1, whose reads every
+    // wave has consumed (its MFMAs were issued) before reaching it.
+    static_assert(!IL || (KG == 1 && !RS), "interleaved schedule: single k group, no row sums");
+    if constexpr (IL) {
+        constexpr int NMF = FM * FN, NR = FM + FN, H = NMF / 2, R2 = NMF - H;
+        auto read_one = [&](int buf, int s, int q, int j) {
+            const T* A = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
+            const T* B = A + AS;
+            if (j < FM) a[buf][j] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + j * 32, q * 16, lane));
+            else b[buf][j - FM] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + (j - FM) * 32, q * 16, lane));
+        };
+        auto mma_one = [&](int buf, int t) {
+            acc[t / FN][t % FN] = Mfma32<T>::run(a[buf][t / FN], b[buf][t % FN], acc[t / FN][t % FN]);
+        };
+        for (int s = 0; s < nk; ++s) {
+#pragma unroll
+            for (int q = 0; q < NQL; ++q) {
+                const int cur = q & 1;
+                if (q + 1 < NQL) {
+#pragma unroll
+                    for (int t = 0; t < NMF; ++t) {
+                        mma_one(cur, t);
+#pragma unroll
+                        for (int j = t * NR / NMF; j < (t + 1) * NR / NMF; ++j) read_one(cur ^ 1, s, q + 1, j);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                } else {
+#pragma unroll
+                    for (int t = 0; t < H; ++t) mma_one(cur, t);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (s + STAGES - 2 < nk) wait_vm<(STAGES - 3) * NL>();
+                    else wait_vm<0>();
+                    __builtin_amdgcn_s_barrier();
+                    asm volatile("" ::: "memory");
+                    __builtin_amdgcn_sched_barrier(0);
+                    const int sn = s + STAGES - 1;
+                    const bool more = sn < nk;
+                    const uint32_t st = base + (uint32_t)((sn % STAGES) * STAGE);
+                    const T* pa = da.prep(g.a, aoff, kb, sn);
+                    const T* pb = db.prep(g.b, boff, kb, sn);
+#pragma unroll
+                    for (int u = 0; u < R2; ++u) {
+                        mma_one(cur, H + u);
+                        if (more) {
+#pragma unroll
+                            for (int c = u * NL / R2; c < (u + 1) * NL / R2; ++c) {
+                                if (c < DA::NV) da.copy(pa, sn, c, st);
+                                else db.copy(pb, sn, c - DA::NV, st + (uint32_t)(AS * sizeof(T)));
+                            }
+                        }
+#pragma unroll
+                        for (int j = u * NR / R2; j < (u + 1) * NR / R2; ++j) read_one(cur ^ 1, s + 1, 0, j);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            }
+        }
+    } else
     // Every 16-wide slice: the next slice's fragments are read while this
     // slice's MFMAs run.  Before the last slice of step s, once step s+1 has
     // landed and this wave's reads of step s are done, one barrier lets the
@@ -1583,7 +1735,20 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
                 if (lane < 32 && m < g.M) prow[m] = v;
             }
         }
-        lean_epilogue<T, FM, FN>(g, acc, mw, nw, z, sidx, splits);
+        // staged stores: every wave is done with the stages (its reads
+        // consumed, the last ones of a stale slot completed) before any
+        // wave reuses their LDS; each wave then owns 32 rows of its tile
+        // width (padded) at a time
+        unsigned char* region = nullptr;
+        if (g.ep_stage & (splits > 1 ? 2 : 1)) {
+            constexpr int OB = WN * 4 + 32;  // bytes per staged row, float output
+            static_assert(32 * OB * WGM * WGN <= STAGES * STAGE, "staging region");
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            region = smem + wl * 32 * OB;
+        }
+        lean_epilogue<T, FM, FN, ACT>(g, acc, mw, nw, z, sidx, splits, region);
     } else {
         // group 0 stores rows [0, FM/2) of the wave tile and group 1 the
         // rest: each group first hands the other half of its partial tile
@@ -1631,11 +1796,11 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG,
-          bool RS = false>
+          bool RS = false, bool IL = false, bool ACT = false>
 __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
     int tm, tn, by;
     tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
-    lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, KG, RS>(g, tm, tn, by);
+    lean_run<T, BM, BN, WGM, WGN, BKS, STAGES, AKC, BKC, KG, RS, IL, ACT>(g, tm, tn, by);
 }
 
 // Two unbatched, unsplit contractions in one launch: blocks (renumbered
@@ -1764,12 +1929,15 @@ struct TileCfg {
 // 19: lean 256x192 kernel (4 waves of 128x96) for outputs whose width is a
 // multiple of 192 but leaves 256x256 tiles short of the CU count (3072
 // columns: 16 x 16 tiles instead of 16 x 12); the 192-wide operand must be
-// contiguous along k (else run as 13).
+// contiguous along k (else run as 13).  20, 21: the tiles of 17 and 19
+// with the interleaved schedule (each MFMA issued next to its share of the
+// fragment reads and copies); contractions they do not take run as 17
+// and 19 would.
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
                             {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}, {128, 128, 2, 2},
-                            {256, 256, 2, 2}, {128, 128, 2, 2}, {256, 192, 2, 2}};
+                            {256, 256, 2, 2}, {128, 128, 2, 2}, {256, 192, 2, 2}, {256, 256, 2, 2}, {256, 192, 2, 2}};
 static_assert(sizeof(CFGS) / sizeof(CFGS[0]) == GEMM_MAX_CFG + 1, "configuration table");
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
@@ -1839,6 +2007,47 @@ void launch_lean(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, KG>), grid, block, 0, st, g);
 }
 
+// Lean kernels that also write the activation output (both operands
+// contiguous along k, as settle_act requires).
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+void launch_lean_act(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch);
+    dim3 block(64 * WGM * WGN);
+    hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, false, true>), grid, block,
+                       0, st, g);
+}
+
+// Lean kernels with the interleaved one-wave-per-SIMD schedule.
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+void launch_lean_il(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig && g.b.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, true>), grid, block, 0,
+                           st, g);
+    else if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, false, 1, false, true>), grid, block, 0,
+                           st, g);
+    else if (g.b.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, 1, false, true>), grid, block, 0,
+                           st, g);
+    else
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, 1, false, true>), grid, block,
+                           0, st, g);
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+void launch_lean_il_bk(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, true>), grid, block, 0,
+                           st, g);
+    else
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, 1, false, true>), grid, block, 0,
+                           st, g);
+}
+
 // Lean kernels whose B tile width only suits a k-contiguous B operand.
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean_bk(const GemmArgs& g, hipStream_t st) {
@@ -1889,16 +2098,20 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
         case 13:
             if (g.c.rsum) launch_lean<T, 256, 256, 2, 4, 32, 4, 1, true>(g, st);
+            else if (g.c.act_out) launch_lean_act<T, 256, 256, 2, 4, 32, 4>(g, st);
             else launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st);
             break;
         case 15:
             if (g.c.rsum) launch_lean<T, 128, 128, 2, 4, 64, 4, 1, true>(g, st);
+            else if (g.c.act_out) launch_lean_act<T, 128, 128, 2, 4, 64, 4>(g, st);
             else launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st);
             break;
         case 16: launch_lean<T, 128, 128, 2, 2, 64, 4, 2>(g, st); break;
         case 17: launch_lean<T, 256, 256, 2, 2, 32, 4>(g, st); break;
         case 18: launch_lean<T, 128, 128, 2, 2, 64, 4>(g, st); break;
         case 19: launch_lean_bk<T, 256, 192, 2, 2, 32, 4>(g, st); break;
+        case 20: launch_lean_il<T, 256, 256, 2, 2, 32, 4>(g, st); break;
+        case 21: launch_lean_il_bk<T, 256, 192, 2, 2, 32, 4>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -1975,7 +2188,8 @@ void choose(GemmArgs& g) {
         g.splits = (g.K + g.kper - 1) / g.kper;
     }
     if (g.cfg == 19 && !g.b.kcontig) g.cfg = 13;
-    if ((g.cfg == 13 || g.cfg == 17 || g.cfg == 19) && !lean_ok(g, 32)) g.cfg = 14;
+    if (g.cfg == 21 && !g.b.kcontig) g.cfg = 20;
+    if ((g.cfg == 13 || g.cfg == 17 || g.cfg == 19 || g.cfg == 20 || g.cfg == 21) && !lean_ok(g, 32)) g.cfg = 14;
     if ((g.cfg == 15 || g.cfg == 16 || g.cfg == 18) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
     // tile counts of the configuration that runs (the fallback from 15 to 8
     // changes the tile width)
@@ -2002,6 +2216,20 @@ void set_affine(GemmArgs& g) {
     g.affine = 1;
 }
 
+// Whether the lean kernels may stage the output (and split partials)
+// through LDS: row-major single-pointer output without a residual, 16-byte
+// aligned rows of whole 8-element pieces.
+void set_ep_stage(GemmArgs& g) {
+    const Epilogue& e = g.c;
+    g.ep_stage = 0;
+    if (g.N % 8) return;
+    if ((uintptr_t)g.split_ws % 16 == 0) g.ep_stage |= 2;
+    const bool bias_ok = !e.bias[0] || g.bias_mode == 1;
+    if (g.affine && e.contig_n && !e.resid && bias_ok && g.ldc % 8 == 0 && (g.batch == 1 || e.batch.s0 % 8 == 0) &&
+        e.batch.r0 == 0 && ((uintptr_t)e.ptr[0] % 16) == 0)
+        g.ep_stage |= 1;
+}
+
 // The plan of the running call (entries keyed by sizes, dtype and operand
 // contiguity) and this thread's launch record.
 thread_local const dm_plan* t_plan = nullptr;
@@ -2026,6 +2254,20 @@ void apply_plan(GemmArgs& g, int dtype) {
         g.splits = s;
         return;
     }
+}
+
+// Keeps the activation-output request only where the staged epilogue
+// writes it: unsplit lean 256x256 or 128x128 kernel (8 waves) with both
+// operands contiguous along k, staged output, 16-bit storage, no alpha
+// scaling or bias (the activation reads the stored C).
+bool settle_act(GemmArgs& g, int dtype) {
+    const Epilogue& e = g.c;
+    const bool ok = e.act_out && dtype != G_F32 && (g.cfg == 13 || g.cfg == 15) && g.a.kcontig && g.b.kcontig &&
+                    !e.rsum && g.splits <= 1 && (g.ep_stage & 1) &&
+                    !e.out_f32 && !e.bias[0] && e.alpha == 1.0f && e.act_bias && g.batch == 1 &&
+                    ((uintptr_t)e.act_out % 16) == 0;
+    if (!ok) g.c.act_out = nullptr;
+    return ok;
 }
 
 thread_local int t_rsum_parts = 0;
@@ -2057,6 +2299,15 @@ void log_launch(const GemmArgs& g, int dtype) {
 
 const dm_plan* current_plan() { return t_plan; }
 int gemm_rowsum_parts() { return t_rsum_parts; }
+
+static int prepare(GemmArgs& g, int dtype, bool pair);
+
+bool gemm_act_fusable(int dtype, const GemmArgs& args) {
+    if (dtype == G_F32 || args.M <= 0 || args.N <= 0 || args.K <= 0 || args.batch != 1) return false;
+    GemmArgs g = args;
+    if (prepare(g, dtype, false)) return false;
+    return settle_act(g, dtype);
+}
 PlanScope::PlanScope(const dm_plan* p) : prev(t_plan) { t_plan = p; }
 PlanScope::~PlanScope() { t_plan = prev; }
 int current_attn_path() { return t_plan ? t_plan->attn_path : 0; }
@@ -2092,6 +2343,7 @@ static int prepare(GemmArgs& g, int dtype, bool pair) {
         return set_error(DM_ERR_UNSUPPORTED, "bias map radix along the output vector must be a multiple of 8");
     if (!g.split_ws) g.splits = 1;
     set_affine(g);
+    set_ep_stage(g);
     if (g.cfg < 0) apply_plan(g, dtype);
     if (pair && g.cfg < 0) { g.cfg = 15; g.splits = 1; }
     choose(g);
@@ -2119,6 +2371,7 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     } else {
         if (int rc = prepare(g, dtype, false)) return rc;
         settle_rowsums(g);
+        settle_act(g, dtype);
         if (dtype == G_F16) launch_t<half_t>(g, st);
         else launch_t<bf16_t>(g, st);
         log_launch(g, dtype);

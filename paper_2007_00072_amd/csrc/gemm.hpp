@@ -76,6 +76,14 @@ struct Epilogue {
     float* rsum;
     int rsum_ld;
     int rsum_cap;
+    // optional (storage-type output, no alpha scaling or bias): also writes
+    // act_out = dropout(act(C + act_bias[n])) at C's addresses, from the
+    // stored (rounded) C, with the dropout's element index m * ldc + n;
+    // only the staged epilogue of the lean kernels does (gemm_act_fusable)
+    void* act_out;
+    const void* act_bias;
+    int act;
+    DropParams act_dp;
 };
 
 struct GemmArgs {
@@ -96,14 +104,23 @@ struct GemmArgs {
     // set by the launcher: output maps affine over aligned blocks of 32
     // rows and columns (offsets then computed once per block)
     int blk32;
+    // set by the launcher: the lean kernels may stage their output tile
+    // through LDS and store 16-byte row pieces (bit 0: the output; bit 1:
+    // split-k partials)
+    int ep_stage;
 };
 
 // Number of Epilogue::rsum partial rows the last launch_gemm on this
 // thread wrote (for launch_gemm_pair: its first contraction's), 0 if none.
 int gemm_rowsum_parts();
 
+// Whether launch_gemm would run this contraction with the staged epilogue
+// that writes Epilogue::act_out (otherwise the request is ignored and the
+// caller applies the activation itself).
+bool gemm_act_fusable(int dtype, const GemmArgs& g);
+
 // Largest tile configuration index (contract's tile_cfg, plan entries).
-constexpr int GEMM_MAX_CFG = 19;
+constexpr int GEMM_MAX_CFG = 21;
 
 // Scratch bytes for a split-K contraction.
 inline size_t gemm_split_ws_bytes(int64_t M, int64_t N, int64_t batch, int splits) {

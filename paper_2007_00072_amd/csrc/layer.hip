@@ -732,20 +732,26 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
                       make_drop(d->p_attn_out, d->seed, 1, d->layer_id), y1, xhat1, rstd1, st, fl.ln_lanes);
     }
     DM_TRY(check_launch("bdrln 1"));
-    // Linear 1
+    // Linear 1, with bias + activation (+ dropout) in its epilogue where
+    // the contraction's kernel stages its output tile (else a launch of its
+    // own): both write H and A = dropout(act(H + b1)) from the stored H
     {
-        TraceScope t_("F7 linear1", st);
-        DM_TRY(launch_gemm(dt,
-                           gemm(T, x.F, x.I, 1, opnd(y1, true, linear_map(x.I)),
-                                opnd(prm->w1, true, linear_map(x.I)),
-                                epi(hbuf, linear_map(x.F), linear_map(1), true, false)),
-                           st));
-    }
-    // bias + activation (+ dropout)
-    {
-        TraceScope t_("F8 bias_act", st);
-        run_bias_act_fwd(dt, T, (int)x.F, hbuf, prm->b1, d->act, make_drop(d->p_ffn_act, d->seed, 3, d->layer_id),
-                         abuf, st);
+        GemmArgs g1 = gemm(T, x.F, x.I, 1, opnd(y1, true, linear_map(x.I)), opnd(prm->w1, true, linear_map(x.I)),
+                           epi(hbuf, linear_map(x.F), linear_map(1), true, false));
+        g1.c.act_out = abuf; g1.c.act_bias = prm->b1; g1.c.act = d->act;
+        g1.c.act_dp = make_drop(d->p_ffn_act, d->seed, 3, d->layer_id);
+        if (gemm_act_fusable(dt, g1)) {
+            TraceScope t_("F7+8 linear1_bias_act", st);
+            DM_TRY(launch_gemm(dt, g1, st));
+        } else {
+            g1.c.act_out = nullptr;
+            {
+                TraceScope t_("F7 linear1", st);
+                DM_TRY(launch_gemm(dt, g1, st));
+            }
+            TraceScope t_("F8 bias_act", st);
+            run_bias_act_fwd(dt, T, (int)x.F, hbuf, prm->b1, d->act, g1.c.act_dp, abuf, st);
+        }
     }
     DM_TRY(check_launch("bias+activation"));
     // Linear 2

@@ -57,6 +57,12 @@ REPLACES = {
 # Contractions the encoder layer issues as one launch (their tiles together
 # fill the chip): the backward's output-projection and Q/K/V weight gradients.
 PAIRED = {"B12+19 out_dw+qkv_dw": ("B12 out_dw", "B19 qkv_dw")}
+# Operators that run inside a contraction's epilogue where its kernel
+# allows (else as launches of their own): Linear 1 with bias + activation;
+# the input-bias gradient's partial sums inside the Q/K/V weight gradient
+# (that launch then also writes the three bias gradients).
+EPILOGUE = {"F7+8 linear1_bias_act": ("F7 linear1", "F8 bias_act")}
+FOLDED = {"B20 qkv_bias_grad": "B12+19 out_dw+qkv_dw"}
 # The launch sets one layer can run: every score step separate, scores on
 # chip, scores on chip with the next contraction in the same launch, and
 # that forward with the key-block backward (head size 64, K a multiple of 128).
@@ -76,10 +82,17 @@ def key_blocks(s: Shape, dtype: str):
     return True, s.K // (32 * kg)
 
 
-def path_groups(w: Dict[str, "Work"], path: str) -> Dict[str, "Work"]:
-    """The launch groups of `w` that path `path` runs."""
+def path_groups(w: Dict[str, "Work"], path: str, epilogue: bool = False, folded: bool = False) -> Dict[str, "Work"]:
+    """The launch groups of `w` that path `path` runs (epilogue: the EPILOGUE
+    groups in place of their parts; folded: without the FOLDED launches)."""
     fused = PATHS[path]
     gone = {p for f in fused for p in REPLACES[f]} | {p for parts in PAIRED.values() for p in parts}
+    if epilogue:
+        gone |= {p for parts in EPILOGUE.values() for p in parts}
+    else:
+        gone |= set(EPILOGUE)
+    if folded:
+        gone |= set(FOLDED)
     return {k: v for k, v in w.items() if (k not in REPLACES or k in fused) and k not in gone}
 
 
@@ -117,6 +130,10 @@ def encoder_layer(s: Shape, dtype: str, elements: bool = False) -> Dict[str, Wor
     w["F6 bdrln1"] = m(4 * N * es + f4 * T + 3 * I * es)
     w["F7 linear1"] = g(T, F, I, N, F * I, Fh)
     w["F8 bias_act"] = m(2 * Fh * es + F * es)
+    # Linear 1 writing H and A = act(H + b1) from its epilogue: H is not
+    # read back
+    w["F7+8 linear1_bias_act"] = Work(w["F7 linear1"].flop, w["F7 linear1"].bytes + Fh * es + F * es, "mfma",
+                                      "contraction")
     w["F9 linear2"] = g(T, I, F, Fh, I * F, N)
     w["F10 bdrln2"] = m(4 * N * es + f4 * T + 3 * I * es)
     # backward
@@ -242,11 +259,16 @@ def unfused_table3(s: Shape, act_dropout: bool = False):
     return r
 
 
-def data_movement(s: Shape, dtype: str, path: str = "scores_next", act_dropout: bool = False) -> Dict[str, float]:
+def data_movement(s: Shape, dtype: str, path: str = "scores_next", act_dropout: bool = False,
+                  epilogue: bool = False, folded: bool = False) -> Dict[str, float]:
     """The data-movement reduction of the fused layer against the operators
     one by one (the analogue of the paper's figure, from its Table 3 I/O
     columns): elements moved per forward + backward step, both ways."""
     unf = sum(i + o for _, i, o in unfused_table3(s, act_dropout))
-    fused = sum(w.bytes for w in path_groups(encoder_layer(s, dtype, elements=True), path).values())
+    w = encoder_layer(s, dtype, elements=True)
+    fused = sum(x.bytes for x in path_groups(w, path, epilogue, folded).values())
+    if folded:
+        # the weight-gradient launch also writes the three bias gradients
+        fused += 3 * s.I
     return {"unfused_Melem": round(unf / 1e6, 2), "fused_Melem": round(fused / 1e6, 2),
             "reduction": round(1.0 - fused / unf, 4)}

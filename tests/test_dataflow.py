@@ -72,3 +72,24 @@ def test_data_movement_reduction_positive():
     # the transposed dO copy is overhead, not algorithmic traffic
     w = dataflow.encoder_layer(s, "f16")
     assert w["B1-2 ln2_bwd"].overhead == s.B * s.J * s.I * 2
+
+
+def test_epilogue_and_folded_groups():
+    # Linear 1 with bias + activation in its epilogue: the contraction's flop,
+    # H not read back; the folded input-bias gradient leaves its launch out
+    s = WORKLOADS["bert_large_f16"].shape
+    w = dataflow.encoder_layer(s, "f16")
+    T, F = s.B * s.J, s.F
+    for k, parts in dataflow.EPILOGUE.items():
+        assert w[k].flop == sum(w[p].flop for p in parts)
+        assert w[k].bytes == sum(w[p].bytes for p in parts) - T * F * 2
+    g = dataflow.path_groups(w, "keys", epilogue=True, folded=True)
+    assert "F7+8 linear1_bias_act" in g and "F7 linear1" not in g and "F8 bias_act" not in g
+    assert "B20 qkv_bias_grad" not in g
+    g0 = dataflow.path_groups(w, "keys")
+    assert "F7+8 linear1_bias_act" not in g0 and "F8 bias_act" in g0 and "B20 qkv_bias_grad" in g0
+    assert sum(x.flop for x in g.values()) == sum(x.flop for x in g0.values())
+    d0 = dataflow.data_movement(s, "f16", "keys")
+    d1 = dataflow.data_movement(s, "f16", "keys", epilogue=True, folded=True)
+    # H (T*F) and dQKV (3*T*I) are read once less; the bias gradients (3*I) move with the pair
+    assert (d0["fused_Melem"] - d1["fused_Melem"]) * 1e6 == pytest.approx(T * F + 3 * T * s.I - 3 * s.I, abs=1e4)

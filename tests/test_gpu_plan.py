@@ -27,16 +27,18 @@ def _launches(wl, plan=None):
 def test_plan_entry_changes_the_kernel_and_keeps_parity():
     wl = small("bert_large_f16", B=2, J=96, K=96, H=4, P=64, W=64, I=256, F=512)
     recs, _ = _launches(wl)
-    lin1 = next(r for r in recs if r.label.decode() == "F7 linear1")
+    # Linear 1 (with bias + activation in its epilogue where its kernel allows)
+    is_lin1 = lambda r: r.label.decode() in ("F7 linear1", "F7+8 linear1_bias_act")
+    lin1 = next(r for r in recs if is_lin1(r))
     builtin = (lin1.tile_cfg, lin1.splits)
     want = 6 if builtin[0] != 6 else 2
     plan = lib.Plan([lib.ContractChoice(*lin1.key(), want, 1)], 0)
     recs2, _ = _launches(wl, plan)
-    got = next(r for r in recs2 if r.label.decode() == "F7 linear1")
+    got = next(r for r in recs2 if is_lin1(r))
     assert (got.tile_cfg, got.splits) == (want, 1)
     # every other contraction kept its built-in choice
     for a, b in zip(recs, recs2):
-        if a.label.decode() != "F7 linear1":
+        if not is_lin1(a):
             assert (a.tile_cfg, a.splits) == (b.tile_cfg, b.splits)
     check_encoder(wl, layer=1, plan=plan)
 
