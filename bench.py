@@ -365,7 +365,7 @@ def main() -> int:
                 "scores_next" if "F2-4 qkt_softmax_gamma" in ops else
                 "scores" if "F2-3 qkt_softmax" in ops else "separate")
         out["data_movement"] = dict(dataflow.data_movement(s, wl.dtype, path,
-                                                           epilogue="F7+8 linear1_bias_act" in ops,
+                                                           epilogue={k for k in dataflow.EPILOGUE if k in ops},
                                                            folded="B20 qkv_bias_grad" not in ops),
                                     per="layer fwd+bwd", paper="22.91% (V100; see paper_context)")
     if a.kernels_json:

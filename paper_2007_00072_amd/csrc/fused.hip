@@ -736,7 +736,9 @@ void softmax_bwd_t(int B, int H, int J, int len, float scale, const void* dalpha
 // its 8 columns' sums over all the rows it sees, the wave's lane groups
 // are added with shuffles at the end, and lane group 0 writes
 // part[q][blockIdx.x][columns].  Blocks stride over the tiles, so the
-// partial count is ln_bwd_blocks(rows, cols).
+// partial count is ln_bwd_blocks(rows, cols).  The blocks of each XCD take
+// a contiguous run of tiles, so the 32-byte pieces of one 128-byte line of
+// the transposed copy meet in one L2.
 constexpr int LN_TILE = 16;
 
 template <typename T, int LG>
@@ -744,6 +746,7 @@ __global__ __launch_bounds__(NTL) void ln_bwd_cs_k(LnBwdArgs a, int nblk) {
     constexpr int NW = NTL / 64;       // column slices
     constexpr int RPP = 64 / LG;       // rows per pass of one wave
     constexpr int NP = LN_TILE / RPP;  // passes per tile
+    static_assert(NP >= 1 && NP * RPP == LN_TILE, "tile rows");
     __shared__ float rowred[2][LN_TILE][NW][2];
     // transposed copy of the tile's dsub (16-bit types): column c's LN_TILE
     // rows at tb[c * LN_TILE ..], written out as 32-byte row pieces of
@@ -772,7 +775,11 @@ __global__ __launch_bounds__(NTL) void ln_bwd_cs_k(LnBwdArgs a, int nblk) {
     for (int q = 0; q < 8; ++q) { p_dyx[q] = 0.f; p_dy[q] = 0.f; p_dsub[q] = 0.f; }
 
     int buf = 0;
-    for (int64_t t0 = (int64_t)blockIdx.x * LN_TILE; t0 < a.rows; t0 += (int64_t)nblk * LN_TILE, buf ^= 1) {
+    // block -> tile: XCD x (blocks x, x + 8, ...) takes tiles
+    // x * nblk / 8 .. of every round of nblk tiles
+    const int b = (int)blockIdx.x;
+    const int tb0 = (nblk & 7) == 0 ? (b & 7) * (nblk >> 3) + (b >> 3) : b;
+    for (int64_t t0 = (int64_t)tb0 * LN_TILE; t0 < a.rows; t0 += (int64_t)nblk * LN_TILE, buf ^= 1) {
         // every load of the tile is issued before any arithmetic (rows past
         // the end re-read the tile's first row; their results are dropped)
         u32x4 ldy[NP], lxh[NP], ldb[NP];

@@ -1388,10 +1388,13 @@ __device__ __forceinline__ void lean_store(const GemmArgs& g, const LeanOut& o, 
 // 16-byte row pieces, so every global store instruction writes whole
 // 128-byte lines.  A wave's LDS accesses run in order, so no barrier is
 // needed between its writes and reads.
-// ACT: also the activation output (Epilogue::act_out) of each stored
-// piece; its read-back loop is not unrolled, so the accumulator loop stays
-// small enough to unroll (the accumulators must stay in registers).
-template <typename OutT, int FM, int FN, bool ACT = false>
+// ACT (Epilogue::act_mode) 1: also the activation output of each stored
+// piece; 2: the activation backward of each piece stored in its place,
+// with the lane's column sums over its rows added across the wave's lanes
+// at the end (partial row mw / (FM * 32)).  The read-back loop of these
+// is not unrolled, so the accumulator loop stays small enough to unroll
+// (the accumulators must stay in registers).
+template <typename OutT, int FM, int FN, int ACT = 0>
 __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanOut& o, const floatx16 (&acc)[FM][FN],
                                                   int mw, int nw, const float (&bn)[FN], float alpha,
                                                   unsigned char* region) {
@@ -1403,6 +1406,10 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
     const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
     const int rr0 = lane / VPR, vc = (lane % VPR) * EPV;
     OutT* out = reinterpret_cast<OutT*>(o.ptr[0]) + o.coff;
+    float cs[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) cs[q] = 0.f;
+
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int mb = mw + i * 32;
@@ -1415,7 +1422,7 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
                 sm[rr * LDR + j * 32 + c] = from_f<OutT>(acc[i][j][r] * alpha + bn[j]);
             }
         const int n = nw + vc;
-        if constexpr (!ACT) {
+        if constexpr (ACT == 0) {
 #pragma unroll
             for (int p = 0; p < NPASS; ++p) {
                 const int rr = p * RPI + rr0;
@@ -1425,7 +1432,7 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
                 }
             }
         } else {
-            static_assert(sizeof(OutT) == 2, "activation output in a 16-bit type");
+            static_assert(sizeof(OutT) == 2, "activation step in a 16-bit type");
 #pragma unroll 1
             for (int p = 0; p < NPASS; ++p) {
                 const int rr = p * RPI + rr0;
@@ -1433,20 +1440,46 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
                     const u32x4 v = *reinterpret_cast<const u32x4*>(sm + rr * LDR + vc);
                     if (mb + rr < g.M && n < g.N) {
                         const int64_t off = (int64_t)(mb + rr) * o.ldc + n;
-                        *reinterpret_cast<u32x4*>(out + off) = v;
-                        // activation of the stored values (the bias + activation
-                        // operator's arithmetic, element index off .. off+7)
                         float a[8], b[8];
                         V8<OutT>::unpack(v, a);
                         V8<OutT>::load(reinterpret_cast<const OutT*>(g.c.act_bias) + n, b);
+                        if constexpr (ACT == 1) {
+                            // the stored values, then their activation (the bias +
+                            // activation operator's arithmetic, element index
+                            // off .. off+7)
+                            *reinterpret_cast<u32x4*>(out + off) = v;
 #pragma unroll
-                        for (int q = 0; q < 8; ++q) a[q] = act_fwd(a[q] + b[q], g.c.act);
-                        dropout8(g.c.act_dp, (uint64_t)off, a);
-                        V8<OutT>::store(reinterpret_cast<OutT*>(g.c.act_out) + o.coff + off, a);
+                            for (int q = 0; q < 8; ++q) a[q] = act_fwd(a[q] + b[q], g.c.act);
+                            dropout8(g.c.act_dp, (uint64_t)off, a);
+                            V8<OutT>::store(reinterpret_cast<OutT*>(g.c.act_out) + o.coff + off, a);
+                        } else {
+                            // the activation backward of the (rounded) dA: the
+                            // activation backward operator's arithmetic
+                            float u[8];
+                            V8<OutT>::load(reinterpret_cast<const OutT*>(g.c.act_in) + o.coff + off, u);
+                            dropout8(g.c.act_dp, (uint64_t)off, a);
+#pragma unroll
+                            for (int q = 0; q < 8; ++q) {
+                                a[q] = to_f(from_f<OutT>(a[q] * act_grad(u[q] + b[q], g.c.act)));
+                                cs[q] += a[q];
+                            }
+                            V8<OutT>::store(out + off, a);
+                        }
                     }
                 }
             }
         }
+    }
+    if constexpr (ACT == 2) {
+        // lanes with the same 8 columns differ by multiples of VPR
+        static_assert((VPR & (VPR - 1)) == 0, "column groups of a power-of-two lane count");
+#pragma unroll
+        for (int d = VPR; d < 64; d <<= 1)
+#pragma unroll
+            for (int q = 0; q < 8; ++q) cs[q] += __shfl_xor(cs[q], d, 64);
+        const int n = nw + vc;
+        if (lane < VPR && n < g.N)
+            V8<float>::store(g.c.act_part + (int64_t)(mw / (FM * 32)) * g.N + n, cs);
     }
 }
 
@@ -1454,7 +1487,7 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
 // (mw, nw): split-k partials as row-major floats through the same store
 // routine as float outputs (one code path keeps registers few).  region:
 // this wave's LDS for the staged stores (nullptr: straight stores).
-template <typename T, int FM, int FN, bool ACT = false>
+template <typename T, int FM, int FN, int ACT = 0>
 __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 (&acc)[FM][FN], int mw, int nw,
                                               uint32_t z, int sidx, int splits, unsigned char* region = nullptr) {
     const int lane = threadIdx.x & 63, c = lane & 31;
@@ -1522,7 +1555,7 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
         }
     }
     if (region) {
-        if constexpr (ACT) lean_store_staged<T, FM, FN, true>(g, o, acc, mw, nw, bn, alpha, region);
+        if constexpr (ACT != 0) lean_store_staged<T, FM, FN, ACT>(g, o, acc, mw, nw, bn, alpha, region);
         else if (part || e.out_f32) lean_store_staged<float, FM, FN>(g, o, acc, mw, nw, bn, alpha, region);
         else lean_store_staged<T, FM, FN>(g, o, acc, mw, nw, bn, alpha, region);
         return;
@@ -1539,7 +1572,7 @@ __device__ __forceinline__ void lean_epilogue(const GemmArgs& g, const floatx16 
 // tile of the output and reads fewer fragments per MFMA; the groups' fp32
 // partial tiles are added through LDS before the stores.
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG,
-          bool RS = false, bool IL = false, bool ACT = false>
+          bool RS = false, bool IL = false, int ACT = 0>
 __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int by) {
     constexpr int NT = 64 * WGM * WGN * KG, WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
     constexpr int NQ = BKS / 16;  // 16-wide k slices per step
@@ -1796,7 +1829,7 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES, bool AKC, bool BKC, int KG,
-          bool RS = false, bool IL = false, bool ACT = false>
+          bool RS = false, bool IL = false, int ACT = 0>
 __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm_lean(GemmArgs g) {
     int tm, tn, by;
     tile_of(g.tiles_m, g.tiles_n, tm, tn, by);
@@ -2007,14 +2040,19 @@ void launch_lean(const GemmArgs& g, hipStream_t st) {
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, false, KG>), grid, block, 0, st, g);
 }
 
-// Lean kernels that also write the activation output (both operands
-// contiguous along k, as settle_act requires).
+// Lean kernels with the activation step in the epilogue (the operand
+// layouts settle_act admits: mode 1 A and B contiguous along k, mode 2 A
+// contiguous along k, B along n).
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean_act(const GemmArgs& g, hipStream_t st) {
     dim3 grid(g.tiles_m * g.tiles_n, g.batch);
     dim3 block(64 * WGM * WGN);
-    hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, false, true>), grid, block,
-                       0, st, g);
+    if (g.c.act_mode == 1)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, false, 1>), grid, block,
+                           0, st, g);
+    else
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, false, 1, false, false, 2>), grid,
+                           block, 0, st, g);
 }
 
 // Lean kernels with the interleaved one-wave-per-SIMD schedule.
@@ -2098,12 +2136,12 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
     switch (g.cfg) {
         case 13:
             if (g.c.rsum) launch_lean<T, 256, 256, 2, 4, 32, 4, 1, true>(g, st);
-            else if (g.c.act_out) launch_lean_act<T, 256, 256, 2, 4, 32, 4>(g, st);
+            else if (g.c.act_mode) launch_lean_act<T, 256, 256, 2, 4, 32, 4>(g, st);
             else launch_lean<T, 256, 256, 2, 4, 32, 4>(g, st);
             break;
         case 15:
             if (g.c.rsum) launch_lean<T, 128, 128, 2, 4, 64, 4, 1, true>(g, st);
-            else if (g.c.act_out) launch_lean_act<T, 128, 128, 2, 4, 64, 4>(g, st);
+            else if (g.c.act_mode) launch_lean_act<T, 128, 128, 2, 4, 64, 4>(g, st);
             else launch_lean<T, 128, 128, 2, 4, 64, 4>(g, st);
             break;
         case 16: launch_lean<T, 128, 128, 2, 2, 64, 4, 2>(g, st); break;
@@ -2256,19 +2294,30 @@ void apply_plan(GemmArgs& g, int dtype) {
     }
 }
 
-// Keeps the activation-output request only where the staged epilogue
-// writes it: unsplit lean 256x256 or 128x128 kernel (8 waves) with both
-// operands contiguous along k, staged output, 16-bit storage, no alpha
-// scaling or bias (the activation reads the stored C).
-bool settle_act(GemmArgs& g, int dtype) {
+// Keeps the activation step only where the staged epilogue takes it:
+// unsplit lean 256x256 or 128x128 kernel (8 waves: 2 wave rows), staged
+// row-major output, 16-bit storage, no alpha scaling or bias; mode 1 with A
+// and B contiguous along k, mode 2 with A contiguous along k and B along
+// n, its partial rows (2 per tile row) within act_part_cap.  Returns the
+// partial rows mode 2 writes (1 for mode 1), 0 when not taken.
+int settle_act(GemmArgs& g, int dtype) {
     const Epilogue& e = g.c;
-    const bool ok = e.act_out && dtype != G_F32 && (g.cfg == 13 || g.cfg == 15) && g.a.kcontig && g.b.kcontig &&
-                    !e.rsum && g.splits <= 1 && (g.ep_stage & 1) &&
-                    !e.out_f32 && !e.bias[0] && e.alpha == 1.0f && e.act_bias && g.batch == 1 &&
-                    ((uintptr_t)e.act_out % 16) == 0;
-    if (!ok) g.c.act_out = nullptr;
-    return ok;
+    bool ok = e.act_mode && dtype != G_F32 && (g.cfg == 13 || g.cfg == 15) && !e.rsum && g.splits <= 1 &&
+              (g.ep_stage & 1) && !e.out_f32 && !e.bias[0] && e.alpha == 1.0f && e.act_bias && g.batch == 1;
+    int parts = 1;
+    if (ok && e.act_mode == 1) ok = g.a.kcontig && g.b.kcontig && e.act_out && ((uintptr_t)e.act_out % 16) == 0;
+    else if (ok && e.act_mode == 2) {
+        parts = g.tiles_m * 2;
+        ok = g.a.kcontig && !g.b.kcontig && e.act_in && e.act_part && parts <= e.act_part_cap &&
+             ((uintptr_t)e.act_in % 16) == 0 && ((uintptr_t)e.act_part % 16) == 0;
+    } else {
+        ok = false;
+    }
+    if (!ok) g.c.act_mode = 0;
+    return ok ? parts : 0;
 }
+
+thread_local int t_act_parts = 0;
 
 thread_local int t_rsum_parts = 0;
 
@@ -2306,8 +2355,10 @@ bool gemm_act_fusable(int dtype, const GemmArgs& args) {
     if (dtype == G_F32 || args.M <= 0 || args.N <= 0 || args.K <= 0 || args.batch != 1) return false;
     GemmArgs g = args;
     if (prepare(g, dtype, false)) return false;
-    return settle_act(g, dtype);
+    return settle_act(g, dtype) > 0;
 }
+
+int gemm_act_parts() { return t_act_parts; }
 PlanScope::PlanScope(const dm_plan* p) : prev(t_plan) { t_plan = p; }
 PlanScope::~PlanScope() { t_plan = prev; }
 int current_attn_path() { return t_plan ? t_plan->attn_path : 0; }
@@ -2355,6 +2406,7 @@ static int prepare(GemmArgs& g, int dtype, bool pair) {
 
 int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     t_rsum_parts = 0;
+    t_act_parts = 0;
     GemmArgs g = args;
     if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return 0;
     if (g.K <= 0) return set_error(DM_ERR_ARG, "contraction with K <= 0");
@@ -2371,7 +2423,8 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     } else {
         if (int rc = prepare(g, dtype, false)) return rc;
         settle_rowsums(g);
-        settle_act(g, dtype);
+        const int ap = settle_act(g, dtype);
+        t_act_parts = g.c.act_mode == 2 ? ap : 0;
         if (dtype == G_F16) launch_t<half_t>(g, st);
         else launch_t<bf16_t>(g, st);
         log_launch(g, dtype);

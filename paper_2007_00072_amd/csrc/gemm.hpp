@@ -76,14 +76,25 @@ struct Epilogue {
     float* rsum;
     int rsum_ld;
     int rsum_cap;
-    // optional (storage-type output, no alpha scaling or bias): also writes
-    // act_out = dropout(act(C + act_bias[n])) at C's addresses, from the
-    // stored (rounded) C, with the dropout's element index m * ldc + n;
-    // only the staged epilogue of the lean kernels does (gemm_act_fusable)
+    // optional activation step in the epilogue (storage-type output, no
+    // alpha scaling or bias; dropout element index m * ldc + n):
+    // act_mode 1: also writes act_out = dropout(act(C + act_bias[n])) from
+    // the stored (rounded) C;
+    // act_mode 2: C is the gradient dA of the activation's output and is not
+    // stored: C's pointer receives dH = dropout(dA) * act'(act_in + act_bias[n])
+    // (dA rounded first, dH rounded as stored), and the partial column sums
+    // of the stored dH go to rows of act_part (N floats each, at most
+    // act_part_cap rows; gemm_act_parts() tells how many were written).
+    // Only the staged epilogue of the lean kernels does this
+    // (gemm_act_fusable tells beforehand).
+    int act_mode;
     void* act_out;
+    const void* act_in;
     const void* act_bias;
     int act;
     DropParams act_dp;
+    float* act_part;
+    int act_part_cap;
 };
 
 struct GemmArgs {
@@ -115,9 +126,12 @@ struct GemmArgs {
 int gemm_rowsum_parts();
 
 // Whether launch_gemm would run this contraction with the staged epilogue
-// that writes Epilogue::act_out (otherwise the request is ignored and the
-// caller applies the activation itself).
+// that takes its Epilogue::act_mode step (otherwise the request is ignored
+// and the caller applies the activation step itself).
 bool gemm_act_fusable(int dtype, const GemmArgs& g);
+// Partial column-sum rows the last launch_gemm on this thread wrote for
+// act_mode 2 (0 if none).
+int gemm_act_parts();
 
 // Largest tile configuration index (contract's tile_cfg, plan entries).
 constexpr int GEMM_MAX_CFG = 21;

@@ -738,13 +738,13 @@ int encoder_layer_fwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     {
         GemmArgs g1 = gemm(T, x.F, x.I, 1, opnd(y1, true, linear_map(x.I)), opnd(prm->w1, true, linear_map(x.I)),
                            epi(hbuf, linear_map(x.F), linear_map(1), true, false));
-        g1.c.act_out = abuf; g1.c.act_bias = prm->b1; g1.c.act = d->act;
+        g1.c.act_mode = 1; g1.c.act_out = abuf; g1.c.act_bias = prm->b1; g1.c.act = d->act;
         g1.c.act_dp = make_drop(d->p_ffn_act, d->seed, 3, d->layer_id);
         if (gemm_act_fusable(dt, g1)) {
             TraceScope t_("F7+8 linear1_bias_act", st);
             DM_TRY(launch_gemm(dt, g1, st));
         } else {
-            g1.c.act_out = nullptr;
+            g1.c.act_mode = 0;
             {
                 TraceScope t_("F7 linear1", st);
                 DM_TRY(launch_gemm(dt, g1, st));
@@ -823,13 +823,30 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
         run_ln_bwd(l2, st);
     }
     DM_TRY(check_launch("LayerNorm-2 backward"));
-    // Linear 2 dX and dW
-    {
+    // (with the plan's layout choice, dH also transposed for the Linear-1
+    // weight gradient)
+    void* dHT = fl.dH_t ? B8(ws, e.dHT) : nullptr;
+    // Linear 2 dX; where its kernel stages the output tile (and dH is not
+    // wanted transposed), the dropout / activation backward runs in its
+    // epilogue: dH is stored in place of dA, with the Linear-1 bias
+    // gradient's partial column sums
+    GemmArgs g3 = gemm(T, F, I, 1, opnd(dO, true, linear_map(I)), opnd(prm->w2, false, linear_map(F)),
+                       epi(dA, linear_map(F), linear_map(1), true, false));
+    g3.c.act_mode = 2; g3.c.act_in = hbuf; g3.c.act_bias = prm->b1; g3.c.act = d->act;
+    g3.c.act_dp = make_drop(d->p_ffn_act, d->seed, 3, d->layer_id);
+    g3.c.act_part = part_act; g3.c.act_part_cap = colsum_blocks(T);
+    g3.c.ptr[0] = dH;
+    int act_parts = 0;
+    if (!dHT && gemm_act_fusable(dt, g3)) {
+        TraceScope t_("B3+5 linear2_dx_act_bwd", st);
+        DM_TRY(launch_gemm(dt, g3, st));
+        act_parts = gemm_act_parts();
+        if (act_parts <= 0) return set_error(DM_ERR_DEVICE, "activation backward epilogue not taken");
+    } else {
+        g3.c.act_mode = 0;
+        g3.c.ptr[0] = dA;
         TraceScope t_("B3 linear2_dx", st);
-        DM_TRY(launch_gemm(dt,
-                           gemm(T, F, I, 1, opnd(dO, true, linear_map(I)), opnd(prm->w2, false, linear_map(F)),
-                                epi(dA, linear_map(F), linear_map(1), true, false)),
-                           st));
+        DM_TRY(launch_gemm(dt, g3, st));
     }
     {
         TraceScope t_("B4 linear2_dw", st);
@@ -839,14 +856,10 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
                                 epi(g->dw2, linear_map(F), linear_map(1), true, true)),
                            st));
     }
-    // dropout / activation backward, Linear-1 bias grad
-    // (with the plan's layout choice, also dH transposed for the Linear-1
-    // weight gradient)
-    void* dHT = fl.dH_t ? B8(ws, e.dHT) : nullptr;
-    {
+    // dropout / activation backward, Linear-1 bias grad (unless in B3)
+    if (!act_parts) {
         TraceScope t_("B5 act_bwd", st);
-        run_act_bwd(dt, T, (int)F, dA, hbuf, prm->b1, d->act, make_drop(d->p_ffn_act, d->seed, 3, d->layer_id), dH,
-                    part_act, st, dHT);
+        run_act_bwd(dt, T, (int)F, dA, hbuf, prm->b1, d->act, g3.c.act_dp, dH, part_act, st, dHT);
     }
     DM_TRY(check_launch("activation backward"));
     // Linear 1 dX and dW
@@ -898,7 +911,8 @@ int encoder_layer_bwd(const dm_layer_desc* d, const dm_layer_params* prm, const 
     // (dgamma1, dbeta1, dbo) and input-bias (dbq, dbk, dbv) column sums
     const int nln = ln_bwd_blocks(T, (int)I, dt, fl.ln_form);
     const FinishJob jobs[4] = {finish_job3(part_ln2, nln, (int)I, g->dg2, g->dbe2, g->db2),
-                               finish_job(part_act, act_bwd_blocks(T, dHT != nullptr), (int)F, g->db1),
+                               finish_job(part_act, act_parts ? act_parts : act_bwd_blocks(T, dHT != nullptr),
+                                          (int)F, g->db1),
                                finish_job3(part_ln1, nln, (int)I, g->dg1, g->dbe1, g->dbo),
                                finish_job_qkv(part, bias.parts ? bias.parts : ncs, (int)x.H, (int)x.P, 3, g->dbq,
                                               g->dbk, g->dbv)};

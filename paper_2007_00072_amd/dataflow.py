@@ -61,7 +61,8 @@ PAIRED = {"B12+19 out_dw+qkv_dw": ("B12 out_dw", "B19 qkv_dw")}
 # allows (else as launches of their own): Linear 1 with bias + activation;
 # the input-bias gradient's partial sums inside the Q/K/V weight gradient
 # (that launch then also writes the three bias gradients).
-EPILOGUE = {"F7+8 linear1_bias_act": ("F7 linear1", "F8 bias_act")}
+EPILOGUE = {"F7+8 linear1_bias_act": ("F7 linear1", "F8 bias_act"),
+            "B3+5 linear2_dx_act_bwd": ("B3 linear2_dx", "B5 act_bwd")}
 FOLDED = {"B20 qkv_bias_grad": "B12+19 out_dw+qkv_dw"}
 # The launch sets one layer can run: every score step separate, scores on
 # chip, scores on chip with the next contraction in the same launch, and
@@ -82,15 +83,15 @@ def key_blocks(s: Shape, dtype: str):
     return True, s.K // (32 * kg)
 
 
-def path_groups(w: Dict[str, "Work"], path: str, epilogue: bool = False, folded: bool = False) -> Dict[str, "Work"]:
+def path_groups(w: Dict[str, "Work"], path: str, epilogue=(), folded: bool = False) -> Dict[str, "Work"]:
     """The launch groups of `w` that path `path` runs (epilogue: the EPILOGUE
-    groups in place of their parts; folded: without the FOLDED launches)."""
+    groups that ran, in place of their parts, True for all of them; folded:
+    without the FOLDED launches)."""
     fused = PATHS[path]
     gone = {p for f in fused for p in REPLACES[f]} | {p for parts in PAIRED.values() for p in parts}
-    if epilogue:
-        gone |= {p for parts in EPILOGUE.values() for p in parts}
-    else:
-        gone |= set(EPILOGUE)
+    ran = set(EPILOGUE) if epilogue is True else set(epilogue or ())
+    for k, parts in EPILOGUE.items():
+        gone |= set(parts) if k in ran else {k}
     if folded:
         gone |= set(FOLDED)
     return {k: v for k, v in w.items() if (k not in REPLACES or k in fused) and k not in gone}
@@ -146,6 +147,10 @@ def encoder_layer(s: Shape, dtype: str, elements: bool = False) -> Dict[str, Wor
     w["B3 linear2_dx"] = g(T, F, I, N, I * F, Fh)
     w["B4 linear2_dw"] = g(I, F, T, N, Fh, I * F, c_es=f4)
     w["B5 act_bwd"] = m(3 * Fh * es + F * es + F * f4)
+    # Linear 2 dX with the activation backward in its epilogue: dA is
+    # neither written nor read back (dH, H, b1 and db1 as in B5)
+    w["B3+5 linear2_dx_act_bwd"] = Work(w["B3 linear2_dx"].flop,
+                                        w["B3 linear2_dx"].bytes + Fh * es + F * es + F * f4, "mfma", "contraction")
     w["B6 linear1_dx"] = g(T, I, F, Fh, F * I, N)
     w["B7 linear1_dw"] = g(F, I, T, Fh, N, F * I, c_es=f4)
     w["B8-10 ln1_bwd"] = m(5 * N * es + f4 * T + I * es + 3 * I * f4)
@@ -260,7 +265,7 @@ def unfused_table3(s: Shape, act_dropout: bool = False):
 
 
 def data_movement(s: Shape, dtype: str, path: str = "scores_next", act_dropout: bool = False,
-                  epilogue: bool = False, folded: bool = False) -> Dict[str, float]:
+                  epilogue=(), folded: bool = False) -> Dict[str, float]:
     """The data-movement reduction of the fused layer against the operators
     one by one (the analogue of the paper's figure, from its Table 3 I/O
     columns): elements moved per forward + backward step, both ways."""

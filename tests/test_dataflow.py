@@ -80,16 +80,23 @@ def test_epilogue_and_folded_groups():
     s = WORKLOADS["bert_large_f16"].shape
     w = dataflow.encoder_layer(s, "f16")
     T, F = s.B * s.J, s.F
+    # H is not read back after Linear 1; dA is neither written nor read
+    saved = {"F7+8 linear1_bias_act": T * F * 2, "B3+5 linear2_dx_act_bwd": 2 * T * F * 2}
     for k, parts in dataflow.EPILOGUE.items():
         assert w[k].flop == sum(w[p].flop for p in parts)
-        assert w[k].bytes == sum(w[p].bytes for p in parts) - T * F * 2
+        assert w[k].bytes == sum(w[p].bytes for p in parts) - saved[k]
     g = dataflow.path_groups(w, "keys", epilogue=True, folded=True)
     assert "F7+8 linear1_bias_act" in g and "F7 linear1" not in g and "F8 bias_act" not in g
+    assert "B3+5 linear2_dx_act_bwd" in g and "B5 act_bwd" not in g
     assert "B20 qkv_bias_grad" not in g
     g0 = dataflow.path_groups(w, "keys")
     assert "F7+8 linear1_bias_act" not in g0 and "F8 bias_act" in g0 and "B20 qkv_bias_grad" in g0
+    g1 = dataflow.path_groups(w, "keys", epilogue={"F7+8 linear1_bias_act"})
+    assert "F7+8 linear1_bias_act" in g1 and "B5 act_bwd" in g1 and "B3+5 linear2_dx_act_bwd" not in g1
     assert sum(x.flop for x in g.values()) == sum(x.flop for x in g0.values())
     d0 = dataflow.data_movement(s, "f16", "keys")
     d1 = dataflow.data_movement(s, "f16", "keys", epilogue=True, folded=True)
-    # H (T*F) and dQKV (3*T*I) are read once less; the bias gradients (3*I) move with the pair
-    assert (d0["fused_Melem"] - d1["fused_Melem"]) * 1e6 == pytest.approx(T * F + 3 * T * s.I - 3 * s.I, abs=1e4)
+    # H (T*F) read once less, dA (T*F) neither written nor read, dQKV
+    # (3*T*I) read once less; the bias gradients (3*I) move with the pair
+    assert (d0["fused_Melem"] - d1["fused_Melem"]) * 1e6 == pytest.approx(3 * T * F + 3 * T * s.I - 3 * s.I,
+                                                                          abs=1e4)
