@@ -172,7 +172,10 @@ class _Layer:
 
     def timed(self, reps: int) -> Dict[str, float]:
         """Mean ms per launch label (an operator's extra launches, e.g. a
-        split-k reduce, are added to it) over `reps` steps."""
+        split-k reduce, are added to it) over `reps` steps.  Labels are
+        canonical (see CANON, FOLD): a contraction with an operator in its
+        epilogue and the same contraction followed by that operator's own
+        launch are one stage."""
         from . import lib
         self.step()
         self.torch.cuda.synchronize()
@@ -184,7 +187,7 @@ class _Layer:
         lib.dm_trace_enable(False)
         tot = defaultdict(float)
         for lab, _sub, ms in recs:
-            tot[lab] += ms
+            tot[canonical(lab)] += ms
         return {k: v / reps for k, v in tot.items()}
 
     def launches(self):
@@ -197,7 +200,21 @@ class _Layer:
         recs = lib.plan_log_read()
         lib.plan_log(False)
         lib.dm_trace_enable(False)
-        return [(r.label.decode(), r) for r in recs]
+        return [(canonical(r.label.decode()), r) for r in recs]
+
+
+# Contractions that take an element-wise operator into their epilogue where
+# their kernel allows: the fused launch's label and the operator's own
+# launch (when the kernel cannot take it) both map to the contraction's
+# stage, so every configuration of the contraction is timed with the
+# operator's cost included.
+CANON = {"F7+8 linear1_bias_act": "F7 linear1", "B3+5 linear2_dx_act_bwd": "B3 linear2_dx"}
+FOLD = {"F8 bias_act": "F7 linear1", "B5 act_bwd": "B3 linear2_dx"}
+
+
+def canonical(label: str) -> str:
+    label = CANON.get(label, label)
+    return FOLD.get(label, label)
 
 
 def _is_fwd(label: str) -> bool:
@@ -209,7 +226,7 @@ def _is_fwd(label: str) -> bool:
 LAYOUT_STAGES = {
     "F6 bdrln1": ("ln_lanes",), "F10 bdrln2": ("ln_lanes",),
     "B1-2 ln2_bwd": ("ln_bwd_form", "dO_transposed", "ln_lanes"), "B8-10 ln1_bwd": ("ln_bwd_form", "ln_lanes"),
-    "B4 linear2_dw": ("dO_transposed",), "B5 act_bwd": ("dH_transposed",), "B7 linear1_dw": ("dH_transposed",),
+    "B4 linear2_dw": ("dO_transposed",), "B3 linear2_dx": ("dH_transposed",), "B7 linear1_dw": ("dH_transposed",),
     "B colsum finish": ("ln_bwd_form", "dH_transposed"),
 }
 
@@ -279,17 +296,26 @@ def tune(workload: str, reps: int = 3, log=print, shape=None, tile_cfgs=TILE_CFG
     where: Dict[tuple, List[str]] = OrderedDict()
     occurs_in: Dict[tuple, int] = {}
     label_key = {}
+    # a contraction shape is swept under the first layout where it occurs;
+    # a layout-dependent stage of it under another layout (e.g. Linear-2 dX
+    # when dH is written transposed and the activation backward runs on its
+    # own) keeps its measured time
+    for (p, li), (tm, launches) in runs.items():
+        if p == SWEEP_PATH:
+            for lab, r in launches:
+                occurs_in.setdefault(r.key(), li)
     for (p, li), (tm, launches) in runs.items():
         lay = combos[li]
         names = {lab: stage_name(lab, lay) for lab in tm}
         if p == SWEEP_PATH:
             for lab, r in launches:
+                if occurs_in[r.key()] != li and stage_name(lab, lay) not in label_key:
+                    continue
                 st = names.get(lab, stage_name(lab, lay))
                 label_key[st] = r.key()
                 where.setdefault(r.key(), [])
                 if st not in where[r.key()]:
                     where[r.key()].append(st)
-                occurs_in.setdefault(r.key(), li)
     for (p, li), (tm, launches) in runs.items():
         lay = combos[li]
         names = {lab: stage_name(lab, lay) for lab in tm}

@@ -123,4 +123,15 @@ def test_layout_options_and_stage_names():
     assert lanes == [64] and combos == [{"ln_bwd_form": 1, "dO_transposed": 0, "dH_transposed": 0}]
     lay = {"ln_bwd_form": 2, "dO_transposed": 1, "dH_transposed": 0, "ln_lanes": 64}
     assert tune.stage_name("B4 linear2_dw", lay) == "B4 linear2_dw [dO_transposed=1]"
-    assert tune.stage_name("B3 linear2_dx", lay) == "B3 linear2_dx"
+    # Linear-2 dX takes the activation backward into its epilogue only when
+    # dH is not written transposed: its stage depends on that choice
+    assert tune.stage_name("B3 linear2_dx", lay) == "B3 linear2_dx [dH_transposed=0]"
+    assert tune.stage_name("B6 linear1_dx", lay) == "B6 linear1_dx"
+
+
+def test_canonical_labels_fold_epilogue_operators():
+    # a fused launch and the unfused pair land on one stage
+    assert tune.canonical("F7+8 linear1_bias_act") == tune.canonical("F7 linear1") == "F7 linear1"
+    assert tune.canonical("F8 bias_act") == "F7 linear1"
+    assert tune.canonical("B3+5 linear2_dx_act_bwd") == tune.canonical("B5 act_bwd") == "B3 linear2_dx"
+    assert tune.canonical("B4 linear2_dw") == "B4 linear2_dw"
