@@ -315,7 +315,8 @@ int attn_backward_form(const dm_layer_desc* d, int32_t* key_blocks);
  * contiguous along k (otherwise run as 13); 20: the tile and waves of 17
  * with each MFMA issued next to its share of the next fragment reads and
  * operand copies (as 14 otherwise), 21: the same schedule on the tile and
- * waves of 19 (as 20 otherwise);
+ * waves of 19 (as 20 otherwise), 22: the same schedule on the tile and
+ * waves of 18 (as 11 otherwise);
  * -1: chosen from the shape; other values are
  * DM_ERR_ARG); splits > 1 splits k, using `ws` (ws_bytes >=
  * splits*batch*M*N*4) for partial sums; splits = 0 chooses (no split
@@ -357,7 +358,7 @@ typedef struct {
     int64_t M, N, K, batch;        /* contraction sizes; batch: contractions in one launch */
     int32_t dtype;                 /* dm_dtype                                             */
     int32_t a_kcontig, b_kcontig;  /* 1: operand contiguous along the contraction index   */
-    int32_t tile_cfg;              /* 0..21 (contract's list)                              */
+    int32_t tile_cfg;              /* 0..22 (contract's list)                              */
     int32_t splits;                /* split-k factor, 1 = none                             */
     char label[48];                /* log only: kernel-timing label, "" when timing is off */
 } dm_contract_choice;

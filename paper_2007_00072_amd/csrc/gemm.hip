@@ -1668,6 +1668,9 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
     static_assert(!IL || (KG == 1 && !RS), "interleaved schedule: single k group, no row sums");
     if constexpr (IL) {
         constexpr int NMF = FM * FN, NR = FM + FN, H = NMF / 2, R2 = NMF - H;
+        // fragment reads / copies per MFMA (fixed trip counts, so every
+        // loop unrolls and every register array index is a constant)
+        constexpr int RPM = (NR + NMF - 1) / NMF, RPL = (NR + R2 - 1) / R2, CPL = (NL + R2 - 1) / R2;
         auto read_one = [&](int buf, int s, int q, int j) {
             const T* A = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
             const T* B = A + AS;
@@ -1686,7 +1689,8 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
                     for (int t = 0; t < NMF; ++t) {
                         mma_one(cur, t);
 #pragma unroll
-                        for (int j = t * NR / NMF; j < (t + 1) * NR / NMF; ++j) read_one(cur ^ 1, s, q + 1, j);
+                        for (int jj = 0; jj < RPM; ++jj)
+                            if (t * RPM + jj < NR) read_one(cur ^ 1, s, q + 1, t * RPM + jj);
                         __builtin_amdgcn_sched_barrier(0);
                     }
                 } else {
@@ -1708,13 +1712,15 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
                         mma_one(cur, H + u);
                         if (more) {
 #pragma unroll
-                            for (int c = u * NL / R2; c < (u + 1) * NL / R2; ++c) {
+                            for (int cc = 0; cc < CPL; ++cc) {
+                                const int c = u * CPL + cc;
                                 if (c < DA::NV) da.copy(pa, sn, c, st);
-                                else db.copy(pb, sn, c - DA::NV, st + (uint32_t)(AS * sizeof(T)));
+                                else if (c < NL) db.copy(pb, sn, c - DA::NV, st + (uint32_t)(AS * sizeof(T)));
                             }
                         }
 #pragma unroll
-                        for (int j = u * NR / R2; j < (u + 1) * NR / R2; ++j) read_one(cur ^ 1, s + 1, 0, j);
+                        for (int jj = 0; jj < RPL; ++jj)
+                            if (u * RPL + jj < NR) read_one(cur ^ 1, s + 1, 0, u * RPL + jj);
                         __builtin_amdgcn_sched_barrier(0);
                     }
                 }
@@ -1962,15 +1968,15 @@ struct TileCfg {
 // 19: lean 256x192 kernel (4 waves of 128x96) for outputs whose width is a
 // multiple of 192 but leaves 256x256 tiles short of the CU count (3072
 // columns: 16 x 16 tiles instead of 16 x 12); the 192-wide operand must be
-// contiguous along k (else run as 13).  20, 21: the tiles of 17 and 19
-// with the interleaved schedule (each MFMA issued next to its share of the
-// fragment reads and copies); contractions they do not take run as 17
-// and 19 would.
+// contiguous along k (else run as 13).  20, 21, 22: the tiles of 17, 19
+// and 18 with the interleaved schedule (each MFMA issued next to its share
+// of the fragment reads and copies); contractions they do not take run as
+// 17, 19 and 18 would.
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
                             {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}, {128, 128, 2, 2},
-                            {256, 256, 2, 2}, {128, 128, 2, 2}, {256, 192, 2, 2}, {256, 256, 2, 2}, {256, 192, 2, 2}};
+                            {256, 256, 2, 2}, {128, 128, 2, 2}, {256, 192, 2, 2}, {256, 256, 2, 2}, {256, 192, 2, 2}, {128, 128, 2, 2}};
 static_assert(sizeof(CFGS) / sizeof(CFGS[0]) == GEMM_MAX_CFG + 1, "configuration table");
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
@@ -2150,6 +2156,7 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
         case 19: launch_lean_bk<T, 256, 192, 2, 2, 32, 4>(g, st); break;
         case 20: launch_lean_il<T, 256, 256, 2, 2, 32, 4>(g, st); break;
         case 21: launch_lean_il_bk<T, 256, 192, 2, 2, 32, 4>(g, st); break;
+        case 22: launch_lean_il<T, 128, 128, 2, 2, 64, 4>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -2214,7 +2221,7 @@ void choose(GemmArgs& g) {
     // maps affine over 32-wide blocks; of them only the lean 128x128 kernel
     // takes a residual operand
     if (((g.c.bias[0] && g.c.bias_on_m) || !g.blk32) && g.cfg >= 9) g.cfg = 8;
-    if (g.c.resid && g.cfg >= 9 && g.cfg != 15 && g.cfg != 16 && g.cfg != 18) g.cfg = 8;
+    if (g.c.resid && g.cfg >= 9 && g.cfg != 15 && g.cfg != 16 && g.cfg != 18 && g.cfg != 22) g.cfg = 8;
     if (g.splits <= 0) {
         int s = split_ok ? want_split : 1;
         while (s > 1 && (g.K / s < 256 || (int64_t)s * g.batch * g.M * g.N > g.split_cap)) --s;
@@ -2228,7 +2235,7 @@ void choose(GemmArgs& g) {
     if (g.cfg == 19 && !g.b.kcontig) g.cfg = 13;
     if (g.cfg == 21 && !g.b.kcontig) g.cfg = 20;
     if ((g.cfg == 13 || g.cfg == 17 || g.cfg == 19 || g.cfg == 20 || g.cfg == 21) && !lean_ok(g, 32)) g.cfg = 14;
-    if ((g.cfg == 15 || g.cfg == 16 || g.cfg == 18) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
+    if ((g.cfg == 15 || g.cfg == 16 || g.cfg == 18 || g.cfg == 22) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;
     // tile counts of the configuration that runs (the fallback from 15 to 8
     // changes the tile width)
     const TileCfg& c = CFGS[g.cfg];

@@ -30,13 +30,24 @@ def short_name(sym: str) -> str:
         mode = lambda b: "k" if b == "1" else "o"
         return f"gemm_dma<{dt},{m.group(2)}x{m.group(3)},waves {m.group(4)}x{m.group(5)},A:{mode(m.group(6))},B:{mode(m.group(7))}>"
     m = re.search(r"gemm_lean(_pair)?I(DF16_|DF16b)Li(\d+)ELi(\d+)ELi(\d)ELi(\d)ELi(\d+)ELi(\d)ELb(\d)ELb(\d)"
-                  r"(?:ELi(\d))?", sym)
+                  r"((?:EL[ib]\d+)*)E", sym)
     if m:
         dt = "f16" if m.group(2) == "DF16_" else "bf16"
         mode = lambda b: "k" if b == "1" else "o"
-        kg = f",k groups {m.group(11)}" if m.group(11) and m.group(11) != "1" else ""
+        # the remaining template arguments: lean (k groups, row sums,
+        # interleaved schedule, activation step) or pair (row sums)
+        rest = re.findall(r"EL([ib])(\d+)", m.group(11))
+        names = ("row sums",) if m.group(1) else ("k groups", "row sums", "interleaved", "act")
+        extra = ""
+        for (kind, val), nm in zip(rest, names):
+            if nm == "k groups" and val != "1":
+                extra += f",k groups {val}"
+            elif nm in ("row sums", "interleaved") and val == "1":
+                extra += f",{nm}"
+            elif nm == "act" and val != "0":
+                extra += f",act {val}"
         return (f"gemm_lean{m.group(1) or ''}<{dt},{m.group(3)}x{m.group(4)},waves {m.group(5)}x{m.group(6)},"
-                f"bk {m.group(7)}{kg},A:{mode(m.group(9))},B:{mode(m.group(10))}>")
+                f"bk {m.group(7)},A:{mode(m.group(9))},B:{mode(m.group(10))}{extra}>")
     m = re.search(r"gemm_(x32|big)I(DF16_|DF16b)", sym)
     if m:
         return f"gemm_{m.group(1)}<{'f16' if m.group(2) == 'DF16_' else 'bf16'}>"
