@@ -369,8 +369,12 @@ def main() -> int:
                                                            folded="B20 qkv_bias_grad" not in ops),
                                     per="layer fwd+bwd", paper="22.91% (V100; see paper_context)")
     if a.kernels_json:
+        # the launch records of one step in issue order (a label recurs where
+        # an operator launches the same kernel pair twice)
+        per_step = len(recs) // a.steps
+        sequence = [lab + (" " + sub if sub else "") for lab, sub, _ in recs[:per_step]]
         with open(a.kernels_json, "w") as f:
-            json.dump({"workload": wl.name, "ms_per_step": ms, "kernels": table}, f, indent=1)
+            json.dump({"workload": wl.name, "ms_per_step": ms, "kernels": table, "sequence": sequence}, f, indent=1)
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, a.cpu_sample or s.B)
     print(json.dumps(out))

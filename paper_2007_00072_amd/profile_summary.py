@@ -73,7 +73,7 @@ def main() -> None:
     a = ap.parse_args()
 
     seq_info = json.load(open(a.kernels))
-    seq = [r["kernel"] for r in seq_info["kernels"]]
+    seq = seq_info.get("sequence") or [r["kernel"] for r in seq_info["kernels"]]
     ev = {r["kernel"]: r["us"] for r in seq_info["kernels"]}
     rows = list(csv.DictReader(open(a.trace)))
     lib = [r for r in rows if "dm::" in r["Kernel_Name"] or "_ZN2dm" in r["Kernel_Name"]]
