@@ -163,3 +163,44 @@ def test_layout_choice_validation():
         lib.Plan([], 0, {"ln_bwd_form": 3})
     with pytest.raises(lib.DmError):
         lib.Plan([], 0, {"dH_transposed": 2})
+
+
+@pytest.mark.parametrize("name,act,p_act", [("bert_large_f16", "gelu", 0.0), ("bert_base_bf16", "relu", 0.1)])
+def test_epilogue_operators_change_no_value(name, act, p_act):
+    # Linear 1 with bias + activation (+ dropout) in its epilogue and
+    # Linear-2 dX with the activation backward in its epilogue, against the
+    # same two contractions moved by a plan entry to the lean 4-wave 128x128
+    # kernel (same MFMA instruction and k order, no epilogue operator), so
+    # that the operators run as launches of their own: H, A, y, dx and every
+    # weight gradient are bit for bit the same; db1, a column sum, differs
+    # only in its summation order
+    wl = small(name, B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
+
+    def run(plan=None):
+        lib.dm_trace_enable(True)
+        lib.plan_log(True)
+        L, _, _, _, y, dx = run_encoder(wl, act=act, p_ffn_act=p_act, plan=plan)
+        recs = lib.plan_log_read()
+        lib.plan_log(False)
+        labels = [lab for lab, _, _ in lib.trace_records()]
+        lib.dm_trace_enable(False)
+        T, F = wl.shape.B * wl.shape.J, wl.shape.F
+        tdt = y.dtype
+        saved = {n: L.saved_tensor(n, (T, F), tdt).clone() for n in ("h", "a")}
+        return L, y, dx, recs, labels, saved
+
+    L0, y0, dx0, recs, labels, s0 = run()
+    assert "F7+8 linear1_bias_act" in labels and "B3+5 linear2_dx_act_bwd" in labels
+    keys = {r.key() for r in recs if r.label.decode() in ("F7+8 linear1_bias_act", "B3+5 linear2_dx_act_bwd")}
+    assert len(keys) == 2
+    plan = lib.Plan([lib.ContractChoice(*k, 18, 1) for k in keys], 0)
+    L1, y1, dx1, _, labels1, s1 = run(plan)
+    assert {"F7 linear1", "F8 bias_act", "B3 linear2_dx", "B5 act_bwd"} <= set(labels1)
+    for n in ("h", "a"):
+        assert torch.equal(s0[n], s1[n]), n
+    assert torch.equal(y0, y1) and torch.equal(dx0, dx1)
+    for n, g in L0.grads.items():
+        if n == "b1":
+            assert torch.allclose(g, L1.grads[n], rtol=1e-5, atol=1e-5 * float(g.abs().max()))
+        else:
+            assert torch.equal(g, L1.grads[n]), n
