@@ -1,5 +1,5 @@
 // MFMA contraction kernel for gfx950 (fp16 / bf16 storage, fp32
-// accumulation) and a plain fp32 kernel for float32 layers.
+// accumulation) and an fp32 MFMA kernel (v_mfma_f32_32x32x2f32) for float32 layers.
 //
 // Block tile BM x BN (256x256 down to 128x64), k-step 64, 4 or 8 wave64s in
 // a WGM x WGN grid of wave tiles, v_mfma_f32_16x16x32 inner products.
@@ -1671,11 +1671,17 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
         // fragment reads / copies per MFMA (fixed trip counts, so every
         // loop unrolls and every register array index is a constant)
         constexpr int RPM = (NR + NMF - 1) / NMF, RPL = (NR + R2 - 1) / R2, CPL = (NL + R2 - 1) / R2;
+        // read j of a slice, in the order the slice's MFMAs (t -> a[t / FN],
+        // b[t % FN]) first need them: a0, b0 .. b(FN-1), a1 .. a(FM-1)
         auto read_one = [&](int buf, int s, int q, int j) {
             const T* A = reinterpret_cast<const T*>(smem + (s % STAGES) * STAGE);
             const T* B = A + AS;
-            if (j < FM) a[buf][j] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + j * 32, q * 16, lane));
-            else b[buf][j - FM] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + (j - FM) * 32, q * 16, lane));
+            if (j >= 1 && j <= FN)
+                b[buf][j - 1] = __builtin_bit_cast(frag, DB::frag(B, wn * WN + (j - 1) * 32, q * 16, lane));
+            else {
+                const int i = j == 0 ? 0 : j - FN;
+                a[buf][i] = __builtin_bit_cast(frag, DA::frag(A, wm * WM + i * 32, q * 16, lane));
+            }
         };
         auto mma_one = [&](int buf, int t) {
             acc[t / FN][t % FN] = Mfma32<T>::run(a[buf][t / FN], b[buf][t % FN], acc[t / FN][t % FN]);
@@ -1925,29 +1931,68 @@ __device__ __forceinline__ float op_elem(const Operand& op, int64_t boff, int ou
     return reinterpret_cast<const float*>(op.ptr[seg])[boff + off + outer];
 }
 
+// Float32 contractions on v_mfma_f32_32x32x2f32: a 64x64 block tile, four
+// waves of 32x32, k-steps of 16 staged through LDS (operands gathered
+// element by element through their index maps, so every layout and ragged
+// size is taken; zeros past M, N, K), fp32 products and accumulation.  Lane
+// l of a 32x32x2 step supplies row l % 32 of A and column l % 32 of B at
+// k = 2 s + l / 32; the result's lane l holds column l % 32 at rows
+// 8 (r / 4) + 4 (l / 32) + r % 4.  The epilogue stores element by element
+// through the output maps (bias, residual, segments as in the 16-bit path).
+constexpr int F32_T = 64, F32_K = 16;
+
 __global__ __launch_bounds__(256) void gemm_f32(GemmArgs g) {
-    const int n = blockIdx.x * 16 + (threadIdx.x & 15);
-    const int m = (blockIdx.y % g.tiles_m) * 16 + (threadIdx.x >> 4);
+    __shared__ float sa[F32_K][F32_T + 1];
+    __shared__ float sb[F32_K][F32_T + 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = (blockIdx.y % g.tiles_m) * F32_T, n0 = blockIdx.x * F32_T;
     const uint32_t z = blockIdx.y / g.tiles_m;
-    if (m >= g.M || n >= g.N) return;
     int dummy = 0;
-    int64_t aoff = map_off(g.a.batch, z, 1, &dummy);
-    int64_t boff = map_off(g.b.batch, z, 1, &dummy);
-    float acc = 0.f;
-    for (int k = 0; k < g.K; ++k) acc = fmaf(op_elem(g.a, aoff, m, k), op_elem(g.b, boff, n, k), acc);
-    const Epilogue& e = g.c;
-    float v = acc * e.alpha;
-    if (e.bias[0]) {
-        int bseg = 0;
-        int64_t bo = map_off(e.bias_map, (uint32_t)(e.bias_on_m ? m : n), e.bias_nseg, &bseg);
-        v += reinterpret_cast<const float*>(e.bias[bseg])[bo];
+    const int64_t aoff = map_off(g.a.batch, z, 1, &dummy);
+    const int64_t boff = map_off(g.b.batch, z, 1, &dummy);
+    floatx16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    for (int k0 = 0; k0 < g.K; k0 += F32_K) {
+        // each thread gathers 4 elements of each operand tile
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int idx = u * 256 + tid, kk = idx / F32_T, o = idx % F32_T;
+            const int k = k0 + kk;
+            sa[kk][o] = (m0 + o < g.M && k < g.K) ? op_elem(g.a, aoff, m0 + o, k) : 0.f;
+            sb[kk][o] = (n0 + o < g.N && k < g.K) ? op_elem(g.b, boff, n0 + o, k) : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int s2 = 0; s2 < F32_K / 2; ++s2) {
+            const int k = 2 * s2 + (lane >> 5);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sa[k][wm * 32 + (lane & 31)], sb[k][wn * 32 + (lane & 31)],
+                                                       acc, 0, 0, 0);
+        }
+        __syncthreads();
     }
-    int sm = 0, sn = 0;
-    int64_t off = map_off(e.batch, z, 1, &dummy) + map_off(e.mmap, (uint32_t)m, e.seg_on_m ? e.nseg : 1, &sm) +
-                  map_off(e.nmap, (uint32_t)n, e.seg_on_m ? 1 : e.nseg, &sn);
-    int seg = e.seg_on_m ? sm : sn;
-    if (e.resid) v += reinterpret_cast<const float*>(e.resid)[off];
-    reinterpret_cast<float*>(e.ptr[seg])[off] = v;
+    const Epilogue& e = g.c;
+    const int n = n0 + wn * 32 + (lane & 31);
+    if (n >= g.N) return;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (m >= g.M) continue;
+        float v = acc[r] * e.alpha;
+        if (e.bias[0]) {
+            int bseg = 0;
+            const int64_t bo = map_off(e.bias_map, (uint32_t)(e.bias_on_m ? m : n), e.bias_nseg, &bseg);
+            v += reinterpret_cast<const float*>(seg_ptr(e.bias, bseg))[bo];
+        }
+        int sm = 0, sn = 0;
+        const int64_t off = map_off(e.batch, z, 1, &dummy) +
+                            map_off(e.mmap, (uint32_t)m, e.seg_on_m ? e.nseg : 1, &sm) +
+                            map_off(e.nmap, (uint32_t)n, e.seg_on_m ? 1 : e.nseg, &sn);
+        const int seg = e.seg_on_m ? sm : sn;
+        if (e.resid) v += reinterpret_cast<const float*>(e.resid)[off];
+        reinterpret_cast<float*>(seg_ptr(e.ptr, seg))[off] = v;
+    }
 }
 
 // Tile configurations: (BM, BN, waves along m, waves along n).
@@ -2419,8 +2464,8 @@ int launch_gemm(int dtype, const GemmArgs& args, hipStream_t st) {
     if (g.K <= 0) return set_error(DM_ERR_ARG, "contraction with K <= 0");
     if (g.batch > 65535) return set_error(DM_ERR_UNSUPPORTED, "contraction batch above 65535");
     if (dtype == G_F32) {
-        g.tiles_m = (g.M + 15) / 16;
-        g.tiles_n = (g.N + 15) / 16;
+        g.tiles_m = (g.M + F32_T - 1) / F32_T;
+        g.tiles_n = (g.N + F32_T - 1) / F32_T;
         if ((int64_t)g.tiles_m * g.batch > 65535)
             return set_error(DM_ERR_UNSUPPORTED, "fp32 contraction grid too large");
         dim3 grid(g.tiles_n, g.tiles_m * g.batch);
