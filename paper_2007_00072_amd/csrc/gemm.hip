@@ -1406,6 +1406,18 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
     const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
     const int rr0 = lane / VPR, vc = (lane % VPR) * EPV;
     OutT* out = reinterpret_cast<OutT*>(o.ptr[0]) + o.coff;
+    // (an output through index maps: the column part of a piece's address
+    // is the lane's for the whole tile, the row part is taken per row)
+    int nseg = 0;
+    int64_t noff = 0;
+    if (!o.affine && nw + vc < g.N)
+        noff = map_off(o.nmap, (uint32_t)(nw + vc), o.seg_on_m ? 1 : o.nseg, &nseg);
+    auto piece = [&](int m) -> OutT* {
+        if (o.affine) return out + (int64_t)m * o.ldc + nw + vc;
+        int mseg = 0;
+        const int64_t moff = map_off(o.mmap, (uint32_t)m, o.seg_on_m ? o.nseg : 1, &mseg);
+        return reinterpret_cast<OutT*>(seg_ptr(o.ptr, o.seg_on_m ? mseg : nseg)) + o.coff + moff + noff;
+    };
     float cs[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) cs[q] = 0.f;
@@ -1428,7 +1440,7 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
                 const int rr = p * RPI + rr0;
                 if (lane < RPI * VPR && rr < 32) {
                     const u32x4 v = *reinterpret_cast<const u32x4*>(sm + rr * LDR + vc);
-                    if (mb + rr < g.M && n < g.N) *reinterpret_cast<u32x4*>(out + (int64_t)(mb + rr) * o.ldc + n) = v;
+                    if (mb + rr < g.M && n < g.N) *reinterpret_cast<u32x4*>(piece(mb + rr)) = v;
                 }
             }
         } else {
@@ -1785,7 +1797,7 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
         // wave reuses their LDS; each wave then owns 32 rows of its tile
         // width (padded) at a time
         unsigned char* region = nullptr;
-        if (g.ep_stage & (splits > 1 ? 2 : 1)) {
+        if (g.ep_stage & (splits > 1 ? 2 : 5)) {
             constexpr int OB = WN * 4 + 32;  // bytes per staged row, float output
             static_assert(32 * OB * WGM * WGN <= STAGES * STAGE, "staging region");
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -2246,16 +2258,11 @@ void choose(GemmArgs& g) {
         if (g.N <= 64) {
             g.cfg = 8;
         } else if (ntiles(CFGS[13], g) * 4 >= CUS * 3) {
+            // (the 256x192 tiles of cfg 19, which give 3072-wide outputs
+            // every CU where 256x256 leaves a quarter idle, measured slower
+            // than cfg 13 with its two waves per SIMD; a plan may still pick
+            // them)
             g.cfg = 13;
-            // 256x192 tiles where they need fewer rounds of the CUs for the
-            // width: estimated time = rounds x tile width, the 4-wave
-            // kernel's lower rate per tile counted as 0.8 (measured 0.79-0.82
-            // on 4096x3072 and 12288x3072 outputs)
-            if (g.N % 192 == 0 && g.b.kcontig) {
-                const int64_t r13 = (ntiles(CFGS[13], g) + CUS - 1) / CUS;
-                const int64_t r19 = (ntiles(CFGS[19], g) + CUS - 1) / CUS;
-                if (r19 * 192 * 10 < r13 * 256 * 8) g.cfg = 19;
-            }
         } else {
             g.cfg = 15;
             const int64_t t = ntiles(CFGS[15], g);
@@ -2316,8 +2323,20 @@ void set_ep_stage(GemmArgs& g) {
     if ((uintptr_t)g.split_ws % 16 == 0) g.ep_stage |= 2;
     const bool bias_ok = !e.bias[0] || g.bias_mode == 1;
     if (g.affine && e.contig_n && !e.resid && bias_ok && g.ldc % 8 == 0 && (g.batch == 1 || e.batch.s0 % 8 == 0) &&
-        e.batch.r0 == 0 && ((uintptr_t)e.ptr[0] % 16) == 0)
+        e.batch.r0 == 0 && ((uintptr_t)e.ptr[0] % 16) == 0) {
         g.ep_stage |= 1;
+        return;
+    }
+    // an output through index maps (head permutation, segments): staged
+    // when every aligned 8-column piece of a row is 8 contiguous elements
+    // at a 16-byte aligned address
+    auto mult8 = [](int64_t v) { return v % 8 == 0; };
+    bool ok = e.contig_n && !e.resid && !(e.bias[0] && e.bias_on_m) && e.nmap.s0 == 1 &&
+              (e.nmap.r0 == 0 || e.nmap.r0 % 8 == 0) && mult8(e.nmap.s1) && mult8(e.nmap.s2) &&
+              mult8(e.mmap.s0) && mult8(e.mmap.s1) && mult8(e.mmap.s2) && mult8(e.batch.s0) &&
+              mult8(e.batch.s1) && mult8(e.batch.s2);
+    for (int i = 0; i < (e.nseg > 0 ? e.nseg : 1); ++i) ok = ok && e.ptr[i] && ((uintptr_t)e.ptr[i] % 16) == 0;
+    if (ok) g.ep_stage |= 4;
 }
 
 // The plan of the running call (entries keyed by sizes, dtype and operand
