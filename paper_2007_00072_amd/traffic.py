@@ -33,7 +33,8 @@ COPY_BYTES = 512 << 20
 def csrc_hash() -> str:
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2007_00072_amd", "csrc")
-    for f in sorted(os.listdir(d)):
+    # kernel and host sources only: build leftovers in the folder change nothing
+    for f in sorted(x for x in os.listdir(d) if x.endswith((".hip", ".hpp", ".h"))):
         h.update(f.encode())
         h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()[:16]
