@@ -49,7 +49,7 @@ def _slope(ks, us):
 def sweep(dev):
     rows = []
     ks = (512, 1024, 2048, 4096)
-    for M, N, cfgs in ((4096, 4096, (13, 20)), (4096, 1024, (15, 18, 22))):
+    for M, N, cfgs in ((4096, 4096, (13, 20, 23, 24)), (4096, 1024, (15, 18, 22))):
         C = torch.empty((M, N), device=dev, dtype=torch.float16)
         fill = _time(lambda: C.fill_(1.0))
         res = {"M": M, "N": N, "fill_us": fill, "cfg": {}}
@@ -81,8 +81,9 @@ def write(rows, copy_gbs, path, command):
            "`torch.matmul` (this PyTorch build's BLAS) on the same operands for reference.  `fill` is a plain "
            "fill of the output tensor.", "",
            f"Plain 1 GiB device copy: {copy_gbs:.0f} GB/s (bytes read + written).", ""]
-    names = {13: "256x256, 8 waves", 20: "256x256, 4 waves, interleaved", 15: "128x128, 8 waves",
-             18: "128x128, 4 waves", 22: "128x128, 4 waves, interleaved"}
+    names = {13: "256x256, 8 waves", 20: "256x256, 4 waves, interleaved", 23: "256x256, 8 waves, ping-pong",
+             24: "256x256, 8 waves, ping-pong, 5 stages", 15: "128x128, 8 waves", 18: "128x128, 4 waves",
+             22: "128x128, 4 waves, interleaved"}
     for r in rows:
         M, N, ks = r["M"], r["N"], r["ks"]
         out += [f"## M = {M}, N = {N} (output fill {r['fill_us']:.1f} us)", "",
