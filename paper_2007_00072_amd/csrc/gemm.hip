@@ -1425,6 +1425,12 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
     float cs[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) cs[q] = 0.f;
+    // activation step: the bias of the lane's 8 columns is the same for
+    // every row of the tile (loaded once, kept packed)
+    const bool lane_on = lane < RPI * VPR && nw + vc < g.N;
+    u32x4 bias_raw = {0u, 0u, 0u, 0u};
+    if constexpr (ACT != 0)
+        if (lane_on) bias_raw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const OutT*>(g.c.act_bias) + nw + vc);
 
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -1437,6 +1443,21 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
                 const int rr = 8 * (r >> 2) + 4 * h + (r & 3);
                 sm[rr * LDR + j * 32 + c] = from_f<OutT>(acc[i][j][r] * alpha + bn[j]);
             }
+        // mode 2: the block's pre-activation pieces, all requested before
+        // the first is used (once the block's accumulators are in LDS, so
+        // that they do not add to the registers held)
+        u32x4 hv[ACT == 2 ? NPASS : 1];
+        if constexpr (ACT == 2) {
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int p = 0; p < NPASS; ++p) {
+                const int rr = p * RPI + rr0;
+                hv[p] = u32x4{0u, 0u, 0u, 0u};
+                if (lane_on && rr < 32 && mb + rr < g.M)
+                    hv[p] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const OutT*>(g.c.act_in) + o.coff +
+                                                            (int64_t)(mb + rr) * o.ldc + nw + vc);
+            }
+        }
         const int n = nw + vc;
         if constexpr (ACT == 0) {
 #pragma unroll
@@ -1449,16 +1470,22 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
             }
         } else {
             static_assert(sizeof(OutT) == 2, "activation step in a 16-bit type");
+            // (passes not unrolled, so that the accumulators of the blocks
+            // still to store stay in registers: the pass's pre-activation
+            // piece is taken from the front of hv, which then shifts)
 #pragma unroll 1
             for (int p = 0; p < NPASS; ++p) {
                 const int rr = p * RPI + rr0;
+                const u32x4 hcur = hv[0];
+#pragma unroll
+                for (int t = 0; t + 1 < (ACT == 2 ? NPASS : 1); ++t) hv[t] = hv[t + 1];
                 if (lane < RPI * VPR && rr < 32) {
                     const u32x4 v = *reinterpret_cast<const u32x4*>(sm + rr * LDR + vc);
                     if (mb + rr < g.M && n < g.N) {
                         const int64_t off = (int64_t)(mb + rr) * o.ldc + n;
                         float a[8], b[8];
                         V8<OutT>::unpack(v, a);
-                        V8<OutT>::load(reinterpret_cast<const OutT*>(g.c.act_bias) + n, b);
+                        V8<OutT>::unpack(bias_raw, b);
                         if constexpr (ACT == 1) {
                             // the stored values, then their activation (the bias +
                             // activation operator's arithmetic, element index
@@ -1472,7 +1499,7 @@ __device__ __forceinline__ void lean_store_staged(const GemmArgs& g, const LeanO
                             // the activation backward of the (rounded) dA: the
                             // activation backward operator's arithmetic
                             float u[8];
-                            V8<OutT>::load(reinterpret_cast<const OutT*>(g.c.act_in) + o.coff + off, u);
+                            V8<OutT>::unpack(hcur, u);
                             dropout8(g.c.act_dp, (uint64_t)off, a);
 #pragma unroll
                             for (int q = 0; q < 8; ++q) {
