@@ -34,16 +34,18 @@ def short_name(sym: str) -> str:
     if m:
         dt = "f16" if m.group(2) == "DF16_" else "bf16"
         mode = lambda b: "k" if b == "1" else "o"
-        # the remaining template arguments: lean (k groups, row sums,
-        # interleaved schedule, activation step) or pair (row sums)
+        # the remaining template arguments: lean (k groups, row sums, k-loop
+        # schedule, activation step) or pair (row sums)
         rest = re.findall(r"EL([ib])(\d+)", m.group(11))
-        names = ("row sums",) if m.group(1) else ("k groups", "row sums", "interleaved", "act")
-        extra = ""
+        names = ("row sums",) if m.group(1) else ("k groups", "row sums", "schedule", "act")
+        extra = "" if m.group(8) == "4" else f",{m.group(8)} stages"
         for (kind, val), nm in zip(rest, names):
             if nm == "k groups" and val != "1":
                 extra += f",k groups {val}"
-            elif nm in ("row sums", "interleaved") and val == "1":
-                extra += f",{nm}"
+            elif nm == "row sums" and val == "1":
+                extra += ",row sums"
+            elif nm == "schedule" and val in ("1", "2"):
+                extra += ",interleaved" if val == "1" else ",ping-pong"
             elif nm == "act" and val != "0":
                 extra += f",act {val}"
         return (f"gemm_lean{m.group(1) or ''}<{dt},{m.group(3)}x{m.group(4)},waves {m.group(5)}x{m.group(6)},"
