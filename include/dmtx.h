@@ -318,7 +318,9 @@ int attn_backward_form(const dm_layer_desc* d, int32_t* key_blocks);
  * waves of 19 (as 20 otherwise), 22: the same schedule on the tile and
  * waves of 18 (as 11 otherwise), 23 and 24: the tile and waves of 13
  * with the two wave rows alternating between reading a k-step's fragments
- * and multiplying them, four and five LDS stages (as 14 otherwise);
+ * and multiplying them, four and five LDS stages (as 14 otherwise), 25: the
+ * same schedule on a 256x192 tile of 8 waves of 64x96, for a B operand
+ * contiguous along k (as 23 otherwise);
  * -1: chosen from the shape; other values are
  * DM_ERR_ARG); splits > 1 splits k, using `ws` (ws_bytes >=
  * splits*batch*M*N*4) for partial sums; splits = 0 chooses (no split
@@ -360,7 +362,7 @@ typedef struct {
     int64_t M, N, K, batch;        /* contraction sizes; batch: contractions in one launch */
     int32_t dtype;                 /* dm_dtype                                             */
     int32_t a_kcontig, b_kcontig;  /* 1: operand contiguous along the contraction index   */
-    int32_t tile_cfg;              /* 0..24 (contract's list)                              */
+    int32_t tile_cfg;              /* 0..25 (contract's list)                              */
     int32_t splits;                /* split-k factor, 1 = none                             */
     char label[48];                /* log only: kernel-timing label, "" when timing is off */
 } dm_contract_choice;

@@ -1628,8 +1628,10 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
     constexpr int STAGE = (AS + BS) * (int)sizeof(T);
     static_assert(STAGES >= 3 && FM >= 1 && FN >= 1 && STAGES * STAGE <= 160 * 1024, "configuration");
     __shared__ __attribute__((aligned(16))) unsigned char smem[STAGES * STAGE];
-    typedef typename LeanSel<T, BM, BKS, NT, AKC>::type DA;
-    typedef typename LeanSel<T, BN, BKS, NT, BKC>::type DB;
+    // (the ping-pong schedule copies each operand with half of the threads)
+    constexpr int NTC = PP ? NT / 2 : NT;
+    typedef typename LeanSel<T, BM, BKS, NTC, AKC>::type DA;
+    typedef typename LeanSel<T, BN, BKS, NTC, BKC>::type DB;
     constexpr int NL = DA::NV + DB::NV;  // copies per thread per step
     typedef typename Mfma32<T>::frag frag;
 
@@ -1779,8 +1781,9 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
             }
         }
     } else if constexpr (PP) {
-        // PP (two waves per SIMD): the waves of tile row 0 (group 0, one per
-        // SIMD) and of tile row 1 (group 1) alternate between a memory phase
+        // PP (two waves per SIMD): the waves of the upper half of the tile
+        // (group 0, one per SIMD) and of the lower half (group 1) alternate
+        // between a memory phase
         // (every fragment of a k-step read from LDS into registers, plus the
         // group's copies of a later step: group 0 copies the A part of every
         // stage, group 1 the B part) and an MFMA phase (the k-step's MFMAs
@@ -1792,12 +1795,15 @@ __device__ __forceinline__ void lean_run(const GemmArgs& g, int tm, int tn, int 
         // on (copies run STAGES - 2 steps ahead).  A group's copies of step
         // s + 1 have landed when its memory phase of step s ends (before that
         // phase's barrier).
-        static_assert(KG == 1 && !RS && WGM == 2, "ping-pong schedule: two wave rows, single k group");
+        static_assert(KG == 1 && !RS && WGM * WGN == 8 && WGM % 2 == 0,
+                      "ping-pong schedule: 8 waves in an even number of wave rows, single k group");
         static_assert(STAGES >= 3, "ping-pong schedule: a stage read, one in flight, one being refilled");
         constexpr int D = STAGES - 2, NH = NT / 2;
         typedef typename LeanSel<T, BM, BKS, NH, AKC>::type PA;
         typedef typename LeanSel<T, BN, BKS, NH, BKC>::type PB;
-        const int grp = wm;
+        // waves 0-3 (the upper half of the wave rows) and 4-7 land on the
+        // four SIMDs in the same order: one wave of each group per SIMD
+        const int grp = wm / (WGM / 2);
         PA pa;
         PB pb;
         if (grp == 0) pa.init(g.a, aoff, kb, m0, g.M);
@@ -2144,13 +2150,15 @@ struct TileCfg {
 // ping-pong schedule (the two wave rows alternate between reading a
 // k-step's fragments and multiplying them), four and five stages (copies
 // two and three k-steps ahead); contractions they do not take run as 13
-// would.
+// would.  25: the ping-pong schedule on a 256x192 tile of 8 waves of 64x96
+// (4 wave rows, 2 columns), for a B operand contiguous along k (otherwise
+// run as 23): 3072-wide outputs get 16 x 16 tiles, every CU one.
 constexpr TileCfg CFGS[] = {{256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 64, 4, 1}, {128, 64, 2, 2},
                             {256, 256, 2, 4}, {256, 128, 2, 2}, {128, 128, 2, 2}, {256, 128, 4, 2},
                             {256, 256, 2, 4}, {256, 256, 2, 4}, {128, 128, 2, 4}, {128, 128, 2, 2},
                             {256, 256, 2, 2}, {128, 128, 2, 2}, {256, 192, 2, 2}, {256, 256, 2, 2}, {256, 192, 2, 2}, {128, 128, 2, 2},
-                            {256, 256, 2, 4}, {256, 256, 2, 4}};
+                            {256, 256, 2, 4}, {256, 256, 2, 4}, {256, 192, 4, 2}};
 static_assert(sizeof(CFGS) / sizeof(CFGS[0]) == GEMM_MAX_CFG + 1, "configuration table");
 constexpr int NCFG = sizeof(CFGS) / sizeof(CFGS[0]);
 
@@ -2292,6 +2300,19 @@ void launch_lean_pp(const GemmArgs& g, hipStream_t st) {
                            0, st, g);
 }
 
+// Ping-pong kernels whose B tile width only suits a k-contiguous B operand.
+template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
+void launch_lean_pp_bk(const GemmArgs& g, hipStream_t st) {
+    dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
+    dim3 block(64 * WGM * WGN);
+    if (g.a.kcontig)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, 2>), grid, block, 0,
+                           st, g);
+    else
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, false, true, 1, false, 2>), grid, block, 0,
+                           st, g);
+}
+
 // Lean kernels whose B tile width only suits a k-contiguous B operand.
 template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean_bk(const GemmArgs& g, hipStream_t st) {
@@ -2359,6 +2380,7 @@ void launch_t(const GemmArgs& g, hipStream_t st) {
         case 22: launch_lean_il<T, 128, 128, 2, 2, 64, 4>(g, st); break;
         case 23: launch_lean_pp<T, 256, 256, 2, 4, 32, 4>(g, st); break;
         case 24: launch_lean_pp<T, 256, 256, 2, 4, 32, 5>(g, st); break;
+        case 25: launch_lean_pp_bk<T, 256, 192, 4, 2, 32, 4>(g, st); break;
         case 14: launch_big<T, 2, 4>(g, st); break;
         case 9: launch_x32<T, 256, 256, 2, 4, 2>(g, st); break;
         case 10: launch_x32<T, 256, 128, 2, 2, 3>(g, st); break;
@@ -2411,6 +2433,12 @@ void choose(GemmArgs& g) {
             // 10 % faster than cfg 13 at the same fixed cost; row sums are
             // produced by cfg 13 only.
             g.cfg = g.c.rsum ? 13 : 23;
+            // a 192-wide tile where 256-wide ones leave CUs idle and 192-wide
+            // ones still fit in one round (3072-wide outputs: 256 against
+            // 192 tiles)
+            if (!g.c.rsum && !g.c.act_mode && g.b.kcontig && g.N % 192 == 0 && ntiles(CFGS[23], g) < CUS &&
+                ntiles(CFGS[25], g) <= CUS)
+                g.cfg = 25;
         } else {
             g.cfg = 15;
             const int64_t t = ntiles(CFGS[15], g);
@@ -2434,7 +2462,9 @@ void choose(GemmArgs& g) {
     }
     if (g.cfg == 19 && !g.b.kcontig) g.cfg = 13;
     if (g.cfg == 21 && !g.b.kcontig) g.cfg = 20;
-    if ((g.cfg == 13 || g.cfg == 17 || g.cfg == 19 || g.cfg == 20 || g.cfg == 21 || g.cfg == 23 || g.cfg == 24) &&
+    if (g.cfg == 25 && !g.b.kcontig) g.cfg = 23;
+    if ((g.cfg == 13 || g.cfg == 17 || g.cfg == 19 || g.cfg == 20 || g.cfg == 21 || g.cfg == 23 || g.cfg == 24 ||
+         g.cfg == 25) &&
         !lean_ok(g, 32))
         g.cfg = 14;
     if ((g.cfg == 15 || g.cfg == 16 || g.cfg == 18 || g.cfg == 22) && !lean_ok(g, 64)) g.cfg = g.c.resid ? 8 : 11;

@@ -134,7 +134,7 @@ bool gemm_act_fusable(int dtype, const GemmArgs& g);
 int gemm_act_parts();
 
 // Largest tile configuration index (contract's tile_cfg, plan entries).
-constexpr int GEMM_MAX_CFG = 24;
+constexpr int GEMM_MAX_CFG = 25;
 
 // Scratch bytes for a split-K contraction.
 inline size_t gemm_split_ws_bytes(int64_t M, int64_t N, int64_t batch, int splits) {

@@ -3,7 +3,8 @@
     python -m paper_2007_00072_amd.gemm_probe --out profiles/contraction_sweep_f16.md
 
 For output shapes of the encoder layer's contractions (4096 tokens at
-BERT-large width), times the library's lean kernels (`contract` with a
+BERT-large width: 4096 x 4096, the fused Q/K/V projection's 4096 x 3072
+and 4096 x 1024), times the library's lean kernels (`contract` with a
 fixed tile configuration) as the contraction length K grows, so the cost
 per k-step (the slope) separates from the fixed cost of launch, prologue
 and output stores (the intercept), next to torch.matmul on the same
@@ -49,7 +50,7 @@ def _slope(ks, us):
 def sweep(dev):
     rows = []
     ks = (512, 1024, 2048, 4096)
-    for M, N, cfgs in ((4096, 4096, (13, 20, 23, 24)), (4096, 1024, (15, 18, 22))):
+    for M, N, cfgs in ((4096, 4096, (13, 20, 23, 24)), (4096, 3072, (23, 25)), (4096, 1024, (15, 18, 22))):
         C = torch.empty((M, N), device=dev, dtype=torch.float16)
         fill = _time(lambda: C.fill_(1.0))
         res = {"M": M, "N": N, "fill_us": fill, "cfg": {}}
@@ -82,7 +83,8 @@ def write(rows, copy_gbs, path, command):
            "fill of the output tensor.", "",
            f"Plain 1 GiB device copy: {copy_gbs:.0f} GB/s (bytes read + written).", ""]
     names = {13: "256x256, 8 waves", 20: "256x256, 4 waves, interleaved", 23: "256x256, 8 waves, ping-pong",
-             24: "256x256, 8 waves, ping-pong, 5 stages", 15: "128x128, 8 waves", 18: "128x128, 4 waves",
+             24: "256x256, 8 waves, ping-pong, 5 stages", 25: "256x192, 8 waves, ping-pong",
+             15: "128x128, 8 waves", 18: "128x128, 4 waves",
              22: "128x128, 4 waves, interleaved"}
     for r in rows:
         M, N, ks = r["M"], r["N"], r["ks"]

@@ -39,7 +39,7 @@ import time
 from collections import OrderedDict, defaultdict
 from typing import Dict, List, Sequence, Tuple
 
-TILE_CFGS = list(range(25))
+TILE_CFGS = list(range(26))
 # A measured difference smaller than the run-to-run spread of these timings
 # does not move a contraction off the library's own choice.
 KEEP_BUILTIN = 0.97

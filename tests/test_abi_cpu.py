@@ -199,7 +199,7 @@ def test_plan_objects_host_only(lib):
     lib.set_plan(d, None)
     assert not d.plan
     for bad in [((), 0, {"ln_lanes": 24}), ((), 0, {"ln_bwd_form": 3}), ((), 0, {"dH_transposed": 2}),
-                ((), 4), ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 25, 1)], 0),
+                ((), 4), ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 26, 1)], 0),
                 ([(64, 64, 64, 1, lib.DM_F16, 1, 1, 5, 0)], 0), ([(0, 64, 64, 1, lib.DM_F16, 1, 1, 5, 1)], 0)]:
         with pytest.raises(lib.DmError):
             lib.Plan(*bad)

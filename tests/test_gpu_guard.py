@@ -154,7 +154,7 @@ def test_fused_operators_write_stay_inside(lib, dt):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("cfg,splits", [(-1, 0), (13, 1), (15, 2), (16, 1), (8, 3), (11, 1), (17, 1), (18, 2), (19, 1), (20, 1), (21, 2), (22, 3), (23, 1), (24, 2)])
+@pytest.mark.parametrize("cfg,splits", [(-1, 0), (13, 1), (15, 2), (16, 1), (8, 3), (11, 1), (17, 1), (18, 2), (19, 1), (20, 1), (21, 2), (22, 3), (23, 1), (24, 2), (25, 1)])
 @pytest.mark.parametrize("bt", [0, 1])
 def test_contract_writes_stay_inside(lib, dt, cfg, splits, bt):
     g = Guard()

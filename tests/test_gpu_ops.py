@@ -301,7 +301,7 @@ def test_contract_modes(lib, dt, a_trans, b_trans, batch, M, N, K):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("cfg", list(range(25)))
+@pytest.mark.parametrize("cfg", list(range(26)))
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (0, 0), (1, 0), (1, 1)])
 def test_contract_tile_configs(lib, dt, cfg, a_trans, b_trans):
     # ragged in every dimension for every block tile
@@ -312,7 +312,7 @@ def test_contract_tile_configs(lib, dt, cfg, a_trans, b_trans):
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (0, 0), (1, 0), (1, 1)])
 @pytest.mark.parametrize("batch,M,N,K,splits", [(2, 264, 328, 256, 1), (1, 512, 256, 512, 1), (1, 264, 520, 1152, 3),
                                                 (3, 136, 40, 128, 1), (1, 8, 8, 64, 1)])
-@pytest.mark.parametrize("cfg", [13, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24])
+@pytest.mark.parametrize("cfg", [13, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25])
 def test_contract_lean(lib, dt, a_trans, b_trans, batch, M, N, K, splits, cfg):
     # the lean kernels themselves (k a multiple of their 32- or 64-wide
     # step): ragged m and n, split k (single batch), bias and float output
@@ -320,7 +320,7 @@ def test_contract_lean(lib, dt, a_trans, b_trans, batch, M, N, K, splits, cfg):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("cfg,splits", [(2, 2), (4, 3), (0, 4), (3, 5), (5, 2), (6, 3), (7, 4), (8, 2), (9, 2), (10, 3), (11, 4), (12, 2), (13, 3), (14, 2), (15, 2), (16, 3), (17, 2), (18, 3), (19, 2), (20, 2), (21, 3), (22, 2), (23, 3), (24, 2)])
+@pytest.mark.parametrize("cfg,splits", [(2, 2), (4, 3), (0, 4), (3, 5), (5, 2), (6, 3), (7, 4), (8, 2), (9, 2), (10, 3), (11, 4), (12, 2), (13, 3), (14, 2), (15, 2), (16, 3), (17, 2), (18, 3), (19, 2), (20, 2), (21, 3), (22, 2), (23, 3), (24, 2), (25, 2)])
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (1, 0)])
 def test_contract_split_k(lib, dt, cfg, splits, a_trans, b_trans):
     _contract_case(lib, dt, a_trans, b_trans, 2, 136, 264, 1096, cfg=cfg, splits=splits)

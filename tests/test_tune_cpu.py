@@ -79,7 +79,7 @@ def test_saved_plans_are_well_formed():
         assert 0 <= int(plan["attn_path"]) <= 3 and int(plan.get("qkv_fusion", 0)) in (0, 1, 2)
         assert plan["entries"]
         for e in plan["entries"]:
-            assert 0 <= e["tile_cfg"] <= 24 and 1 <= e["splits"] <= 64, (path, e)
+            assert 0 <= e["tile_cfg"] <= 25 and 1 <= e["splits"] <= 64, (path, e)
             assert e["M"] > 0 and e["N"] > 0 and e["K"] > 0 and e["batch"] >= 1
 
 
