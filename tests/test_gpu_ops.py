@@ -320,6 +320,41 @@ def test_contract_lean(lib, dt, a_trans, b_trans, batch, M, N, K, splits, cfg):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (0, 0), (1, 0), (1, 1)])
+def test_contract_schedules_bit_identical(lib, dt, a_trans, b_trans):
+    # the lean 32x32x16 kernels differ only in tiling and in how loads, reads
+    # and MFMAs are scheduled: every output element takes the same MFMA
+    # instruction over the same 16-wide k slices in the same order, so the
+    # interleaved and ping-pong schedules (cfg 20, 23, 24; 21 and 25 on the
+    # 192-wide tiles) reproduce the two-waves-per-SIMD kernel (cfg 13, 19)
+    # bit for bit, also with bias and split partials; ragged m and n
+    batch, M, N, K = 1, 520, 392, 1024
+    A = make_tensor((batch, K, M) if a_trans else (batch, M, K), dt, 111)
+    B = make_tensor((batch, N, K) if b_trans else (batch, K, N), dt, 112)
+    bias = make_tensor((N,), dt, 113)
+
+    def run(cfg, splits=1, out_f32=0):
+        C = torch.empty((batch, M, N), dtype=torch.float32 if out_f32 else A.dtype, device=DEV)
+        wsb = splits * batch * M * N * 4 if splits > 1 else 0
+        ws = torch.empty(wsb, dtype=torch.uint8, device=DEV) if wsb else None
+        lib.contract(DT[dt], batch, M, N, K, 0.5, dev(A), a_trans, M * K, dev(B), b_trans, N * K,
+                     None if out_f32 else dev(bias), C, out_f32, M * N, cfg, splits, ws, wsb)
+        torch.cuda.synchronize()
+        return C.cpu()
+
+    for out_f32 in (0, 1):
+        for splits in (1, 2):
+            ref = run(13, splits, out_f32)
+            for cfg in (20, 23, 24):
+                assert torch.equal(run(cfg, splits, out_f32), ref), (cfg, splits, out_f32)
+            if b_trans:  # the 192-wide tiles take a B contiguous along k
+                ref192 = run(19, splits, out_f32)
+                assert torch.equal(ref192, ref)
+                for cfg in (21, 25):
+                    assert torch.equal(run(cfg, splits, out_f32), ref), (cfg, splits, out_f32)
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
 @pytest.mark.parametrize("cfg,splits", [(2, 2), (4, 3), (0, 4), (3, 5), (5, 2), (6, 3), (7, 4), (8, 2), (9, 2), (10, 3), (11, 4), (12, 2), (13, 3), (14, 2), (15, 2), (16, 3), (17, 2), (18, 3), (19, 2), (20, 2), (21, 3), (22, 2), (23, 3), (24, 2), (25, 2)])
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (1, 0)])
 def test_contract_split_k(lib, dt, cfg, splits, a_trans, b_trans):
