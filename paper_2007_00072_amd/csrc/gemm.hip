@@ -2305,7 +2305,10 @@ template <typename T, int BM, int BN, int WGM, int WGN, int BKS, int STAGES>
 void launch_lean_pp_bk(const GemmArgs& g, hipStream_t st) {
     dim3 grid(g.tiles_m * g.tiles_n, g.batch * (g.splits > 1 ? g.splits : 1));
     dim3 block(64 * WGM * WGN);
-    if (g.a.kcontig)
+    if (g.c.act_mode == 1)
+        hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, 2, 1>), grid, block,
+                           0, st, g);
+    else if (g.a.kcontig)
         hipLaunchKernelGGL((gemm_lean<T, BM, BN, WGM, WGN, BKS, STAGES, true, true, 1, false, 2>), grid, block, 0,
                            st, g);
     else
@@ -2436,7 +2439,7 @@ void choose(GemmArgs& g) {
             // a 192-wide tile where 256-wide ones leave CUs idle and 192-wide
             // ones still fit in one round (3072-wide outputs: 256 against
             // 192 tiles)
-            if (!g.c.rsum && !g.c.act_mode && g.b.kcontig && g.N % 192 == 0 && ntiles(CFGS[23], g) < CUS &&
+            if (!g.c.rsum && g.c.act_mode != 2 && g.b.kcontig && g.N % 192 == 0 && ntiles(CFGS[23], g) < CUS &&
                 ntiles(CFGS[25], g) <= CUS)
                 g.cfg = 25;
         } else {
@@ -2547,15 +2550,19 @@ void apply_plan(GemmArgs& g, int dtype) {
 
 // Keeps the activation step only where the staged epilogue takes it:
 // unsplit lean 256x256 or 128x128 kernel of 8 waves (2 wave rows: cfg 13,
-// 15 and the ping-pong forms of 13, 23 and 24), staged
+// 15 and the ping-pong forms of 13, 23 and 24; mode 1 also on the 256x192
+// ping-pong tile, cfg 25), staged
 // row-major output, 16-bit storage, no alpha scaling or bias; mode 1 with A
 // and B contiguous along k, mode 2 with A contiguous along k and B along
 // n, its partial rows (2 per tile row) within act_part_cap.  Returns the
 // partial rows mode 2 writes (1 for mode 1), 0 when not taken.
 int settle_act(GemmArgs& g, int dtype) {
     const Epilogue& e = g.c;
-    bool ok = e.act_mode && dtype != G_F32 && (g.cfg == 13 || g.cfg == 15 || g.cfg == 23 || g.cfg == 24) &&
-              !e.rsum && g.splits <= 1 &&
+    // (cfg 25, 4 wave rows and 96-column waves, takes mode 1 only: mode 2's
+    // partial rows assume 2 wave rows and its column groups a power-of-two
+    // lane count)
+    const bool tile_ok = g.cfg == 13 || g.cfg == 15 || g.cfg == 23 || g.cfg == 24 || (g.cfg == 25 && e.act_mode == 1);
+    bool ok = e.act_mode && dtype != G_F32 && tile_ok && !e.rsum && g.splits <= 1 &&
               (g.ep_stage & 1) && !e.out_f32 && !e.bias[0] && e.alpha == 1.0f && e.act_bias && g.batch == 1;
     int parts = 1;
     if (ok && e.act_mode == 1) ok = g.a.kcontig && g.b.kcontig && e.act_out && ((uintptr_t)e.act_out % 16) == 0;

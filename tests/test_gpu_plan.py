@@ -204,3 +204,37 @@ def test_epilogue_operators_change_no_value(name, act, p_act):
             assert torch.allclose(g, L1.grads[n], rtol=1e-5, atol=1e-5 * float(g.abs().max()))
         else:
             assert torch.equal(g, L1.grads[n]), n
+
+
+@pytest.mark.parametrize("name,act,p_act", [("bert_large_f16", "gelu", 0.0), ("bert_base_bf16", "relu", 0.1)])
+def test_bias_act_epilogue_on_the_192_wide_tile(name, act, p_act):
+    # Linear 1 with its bias + activation epilogue moved by a plan entry to
+    # the 256x192 ping-pong kernel (4 wave rows, ragged last tile column at
+    # F = 1024): the same MFMA instruction and k order, the same epilogue
+    # arithmetic, so H, A, y, dx and every weight gradient are bit for bit
+    # those of the built-in kernel
+    wl = small(name, B=2, J=128, K=128, H=4, P=64, W=64, I=256, F=1024)
+
+    def run(plan=None):
+        lib.dm_trace_enable(True)
+        lib.plan_log(True)
+        L, _, _, _, y, dx = run_encoder(wl, act=act, p_ffn_act=p_act, plan=plan)
+        recs = lib.plan_log_read()
+        lib.plan_log(False)
+        labels = [lab for lab, _, _ in lib.trace_records()]
+        lib.dm_trace_enable(False)
+        T, F = wl.shape.B * wl.shape.J, wl.shape.F
+        saved = {n: L.saved_tensor(n, (T, F), y.dtype).clone() for n in ("h", "a")}
+        return L, y, dx, recs, labels, saved
+
+    L0, y0, dx0, recs, labels, s0 = run()
+    keys = [r.key() for r in recs if r.label.decode() == "F7+8 linear1_bias_act"]
+    assert len(keys) == 1
+    L1, y1, dx1, recs1, labels1, s1 = run(lib.Plan([lib.ContractChoice(*keys[0], 25, 1)], 0))
+    assert "F7+8 linear1_bias_act" in labels1
+    assert [r.tile_cfg for r in recs1 if r.label.decode() == "F7+8 linear1_bias_act"] == [25]
+    for n in ("h", "a"):
+        assert torch.equal(s0[n], s1[n]), n
+    assert torch.equal(y0, y1) and torch.equal(dx0, dx1)
+    for n, g in L0.grads.items():
+        assert torch.equal(g, L1.grads[n]), n
