@@ -311,11 +311,14 @@ def test_contract_tile_configs(lib, dt, cfg, a_trans, b_trans):
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 @pytest.mark.parametrize("a_trans,b_trans", [(0, 1), (0, 0), (1, 0), (1, 1)])
 @pytest.mark.parametrize("batch,M,N,K,splits", [(2, 264, 328, 256, 1), (1, 512, 256, 512, 1), (1, 264, 520, 1152, 3),
-                                                (3, 136, 40, 128, 1), (1, 8, 8, 64, 1)])
+                                                (3, 136, 40, 128, 1), (1, 8, 8, 64, 1), (2, 40, 200, 32, 1),
+                                                (1, 296, 200, 96, 1)])
 @pytest.mark.parametrize("cfg", [13, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25])
 def test_contract_lean(lib, dt, a_trans, b_trans, batch, M, N, K, splits, cfg):
     # the lean kernels themselves (k a multiple of their 32- or 64-wide
-    # step): ragged m and n, split k (single batch), bias and float output
+    # step): ragged m and n, split k (single batch), bias and float output;
+    # k of one and three 32-wide steps (fewer steps than the ping-pong
+    # schedule keeps in flight)
     _contract_case(lib, dt, a_trans, b_trans, batch, M, N, K, cfg=cfg, splits=splits)
 
 
